@@ -1,0 +1,793 @@
+// libsdnn: Sparse DNN Challenge inference (Kepner et al., 2019) on MI355X (gfx950).
+//
+// Per layer (Sec. II batched equation, Sec. V listing):
+//   z[r][j] = fma chain over the sources k of column j, ascending, of Y[r][k] * W(k, j)
+//   Y'[r][j] = (z != 0) ? min(ymax, max(0, z + b[j])) : 0
+// followed by dropping rows that became all zero (they stay zero) and, after the last layer, the
+// categories: rows with any entry > 0 (Sec. V).
+//
+// Data layout in HBM
+//   Activations: row-major [M][N] fp32, indexed by input row id. Layer 0 reads the caller's y0;
+//   layers then ping-pong between two workspace buffers. A list of live row ids (ascending) selects
+//   which rows a layer reads; rows off the list are never touched again.
+//   Weights: per layer an ELL table [N][K] of (byte offset of the source row in the kernel's tile,
+//   fp32 weight) pairs, sources ascending within each output, padded with (0, 0.0f). Padding adds
+//   fma(y, 0, acc) = acc exactly because activations are finite.
+//
+// Kernels
+//   k_layer_lds<B>: one workgroup takes a tile of B live rows, stages it in LDS transposed to
+//     [k][B] (feature-major, so the B values of one source are contiguous), then every output j is
+//     computed by B/4 lanes, each holding 4 rows: one 16-byte LDS read per term serves 4 rows, and
+//     the term order is the ELL order (ascending source). Bias, ReLU and the YMAX clamp are applied
+//     before the store; a row's liveness is OR-reduced in LDS and written once per tile.
+//   k_to_fm + k_layer_gfm (widths whose tile does not fit LDS): the live rows are first copied into
+//     feature-major tiles of 32 rows in global memory ([N][32] per tile, 128 bytes per source), then
+//     workgroups gather 128-byte segments from a tile that stays resident in the L2 of the XCD that
+//     works on it (workgroup ids are mapped so that one XCD's workgroups share a tile).
+//   k_compact: stable compaction of the live-row list (wave ballot + prefix count).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "sdnn.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+sdnn_status fail(sdnn_status s, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+constexpr int kMaxNeurons = 65536;
+constexpr int kMaxLayers = 1000000;
+constexpr int kMaxDegree = 4096;
+constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
+constexpr int kFmRows = 32;                // rows per global feature-major tile
+constexpr int kGfmOutputs = 64;            // outputs per work item of k_layer_gfm
+constexpr int kPollEvery = 4;              // layers between live-count read-backs
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ------------------------------------------------------------------------------------------------
+// Device code
+
+__device__ __forceinline__ float activate(float z, float b, float ymax) {
+  // Sec. V: Y = Z + logical(Z).*b; Y(Y<0) = 0; Y(Y>YMAX) = YMAX. Zeros come out as +0.
+  if (z == 0.0f) return 0.0f;
+  const float t = z + b;
+  return t > ymax ? ymax : (t > 0.0f ? t : 0.0f);
+}
+
+__device__ __forceinline__ bool any_nonzero(float4 v) {
+  return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
+}
+
+__global__ void k_init(int *__restrict__ ids, int *__restrict__ flags, int *__restrict__ rownz,
+                       int *__restrict__ counts, int M, int L) {
+  const int st = gridDim.x * blockDim.x;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
+    ids[i] = i;
+    flags[i] = 0;
+    rownz[i] = 0;
+  }
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i <= L; i += st) counts[i] = (i == 0) ? M : 0;
+}
+
+// Stable compaction: ids_out = [ids_in[p] for p < R if flags[p]], count_out = its length.
+// Flags are reset to 0 for the next layer. One workgroup of 1024 threads.
+__global__ __launch_bounds__(1024) void k_compact(int *__restrict__ flags, const int *__restrict__ ids_in,
+                                                  int *__restrict__ ids_out, const int *__restrict__ count_in,
+                                                  int *__restrict__ count_out) {
+  __shared__ int wsum[16];
+  const int R = *count_in;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int base = 0;
+  for (int c0 = 0; c0 < R; c0 += 1024) {
+    const int i = c0 + tid;
+    int f = 0;
+    if (i < R) {
+      f = flags[i];
+      flags[i] = 0;
+    }
+    const unsigned long long m = __ballot(f != 0);
+    const int below = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) wsum[wave] = __popcll(m);
+    __syncthreads();
+    int off = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      const int s = wsum[w];
+      off += (w < wave) ? s : 0;
+      total += s;
+    }
+    if (f) ids_out[base + off + below] = ids_in[i];
+    base += total;
+    __syncthreads();
+  }
+  if (tid == 0) *count_out = base;
+}
+
+__global__ void k_final_ids(const int *__restrict__ ids, const int *__restrict__ count, long long *__restrict__ out) {
+  const int R = *count;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < R; i += gridDim.x * blockDim.x) out[i] = ids[i];
+}
+
+// One layer with the activation tile staged in LDS. B rows per tile (a multiple of 4); blockDim 1024.
+template <int B>
+__global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
+                                                    const int2 *__restrict__ ell, int K,
+                                                    const float *__restrict__ bias, float ymax,
+                                                    const int *__restrict__ ids, const int *__restrict__ count,
+                                                    int *__restrict__ flags, int *__restrict__ rownz) {
+  extern __shared__ float4 smem[];
+  char *tile = reinterpret_cast<char *>(smem);
+  float *tilef = reinterpret_cast<float *>(smem);
+  __shared__ int rowlive[B];
+  __shared__ int rowany[B];
+  constexpr int LPO = B / 4;    // lanes per output
+  constexpr int OPW = 64 / LPO; // outputs per wave instruction
+  const int R = *count;
+  const int ntiles = (R + B - 1) / B;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int quad = lane % LPO, jl = lane / LPO;
+  if (tid < B) {
+    rowlive[tid] = 0;
+    rowany[tid] = 0;
+  }
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+    const int p0 = t * B;
+    const int nvalid = min(B, R - p0);
+    // ---- stage rows ids[p0 .. p0+nvalid) as tile[k][b]; missing rows are zero
+    if ((N & 3) == 0) {
+      const int NQ = N >> 2;
+      const int items = NQ * (B / 4);
+      for (int it = tid; it < items; it += blockDim.x) {
+        const int bq = it % (B / 4), q = it / (B / 4);
+        float4 v[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const int b = bq * 4 + c;
+          v[c] = (b < nvalid) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p0 + b] * N)[q]
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        float4 *dst = reinterpret_cast<float4 *>(tilef + (size_t)(4 * q) * B + bq * 4);
+        dst[0] = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
+        dst[B / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
+        dst[2 * (B / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
+        dst[3 * (B / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
+        if (rownz) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if (any_nonzero(v[c])) rowany[bq * 4 + c] = 1;
+        }
+      }
+    } else {
+      for (int it = tid; it < N * B; it += blockDim.x) {
+        const int b = it % B, k = it / B;
+        const float v = (b < nvalid) ? yin[(size_t)ids[p0 + b] * N + k] : 0.0f;
+        tilef[(size_t)k * B + b] = v;
+        if (rownz && v != 0.0f) rowany[b] = 1;
+      }
+    }
+    __syncthreads();
+    // ---- compute: lane (quad, jl) owns rows 4*quad..4*quad+3 of output j
+    int row[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int b = quad * 4 + c;
+      row[c] = (b < nvalid) ? ids[p0 + b] : -1;
+    }
+    int live_mask = 0;
+    for (int j0 = wave * OPW; j0 < N; j0 += nw * OPW) {
+      const int j = j0 + jl;
+      if (j < N) {
+        const int2 *e = ell + (size_t)j * K;
+        float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+        for (int s = 0; s < K; ++s) {
+          const int2 p = e[s];
+          const float4 v = *reinterpret_cast<const float4 *>(tile + p.x + quad * 16);
+          const float w = __int_as_float(p.y);
+          a0 = fmaf(v.x, w, a0);
+          a1 = fmaf(v.y, w, a1);
+          a2 = fmaf(v.z, w, a2);
+          a3 = fmaf(v.w, w, a3);
+        }
+        const float bj = bias[j];
+        const float y[4] = {activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
+                            activate(a3, bj, ymax)};
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          if (row[c] >= 0) {
+            yout[(size_t)row[c] * N + j] = y[c];
+            if (y[c] > 0.0f) live_mask |= 1 << c;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (live_mask & (1 << c)) rowlive[quad * 4 + c] = 1;
+    __syncthreads();
+    if (tid < nvalid) {
+      flags[p0 + tid] = rowlive[tid];
+      if (rownz && rowany[tid]) rownz[ids[p0 + tid]] = 1;
+    }
+    if (tid < B) {
+      rowlive[tid] = 0;
+      rowany[tid] = 0;
+    }
+    __syncthreads();
+  }
+}
+
+// Copy live rows into feature-major tiles of kFmRows rows: fm[t][k][b] = Y[ids[t*32 + b]][k], zero
+// for positions past the live count.
+__global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, float *__restrict__ fm, int N,
+                                               const int *__restrict__ ids, const int *__restrict__ count,
+                                               int *__restrict__ rownz) {
+  const int R = *count;
+  const int ntiles = (R + kFmRows - 1) / kFmRows;
+  const size_t st = (size_t)gridDim.x * blockDim.x;
+  if ((N & 3) == 0) {
+    const int NQ = N >> 2;
+    const size_t items = (size_t)ntiles * NQ * (kFmRows / 4);
+    for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += st) {
+      const int bq = (int)(it % (kFmRows / 4));
+      const size_t rest = it / (kFmRows / 4);
+      const int q = (int)(rest % NQ);
+      const int t = (int)(rest / NQ);
+      float4 v[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int p = t * kFmRows + bq * 4 + c;
+        v[c] = (p < R) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p] * N)[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+        if (rownz && p < R && any_nonzero(v[c])) rownz[ids[p]] = 1;
+      }
+      float4 *dst = reinterpret_cast<float4 *>(fm + ((size_t)t * N + 4 * q) * kFmRows + bq * 4);
+      dst[0] = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
+      dst[kFmRows / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
+      dst[2 * (kFmRows / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
+      dst[3 * (kFmRows / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
+    }
+  } else {
+    const size_t items = (size_t)ntiles * N * kFmRows;
+    for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += st) {
+      const int b = (int)(it % kFmRows);
+      const size_t rest = it / kFmRows;
+      const int k = (int)(rest % N);
+      const int t = (int)(rest / N);
+      const int p = t * kFmRows + b;
+      const float v = (p < R) ? yin[(size_t)ids[p] * N + k] : 0.0f;
+      fm[((size_t)t * N + k) * kFmRows + b] = v;
+      if (rownz && v != 0.0f) rownz[ids[p]] = 1;
+    }
+  }
+}
+
+// One layer gathering from global feature-major tiles. blockDim 256 (4 waves); a work item is a
+// chunk of kGfmOutputs outputs of one tile. Lane = (row b = lane % 32, output half h = lane / 32).
+// gridDim must be a multiple of 8: workgroup x runs on XCD x % 8, and the items of one XCD walk
+// the output chunks of one tile before moving on, so the tile stays in that XCD's L2.
+__global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm, float *__restrict__ yout, int N,
+                                                   const int2 *__restrict__ ell, int K,
+                                                   const float *__restrict__ bias, float ymax,
+                                                   const int *__restrict__ ids, const int *__restrict__ count,
+                                                   int *__restrict__ flags) {
+  __shared__ float stage[kFmRows][kGfmOutputs + 1];
+  __shared__ int rowlive[kFmRows];
+  const int R = *count;
+  const int ntiles = (R + kFmRows - 1) / kFmRows;
+  const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = lane & 31, h = lane >> 5;
+  const int xcd = blockIdx.x & 7;
+  const int per_xcd = gridDim.x >> 3;
+  if (tid < kFmRows) rowlive[tid] = 0;
+  __syncthreads();
+  for (long long local = blockIdx.x >> 3;; local += per_xcd) {
+    const long long grp = local / nchunks;
+    const int chunk = (int)(local % nchunks);
+    const long long tl = grp * 8 + xcd;
+    if (tl >= ntiles) break;
+    const int t = (int)tl;
+    const int p0 = t * kFmRows;
+    const int nvalid = min(kFmRows, R - p0);
+    const int c0 = chunk * kGfmOutputs;
+    const char *tb = reinterpret_cast<const char *>(fm + (size_t)t * N * kFmRows) + b * 4;
+    bool live = false;
+    for (int i = 0; i < kGfmOutputs / 8; ++i) {
+      const int jj = i * 8 + wave * 2 + h;
+      const int j = c0 + jj;
+      if (j < N) {
+        const int2 *e = ell + (size_t)j * K;
+        float a = 0.0f;
+        for (int s = 0; s < K; ++s) {
+          const int2 p = e[s];
+          a = fmaf(*reinterpret_cast<const float *>(tb + p.x), __int_as_float(p.y), a);
+        }
+        const float y = activate(a, bias[j], ymax);
+        stage[b][jj] = y;
+        live |= (y > 0.0f);
+      }
+    }
+    if (live && b < nvalid) rowlive[b] = 1;
+    __syncthreads();
+    // write the staged block row by row: 8 threads per row, 8 outputs each
+    {
+      const int rb = tid >> 3, seg = (tid & 7) * 8;
+      if (rb < nvalid) {
+        float *dst = yout + (size_t)ids[p0 + rb] * N + c0 + seg;
+        for (int x = 0; x < 8; ++x)
+          if (c0 + seg + x < N) dst[x] = stage[rb][seg + x];
+      }
+    }
+    if (tid < nvalid && rowlive[tid]) flags[p0 + tid] = 1;
+    __syncthreads();
+    if (tid < kFmRows) rowlive[tid] = 0;
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Host side
+
+struct LayerDev {
+  const int2 *ell = nullptr;
+  const float *bias = nullptr;
+  int K = 0;
+};
+
+}  // namespace
+
+struct sdnn_net {
+  int32_t N = 0, L = 0;
+  float ymax = 32.0f;
+  int path = 0;  // 0: LDS tiles, 1: global feature-major tiles
+  int B = 0;     // rows per LDS tile (path 0)
+  int device = -1;
+  int cus = 0;
+  bool poisoned = false;
+  std::vector<LayerDev> layers;
+  std::vector<void *> allocations;
+  int32_t n_loaded = 0;
+  // last run
+  bool ran = false;
+  int64_t M = 0;
+  hipStream_t stream = nullptr;
+  char *ws = nullptr;
+  float *ybuf[2] = {nullptr, nullptr};
+  float *fm = nullptr;
+  int *ids[2] = {nullptr, nullptr};
+  int *flags = nullptr, *rownz = nullptr, *counts = nullptr;
+  long long *final_ids = nullptr;
+  int final_list = 0;        // which ids buffer holds the final list
+  int32_t layers_run = 0;    // layers enqueued by the last infer
+  const float *final_y = nullptr;
+  int32_t *pinned = nullptr; // live-count read-back slots
+  std::vector<hipEvent_t> events;
+  // profiling
+  bool profiling = false;
+  bool pending_times = false;
+  std::vector<hipEvent_t> prof_start, prof_end;
+  std::vector<double> prof_ms;
+  std::vector<int64_t> prof_runs;
+};
+
+namespace {
+
+#define HIP_OR_POISON(net, call)                                                                   \
+  do {                                                                                             \
+    hipError_t e_ = (call);                                                                        \
+    if (e_ != hipSuccess) {                                                                        \
+      (net)->poisoned = true;                                                                      \
+      return fail(SDNN_EDEVICE, "%s failed: %s", #call, hipGetErrorString(e_));                   \
+    }                                                                                              \
+  } while (0)
+
+struct WsLayout {
+  size_t ybuf[2], fm, ids[2], flags, rownz, counts, final_ids, total;
+};
+
+WsLayout layout_for(const sdnn_net *net, int64_t M) {
+  WsLayout w{};
+  const size_t a = 256;
+  size_t off = 0;
+  const size_t ybytes = align_up((size_t)M * (size_t)net->N * sizeof(float), a);
+  w.ybuf[0] = off; off += ybytes;
+  w.ybuf[1] = off; off += ybytes;
+  w.fm = off;
+  if (net->path == 1) off += align_up((size_t)((M + kFmRows - 1) / kFmRows) * kFmRows * (size_t)net->N * sizeof(float), a);
+  const size_t ib = align_up((size_t)std::max<int64_t>(M, 1) * sizeof(int), a);
+  w.ids[0] = off; off += ib;
+  w.ids[1] = off; off += ib;
+  w.flags = off; off += ib;
+  w.rownz = off; off += ib;
+  w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
+  w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
+  w.total = off;
+  return w;
+}
+
+sdnn_status check_usable(const sdnn_net *net) {
+  if (!net) return fail(SDNN_EINVAL, "null handle");
+  if (net->poisoned) return fail(SDNN_EDEVICE, "handle is poisoned by an earlier device error");
+  return SDNN_OK;
+}
+
+template <int B>
+hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerDev &ld, const int *ids,
+                      const int *count, int *rownz) {
+  static bool configured = false;
+  const size_t lds = (size_t)B * net->N * sizeof(float);
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_lds<B>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsTileBytes);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  const int per_cu = lds <= 64 * 1024 ? 2 : 1;
+  hipLaunchKernelGGL(k_layer_lds<B>, dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
+                     ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->flags, rownz);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count) {
+  const LayerDev &ld = net->layers[l];
+  int *rownz = (l == 0) ? net->rownz : nullptr;
+  if (net->path == 0) {
+    switch (net->B) {
+      case 32: return launch_lds<32>(net, yin, yout, ld, ids, count, rownz);
+      case 16: return launch_lds<16>(net, yin, yout, ld, ids, count, rownz);
+      default: return launch_lds<8>(net, yin, yout, ld, ids, count, rownz);
+    }
+  }
+  hipLaunchKernelGGL(k_to_fm, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, net->fm, net->N, ids, count, rownz);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_layer_gfm, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell, ld.K,
+                     ld.bias, net->ymax, ids, count, net->flags);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sdnn_last_error(void) { return g_err.c_str(); }
+
+sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, float ymax) {
+  if (!out) return fail(SDNN_EINVAL, "out is null");
+  *out = nullptr;
+  if (n_neurons < 1 || n_neurons > kMaxNeurons) return fail(SDNN_EINVAL, "n_neurons %d not in [1, %d]", n_neurons, kMaxNeurons);
+  if (n_layers < 1 || n_layers > kMaxLayers) return fail(SDNN_EINVAL, "n_layers %d not in [1, %d]", n_layers, kMaxLayers);
+  if (!std::isfinite(ymax) || !(ymax > 0.0f)) return fail(SDNN_EINVAL, "ymax must be finite and > 0");
+  sdnn_net *net = new (std::nothrow) sdnn_net;
+  if (!net) return fail(SDNN_ENOMEM, "out of host memory");
+  net->N = n_neurons;
+  net->L = n_layers;
+  net->ymax = ymax;
+  net->layers.resize((size_t)n_layers);
+  // LDS tile of B rows x N fp32 must fit the budget with B >= 8
+  if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
+  else if ((size_t)16 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 16; }
+  else if ((size_t)8 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 8; }
+  else { net->path = 1; net->B = kFmRows; }
+  *out = net;
+  g_err.clear();
+  return SDNN_OK;
+}
+
+int32_t sdnn_kernel_path(const sdnn_net *net) { return net ? net->path : -1; }
+
+sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_t *col_ptr, const int32_t *row_idx,
+                             const float *val, const float *bias, void *hip_stream) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (nl < 1 || l0 < 0 || (int64_t)l0 + nl > net->L) return fail(SDNN_EINVAL, "layers [%d, %d) outside [0, %d)", l0, l0 + nl, net->L);
+  if (!col_ptr || !row_idx || !val || !bias) return fail(SDNN_EINVAL, "null array");
+  for (int32_t i = 0; i < nl; ++i)
+    if (net->layers[(size_t)l0 + i].ell) return fail(SDNN_ESTATE, "layer %d already loaded", l0 + i);
+  const int32_t N = net->N;
+  // ---- validate everything before touching the device
+  std::vector<int> K((size_t)nl);
+  for (int32_t i = 0; i < nl; ++i) {
+    const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+    if (i > 0 && cp[0] != col_ptr[(size_t)(i - 1) * (N + 1) + N])
+      return fail(SDNN_EINVAL, "layer %d does not start where layer %d ends", l0 + i, l0 + i - 1);
+    if (cp[0] < 0) return fail(SDNN_EINVAL, "negative column offset");
+    int kmax = 0;
+    for (int32_t j = 0; j < N; ++j) {
+      const int64_t a = cp[j], b = cp[j + 1];
+      if (b < a) return fail(SDNN_EINVAL, "layer %d column %d: decreasing offsets", l0 + i, j);
+      if (b - a > kMaxDegree) return fail(SDNN_EINVAL, "layer %d column %d: %lld sources exceed %d", l0 + i, j, (long long)(b - a), kMaxDegree);
+      for (int64_t e = a; e < b; ++e) {
+        const int32_t k = row_idx[e];
+        if (k < 0 || k >= N) return fail(SDNN_EINVAL, "layer %d column %d: source %d out of range", l0 + i, j, k);
+        if (e > a && k <= row_idx[e - 1]) return fail(SDNN_EINVAL, "layer %d column %d: sources not strictly ascending", l0 + i, j);
+        if (!std::isfinite(val[e])) return fail(SDNN_EINVAL, "layer %d column %d: non-finite weight", l0 + i, j);
+      }
+      kmax = std::max<int>(kmax, (int)(b - a));
+    }
+    for (int32_t j = 0; j < N; ++j)
+      if (!std::isfinite(bias[(size_t)i * N + j])) return fail(SDNN_EINVAL, "layer %d: non-finite bias", l0 + i);
+    K[(size_t)i] = std::max(kmax, 1);
+  }
+  // ---- pack: ELL [N][K] of (byte offset of source row in the tile, weight bits)
+  const int stride = (net->path == 0 ? net->B : kFmRows) * (int)sizeof(float);
+  size_t ell_words = 0;
+  for (int32_t i = 0; i < nl; ++i) ell_words += (size_t)N * K[(size_t)i];
+  const size_t ell_bytes = align_up(ell_words * sizeof(int2), 256);
+  const size_t bias_bytes = (size_t)nl * N * sizeof(float);
+  std::vector<int2> host_ell;
+  try {
+    host_ell.resize(ell_words);
+  } catch (...) {
+    return fail(SDNN_ENOMEM, "out of host memory packing %zu bytes", ell_words * sizeof(int2));
+  }
+  size_t off = 0;
+  for (int32_t i = 0; i < nl; ++i) {
+    const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+    const int Ki = K[(size_t)i];
+    for (int32_t j = 0; j < N; ++j) {
+      int2 *dst = host_ell.data() + off + (size_t)j * Ki;
+      int s = 0;
+      for (int64_t e = cp[j]; e < cp[j + 1]; ++e, ++s) {
+        int wbits;
+        std::memcpy(&wbits, &val[e], sizeof(int));
+        dst[s] = make_int2(row_idx[e] * stride, wbits);
+      }
+      for (; s < Ki; ++s) dst[s] = make_int2(0, 0);
+    }
+    off += (size_t)N * Ki;
+  }
+  // ---- device copy
+  if (net->device < 0) {
+    HIP_OR_POISON(net, hipGetDevice(&net->device));
+    HIP_OR_POISON(net, hipDeviceGetAttribute(&net->cus, hipDeviceAttributeMultiprocessorCount, net->device));
+  } else {
+    int dev = -1;
+    HIP_OR_POISON(net, hipGetDevice(&dev));
+    if (dev != net->device) return fail(SDNN_EINVAL, "current device %d differs from the handle's device %d", dev, net->device);
+  }
+  char *mem = nullptr;
+  hipError_t e = hipMalloc(reinterpret_cast<void **>(&mem), ell_bytes + bias_bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", ell_bytes + bias_bytes, hipGetErrorString(e));
+  }
+  net->allocations.push_back(mem);
+  hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  HIP_OR_POISON(net, hipMemcpyAsync(mem, host_ell.data(), ell_words * sizeof(int2), hipMemcpyHostToDevice, s));
+  HIP_OR_POISON(net, hipMemcpyAsync(mem + ell_bytes, bias, bias_bytes, hipMemcpyHostToDevice, s));
+  HIP_OR_POISON(net, hipStreamSynchronize(s));
+  off = 0;
+  for (int32_t i = 0; i < nl; ++i) {
+    LayerDev &ld = net->layers[(size_t)l0 + i];
+    ld.ell = reinterpret_cast<const int2 *>(mem) + off;
+    ld.bias = reinterpret_cast<const float *>(mem + ell_bytes) + (size_t)i * N;
+    ld.K = K[(size_t)i];
+    off += (size_t)N * ld.K;
+  }
+  net->n_loaded += nl;
+  g_err.clear();
+  return SDNN_OK;
+}
+
+size_t sdnn_workspace_bytes(const sdnn_net *net, int64_t n_rows) {
+  if (!net || n_rows < 0) return 0;
+  return layout_for(net, n_rows).total;
+}
+
+sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
+                       void *hip_stream) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (net->n_loaded != net->L) return fail(SDNN_ESTATE, "%d of %d layers loaded", net->n_loaded, net->L);
+  if (n_rows < 0 || n_rows > (int64_t)0x7fffffff) return fail(SDNN_EINVAL, "n_rows %lld out of range", (long long)n_rows);
+  if (n_rows > 0 && !y0) return fail(SDNN_EINVAL, "y0 is null");
+  if (!workspace) return fail(SDNN_EINVAL, "workspace is null");
+  if (reinterpret_cast<uintptr_t>(workspace) % 256) return fail(SDNN_EINVAL, "workspace is not 256-byte aligned");
+  if (n_rows > 0 && reinterpret_cast<uintptr_t>(y0) % 16 && net->N % 4 == 0)
+    return fail(SDNN_EINVAL, "y0 must be 16-byte aligned");
+  const WsLayout w = layout_for(net, n_rows);
+  if (workspace_bytes < w.total) return fail(SDNN_EINVAL, "workspace has %zu bytes, needs %zu", workspace_bytes, w.total);
+  int dev = -1;
+  HIP_OR_POISON(net, hipGetDevice(&dev));
+  if (dev != net->device) return fail(SDNN_EINVAL, "current device %d differs from the handle's device %d", dev, net->device);
+  if (net->events.empty()) {
+    net->events.resize(4);
+    for (auto &ev : net->events) HIP_OR_POISON(net, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 4 * sizeof(int32_t), hipHostMallocDefault));
+  }
+  char *ws = static_cast<char *>(workspace);
+  net->M = n_rows;
+  net->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  net->ws = ws;
+  net->ybuf[0] = reinterpret_cast<float *>(ws + w.ybuf[0]);
+  net->ybuf[1] = reinterpret_cast<float *>(ws + w.ybuf[1]);
+  net->fm = reinterpret_cast<float *>(ws + w.fm);
+  net->ids[0] = reinterpret_cast<int *>(ws + w.ids[0]);
+  net->ids[1] = reinterpret_cast<int *>(ws + w.ids[1]);
+  net->flags = reinterpret_cast<int *>(ws + w.flags);
+  net->rownz = reinterpret_cast<int *>(ws + w.rownz);
+  net->counts = reinterpret_cast<int *>(ws + w.counts);
+  net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
+  net->ran = false;
+
+  const int M = (int)n_rows;
+  hipStream_t s = net->stream;
+  hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
+                     net->ids[0], net->flags, net->rownz, net->counts, M, net->L);
+  HIP_OR_POISON(net, hipGetLastError());
+
+  const float *yin = y0;
+  int cur = 0;
+  int32_t l = 0;
+  // read-back ring: (event slot, layer boundary) of chunks not yet checked
+  int ring_slot[4], ring_bound[4], ring_n = 0, ring_head = 0, next_slot = 0;
+  bool all_dead = (M == 0);
+  for (; l < net->L && !all_dead; ++l) {
+    float *yout = net->ybuf[l & 1];
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l));
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->flags, net->ids[cur], net->ids[cur ^ 1],
+                       net->counts + l, net->counts + l + 1);
+    HIP_OR_POISON(net, hipGetLastError());
+    cur ^= 1;
+    yin = yout;
+    if ((l + 1) % kPollEvery == 0 && l + 1 < net->L) {
+      const int slot = next_slot;
+      next_slot = (next_slot + 1) % 4;
+      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + slot, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      HIP_OR_POISON(net, hipEventRecord(net->events[(size_t)slot], s));
+      ring_slot[(ring_head + ring_n) % 4] = slot;
+      ring_bound[(ring_head + ring_n) % 4] = l + 1;
+      ++ring_n;
+      while (ring_n > 2) {
+        const int sl = ring_slot[ring_head];
+        HIP_OR_POISON(net, hipEventSynchronize(net->events[(size_t)sl]));
+        ring_head = (ring_head + 1) % 4;
+        --ring_n;
+        if (net->pinned[sl] == 0) { all_dead = true; break; }
+      }
+    }
+  }
+  net->layers_run = l;
+  net->final_list = cur;
+  net->final_y = (l == net->L && net->L > 0) ? net->ybuf[(net->L - 1) & 1] : nullptr;
+  hipLaunchKernelGGL(k_final_ids, dim3(std::max(1, std::min(net->cus, (M + 255) / 256 + 1))), dim3(256), 0, s,
+                     net->ids[cur], net->counts + l, net->final_ids);
+  HIP_OR_POISON(net, hipGetLastError());
+  net->ran = true;
+  net->pending_times = net->profiling;
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_categories(sdnn_net *net, int64_t *ids, int64_t capacity, int64_t *count) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (!net->ran) return fail(SDNN_ESTATE, "no inference has run");
+  if (!count) return fail(SDNN_EINVAL, "count is null");
+  HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
+  if (net->pending_times) {
+    for (int32_t l = 0; l < net->layers_run; ++l) {
+      float ms = 0.0f;
+      HIP_OR_POISON(net, hipEventElapsedTime(&ms, net->prof_start[(size_t)l], net->prof_end[(size_t)l]));
+      net->prof_ms[(size_t)l] += ms;
+      net->prof_runs[(size_t)l] += 1;
+    }
+    net->pending_times = false;
+  }
+  int32_t c = 0;
+  HIP_OR_POISON(net, hipMemcpy(&c, net->counts + net->layers_run, sizeof(int32_t), hipMemcpyDeviceToHost));
+  *count = c;
+  if (!ids || capacity < c) return fail(SDNN_ERANGE, "need capacity %d", c);
+  if (c > 0) HIP_OR_POISON(net, hipMemcpy(ids, net->final_ids, (size_t)c * sizeof(long long), hipMemcpyDeviceToHost));
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_live_counts(sdnn_net *net, int64_t *counts) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (!net->ran) return fail(SDNN_ESTATE, "no inference has run");
+  if (!counts) return fail(SDNN_EINVAL, "counts is null");
+  HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
+  std::vector<int32_t> c((size_t)net->L + 1);
+  HIP_OR_POISON(net, hipMemcpy(c.data(), net->counts, c.size() * sizeof(int32_t), hipMemcpyDeviceToHost));
+  std::vector<int32_t> nz((size_t)std::max<int64_t>(net->M, 1));
+  if (net->M > 0) HIP_OR_POISON(net, hipMemcpy(nz.data(), net->rownz, (size_t)net->M * sizeof(int32_t), hipMemcpyDeviceToHost));
+  int64_t r0 = 0;
+  for (int64_t i = 0; i < net->M; ++i) r0 += nz[(size_t)i] != 0;
+  counts[0] = r0;
+  for (int32_t l = 1; l <= net->L; ++l) counts[l] = c[(size_t)l];
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float *out_host) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (!net->ran) return fail(SDNN_ESTATE, "no inference has run");
+  if (n < 0 || (n > 0 && (!ids || !out_host))) return fail(SDNN_EINVAL, "bad arguments");
+  for (int64_t q = 0; q < n; ++q)
+    if (ids[q] < 0 || ids[q] >= net->M) return fail(SDNN_EINVAL, "row id %lld out of range", (long long)ids[q]);
+  HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
+  int32_t c = 0;
+  HIP_OR_POISON(net, hipMemcpy(&c, net->counts + net->layers_run, sizeof(int32_t), hipMemcpyDeviceToHost));
+  std::vector<long long> live((size_t)std::max(c, 1));
+  if (c > 0) HIP_OR_POISON(net, hipMemcpy(live.data(), net->final_ids, (size_t)c * sizeof(long long), hipMemcpyDeviceToHost));
+  const size_t rowb = (size_t)net->N * sizeof(float);
+  for (int64_t q = 0; q < n; ++q) {
+    float *dst = out_host + (size_t)q * net->N;
+    const bool is_live = c > 0 && net->final_y && std::binary_search(live.begin(), live.begin() + c, (long long)ids[q]);
+    if (is_live) HIP_OR_POISON(net, hipMemcpy(dst, net->final_y + (size_t)ids[q] * net->N, rowb, hipMemcpyDeviceToHost));
+    else std::memset(dst, 0, rowb);
+  }
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  net->pending_times = false;
+  if (!enable) {
+    net->profiling = false;
+    g_err.clear();
+    return SDNN_OK;
+  }
+  if (net->prof_start.empty()) {
+    net->prof_start.resize((size_t)net->L);
+    net->prof_end.resize((size_t)net->L);
+    for (int32_t l = 0; l < net->L; ++l) {
+      HIP_OR_POISON(net, hipEventCreate(&net->prof_start[(size_t)l]));
+      HIP_OR_POISON(net, hipEventCreate(&net->prof_end[(size_t)l]));
+    }
+  }
+  net->prof_ms.assign((size_t)net->L, 0.0);
+  net->prof_runs.assign((size_t)net->L, 0);
+  net->profiling = true;
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_layer_times(sdnn_net *net, double *ms, int64_t *runs) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (!ms || !runs) return fail(SDNN_EINVAL, "null array");
+  for (int32_t l = 0; l < net->L; ++l) {
+    ms[l] = net->prof_ms.empty() ? 0.0 : net->prof_ms[(size_t)l];
+    runs[l] = net->prof_runs.empty() ? 0 : net->prof_runs[(size_t)l];
+  }
+  g_err.clear();
+  return SDNN_OK;
+}
+
+void sdnn_destroy(sdnn_net *net) {
+  if (!net) return;
+  for (auto &ev : net->prof_start) (void)hipEventDestroy(ev);
+  for (auto &ev : net->prof_end) (void)hipEventDestroy(ev);
+  for (void *p : net->allocations) (void)hipFree(p);
+  for (auto &ev : net->events) (void)hipEventDestroy(ev);
+  if (net->pinned) (void)hipHostFree(net->pinned);
+  delete net;
+}
+
+}  // extern "C"

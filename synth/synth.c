@@ -24,7 +24,7 @@
  * set is not available, so three synthetic kinds stand in:
  *   kind 0 "strokes": per image a target density d = clip(mean + sd * g, 0.05, 0.40), g an
  *            Irwin-Hall(12) - 6 approximately-normal draw; polyline pen strokes (2-5 segments,
- *            lengths U(0.15R, 0.45R), heading turns U(-60, 60) degrees, disc brush radius
+ *            lengths U(0.15R, 0.45R), heading turns U(-60, 60) degrees, round pen of radius
  *            max(1, round(R * U(0.03, 0.06)))) or, with probability 0.2, a filled rotated ellipse
  *            (semi-axes U(0.05R, 0.15R)), stamped until at least d*R*R pixels are set.
  *   kind 1 "bernoulli": every pixel independently 1 with probability p.
@@ -219,14 +219,24 @@ static double dcos(double x) { return dsin(x + PI / 2); }
 
 static inline int64_t iround(double v) { return (int64_t)(v < 0 ? v - 0.5 : v + 0.5); }
 
-static int64_t stamp_disc(float *img, int32_t R, double cx, double cy, int32_t rad) {
+/* Set every pixel whose center lies within rad of the segment (x0,y0)-(x1,y1): a pen stroke of
+   radius rad (the union of discs centered on the segment). Returns the number of new ones. */
+static int64_t stamp_capsule(float *img, int32_t R, double x0, double y0, double x1, double y1, int32_t rad) {
   int64_t added = 0;
-  int64_t x0 = iround(cx), y0 = iround(cy);
-  for (int64_t dy = -rad; dy <= rad; ++dy)
-    for (int64_t dx = -rad; dx <= rad; ++dx) {
-      if (dx * dx + dy * dy > (int64_t)rad * rad) continue;
-      int64_t x = x0 + dx, y = y0 + dy;
-      if (x < 0 || y < 0 || x >= R || y >= R) continue;
+  const double dx = x1 - x0, dy = y1 - y0, len2 = dx * dx + dy * dy, r2 = (double)rad * rad;
+  int64_t xa = (int64_t)(x0 < x1 ? x0 : x1) - rad - 1, xb = (int64_t)(x0 > x1 ? x0 : x1) + rad + 1;
+  int64_t ya = (int64_t)(y0 < y1 ? y0 : y1) - rad - 1, yb = (int64_t)(y0 > y1 ? y0 : y1) + rad + 1;
+  if (xa < 0) xa = 0;
+  if (ya < 0) ya = 0;
+  if (xb > R - 1) xb = R - 1;
+  if (yb > R - 1) yb = R - 1;
+  for (int64_t y = ya; y <= yb; ++y)
+    for (int64_t x = xa; x <= xb; ++x) {
+      double t = len2 > 0 ? ((x - x0) * dx + (y - y0) * dy) / len2 : 0.0;
+      if (t < 0) t = 0;
+      if (t > 1) t = 1;
+      const double ex = x - (x0 + t * dx), ey = y - (y0 + t * dy);
+      if (ex * ex + ey * ey > r2) continue;
       float *p = img + y * R + x;
       if (*p == 0.0f) { *p = 1.0f; ++added; }
     }
@@ -267,11 +277,7 @@ static void image_strokes(uint64_t key, int32_t R, double mean, double sd, float
       for (int sgm = 0; sgm < nseg; ++sgm) {
         double len = R * (0.15 + 0.30 * unit(key, &ctr));
         double dx = dcos(h), dy = dsin(h);
-        int64_t steps = (int64_t)(len * 2) + 1;
-        for (int64_t t = 0; t <= steps; ++t) {
-          double f = (double)t / (double)steps * len;
-          ones += stamp_disc(img, R, x + f * dx, y + f * dy, rad);
-        }
+        ones += stamp_capsule(img, R, x, y, x + len * dx, y + len * dy, rad);
         x += len * dx; y += len * dy;
         if (x < 0) x = 0;
         if (y < 0) y = 0;

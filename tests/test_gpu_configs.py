@@ -1,0 +1,61 @@
+"""GPU parity at the full sizes of the five workloads (Table 1 widths and biases, Table 2 depths,
+60,000 inputs as in Sec. IV; 2,000 for the small case), in the launch configuration the benchmark
+times. The two smaller widths are checked against the oracle on every row; the two largest on a
+seeded sample of rows the oracle recomputes on its own (rows are independent, Sec. V), plus the
+invariants that hold for every row."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import GpuRun, assert_parity, log
+
+pytestmark = pytest.mark.gpu
+
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def gpu_config_run(cfg):
+    log(f"{cfg.name}: generating inputs")
+    y0 = synth.config_inputs(cfg)
+    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax)
+    log(f"{cfg.name}: loading {cfg.n_layers} layers")
+    gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
+    log(f"{cfg.name}: running the GPU")
+    cats = gpu.run(y0)
+    log(f"{cfg.name}: {cats.size} categories; live counts {gpu.net.live_counts()[:8].tolist()}")
+    return y0, gpu, cats
+
+
+@pytest.mark.parametrize("ci", [0, 1, 2])
+def test_full_config_every_row(ci):
+    cfg = synth.CONFIGS[ci]
+    y0, gpu, cats = gpu_config_run(cfg)
+    log(f"{cfg.name}: oracle on all {cfg.n_rows} rows")
+    o = oracle.run_config_layers(y0, cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
+                                 cfg.ymax, threads=THREADS)
+    assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("ci", [3, 4])
+def test_full_config_sampled_rows(ci):
+    cfg = synth.CONFIGS[ci]
+    y0, gpu, cats = gpu_config_run(cfg)
+    counts = gpu.net.live_counts()
+    assert (np.diff(counts) <= 0).all() and counts[0] == int((y0 != 0).any(axis=1).sum())
+    assert cats.size == counts[-1]
+    rng = np.random.default_rng(ci)
+    sample = np.sort(rng.choice(cfg.n_rows, size=1500, replace=False))
+    log(f"{cfg.name}: oracle on {sample.size} sampled rows")
+    o = oracle.run_config_layers(y0[sample], cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
+                                 cfg.ymax, threads=THREADS)
+    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
+    oc = o.live_counts()
+    # every sampled row's survival layer agrees: counts over the sample can be recomputed from the
+    # oracle alone, and must not exceed the GPU's counts over all rows
+    assert (oracle.padded_live_counts(o, cfg.n_layers) <= counts).all()
+    if o.categories().size:
+        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
+    log(f"{cfg.name}: sample live counts {oc[:6].tolist()}")

@@ -1,0 +1,126 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle on the same seeded inputs.
+
+Bar: categories and per-layer live counts bit-exact; surviving final activations within 1e-5
+relative (fp32), and in fact bit-identical because both sides sum in the same canonical order."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from tests.gpu_util import GpuRun, assert_parity, log
+
+pytestmark = pytest.mark.gpu
+
+
+def random_layers(rng, n, nl, max_deg, signed=True):
+    layers = []
+    for _ in range(nl):
+        deg = rng.integers(0, max_deg + 1, size=n)
+        cp, ri, v = synth.random_csc(rng, n, deg, -1.0 if signed else 0.0, 1.0)
+        v = (v * rng.choice([0.25, 1.0, 3.0])).astype(np.float32)
+        b = rng.uniform(-0.6, 0.4, size=n).astype(np.float32)
+        layers.append((cp, ri, v, b))
+    return layers
+
+
+def run_both(n, layers, y0, ymax=32.0):
+    gpu = GpuRun(n, len(layers), ymax)
+    for l, (cp, ri, v, b) in enumerate(layers):
+        gpu.load(l, cp, ri, v, b)
+    cats = gpu.run(y0)
+    o = oracle.run(y0, layers, ymax, threads=4)
+    return gpu, o, cats
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_tiny_random_networks(seed):
+    """Random widths (including widths that are not multiples of 4), ragged row counts, random column
+    degrees up to the width, signed weights, biases of both signs and several YMAX values."""
+    rng = np.random.default_rng(seed)
+    n = int(rng.choice([1, 2, 3, 5, 8, 13, 31, 32, 33, 64, 100, 257]))
+    m = int(rng.integers(1, 80))
+    nl = int(rng.integers(1, 7))
+    ymax = float(rng.choice([1.5, 4.0, 32.0]))
+    layers = random_layers(rng, n, nl, max_deg=min(n, 40))
+    y0 = (rng.random((m, n)) < rng.uniform(0.2, 0.9)).astype(np.float32) * rng.uniform(0, 2, (m, n)).astype(np.float32)
+    if seed % 4 == 0:
+        y0[rng.random(m) < 0.3] = 0  # all-zero input rows
+    if seed % 5 == 0:
+        y0 -= np.float32(0.5) * (rng.random((m, n)) < 0.1)  # negative inputs
+    log(f"tiny seed={seed} n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0, ymax)
+    assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("n", [1024, 2048, 4096, 16384, 65536])
+def test_config_networks_mixed_inputs(n):
+    """The configs' permutation-union networks (32 weights of 1/16 per column) with inputs whose
+    densities straddle the survival threshold, so categories are neither empty nor full; covers both
+    kernel paths and the tile sizes of every width."""
+    bias = {1024: -0.30, 2048: -0.30, 4096: -0.35, 16384: -0.40, 65536: -0.45}[n]
+    side = int(round(n ** 0.5)) if int(round(n ** 0.5)) ** 2 == n else None
+    m = {1024: 300, 2048: 200, 4096: 150, 16384: 70, 65536: 40}[n]
+    nl = {1024: 24, 2048: 16, 4096: 16, 16384: 8, 65536: 6}[n]
+    if side:
+        y0 = synth.inputs(20 + n % 7, side, 0, m, "mixed", 0.2, 0.7)
+    else:
+        y0 = (np.random.default_rng(4).random((m, n)) < np.random.default_rng(5).uniform(0.2, 0.7, (m, 1))).astype(np.float32)
+    cp, ri, v = synth.layers_csc(9, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    log(f"config-net n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert 0 < cats.size < m
+    assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("bias", [-0.30, -0.45])
+def test_closed_form_and_tie_rows(bias):
+    """All-ones rows follow y_{l+1} = min(32, 2 y_l + b) to exactly 32; constant rows c = -b/2 sit on
+    the survival threshold, where only the ascending-order fp32 sum decides the outcome."""
+    n, nl = 1024, 10
+    c = np.float32(-np.float32(bias)) / np.float32(2.0)
+    y0 = np.stack([np.ones(n, np.float32), np.full(n, c, np.float32), np.zeros(n, np.float32)])
+    cp, ri, v = synth.layers_csc(1, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    gpu, o, cats = run_both(n, layers, y0)
+    assert_parity(gpu, o, cats)
+    assert 0 in cats
+    np.testing.assert_array_equal(gpu.net.final_rows([0]), np.full((1, n), 32.0, np.float32))
+
+
+def test_edge_cases():
+    """Empty batch, one row, one neuron, empty columns, a single layer, values clamped at YMAX."""
+    rng = np.random.default_rng(11)
+    # empty batch
+    cp, ri, v = synth.layers_csc(1, 0, 2, 1024)
+    layers = [(cp[l], ri, v, np.full(1024, -0.3, np.float32)) for l in range(2)]
+    gpu, o, cats = run_both(1024, layers, np.zeros((0, 1024), np.float32))
+    assert cats.size == 0 and list(gpu.net.live_counts()) == [0, 0, 0]
+    # one neuron, self loop, clamp
+    lay = [(np.array([0, 1], np.int64), np.array([0], np.int32), np.array([3.0], np.float32), np.array([0.5], np.float32))] * 3
+    gpu, o, cats = run_both(1, lay, np.array([[1.0], [0.0], [2.0]], np.float32), ymax=10.0)
+    assert_parity(gpu, o, cats)
+    np.testing.assert_array_equal(gpu.net.final_rows([0, 1, 2])[:, 0], [10.0, 0.0, 10.0])
+    # empty columns everywhere but one
+    n = 40
+    cp = np.zeros(n + 1, np.int64); cp[8:] = 3
+    lay = [(cp, np.array([1, 5, 9], np.int32), np.array([1, 1, 1], np.float32), np.zeros(n, np.float32))]
+    y0 = rng.random((37, n)).astype(np.float32)
+    gpu, o, cats = run_both(n, lay, y0)
+    assert_parity(gpu, o, cats)
+
+
+def test_rerun_is_deterministic_and_batches_independent():
+    """Two runs give identical results; a run on a prefix of the rows gives that prefix's results."""
+    n, nl, m = 4096, 12, 130
+    y0 = synth.inputs(31, 64, 0, m, "mixed", 0.3, 0.6)
+    cp, ri, v = synth.layers_csc(2, 0, nl, n)
+    gpu = GpuRun(n, nl)
+    gpu.load(0, cp, ri, v, np.full((nl, n), -0.35, np.float32))
+    a = gpu.run(y0)
+    ra = gpu.net.final_rows(a)
+    b = gpu.run(y0)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(ra, gpu.net.final_rows(b))
+    p = gpu.run(y0[:61])
+    np.testing.assert_array_equal(p, a[a < 61])
