@@ -1,0 +1,215 @@
+#!/usr/bin/env python3
+"""Benchmark: Sparse DNN Challenge inference (Kepner et al., 2019) on one MI355X.
+
+A step is the challenge's timed region (Sec. V): evaluate every layer for all input rows and identify
+the categories -- one sdnn_infer + sdnn_categories through the C ABI, with the inputs and weights
+already resident in HBM. The metric is the paper's rate (Sec. V, Sec. VI-B):
+(# inputs) x (# connections) / time, in inputs*edges/s.
+
+Workloads are the seeded synthetic stand-ins for the paper's networks and MNIST-derived inputs
+(synth.CONFIGS; Table 1 widths and biases, Table 2 depths). The default is the 65536-neuron,
+1920-layer network on 60,000 inputs.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+
+
+def log(msg: str) -> None:
+    print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_layer_bytes(n: int, nnz: int, r_in: int, r_out: int) -> int:
+    """Bytes one layer must move with dense fp32 live rows: read the live input rows, write the rows
+    that stay live, read the weights (index + value) and the bias once."""
+    if r_in == 0:
+        return 0
+    return 4 * n * (r_in + r_out) + 8 * nnz + 4 * n
+
+
+def cpu_baseline(cfg, target_s: float, threads: int) -> dict:
+    """The oracle as it is, on a bounded sample of the same workload (first rows of the input set),
+    timing only its layer evaluations (weight generation is loading, untimed as on the GPU side)."""
+    import oracle
+    import synth
+
+    def run(rows: int) -> float:
+        y0 = synth.config_inputs(cfg, 0, rows)
+        o = oracle.Oracle(y0, cfg.ymax)
+        bias = np.full(cfg.n_neurons, cfg.bias, np.float32)
+        spent, l, chunk = 0.0, 0, 8
+        while l < cfg.n_layers and o.live > 0:
+            nl = min(chunk, cfg.n_layers - l)
+            cp, ri, v = synth.layers_csc(cfg.net_id, l, nl, cfg.n_neurons, cfg.k, cfg.weight)
+            for i in range(nl):
+                t0 = time.perf_counter()
+                o.layer(cp[i], ri, v, bias, threads)
+                spent += time.perf_counter() - t0
+                if o.live == 0:
+                    break
+            l += nl
+        cats = o.categories().size
+        o.close()
+        log(f"cpu baseline: {rows} rows in {spent:.2f} s ({cats} categories)")
+        return spent
+
+    rows = min(cfg.n_rows, 64)
+    t = run(rows)
+    while t < target_s / 3 and rows < cfg.n_rows:
+        rows = int(min(cfg.n_rows, max(rows * 2, rows * target_s / max(t, 1e-3))))
+        t = run(rows)
+    rate = rows * cfg.total_nnz / t
+    return {"value": rate, "unit": "inputs*edges/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {rows} of {cfg.n_rows} input rows of {cfg.name}, all {cfg.n_layers} layers "
+                      f"(rows stop when dead, as on the GPU); {t:.2f} s of oracle layer evaluation on "
+                      f"{threads} host threads"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4, help="index into synth.CONFIGS (0-4)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline time")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true", help="skip the per-layer events (no roofline)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build measures the single-GPU share of the "
+              "data-parallel path (inputs split across GPUs, weights replicated); use --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+
+    import synth
+    from paper_1909_05631_amd import sdnn
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 2
+    torch.cuda.set_device(0)
+    cfg = synth.CONFIGS[args.config]
+    n, L, m = cfg.n_neurons, cfg.n_layers, cfg.n_rows
+    stream = torch.cuda.current_stream()
+
+    # ---------------- untimed: load the network and inputs into HBM (Sec. V, load steps)
+    t0 = time.time()
+    y0 = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    chunk = max(1, (1 << 28) // (4 * n))
+    for r0 in range(0, m, chunk):
+        nr = min(chunk, m - r0)
+        y0[r0:r0 + nr].copy_(torch.from_numpy(synth.config_inputs(cfg, r0, nr)))
+    density = float(y0.mean().item())
+    log(f"{cfg.name}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
+    t0 = time.time()
+    net = sdnn.Net(n, L, cfg.ymax)
+    lchunk = max(1, min(64, (1 << 27) // (n * cfg.k)))
+    for l0 in range(0, L, lchunk):
+        nl = min(lchunk, L - l0)
+        cp, ri, v = synth.layers_csc(cfg.net_id, l0, nl, n, cfg.k, cfg.weight)
+        net.load_layers(l0, cp, ri, v, np.full((nl, n), cfg.bias, np.float32))
+        if (l0 // lchunk) % 8 == 0:
+            log(f"loaded layers {l0 + nl}/{L}")
+    log(f"network loaded ({L} layers, {cfg.total_nnz} connections) in {time.time() - t0:.1f} s; "
+        f"kernel path {net.kernel_path}")
+    nb = net.workspace_bytes(m)
+    ws = torch.empty(nb, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+
+    def step():
+        net.infer(y0, m, ws, nb, stream)
+        return net.categories()
+
+    for i in range(args.warmup):
+        cats = step()
+        log(f"warmup {i}: {cats.size} categories")
+    if not args.no_profile:
+        net.set_profiling(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for _ in range(args.steps):
+        cats = step()
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    t_step = t_total / max(args.steps, 1)
+    counts = net.live_counts()
+    log(f"timed {args.steps} steps: {t_step * 1e3:.3f} ms/step; categories {cats.size}; "
+        f"live counts {counts[:8].tolist()}")
+
+    edges = m * cfg.total_nnz
+    value = edges / t_step
+    nnz = cfg.nnz_per_layer
+    live_edges = int(sum(int(counts[l]) * nnz for l in range(L)))
+
+    roofline = None
+    if not args.no_profile:
+        ms, runs = net.layer_times()
+        tot_bytes = sum(algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1])) * int(runs[l])
+                        for l in range(L))
+        tot_ms = float(ms.sum())
+        launches = int(runs.sum())
+        achieved = tot_bytes / (tot_ms * 1e-3) / 1e9 if tot_ms > 0 else 0.0
+        nz = [l for l in range(L) if runs[l] > 0]
+        per = ms / np.maximum(runs, 1)
+        head = ", ".join(f"{l}:{per[l] * 1e3:.1f}us(R={int(counts[l])})" for l in nz[:6])
+        tail = [l for l in nz if int(counts[l]) < 64]
+        tail_avg = float(np.mean(per[tail]) * 1e3) if tail else 0.0
+        log(f"layer kernel times: {head}; {len(tail)} layers with <64 live rows average {tail_avg:.1f}us")
+        kname = f"k_layer_lds<{32 if n <= 1024 else 16 if n <= 2048 else 8}>" if net.kernel_path == 0 \
+            else "k_to_fm+k_layer_gfm"
+        roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None, "kernel": kname,
+                    "launches": launches, "avg_launch_ms": round(tot_ms / max(launches, 1), 5),
+                    "algorithmic_bytes_per_launch": int(tot_bytes / max(launches, 1))}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        threads = max(1, min(16, os.cpu_count() or 1))
+        cpu = cpu_baseline(cfg, args.cpu_seconds, threads)
+
+    out = {
+        "metric": "inference edges/sec (Ninputs*sum nnz(W)/t) + % HBM roofline, 1 MI355X",
+        "value": value,
+        "unit": "inputs*edges/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": t_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n_neurons": n, "n_layers": L, "n_rows": m, "bias": cfg.bias,
+                   "ymax": cfg.ymax, "connections": cfg.total_nnz, "input_density": round(density, 4),
+                   "parallelism": "none (1 GPU)"},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "live_edges_per_s": live_edges / t_step,
+        "categories": int(cats.size),
+        "live_counts_head": [int(c) for c in counts[:8]],
+    }
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -28,12 +28,15 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "sdnn.h"
@@ -57,10 +60,27 @@ constexpr int kMaxLayers = 1000000;
 constexpr int kMaxDegree = 4096;
 constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
 constexpr int kFmRows = 32;                // rows per global feature-major tile
-constexpr int kGfmOutputs = 64;            // outputs per work item of k_layer_gfm
+constexpr int kGfmOutputs = 32;            // outputs per work item of k_layer_gfm
 constexpr int kPollEvery = 4;              // layers between live-count read-backs
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Run f(i) for i in [0, n) on up to 16 host threads (used for host-side validation and packing).
+template <class F>
+void parallel_for(int32_t n, F f) {
+  const int32_t nt = std::max<int32_t>(1, std::min<int32_t>({n, 16, (int32_t)std::max(1u, std::thread::hardware_concurrency())}));
+  if (nt == 1) {
+    for (int32_t i = 0; i < n; ++i) f(i);
+    return;
+  }
+  std::atomic<int32_t> next{0};
+  std::vector<std::thread> th;
+  for (int32_t t = 0; t < nt; ++t)
+    th.emplace_back([&]() {
+      for (int32_t i = next++; i < n; i = next++) f(i);
+    });
+  for (auto &x : th) x.join();
+}
 
 // ------------------------------------------------------------------------------------------------
 // Device code
@@ -76,45 +96,82 @@ __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
 }
 
-__global__ void k_init(int *__restrict__ ids, int *__restrict__ flags, int *__restrict__ rownz,
+__global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, int *__restrict__ rownz,
                        int *__restrict__ counts, int M, int L) {
   const int st = gridDim.x * blockDim.x;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
-    flags[i] = 0;
+    masks[i] = 0u;
     rownz[i] = 0;
   }
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i <= L; i += st) counts[i] = (i == 0) ? M : 0;
 }
 
-// Stable compaction: ids_out = [ids_in[p] for p < R if flags[p]], count_out = its length.
-// Flags are reset to 0 for the next layer. One workgroup of 1024 threads.
-__global__ __launch_bounds__(1024) void k_compact(int *__restrict__ flags, const int *__restrict__ ids_in,
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int wave_inclusive_sum(int v, int lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int u = __shfl_up(v, d, 64);
+    if (lane >= d) v += u;
+  }
+  return v;
+}
+
+// Stable compaction over per-tile liveness masks: bit b of masks[t] says that list position
+// t*B + b is live. ids_out = the live ids in list order, count_out = their number. The masks are
+// cleared for the next layer. One workgroup of 1024 threads; tiles are taken 4096 at a time: an
+// exclusive scan of their popcounts gives each tile's output offset, then every position is placed.
+constexpr int kCompactTiles = 4096;
+__global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, int B, const int *__restrict__ ids_in,
                                                   int *__restrict__ ids_out, const int *__restrict__ count_in,
                                                   int *__restrict__ count_out) {
+  __shared__ int toff[kCompactTiles];
+  __shared__ unsigned tmask[kCompactTiles];
   __shared__ int wsum[16];
   const int R = *count_in;
+  const int ntiles = (R + B - 1) / B;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int base = 0;
-  for (int c0 = 0; c0 < R; c0 += 1024) {
-    const int i = c0 + tid;
-    int f = 0;
-    if (i < R) {
-      f = flags[i];
-      flags[i] = 0;
+  for (int c0 = 0; c0 < ntiles; c0 += kCompactTiles) {
+    unsigned m[4];
+    int local = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int t = c0 + tid * 4 + q;
+      m[q] = 0u;
+      if (t < ntiles) {
+        m[q] = masks[t];
+        masks[t] = 0u;
+      }
+      local += __popc(m[q]);
     }
-    const unsigned long long m = __ballot(f != 0);
-    const int below = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) wsum[wave] = __popcll(m);
+    const int incl = wave_inclusive_sum(local, lane);
+    if (lane == 63) wsum[wave] = incl;
     __syncthreads();
     int off = 0, total = 0;
 #pragma unroll
     for (int w = 0; w < 16; ++w) {
-      const int s = wsum[w];
-      off += (w < wave) ? s : 0;
-      total += s;
+      const int x = wsum[w];
+      off += (w < wave) ? x : 0;
+      total += x;
     }
-    if (f) ids_out[base + off + below] = ids_in[i];
+    int excl = base + off + incl - local;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      toff[tid * 4 + q] = excl;
+      tmask[tid * 4 + q] = m[q];
+      excl += __popc(m[q]);
+    }
+    __syncthreads();
+    const int p_end = min(R, (c0 + kCompactTiles) * B);
+    for (int p = c0 * B + tid; p < p_end; p += 1024) {
+      const int tl = p / B - c0, b = p % B;
+      const unsigned mk = tmask[tl];
+      if ((mk >> b) & 1u) {
+        const unsigned below = b == 0 ? 0u : (mk & (0xffffffffu >> (32 - b)));
+        ids_out[toff[tl] + __popc(below)] = ids_in[p];
+      }
+    }
     base += total;
     __syncthreads();
   }
@@ -126,53 +183,72 @@ __global__ void k_final_ids(const int *__restrict__ ids, const int *__restrict__
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < R; i += gridDim.x * blockDim.x) out[i] = ids[i];
 }
 
-// One layer with the activation tile staged in LDS. B rows per tile (a multiple of 4); blockDim 1024.
-template <int B>
+// Split a tile's outputs into chunks so that small live counts still spread over the whole grid:
+// with many tiles every work item is a whole tile; with few, each tile's outputs are divided.
+struct Chunking {
+  int nchunks, rounds_per_chunk;
+};
+__device__ __forceinline__ Chunking chunking(int ntiles, int rounds) {
+  int nchunks = ntiles > 0 ? (int)gridDim.x / ntiles : 1;
+  nchunks = max(1, min(nchunks, rounds));
+  const int rpc = (rounds + nchunks - 1) / nchunks;
+  return {(rounds + rpc - 1) / rpc, rpc};
+}
+
+// One layer with the activation tile staged in LDS. B rows per tile (4 <= B <= 32, a multiple of 4);
+// blockDim 1024. KC is the compile-time ELL width (0: use the runtime K).
+template <int B, int KC>
 __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                     const int2 *__restrict__ ell, int K,
                                                     const float *__restrict__ bias, float ymax,
                                                     const int *__restrict__ ids, const int *__restrict__ count,
-                                                    int *__restrict__ flags, int *__restrict__ rownz) {
+                                                    unsigned *__restrict__ masks, int *__restrict__ rownz) {
   extern __shared__ float4 smem[];
-  char *tile = reinterpret_cast<char *>(smem);
+  const char *tile = reinterpret_cast<const char *>(smem);
   float *tilef = reinterpret_cast<float *>(smem);
   __shared__ int rowlive[B];
   __shared__ int rowany[B];
-  constexpr int LPO = B / 4;    // lanes per output
+  constexpr int LPO = B / 4;    // lanes per output, 4 rows each
   constexpr int OPW = 64 / LPO; // outputs per wave instruction
   const int R = *count;
   const int ntiles = (R + B - 1) / B;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int quad = lane % LPO, jl = lane / LPO;
+  const int per_round = nw * OPW;
+  const int rounds = (N + per_round - 1) / per_round;
+  const Chunking ch = chunking(ntiles, rounds);
+  const int items = ntiles * ch.nchunks;
   if (tid < B) {
     rowlive[tid] = 0;
     rowany[tid] = 0;
   }
-  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  for (int w = blockIdx.x; w < items; w += gridDim.x) {
+    const int t = w / ch.nchunks, c = w % ch.nchunks;
     const int p0 = t * B;
     const int nvalid = min(B, R - p0);
+    const bool count_nz = rownz != nullptr && c == 0;
     // ---- stage rows ids[p0 .. p0+nvalid) as tile[k][b]; missing rows are zero
     if ((N & 3) == 0) {
       const int NQ = N >> 2;
-      const int items = NQ * (B / 4);
-      for (int it = tid; it < items; it += blockDim.x) {
+      const int nitems = NQ * (B / 4);
+      for (int it = tid; it < nitems; it += blockDim.x) {
         const int bq = it % (B / 4), q = it / (B / 4);
         float4 v[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const int b = bq * 4 + c;
-          v[c] = (b < nvalid) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p0 + b] * N)[q]
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int c4 = 0; c4 < 4; ++c4) {
+          const int b = bq * 4 + c4;
+          v[c4] = (b < nvalid) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p0 + b] * N)[q]
+                               : make_float4(0.f, 0.f, 0.f, 0.f);
         }
         float4 *dst = reinterpret_cast<float4 *>(tilef + (size_t)(4 * q) * B + bq * 4);
         dst[0] = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
         dst[B / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
         dst[2 * (B / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
         dst[3 * (B / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
-        if (rownz) {
+        if (count_nz) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c)
-            if (any_nonzero(v[c])) rowany[bq * 4 + c] = 1;
+          for (int c4 = 0; c4 < 4; ++c4)
+            if (any_nonzero(v[c4])) rowany[bq * 4 + c4] = 1;
         }
       }
     } else {
@@ -180,51 +256,90 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
         const int b = it % B, k = it / B;
         const float v = (b < nvalid) ? yin[(size_t)ids[p0 + b] * N + k] : 0.0f;
         tilef[(size_t)k * B + b] = v;
-        if (rownz && v != 0.0f) rowany[b] = 1;
+        if (count_nz && v != 0.0f) rowany[b] = 1;
       }
     }
     __syncthreads();
     // ---- compute: lane (quad, jl) owns rows 4*quad..4*quad+3 of output j
     int row[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int b = quad * 4 + c;
-      row[c] = (b < nvalid) ? ids[p0 + b] : -1;
+    for (int c4 = 0; c4 < 4; ++c4) {
+      const int b = quad * 4 + c4;
+      row[c4] = (b < nvalid) ? ids[p0 + b] : -1;
     }
+    const int qoff = quad * 16;
     int live_mask = 0;
-    for (int j0 = wave * OPW; j0 < N; j0 += nw * OPW) {
-      const int j = j0 + jl;
-      if (j < N) {
-        const int2 *e = ell + (size_t)j * K;
-        float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
-        for (int s = 0; s < K; ++s) {
-          const int2 p = e[s];
-          const float4 v = *reinterpret_cast<const float4 *>(tile + p.x + quad * 16);
-          const float w = __int_as_float(p.y);
-          a0 = fmaf(v.x, w, a0);
-          a1 = fmaf(v.y, w, a1);
-          a2 = fmaf(v.z, w, a2);
-          a3 = fmaf(v.w, w, a3);
-        }
-        const float bj = bias[j];
-        const float y[4] = {activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
-                            activate(a3, bj, ymax)};
+    const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
+    for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
+      const int j = r * per_round + wave * OPW + jl;
+      if (j >= N) continue;
+      float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      if constexpr (KC > 0) {
+        // groups of 8 terms: the next group's ELL entries load while this group's LDS reads and
+        // fma chain run; terms stay in ascending source order
+        static_assert(KC % 8 == 0, "KC must be a multiple of 8");
+        const int4 *e4 = reinterpret_cast<const int4 *>(ell + (size_t)j * KC);
+        int4 cur[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          if (row[c] >= 0) {
-            yout[(size_t)row[c] * N + j] = y[c];
-            if (y[c] > 0.0f) live_mask |= 1 << c;
+        for (int q = 0; q < 4; ++q) cur[q] = e4[q];
+#pragma unroll 1
+        for (int g = 0; g < KC / 8; ++g) {
+          int4 nxt[4];
+          const int4 *en = e4 + 4 * min(g + 1, KC / 8 - 1);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) nxt[q] = en[q];
+          float4 v[8];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            v[2 * q] = *reinterpret_cast<const float4 *>(tile + cur[q].x + qoff);
+            v[2 * q + 1] = *reinterpret_cast<const float4 *>(tile + cur[q].z + qoff);
           }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float wv = __int_as_float(cur[q].y), wu = __int_as_float(cur[q].w);
+            a0 = fmaf(v[2 * q].x, wv, a0);
+            a1 = fmaf(v[2 * q].y, wv, a1);
+            a2 = fmaf(v[2 * q].z, wv, a2);
+            a3 = fmaf(v[2 * q].w, wv, a3);
+            a0 = fmaf(v[2 * q + 1].x, wu, a0);
+            a1 = fmaf(v[2 * q + 1].y, wu, a1);
+            a2 = fmaf(v[2 * q + 1].z, wu, a2);
+            a3 = fmaf(v[2 * q + 1].w, wu, a3);
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
+        }
+      } else {
+        const int2 *e = ell + (size_t)j * K;
+        for (int s2 = 0; s2 < K; ++s2) {
+          const int2 p = e[s2];
+          const float4 v = *reinterpret_cast<const float4 *>(tile + p.x + qoff);
+          const float wv = __int_as_float(p.y);
+          a0 = fmaf(v.x, wv, a0);
+          a1 = fmaf(v.y, wv, a1);
+          a2 = fmaf(v.z, wv, a2);
+          a3 = fmaf(v.w, wv, a3);
+        }
+      }
+      const float bj = bias[j];
+      const float y[4] = {activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
+                          activate(a3, bj, ymax)};
+#pragma unroll
+      for (int c4 = 0; c4 < 4; ++c4) {
+        if (row[c4] >= 0) {
+          yout[(size_t)row[c4] * N + j] = y[c4];
+          if (y[c4] > 0.0f) live_mask |= 1 << c4;
         }
       }
     }
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
-      if (live_mask & (1 << c)) rowlive[quad * 4 + c] = 1;
+    for (int c4 = 0; c4 < 4; ++c4)
+      if (live_mask & (1 << c4)) rowlive[quad * 4 + c4] = 1;
     __syncthreads();
-    if (tid < nvalid) {
-      flags[p0 + tid] = rowlive[tid];
-      if (rownz && rowany[tid]) rownz[ids[p0 + tid]] = 1;
+    if (tid < 64) {
+      const unsigned long long m = __ballot(tid < nvalid && rowlive[tid] != 0);
+      if (tid == 0 && m) atomicOr(&masks[t], (unsigned)m);
+      if (count_nz && tid < nvalid && rowany[tid]) rownz[ids[p0 + tid]] = 1;
     }
     if (tid < B) {
       rowlive[tid] = 0;
@@ -280,18 +395,26 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
 
 // One layer gathering from global feature-major tiles. blockDim 256 (4 waves); a work item is a
 // chunk of kGfmOutputs outputs of one tile. Lane = (row b = lane % 32, output half h = lane / 32).
-// gridDim must be a multiple of 8: workgroup x runs on XCD x % 8, and the items of one XCD walk
-// the output chunks of one tile before moving on, so the tile stays in that XCD's L2.
+// gridDim must be a multiple of 8: workgroup x runs on XCD x % 8. With 8 or more tiles, XCD x
+// walks all output chunks of tiles x, x+8, ... so one tile at a time stays in its L2; with fewer
+// tiles, each tile's chunks are split over 8 / ntiles XCDs. For KC > 0 the item's ELL rows are
+// staged in LDS first, so the gathers are the only vector-memory requests of the inner loop.
+template <int KC>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm, float *__restrict__ yout, int N,
                                                    const int2 *__restrict__ ell, int K,
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ ids, const int *__restrict__ count,
-                                                   int *__restrict__ flags) {
+                                                   unsigned *__restrict__ masks) {
+  constexpr int KS = KC > 0 ? KC : 2;
   __shared__ float stage[kFmRows][kGfmOutputs + 1];
+  __shared__ int4 ells[kGfmOutputs * KS / 2];
   __shared__ int rowlive[kFmRows];
   const int R = *count;
   const int ntiles = (R + kFmRows - 1) / kFmRows;
   const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
+  const int parts = ntiles >= 8 ? 1 : 8 / max(ntiles, 1);
+  const int nvt = ntiles * parts;
+  const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = lane & 31, h = lane >> 5;
   const int xcd = blockIdx.x & 7;
@@ -299,25 +422,53 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
   if (tid < kFmRows) rowlive[tid] = 0;
   __syncthreads();
   for (long long local = blockIdx.x >> 3;; local += per_xcd) {
-    const long long grp = local / nchunks;
-    const int chunk = (int)(local % nchunks);
-    const long long tl = grp * 8 + xcd;
-    if (tl >= ntiles) break;
-    const int t = (int)tl;
+    const long long vt = (local / cpp) * 8 + xcd;
+    if (vt >= nvt) break;
+    const int t = (int)(vt / parts);
+    const int chunk = (int)(vt % parts) * cpp + (int)(local % cpp);
+    if (chunk >= nchunks) continue;
     const int p0 = t * kFmRows;
     const int nvalid = min(kFmRows, R - p0);
     const int c0 = chunk * kGfmOutputs;
-    const char *tb = reinterpret_cast<const char *>(fm + (size_t)t * N * kFmRows) + b * 4;
+    const int nout = min(kGfmOutputs, N - c0);
+    const char *tbase = reinterpret_cast<const char *>(fm + (size_t)t * N * kFmRows);
+    const unsigned boff = (unsigned)b * 4u;
+    if constexpr (KC > 0) {
+      const int4 *src = reinterpret_cast<const int4 *>(ell + (size_t)c0 * KC);
+      for (int i = tid; i < nout * KC / 2; i += blockDim.x) ells[i] = src[i];
+      __syncthreads();
+    }
     bool live = false;
     for (int i = 0; i < kGfmOutputs / 8; ++i) {
       const int jj = i * 8 + wave * 2 + h;
       const int j = c0 + jj;
       if (j < N) {
-        const int2 *e = ell + (size_t)j * K;
         float a = 0.0f;
-        for (int s = 0; s < K; ++s) {
-          const int2 p = e[s];
-          a = fmaf(*reinterpret_cast<const float *>(tb + p.x), __int_as_float(p.y), a);
+        if constexpr (KC > 0) {
+          const int4 *e4 = &ells[jj * (KC / 2)];
+#pragma unroll 1
+          for (int g = 0; g < KC / 16; ++g) {
+            int4 ev[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) ev[q] = e4[g * 8 + q];
+            float gv[16];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              gv[2 * q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)ev[q].x));
+              gv[2 * q + 1] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)ev[q].z));
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+              a = fmaf(gv[2 * q], __int_as_float(ev[q].y), a);
+              a = fmaf(gv[2 * q + 1], __int_as_float(ev[q].w), a);
+            }
+          }
+        } else {
+          const int2 *e = ell + (size_t)j * K;
+          for (int s2 = 0; s2 < K; ++s2) {
+            const int2 p = e[s2];
+            a = fmaf(*reinterpret_cast<const float *>(tbase + (boff + (unsigned)p.x)), __int_as_float(p.y), a);
+          }
         }
         const float y = activate(a, bias[j], ymax);
         stage[b][jj] = y;
@@ -326,16 +477,21 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
     }
     if (live && b < nvalid) rowlive[b] = 1;
     __syncthreads();
-    // write the staged block row by row: 8 threads per row, 8 outputs each
+    // write the staged block row by row: 8 threads per row, kGfmOutputs / 8 outputs each
     {
-      const int rb = tid >> 3, seg = (tid & 7) * 8;
+      constexpr int PER = kGfmOutputs / 8;
+      const int rb = tid >> 3, seg = (tid & 7) * PER;
       if (rb < nvalid) {
         float *dst = yout + (size_t)ids[p0 + rb] * N + c0 + seg;
-        for (int x = 0; x < 8; ++x)
-          if (c0 + seg + x < N) dst[x] = stage[rb][seg + x];
+#pragma unroll
+        for (int x = 0; x < PER; ++x)
+          if (seg + x < nout) dst[x] = stage[rb][seg + x];
       }
     }
-    if (tid < nvalid && rowlive[tid]) flags[p0 + tid] = 1;
+    if (tid < 64) {
+      const unsigned long long m = __ballot(tid < nvalid && rowlive[tid] != 0);
+      if (tid == 0 && m) atomicOr(&masks[t], (unsigned)m);
+    }
     __syncthreads();
     if (tid < kFmRows) rowlive[tid] = 0;
     __syncthreads();
@@ -372,7 +528,8 @@ struct sdnn_net {
   float *ybuf[2] = {nullptr, nullptr};
   float *fm = nullptr;
   int *ids[2] = {nullptr, nullptr};
-  int *flags = nullptr, *rownz = nullptr, *counts = nullptr;
+  unsigned *masks = nullptr;  // per-tile liveness bits
+  int *rownz = nullptr, *counts = nullptr;
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
@@ -399,7 +556,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t ybuf[2], fm, ids[2], flags, rownz, counts, final_ids, total;
+  size_t ybuf[2], fm, ids[2], masks, rownz, counts, final_ids, total;
 };
 
 WsLayout layout_for(const sdnn_net *net, int64_t M) {
@@ -414,7 +571,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   const size_t ib = align_up((size_t)std::max<int64_t>(M, 1) * sizeof(int), a);
   w.ids[0] = off; off += ib;
   w.ids[1] = off; off += ib;
-  w.flags = off; off += ib;
+  w.masks = off; off += ib;
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
@@ -428,21 +585,28 @@ sdnn_status check_usable(const sdnn_net *net) {
   return SDNN_OK;
 }
 
-template <int B>
+template <int B, int KC>
 hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerDev &ld, const int *ids,
                       const int *count, int *rownz) {
   static bool configured = false;
   const size_t lds = (size_t)B * net->N * sizeof(float);
   if (!configured) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_lds<B>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_lds<B, KC>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, kLdsTileBytes);
     if (e != hipSuccess) return e;
     configured = true;
   }
   const int per_cu = lds <= 64 * 1024 ? 2 : 1;
-  hipLaunchKernelGGL(k_layer_lds<B>, dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
-                     ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->flags, rownz);
+  hipLaunchKernelGGL((k_layer_lds<B, KC>), dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
+                     ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, rownz);
   return hipGetLastError();
+}
+
+template <int B>
+hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const LayerDev &ld, const int *ids,
+                        const int *count, int *rownz) {
+  if (ld.K == 32) return launch_lds<B, 32>(net, yin, yout, ld, ids, count, rownz);
+  return launch_lds<B, 0>(net, yin, yout, ld, ids, count, rownz);
 }
 
 hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count) {
@@ -450,16 +614,20 @@ hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, con
   int *rownz = (l == 0) ? net->rownz : nullptr;
   if (net->path == 0) {
     switch (net->B) {
-      case 32: return launch_lds<32>(net, yin, yout, ld, ids, count, rownz);
-      case 16: return launch_lds<16>(net, yin, yout, ld, ids, count, rownz);
-      default: return launch_lds<8>(net, yin, yout, ld, ids, count, rownz);
+      case 32: return launch_lds_k<32>(net, yin, yout, ld, ids, count, rownz);
+      case 16: return launch_lds_k<16>(net, yin, yout, ld, ids, count, rownz);
+      default: return launch_lds_k<8>(net, yin, yout, ld, ids, count, rownz);
     }
   }
   hipLaunchKernelGGL(k_to_fm, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, net->fm, net->N, ids, count, rownz);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_layer_gfm, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell, ld.K,
-                     ld.bias, net->ymax, ids, count, net->flags);
+  if (ld.K == 32)
+    hipLaunchKernelGGL(k_layer_gfm<32>, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell,
+                       ld.K, ld.bias, net->ymax, ids, count, net->masks);
+  else
+    hipLaunchKernelGGL(k_layer_gfm<0>, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell,
+                       ld.K, ld.bias, net->ymax, ids, count, net->masks);
   return hipGetLastError();
 }
 
@@ -482,7 +650,11 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
   net->ymax = ymax;
   net->layers.resize((size_t)n_layers);
   // LDS tile of B rows x N fp32 must fit the budget with B >= 8
-  if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
+  int want = 32;
+  if (const char *e = std::getenv("SDNN_LDS_ROWS")) want = std::atoi(e);
+  if (want != 8 && want != 16 && want != 32) want = 32;
+  if ((size_t)want * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = want; }
+  else if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
   else if ((size_t)16 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 16; }
   else if ((size_t)8 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 8; }
   else { net->path = 1; net->B = kFmRows; }
@@ -502,34 +674,40 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   for (int32_t i = 0; i < nl; ++i)
     if (net->layers[(size_t)l0 + i].ell) return fail(SDNN_ESTATE, "layer %d already loaded", l0 + i);
   const int32_t N = net->N;
-  // ---- validate everything before touching the device
-  std::vector<int> K((size_t)nl);
-  for (int32_t i = 0; i < nl; ++i) {
-    const int64_t *cp = col_ptr + (size_t)i * (N + 1);
-    if (i > 0 && cp[0] != col_ptr[(size_t)(i - 1) * (N + 1) + N])
+  for (int32_t i = 1; i < nl; ++i)
+    if (col_ptr[(size_t)i * (N + 1)] != col_ptr[(size_t)(i - 1) * (N + 1) + N])
       return fail(SDNN_EINVAL, "layer %d does not start where layer %d ends", l0 + i, l0 + i - 1);
-    if (cp[0] < 0) return fail(SDNN_EINVAL, "negative column offset");
+  if (col_ptr[0] < 0) return fail(SDNN_EINVAL, "negative column offset");
+  // ---- validate every layer before touching the device (layers in parallel on host threads)
+  std::vector<int> K((size_t)nl, 0);
+  std::vector<std::string> err((size_t)nl);
+  parallel_for(nl, [&](int32_t i) {
+    const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+    char buf[256];
     int kmax = 0;
     for (int32_t j = 0; j < N; ++j) {
       const int64_t a = cp[j], b = cp[j + 1];
-      if (b < a) return fail(SDNN_EINVAL, "layer %d column %d: decreasing offsets", l0 + i, j);
-      if (b - a > kMaxDegree) return fail(SDNN_EINVAL, "layer %d column %d: %lld sources exceed %d", l0 + i, j, (long long)(b - a), kMaxDegree);
+      if (b < a) { snprintf(buf, sizeof buf, "layer %d column %d: decreasing offsets", l0 + i, j); err[(size_t)i] = buf; return; }
+      if (b - a > kMaxDegree) { snprintf(buf, sizeof buf, "layer %d column %d: %lld sources exceed %d", l0 + i, j, (long long)(b - a), kMaxDegree); err[(size_t)i] = buf; return; }
       for (int64_t e = a; e < b; ++e) {
         const int32_t k = row_idx[e];
-        if (k < 0 || k >= N) return fail(SDNN_EINVAL, "layer %d column %d: source %d out of range", l0 + i, j, k);
-        if (e > a && k <= row_idx[e - 1]) return fail(SDNN_EINVAL, "layer %d column %d: sources not strictly ascending", l0 + i, j);
-        if (!std::isfinite(val[e])) return fail(SDNN_EINVAL, "layer %d column %d: non-finite weight", l0 + i, j);
+        if (k < 0 || k >= N) { snprintf(buf, sizeof buf, "layer %d column %d: source %d out of range", l0 + i, j, k); err[(size_t)i] = buf; return; }
+        if (e > a && k <= row_idx[e - 1]) { snprintf(buf, sizeof buf, "layer %d column %d: sources not strictly ascending", l0 + i, j); err[(size_t)i] = buf; return; }
+        if (!std::isfinite(val[e])) { snprintf(buf, sizeof buf, "layer %d column %d: non-finite weight", l0 + i, j); err[(size_t)i] = buf; return; }
       }
       kmax = std::max<int>(kmax, (int)(b - a));
     }
     for (int32_t j = 0; j < N; ++j)
-      if (!std::isfinite(bias[(size_t)i * N + j])) return fail(SDNN_EINVAL, "layer %d: non-finite bias", l0 + i);
+      if (!std::isfinite(bias[(size_t)i * N + j])) { snprintf(buf, sizeof buf, "layer %d: non-finite bias", l0 + i); err[(size_t)i] = buf; return; }
     K[(size_t)i] = std::max(kmax, 1);
-  }
+  });
+  for (int32_t i = 0; i < nl; ++i)
+    if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
   // ---- pack: ELL [N][K] of (byte offset of source row in the tile, weight bits)
   const int stride = (net->path == 0 ? net->B : kFmRows) * (int)sizeof(float);
-  size_t ell_words = 0;
-  for (int32_t i = 0; i < nl; ++i) ell_words += (size_t)N * K[(size_t)i];
+  std::vector<size_t> layer_off((size_t)nl + 1, 0);
+  for (int32_t i = 0; i < nl; ++i) layer_off[(size_t)i + 1] = layer_off[(size_t)i] + (size_t)N * K[(size_t)i];
+  const size_t ell_words = layer_off[(size_t)nl];
   const size_t ell_bytes = align_up(ell_words * sizeof(int2), 256);
   const size_t bias_bytes = (size_t)nl * N * sizeof(float);
   std::vector<int2> host_ell;
@@ -538,12 +716,11 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   } catch (...) {
     return fail(SDNN_ENOMEM, "out of host memory packing %zu bytes", ell_words * sizeof(int2));
   }
-  size_t off = 0;
-  for (int32_t i = 0; i < nl; ++i) {
+  parallel_for(nl, [&](int32_t i) {
     const int64_t *cp = col_ptr + (size_t)i * (N + 1);
     const int Ki = K[(size_t)i];
     for (int32_t j = 0; j < N; ++j) {
-      int2 *dst = host_ell.data() + off + (size_t)j * Ki;
+      int2 *dst = host_ell.data() + layer_off[(size_t)i] + (size_t)j * Ki;
       int s = 0;
       for (int64_t e = cp[j]; e < cp[j + 1]; ++e, ++s) {
         int wbits;
@@ -552,8 +729,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       }
       for (; s < Ki; ++s) dst[s] = make_int2(0, 0);
     }
-    off += (size_t)N * Ki;
-  }
+  });
   // ---- device copy
   if (net->device < 0) {
     HIP_OR_POISON(net, hipGetDevice(&net->device));
@@ -574,13 +750,11 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   HIP_OR_POISON(net, hipMemcpyAsync(mem, host_ell.data(), ell_words * sizeof(int2), hipMemcpyHostToDevice, s));
   HIP_OR_POISON(net, hipMemcpyAsync(mem + ell_bytes, bias, bias_bytes, hipMemcpyHostToDevice, s));
   HIP_OR_POISON(net, hipStreamSynchronize(s));
-  off = 0;
   for (int32_t i = 0; i < nl; ++i) {
     LayerDev &ld = net->layers[(size_t)l0 + i];
-    ld.ell = reinterpret_cast<const int2 *>(mem) + off;
+    ld.ell = reinterpret_cast<const int2 *>(mem) + layer_off[(size_t)i];
     ld.bias = reinterpret_cast<const float *>(mem + ell_bytes) + (size_t)i * N;
     ld.K = K[(size_t)i];
-    off += (size_t)N * ld.K;
   }
   net->n_loaded += nl;
   g_err.clear();
@@ -622,7 +796,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->fm = reinterpret_cast<float *>(ws + w.fm);
   net->ids[0] = reinterpret_cast<int *>(ws + w.ids[0]);
   net->ids[1] = reinterpret_cast<int *>(ws + w.ids[1]);
-  net->flags = reinterpret_cast<int *>(ws + w.flags);
+  net->masks = reinterpret_cast<unsigned *>(ws + w.masks);
   net->rownz = reinterpret_cast<int *>(ws + w.rownz);
   net->counts = reinterpret_cast<int *>(ws + w.counts);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
@@ -631,7 +805,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   const int M = (int)n_rows;
   hipStream_t s = net->stream;
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
-                     net->ids[0], net->flags, net->rownz, net->counts, M, net->L);
+                     net->ids[0], net->masks, net->rownz, net->counts, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
 
   const float *yin = y0;
@@ -645,7 +819,8 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l));
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->flags, net->ids[cur], net->ids[cur ^ 1],
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->path == 0 ? net->B : kFmRows,
+                       net->ids[cur], net->ids[cur ^ 1],
                        net->counts + l, net->counts + l + 1);
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;
