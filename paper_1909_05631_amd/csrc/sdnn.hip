@@ -10,9 +10,10 @@
 //   Activations: row-major [M][N] fp32, indexed by input row id. Layer 0 reads the caller's y0;
 //   layers then ping-pong between two workspace buffers. A list of live row ids (ascending) selects
 //   which rows a layer reads; rows off the list are never touched again.
-//   Weights: per layer an ELL table [N][K] of (byte offset of the source row in the kernel's tile,
-//   fp32 weight) pairs, sources ascending within each output, padded with (0, 0.0f). Padding adds
-//   fma(y, 0, acc) = acc exactly because activations are finite.
+//   Weights: per layer a slot-major ELL table [K][N] of (byte offset of the source row in the
+//   kernel's tile, fp32 weight) pairs: entry [s][j] is the s-th smallest source of output j, padded
+//   with (0, 0.0f) past the column's degree. Padding adds fma(y, 0, acc) = acc exactly because
+//   activations are finite. Slot-major order makes the entries a wave needs for one slot contiguous.
 //
 // Kernels
 //   k_layer_lds<B>: one workgroup takes a tile of B live rows, stages it in LDS transposed to
@@ -59,7 +60,6 @@ constexpr int kMaxNeurons = 65536;
 constexpr int kMaxLayers = 1000000;
 constexpr int kMaxDegree = 4096;
 constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
-constexpr int kFmRows = 32;                // rows per global feature-major tile
 constexpr int kGfmOutputs = 32;            // outputs per work item of k_layer_gfm
 constexpr int kPollEvery = 4;              // layers between live-count read-backs
 
@@ -274,45 +274,49 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
       const int j = r * per_round + wave * OPW + jl;
       if (j >= N) continue;
       float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      // ELL is slot-major ([s][j]): for a given slot the lanes of a wave read consecutive entries.
+      // Terms go in groups of 8 in ascending source order; with KC known, the next group's
+      // entries are loaded (unconditionally, so no branch delays the wait counts) while the
+      // current group's LDS reads and fma chain run.
+      const int2 *ej = ell + j;
       if constexpr (KC > 0) {
-        // groups of 8 terms: the next group's ELL entries load while this group's LDS reads and
-        // fma chain run; terms stay in ascending source order
         static_assert(KC % 8 == 0, "KC must be a multiple of 8");
-        const int4 *e4 = reinterpret_cast<const int4 *>(ell + (size_t)j * KC);
-        int4 cur[4];
+        int2 cur[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) cur[q] = e4[q];
+        for (int q = 0; q < 8; ++q) cur[q] = ej[(size_t)q * N];
 #pragma unroll 1
-        for (int g = 0; g < KC / 8; ++g) {
-          int4 nxt[4];
-          const int4 *en = e4 + 4 * min(g + 1, KC / 8 - 1);
+        for (int g = 0; g < KC - 8; g += 8) {
+          int2 nxt[8];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) nxt[q] = en[q];
+          for (int q = 0; q < 8; ++q) nxt[q] = ej[(size_t)(g + 8 + q) * N];
           float4 v[8];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            v[2 * q] = *reinterpret_cast<const float4 *>(tile + cur[q].x + qoff);
-            v[2 * q + 1] = *reinterpret_cast<const float4 *>(tile + cur[q].z + qoff);
+          for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const float4 *>(tile + cur[q].x + qoff);
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const float wv = __int_as_float(cur[q].y);
+            a0 = fmaf(v[q].x, wv, a0);
+            a1 = fmaf(v[q].y, wv, a1);
+            a2 = fmaf(v[q].z, wv, a2);
+            a3 = fmaf(v[q].w, wv, a3);
           }
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float wv = __int_as_float(cur[q].y), wu = __int_as_float(cur[q].w);
-            a0 = fmaf(v[2 * q].x, wv, a0);
-            a1 = fmaf(v[2 * q].y, wv, a1);
-            a2 = fmaf(v[2 * q].z, wv, a2);
-            a3 = fmaf(v[2 * q].w, wv, a3);
-            a0 = fmaf(v[2 * q + 1].x, wu, a0);
-            a1 = fmaf(v[2 * q + 1].y, wu, a1);
-            a2 = fmaf(v[2 * q + 1].z, wu, a2);
-            a3 = fmaf(v[2 * q + 1].w, wu, a3);
-          }
+          for (int q = 0; q < 8; ++q) cur[q] = nxt[q];
+        }
+        float4 v[8];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) cur[q] = nxt[q];
+        for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const float4 *>(tile + cur[q].x + qoff);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float wv = __int_as_float(cur[q].y);
+          a0 = fmaf(v[q].x, wv, a0);
+          a1 = fmaf(v[q].y, wv, a1);
+          a2 = fmaf(v[q].z, wv, a2);
+          a3 = fmaf(v[q].w, wv, a3);
         }
       } else {
-        const int2 *e = ell + (size_t)j * K;
         for (int s2 = 0; s2 < K; ++s2) {
-          const int2 p = e[s2];
+          const int2 p = ej[(size_t)s2 * N];
           const float4 v = *reinterpret_cast<const float4 *>(tile + p.x + qoff);
           const float wv = __int_as_float(p.y);
           a0 = fmaf(v.x, wv, a0);
@@ -349,143 +353,176 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
   }
 }
 
-// Copy live rows into feature-major tiles of kFmRows rows: fm[t][k][b] = Y[ids[t*32 + b]][k], zero
+// Copy live rows into feature-major tiles of FMR rows: fm[t][k][b] = Y[ids[t*FMR + b]][k], zero
 // for positions past the live count.
+template <int FMR>
 __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, float *__restrict__ fm, int N,
                                                const int *__restrict__ ids, const int *__restrict__ count,
                                                int *__restrict__ rownz) {
   const int R = *count;
-  const int ntiles = (R + kFmRows - 1) / kFmRows;
+  const int ntiles = (R + FMR - 1) / FMR;
   const size_t st = (size_t)gridDim.x * blockDim.x;
   if ((N & 3) == 0) {
     const int NQ = N >> 2;
-    const size_t items = (size_t)ntiles * NQ * (kFmRows / 4);
+    const size_t items = (size_t)ntiles * NQ * (FMR / 4);
     for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += st) {
-      const int bq = (int)(it % (kFmRows / 4));
-      const size_t rest = it / (kFmRows / 4);
+      const int bq = (int)(it % (FMR / 4));
+      const size_t rest = it / (FMR / 4);
       const int q = (int)(rest % NQ);
       const int t = (int)(rest / NQ);
       float4 v[4];
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const int p = t * kFmRows + bq * 4 + c;
+        const int p = t * FMR + bq * 4 + c;
         v[c] = (p < R) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p] * N)[q] : make_float4(0.f, 0.f, 0.f, 0.f);
-        if (rownz && p < R && any_nonzero(v[c])) rownz[ids[p]] = 1;
+        if (rownz && p < R && any_nonzero(v[c]) && !rownz[ids[p]]) rownz[ids[p]] = 1;
       }
-      float4 *dst = reinterpret_cast<float4 *>(fm + ((size_t)t * N + 4 * q) * kFmRows + bq * 4);
+      float4 *dst = reinterpret_cast<float4 *>(fm + ((size_t)t * N + 4 * q) * FMR + bq * 4);
       dst[0] = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
-      dst[kFmRows / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
-      dst[2 * (kFmRows / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
-      dst[3 * (kFmRows / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
+      dst[FMR / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
+      dst[2 * (FMR / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
+      dst[3 * (FMR / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
     }
   } else {
-    const size_t items = (size_t)ntiles * N * kFmRows;
+    const size_t items = (size_t)ntiles * N * FMR;
     for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += st) {
-      const int b = (int)(it % kFmRows);
-      const size_t rest = it / kFmRows;
+      const int b = (int)(it % FMR);
+      const size_t rest = it / FMR;
       const int k = (int)(rest % N);
       const int t = (int)(rest / N);
-      const int p = t * kFmRows + b;
+      const int p = t * FMR + b;
       const float v = (p < R) ? yin[(size_t)ids[p] * N + k] : 0.0f;
-      fm[((size_t)t * N + k) * kFmRows + b] = v;
-      if (rownz && v != 0.0f) rownz[ids[p]] = 1;
+      fm[((size_t)t * N + k) * FMR + b] = v;
+      if (rownz && v != 0.0f && !rownz[ids[p]]) rownz[ids[p]] = 1;
     }
   }
 }
 
-// One layer gathering from global feature-major tiles. blockDim 256 (4 waves); a work item is a
-// chunk of kGfmOutputs outputs of one tile. Lane = (row b = lane % 32, output half h = lane / 32).
-// gridDim must be a multiple of 8: workgroup x runs on XCD x % 8. With 8 or more tiles, XCD x
-// walks all output chunks of tiles x, x+8, ... so one tile at a time stays in its L2; with fewer
-// tiles, each tile's chunks are split over 8 / ntiles XCDs. For KC > 0 the item's ELL rows are
-// staged in LDS first, so the gathers are the only vector-memory requests of the inner loop.
-template <int KC>
+// One round of a layer gathering from global feature-major tiles of FMR rows: tiles
+// [tile0, tile0 + 8) of the live list, one per XCD. blockDim 256 (4 waves); a work item is a chunk
+// of kGfmOutputs outputs. Lane = (row b = lane % FMR, output slot h = lane / FMR), so a wave
+// instruction reads 64 / FMR segments of FMR * 4 bytes. gridDim must be a multiple of 8:
+// workgroup x runs on XCD x % 8, and the workgroups of XCD x share the output chunks of one tile,
+// which therefore stays in that XCD's L2 (or, for the widest layers, in the Infinity Cache) for
+// the whole launch. With fewer than 8 tiles left, each tile's chunks are split over 8 / ntiles
+// XCDs. For KC > 0 the item's ELL rows are staged in LDS first, so the gathers are the only
+// vector-memory requests of the inner loop.
+template <int FMR, int KC>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm, float *__restrict__ yout, int N,
                                                    const int2 *__restrict__ ell, int K,
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ ids, const int *__restrict__ count,
-                                                   unsigned *__restrict__ masks) {
-  constexpr int KS = KC > 0 ? KC : 2;
-  __shared__ float stage[kFmRows][kGfmOutputs + 1];
-  __shared__ int4 ells[kGfmOutputs * KS / 2];
-  __shared__ int rowlive[kFmRows];
+                                                   unsigned *__restrict__ masks, int tile0) {
+  constexpr int KS = KC > 0 ? KC : 1;
+  constexpr int OPI = 64 / FMR;             // outputs per wave instruction
+  constexpr int PER_ROUND = 4 * OPI;        // outputs per workgroup round
+  static_assert(KC % 16 == 0, "KC must be a multiple of 16");
+  static_assert(kGfmOutputs % PER_ROUND == 0, "chunk must be whole rounds");
+  __shared__ float stage[FMR][kGfmOutputs + 1];
+  __shared__ int2 ells2[kGfmOutputs * KS];
+  __shared__ float bstage[kGfmOutputs];
+  __shared__ int rowlive[FMR];
   const int R = *count;
-  const int ntiles = (R + kFmRows - 1) / kFmRows;
-  const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
-  const int parts = ntiles >= 8 ? 1 : 8 / max(ntiles, 1);
-  const int nvt = ntiles * parts;
-  const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int b = lane & 31, h = lane >> 5;
+  const int nt = min(8, (R + FMR - 1) / FMR - tile0);  // tiles in this round
+  if (nt <= 0) return;
+  const int parts = 8 / nt;
   const int xcd = blockIdx.x & 7;
+  if (xcd >= nt * parts) return;
+  const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
+  const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
+  const int t = tile0 + xcd / parts;
+  const int cbeg = (xcd % parts) * cpp, cend = min(nchunks, cbeg + cpp);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b = lane % FMR, h = lane / FMR;
   const int per_xcd = gridDim.x >> 3;
-  if (tid < kFmRows) rowlive[tid] = 0;
+  if (tid < FMR) rowlive[tid] = 0;
   __syncthreads();
-  for (long long local = blockIdx.x >> 3;; local += per_xcd) {
-    const long long vt = (local / cpp) * 8 + xcd;
-    if (vt >= nvt) break;
-    const int t = (int)(vt / parts);
-    const int chunk = (int)(vt % parts) * cpp + (int)(local % cpp);
-    if (chunk >= nchunks) continue;
-    const int p0 = t * kFmRows;
-    const int nvalid = min(kFmRows, R - p0);
+  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+    const int p0 = t * FMR;
+    const int nvalid = min(FMR, R - p0);
     const int c0 = chunk * kGfmOutputs;
     const int nout = min(kGfmOutputs, N - c0);
-    const char *tbase = reinterpret_cast<const char *>(fm + (size_t)t * N * kFmRows);
+    const char *tbase = reinterpret_cast<const char *>(fm + (size_t)t * N * FMR);
     const unsigned boff = (unsigned)b * 4u;
+    // stage this chunk's biases (and, for KC > 0, its ELL entries as [slot][output]); the ELL is
+    // read once per tile, streamed so it does not displace the tile from L2
+    for (int i = tid; i < kGfmOutputs; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
     if constexpr (KC > 0) {
-      const int4 *src = reinterpret_cast<const int4 *>(ell + (size_t)c0 * KC);
-      for (int i = tid; i < nout * KC / 2; i += blockDim.x) ells[i] = src[i];
-      __syncthreads();
+      for (int i = tid; i < KC * kGfmOutputs; i += blockDim.x) {
+        const int sl = i / kGfmOutputs, jj = i % kGfmOutputs;
+        long long e = 0;
+        if (jj < nout) e = __builtin_nontemporal_load(reinterpret_cast<const long long *>(ell + (size_t)sl * N + c0 + jj));
+        reinterpret_cast<long long *>(ells2)[sl * kGfmOutputs + jj] = e;
+      }
     }
+    __syncthreads();
     bool live = false;
-    for (int i = 0; i < kGfmOutputs / 8; ++i) {
-      const int jj = i * 8 + wave * 2 + h;
-      const int j = c0 + jj;
-      if (j < N) {
-        float a = 0.0f;
-        if constexpr (KC > 0) {
-          const int4 *e4 = &ells[jj * (KC / 2)];
+    if constexpr (KC > 0) {
+      // two outputs per lane at a time: 32 gathers in flight, each chain in ascending order
+      static_assert((kGfmOutputs / PER_ROUND) % 2 == 0, "rounds come in pairs");
+      for (int i = 0; i < kGfmOutputs / PER_ROUND; i += 2) {
+        const int jA = i * PER_ROUND + wave * OPI + h, jB = jA + PER_ROUND;
+        const bool okA = c0 + jA < N, okB = c0 + jB < N;
+        const int2 *eA = ells2 + jA, *eB = ells2 + jB;
+        float aA = 0.0f, aB = 0.0f;
 #pragma unroll 1
-          for (int g = 0; g < KC / 16; ++g) {
-            int4 ev[8];
+        for (int g = 0; g < KC; g += 16) {
+          int2 evA[16], evB[16];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) ev[q] = e4[g * 8 + q];
-            float gv[16];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              gv[2 * q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)ev[q].x));
-              gv[2 * q + 1] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)ev[q].z));
-            }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-              a = fmaf(gv[2 * q], __int_as_float(ev[q].y), a);
-              a = fmaf(gv[2 * q + 1], __int_as_float(ev[q].w), a);
-            }
+          for (int q = 0; q < 16; ++q) {
+            evA[q] = eA[(g + q) * kGfmOutputs];
+            evB[q] = eB[(g + q) * kGfmOutputs];
           }
-        } else {
-          const int2 *e = ell + (size_t)j * K;
-          for (int s2 = 0; s2 < K; ++s2) {
-            const int2 p = e[s2];
-            a = fmaf(*reinterpret_cast<const float *>(tbase + (boff + (unsigned)p.x)), __int_as_float(p.y), a);
+          float gA[16], gB[16];
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            gA[q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)evA[q].x));
+            gB[q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)evB[q].x));
+          }
+#pragma unroll
+          for (int q = 0; q < 16; ++q) {
+            aA = fmaf(gA[q], __int_as_float(evA[q].y), aA);
+            aB = fmaf(gB[q], __int_as_float(evB[q].y), aB);
           }
         }
-        const float y = activate(a, bias[j], ymax);
-        stage[b][jj] = y;
-        live |= (y > 0.0f);
+        if (okA) {
+          const float y = activate(aA, bstage[jA], ymax);
+          stage[b][jA] = y;
+          live |= (y > 0.0f);
+        }
+        if (okB) {
+          const float y = activate(aB, bstage[jB], ymax);
+          stage[b][jB] = y;
+          live |= (y > 0.0f);
+        }
+      }
+    } else {
+      for (int i = 0; i < kGfmOutputs / PER_ROUND; ++i) {
+        const int jj = i * PER_ROUND + wave * OPI + h;
+        const int j = c0 + jj;
+        if (j < N) {
+          float a = 0.0f;
+          for (int s2 = 0; s2 < K; ++s2) {
+            const int2 p = ell[(size_t)s2 * N + j];
+            a = fmaf(*reinterpret_cast<const float *>(tbase + (boff + (unsigned)p.x)), __int_as_float(p.y), a);
+          }
+          const float y = activate(a, bstage[jj], ymax);
+          stage[b][jj] = y;
+          live |= (y > 0.0f);
+        }
       }
     }
     if (live && b < nvalid) rowlive[b] = 1;
     __syncthreads();
-    // write the staged block row by row: 8 threads per row, kGfmOutputs / 8 outputs each
+    // write the staged block row by row: 256 / FMR threads per row
     {
-      constexpr int PER = kGfmOutputs / 8;
-      const int rb = tid >> 3, seg = (tid & 7) * PER;
+      constexpr int TPR = 256 / FMR, PER = kGfmOutputs / TPR;
+      const int rb = tid / TPR, seg = (tid % TPR) * PER;
       if (rb < nvalid) {
         float *dst = yout + (size_t)ids[p0 + rb] * N + c0 + seg;
 #pragma unroll
         for (int x = 0; x < PER; ++x)
-          if (seg + x < nout) dst[x] = stage[rb][seg + x];
+          if (seg + x < nout) __builtin_nontemporal_store(stage[rb][seg + x], dst + x);
       }
     }
     if (tid < 64) {
@@ -493,7 +530,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
       if (tid == 0 && m) atomicOr(&masks[t], (unsigned)m);
     }
     __syncthreads();
-    if (tid < kFmRows) rowlive[tid] = 0;
+    if (tid < FMR) rowlive[tid] = 0;
     __syncthreads();
   }
 }
@@ -534,7 +571,7 @@ struct sdnn_net {
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
   const float *final_y = nullptr;
-  int32_t *pinned = nullptr; // live-count read-back slots
+  int32_t *pinned = nullptr; // live-count read-back slots (0-3: polling ring, 7: exact count)
   std::vector<hipEvent_t> events;
   // profiling
   bool profiling = false;
@@ -567,7 +604,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.ybuf[0] = off; off += ybytes;
   w.ybuf[1] = off; off += ybytes;
   w.fm = off;
-  if (net->path == 1) off += align_up((size_t)((M + kFmRows - 1) / kFmRows) * kFmRows * (size_t)net->N * sizeof(float), a);
+  if (net->path == 1) off += align_up((size_t)((M + net->B - 1) / net->B) * net->B * (size_t)net->N * sizeof(float), a);
   const size_t ib = align_up((size_t)std::max<int64_t>(M, 1) * sizeof(int), a);
   w.ids[0] = off; off += ib;
   w.ids[1] = off; off += ib;
@@ -609,7 +646,30 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
   return launch_lds<B, 0>(net, yin, yout, ld, ids, count, rownz);
 }
 
-hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count) {
+template <int FMR>
+hipError_t launch_gfm(sdnn_net *net, const float *yin, float *yout, const LayerDev &ld, const int *ids,
+                      const int *count, int *rownz, int rounds) {
+  hipLaunchKernelGGL(k_to_fm<FMR>, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, net->fm, net->N, ids, count,
+                     rownz);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  for (int r = 0; r < rounds; ++r) {
+    if (ld.K == 32)
+      hipLaunchKernelGGL((k_layer_gfm<FMR, 32>), dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N,
+                         ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, r * 8);
+    else
+      hipLaunchKernelGGL((k_layer_gfm<FMR, 0>), dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout,
+                         net->N, ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, r * 8);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// rounds: launches of the global-tile kernel (8 tiles each) the live count needs; 1 when the
+// count is known to fit in one round.
+hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count,
+                        int rounds) {
   const LayerDev &ld = net->layers[l];
   int *rownz = (l == 0) ? net->rownz : nullptr;
   if (net->path == 0) {
@@ -619,16 +679,8 @@ hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, con
       default: return launch_lds_k<8>(net, yin, yout, ld, ids, count, rownz);
     }
   }
-  hipLaunchKernelGGL(k_to_fm, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, net->fm, net->N, ids, count, rownz);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (ld.K == 32)
-    hipLaunchKernelGGL(k_layer_gfm<32>, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell,
-                       ld.K, ld.bias, net->ymax, ids, count, net->masks);
-  else
-    hipLaunchKernelGGL(k_layer_gfm<0>, dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N, ld.ell,
-                       ld.K, ld.bias, net->ymax, ids, count, net->masks);
-  return hipGetLastError();
+  if (net->B == 16) return launch_gfm<16>(net, yin, yout, ld, ids, count, rownz, rounds);
+  return launch_gfm<32>(net, yin, yout, ld, ids, count, rownz, rounds);
 }
 
 }  // namespace
@@ -657,7 +709,12 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
   else if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
   else if ((size_t)16 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 16; }
   else if ((size_t)8 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 8; }
-  else { net->path = 1; net->B = kFmRows; }
+  else {
+    // global feature-major tiles of 32 rows (128-byte segments per source); one tile per XCD per
+    // launch, held in that XCD's L2 up to 16384 neurons and in the Infinity Cache beyond
+    net->path = 1;
+    net->B = 32;
+  }
   *out = net;
   g_err.clear();
   return SDNN_OK;
@@ -703,8 +760,8 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   });
   for (int32_t i = 0; i < nl; ++i)
     if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
-  // ---- pack: ELL [N][K] of (byte offset of source row in the tile, weight bits)
-  const int stride = (net->path == 0 ? net->B : kFmRows) * (int)sizeof(float);
+  // ---- pack: slot-major ELL [K][N] of (byte offset of source row in the tile, weight bits)
+  const int stride = net->B * (int)sizeof(float);
   std::vector<size_t> layer_off((size_t)nl + 1, 0);
   for (int32_t i = 0; i < nl; ++i) layer_off[(size_t)i + 1] = layer_off[(size_t)i] + (size_t)N * K[(size_t)i];
   const size_t ell_words = layer_off[(size_t)nl];
@@ -719,15 +776,15 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   parallel_for(nl, [&](int32_t i) {
     const int64_t *cp = col_ptr + (size_t)i * (N + 1);
     const int Ki = K[(size_t)i];
+    int2 *base = host_ell.data() + layer_off[(size_t)i];
     for (int32_t j = 0; j < N; ++j) {
-      int2 *dst = host_ell.data() + layer_off[(size_t)i] + (size_t)j * Ki;
       int s = 0;
       for (int64_t e = cp[j]; e < cp[j + 1]; ++e, ++s) {
         int wbits;
         std::memcpy(&wbits, &val[e], sizeof(int));
-        dst[s] = make_int2(row_idx[e] * stride, wbits);
+        base[(size_t)s * N + j] = make_int2(row_idx[e] * stride, wbits);
       }
-      for (; s < Ki; ++s) dst[s] = make_int2(0, 0);
+      for (; s < Ki; ++s) base[(size_t)s * N + j] = make_int2(0, 0);
     }
   });
   // ---- device copy
@@ -785,7 +842,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   if (net->events.empty()) {
     net->events.resize(4);
     for (auto &ev : net->events) HIP_OR_POISON(net, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
-    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 4 * sizeof(int32_t), hipHostMallocDefault));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 8 * sizeof(int32_t), hipHostMallocDefault));
   }
   char *ws = static_cast<char *>(workspace);
   net->M = n_rows;
@@ -811,17 +868,31 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   const float *yin = y0;
   int cur = 0;
   int32_t l = 0;
+  // Upper bound of the live count known on the host (rows only die). The global-tile path needs
+  // the exact count before a layer with more than one round of tiles: it reads it back then,
+  // which costs one stream synchronization per such (large) layer.
+  int64_t known = M;
+  const int64_t one_round = 8 * (int64_t)net->B;
   // read-back ring: (event slot, layer boundary) of chunks not yet checked
   int ring_slot[4], ring_bound[4], ring_n = 0, ring_head = 0, next_slot = 0;
   bool all_dead = (M == 0);
   for (; l < net->L && !all_dead; ++l) {
     float *yout = net->ybuf[l & 1];
+    int rounds = 1;
+    if (net->path == 1 && known > one_round) {
+      int32_t r = 0;
+      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      HIP_OR_POISON(net, hipStreamSynchronize(s));
+      r = net->pinned[7];
+      known = r;
+      if (r == 0) { all_dead = true; break; }
+      rounds = (int)((((int64_t)r + net->B - 1) / net->B + 7) / 8);
+    }
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l));
+    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds));
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->path == 0 ? net->B : kFmRows,
-                       net->ids[cur], net->ids[cur ^ 1],
-                       net->counts + l, net->counts + l + 1);
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B,
+                       net->ids[cur], net->ids[cur ^ 1], net->counts + l, net->counts + l + 1);
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;
     yin = yout;

@@ -124,3 +124,17 @@ def test_rerun_is_deterministic_and_batches_independent():
     np.testing.assert_array_equal(ra, gpu.net.final_rows(b))
     p = gpu.run(y0[:61])
     np.testing.assert_array_equal(p, a[a < 61])
+
+
+@pytest.mark.parametrize("n,seed", [(5001, 1), (12001, 2), (8192, 3)])
+def test_global_tile_path_random_networks(n, seed):
+    """Widths past the LDS budget use feature-major tiles in global memory (32 or 16 rows per tile);
+    random degrees (including empty columns), signed weights, widths that are not multiples of 4."""
+    rng = np.random.default_rng(100 + seed)
+    m, nl = int(rng.integers(20, 70)), 3
+    layers = random_layers(rng, n, nl, max_deg=40)
+    y0 = (rng.random((m, n)) < 0.5).astype(np.float32) * rng.uniform(0, 2, (m, n)).astype(np.float32)
+    log(f"global-tile n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert gpu.net.kernel_path == 1
+    assert_parity(gpu, o, cats)
