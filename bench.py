@@ -79,6 +79,39 @@ def cpu_baseline(cfg, target_s: float, threads: int) -> dict:
                       f"{threads} host threads"}
 
 
+def calibrate_copy(nbytes: int) -> int:
+    """A plain device-to-device copy of known size, run under rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE
+    to scale those counters to bytes."""
+    import torch
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": nbytes}))
+    return 0
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    with open(os.path.join(ROOT, "paper_1909_05631_amd", "csrc", "sdnn.hip"), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def committed_traffic(workload: str):
+    """HBM bytes per layer launch measured with rocprofv3 counters for this workload, if the record
+    in profiles/ was taken with the current kernel source; None otherwise."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha():
+        return None
+    return rec.get("bytes_per_launch")
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,7 +121,11 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-layer events (no roofline)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="BYTES",
+                    help="only copy BYTES between two device buffers (for scaling HBM byte counters)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        return calibrate_copy(args.calibrate_copy)
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -176,7 +213,8 @@ def main() -> int:
         kname = f"k_layer_lds<{32 if n <= 1024 else 16 if n <= 2048 else 8}>" if net.kernel_path == 0 \
             else "k_to_fm+k_layer_gfm"
         roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": None, "kernel": kname,
+                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(cfg.name),
+                    "kernel": kname,
                     "launches": launches, "avg_launch_ms": round(tot_ms / max(launches, 1), 5),
                     "algorithmic_bytes_per_launch": int(tot_bytes / max(launches, 1))}
 
