@@ -97,8 +97,9 @@ __device__ __forceinline__ bool any_nonzero(float4 v) {
 }
 
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, int *__restrict__ rownz,
-                       int *__restrict__ counts, int M, int L) {
+                       int *__restrict__ counts, int *__restrict__ misc, int M, int L) {
   const int st = gridDim.x * blockDim.x;
+  if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
     masks[i] = 0u;
@@ -535,6 +536,164 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
   }
 }
 
+template <int T>
+struct BitWord;
+template <>
+struct BitWord<16> {
+  using type = unsigned short;
+};
+template <>
+struct BitWord<32> {
+  using type = unsigned int;
+};
+
+// Layer-0 inputs as bits (the challenge inputs are binary images, Sec. IV): pack the live rows into
+// feature-major bit tiles, bits[t][k] bit b = (Y[ids[t*T + b]][k] != 0). Any entry other than 0
+// and 1 (or not finite) sets *nonbinary, and the bit route is then not used. Rows with a nonzero
+// entry are recorded in rownz. One wave per (tile, run of kPackBlocks blocks of 64 sources),
+// lane = source; the rows' nonzero bits are gathered over the run and stored once.
+constexpr int kPackBlocks = 16;
+template <int T>
+__global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin, typename BitWord<T>::type *__restrict__ bits,
+                                                   int N, const int *__restrict__ ids, const int *__restrict__ count,
+                                                   int *__restrict__ rownz, int *__restrict__ nonbinary) {
+  using W = typename BitWord<T>::type;
+  const int R = *count;
+  const int ntiles = (R + T - 1) / T;
+  const int kblocks = (N + 63) / 64;
+  const int runs = (kblocks + kPackBlocks - 1) / kPackBlocks;
+  const int lane = threadIdx.x & 63;
+  const long long nwaves = (long long)gridDim.x * (blockDim.x >> 6);
+  bool bad = false;
+  for (long long item = blockIdx.x * (long long)(blockDim.x >> 6) + (threadIdx.x >> 6);
+       item < (long long)ntiles * runs; item += nwaves) {
+    const int t = (int)(item / runs), run = (int)(item % runs);
+    const int nvalid = min(T, R - t * T);
+    const float *rowp[T];
+#pragma unroll
+    for (int b = 0; b < T; ++b) rowp[b] = yin + (size_t)ids[t * T + min(b, nvalid - 1)] * N;
+    unsigned rows_nz = 0u;
+    const int kb_end = min(kblocks, (run + 1) * kPackBlocks);
+    for (int kb = run * kPackBlocks; kb < kb_end; ++kb) {
+      const int k = kb * 64 + lane;
+      const bool kin = k < N;
+      float v[T];
+#pragma unroll
+      for (int b = 0; b < T; ++b) v[b] = (b < nvalid && kin) ? rowp[b][k] : 0.0f;
+      unsigned word = 0u;
+#pragma unroll
+      for (int b = 0; b < T; ++b) {
+        const bool nz = v[b] != 0.0f;
+        bad |= nz && v[b] != 1.0f;
+        word |= (unsigned)nz << b;
+      }
+      rows_nz |= word;
+      if (kin) bits[(size_t)t * N + k] = (W)word;
+    }
+    // rows with a nonzero anywhere in this run: OR over the wave, then lane b stores row b's flag
+    unsigned all = rows_nz;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) all |= __shfl_xor(all, d, 64);
+    if (lane < nvalid && ((all >> lane) & 1u)) rownz[ids[t * T + lane]] = 1;
+  }
+  if (__ballot(bad) && lane == 0) *nonbinary = 1;
+}
+
+// Layer 0 from bit tiles of T rows (T = 16 or 32): every term is fma(bit, w, acc) with bit 0 or 1,
+// the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim 1024. LDS holds
+// the tile's N words and a 16-entry table that turns 4 bits into 4 floats. Lane = output j; each
+// lane carries the T rows of its output, so one ELL entry and one word serve T edge-rows, and the
+// stores of one row are 64 consecutive outputs.
+template <int T>
+__global__ __launch_bounds__(1024) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
+                                                     float *__restrict__ yout, int N, const int2 *__restrict__ ell,
+                                                     int K, int ell_shift, const float *__restrict__ bias,
+                                                     float ymax, const int *__restrict__ ids,
+                                                     const int *__restrict__ count, unsigned *__restrict__ masks,
+                                                     int B) {
+  using W = typename BitWord<T>::type;
+  // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), then the tile
+  extern __shared__ float4 smem[];
+  float4 *lut = smem;
+  unsigned &tilemask = *reinterpret_cast<unsigned *>(smem + 16);
+  W *tile = reinterpret_cast<W *>(smem + 17);
+  const int R = *count;
+  const int ntiles = (R + T - 1) / T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int blocks = (N + 63) / 64;                 // output blocks of 64
+  const int rounds = (blocks + nw - 1) / nw;        // rounds of one block per wave
+  const Chunking ch = chunking(ntiles, rounds);
+  const int items = ntiles * ch.nchunks;
+  if (tid < 16) lut[tid] = make_float4((float)(tid & 1), (float)((tid >> 1) & 1), (float)((tid >> 2) & 1), (float)((tid >> 3) & 1));
+  if (tid == 0) tilemask = 0u;
+  for (int w = blockIdx.x; w < items; w += gridDim.x) {
+    const int t = w / ch.nchunks, c = w % ch.nchunks;
+    const int p0 = t * T;
+    const int nvalid = min(T, R - p0);
+    {
+      const W *src = bits + (size_t)t * N;
+      if ((reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+        const int n16 = (int)(((size_t)N * sizeof(W)) / 16);
+        for (int i = tid; i < n16; i += blockDim.x) reinterpret_cast<int4 *>(tile)[i] = reinterpret_cast<const int4 *>(src)[i];
+        for (int k = n16 * (int)(16 / sizeof(W)) + tid; k < N; k += blockDim.x) tile[k] = src[k];
+      } else {
+        for (int k = tid; k < N; k += blockDim.x) tile[k] = src[k];
+      }
+    }
+    __syncthreads();
+    const char *tb = reinterpret_cast<const char *>(tile);
+    unsigned live = 0u;
+    const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
+    for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
+      const int blk = r * nw + wave;
+      if (blk >= blocks) break;
+      const int j = blk * 64 + lane;
+      const bool jin = j < N;
+      const int2 *ej = ell + (jin ? j : 0);
+      float acc[T];
+#pragma unroll
+      for (int b = 0; b < T; ++b) acc[b] = 0.0f;
+#pragma unroll 4
+      for (int sl = 0; sl < K; ++sl) {
+        const int2 e = ej[(size_t)sl * N];
+        const unsigned word = *reinterpret_cast<const W *>(tb + (size_t)(e.x >> ell_shift) * sizeof(W));
+        const float wv = __int_as_float(e.y);
+#pragma unroll
+        for (int n = 0; n < T / 4; ++n) {
+          const float4 v = lut[(word >> (4 * n)) & 15u];
+          acc[4 * n] = fmaf(v.x, wv, acc[4 * n]);
+          acc[4 * n + 1] = fmaf(v.y, wv, acc[4 * n + 1]);
+          acc[4 * n + 2] = fmaf(v.z, wv, acc[4 * n + 2]);
+          acc[4 * n + 3] = fmaf(v.w, wv, acc[4 * n + 3]);
+        }
+      }
+      if (jin) {
+        const float bj = bias[j];
+#pragma unroll
+        for (int b = 0; b < T; ++b) {
+          if (b < nvalid) {
+            const float y = activate(acc[b], bj, ymax);
+            yout[(size_t)ids[p0 + b] * N + j] = y;
+            live |= (y > 0.0f ? 1u : 0u) << b;
+          }
+        }
+      }
+    }
+    if (live) atomicOr(&tilemask, live);
+    __syncthreads();
+    if (tid == 0) {
+      unsigned m = tilemask;
+      tilemask = 0u;
+      while (m) {
+        const int bb = __ffs(m) - 1;
+        m &= m - 1u;
+        atomicOr(&masks[(p0 + bb) / B], 1u << ((p0 + bb) % B));
+      }
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------------------------------------------
 // Host side
 
@@ -550,7 +709,8 @@ struct sdnn_net {
   int32_t N = 0, L = 0;
   float ymax = 32.0f;
   int path = 0;  // 0: LDS tiles, 1: global feature-major tiles
-  int B = 0;     // rows per LDS tile (path 0)
+  int B = 0;     // rows per tile: LDS tile (path 0) or global feature-major tile (path 1)
+  int bitsT = 0; // rows per layer-0 bit tile (path 1), 0 if the bit route is not available
   int device = -1;
   int cus = 0;
   bool poisoned = false;
@@ -567,11 +727,12 @@ struct sdnn_net {
   int *ids[2] = {nullptr, nullptr};
   unsigned *masks = nullptr;  // per-tile liveness bits
   int *rownz = nullptr, *counts = nullptr;
+  int *misc = nullptr;  // device flags: [0] a layer-0 input is not 0 or 1
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
   const float *final_y = nullptr;
-  int32_t *pinned = nullptr; // live-count read-back slots (0-3: polling ring, 7: exact count)
+  int32_t *pinned = nullptr; // read-back slots (0-3: polling ring, 6: input-not-binary flag, 7: exact count)
   std::vector<hipEvent_t> events;
   // profiling
   bool profiling = false;
@@ -593,7 +754,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t ybuf[2], fm, ids[2], masks, rownz, counts, final_ids, total;
+  size_t ybuf[2], fm, ids[2], masks, rownz, counts, misc, final_ids, total;
 };
 
 WsLayout layout_for(const sdnn_net *net, int64_t M) {
@@ -611,6 +772,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.masks = off; off += ib;
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
+  w.misc = off; off += a;
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
   w.total = off;
   return w;
@@ -666,12 +828,45 @@ hipError_t launch_gfm(sdnn_net *net, const float *yin, float *yout, const LayerD
   return hipSuccess;
 }
 
+template <int T>
+size_t bits_lds_bytes(const sdnn_net *net, int) {
+  using W = typename BitWord<T>::type;
+  return 17 * 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+}
+
+template <int T>
+hipError_t launch_pack_bits(sdnn_net *net, const float *yin, const int *ids, const int *count) {
+  using W = typename BitWord<T>::type;
+  hipLaunchKernelGGL(k_pack_bits<T>, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, reinterpret_cast<W *>(net->fm),
+                     net->N, ids, count, net->rownz, net->misc);
+  return hipGetLastError();
+}
+
+template <int T>
+hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, float *yout, const int *ids, const int *count) {
+  using W = typename BitWord<T>::type;
+  static bool configured = false;
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  const size_t lds = bits_lds_bytes<T>(net, ld.K);
+  const int per_cu = lds <= 72 * 1024 ? 2 : 1;
+  int shift = 0;
+  while ((1 << shift) < net->B * (int)sizeof(float)) ++shift;
+  hipLaunchKernelGGL(k_layer_bits<T>, dim3(net->cus * per_cu), dim3(1024), lds, net->stream,
+                     reinterpret_cast<const W *>(net->fm), yout, net->N, ld.ell, ld.K, shift, ld.bias, net->ymax, ids,
+                     count, net->masks, net->B);
+  return hipGetLastError();
+}
+
 // rounds: launches of the global-tile kernel (8 tiles each) the live count needs; 1 when the
 // count is known to fit in one round.
 hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count,
-                        int rounds) {
+                        int rounds, int *rownz) {
   const LayerDev &ld = net->layers[l];
-  int *rownz = (l == 0) ? net->rownz : nullptr;
   if (net->path == 0) {
     switch (net->B) {
       case 32: return launch_lds_k<32>(net, yin, yout, ld, ids, count, rownz);
@@ -714,6 +909,8 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
     // launch, held in that XCD's L2 up to 16384 neurons and in the Infinity Cache beyond
     net->path = 1;
     net->B = 32;
+    // layer 0 from bit tiles: 32-row tiles while their words fit 64 KiB of LDS, else 16-row tiles
+    net->bitsT = (size_t)n_neurons * 4 <= 64 * 1024 ? 32 : ((size_t)n_neurons * 2 <= 128 * 1024 ? 16 : 0);
   }
   *out = net;
   g_err.clear();
@@ -856,13 +1053,14 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->masks = reinterpret_cast<unsigned *>(ws + w.masks);
   net->rownz = reinterpret_cast<int *>(ws + w.rownz);
   net->counts = reinterpret_cast<int *>(ws + w.counts);
+  net->misc = reinterpret_cast<int *>(ws + w.misc);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
   net->ran = false;
 
   const int M = (int)n_rows;
   hipStream_t s = net->stream;
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
-                     net->ids[0], net->masks, net->rownz, net->counts, M, net->L);
+                     net->ids[0], net->masks, net->rownz, net->counts, net->misc, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
 
   const float *yin = y0;
@@ -878,18 +1076,40 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   bool all_dead = (M == 0);
   for (; l < net->L && !all_dead; ++l) {
     float *yout = net->ybuf[l & 1];
+    int *rownz = (l == 0) ? net->rownz : nullptr;
     int rounds = 1;
-    if (net->path == 1 && known > one_round) {
-      int32_t r = 0;
-      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    bool bits_route = false;
+    const bool try_bits = l == 0 && net->bitsT > 0 && net->layers[0].K <= 32 &&
+                          (net->bitsT == 32 ? bits_lds_bytes<32>(net, 32) : bits_lds_bytes<16>(net, 32)) <= 160 * 1024;
+    if (try_bits) {
+      // layer 0 of a wide network: pack the inputs to bits (this also finds the nonzero rows), then
+      // read back whether every input was 0 or 1
+      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+      HIP_OR_POISON(net, net->bitsT == 32 ? launch_pack_bits<32>(net, yin, net->ids[cur], net->counts)
+                                          : launch_pack_bits<16>(net, yin, net->ids[cur], net->counts));
+      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 6, net->misc, sizeof(int32_t), hipMemcpyDeviceToHost, s));
       HIP_OR_POISON(net, hipStreamSynchronize(s));
-      r = net->pinned[7];
-      known = r;
-      if (r == 0) { all_dead = true; break; }
-      rounds = (int)((((int64_t)r + net->B - 1) / net->B + 7) / 8);
+      bits_route = net->pinned[6] == 0;
+      rownz = nullptr;
+      if (bits_route) {
+        HIP_OR_POISON(net, net->bitsT == 32 ? launch_layer_bits<32>(net, net->layers[0], yout, net->ids[cur], net->counts)
+                                            : launch_layer_bits<16>(net, net->layers[0], yout, net->ids[cur], net->counts));
+      } else {
+        rounds = (int)((((int64_t)M + net->B - 1) / net->B + 7) / 8);
+        HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds, rownz));
+      }
+    } else {
+      if (net->path == 1 && known > one_round) {
+        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        HIP_OR_POISON(net, hipStreamSynchronize(s));
+        const int32_t r = net->pinned[7];
+        known = r;
+        if (r == 0) { all_dead = true; break; }
+        rounds = (int)((((int64_t)r + net->B - 1) / net->B + 7) / 8);
+      }
+      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+      HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds, rownz));
     }
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds));
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B,
                        net->ids[cur], net->ids[cur ^ 1], net->counts + l, net->counts + l + 1);

@@ -138,3 +138,29 @@ def test_global_tile_path_random_networks(n, seed):
     gpu, o, cats = run_both(n, layers, y0)
     assert gpu.net.kernel_path == 1
     assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("n,kind", [(5001, "binary"), (12001, "binary"), (40000, "binary"), (16384, "signed-zero"),
+                                    (12001, "not-binary")])
+def test_layer0_bit_route(n, kind):
+    """Wide layers take layer 0 from bit-packed inputs when every input is 0 or 1 (32-row bit tiles up
+    to 16384 neurons, 16-row tiles beyond); -0.0 counts as 0; a single other value sends layer 0 back
+    to the fp32 route. Either way the result must equal the oracle's."""
+    rng = np.random.default_rng(n)
+    m, nl = 75, 3
+    cp, ri, v = synth.layers_csc(11, 0, nl, n) if n in (16384,) else (None, None, None)
+    if cp is not None:
+        layers = [(cp[l], ri, v, np.full(n, -0.40, np.float32)) for l in range(nl)]
+    else:
+        layers = random_layers(rng, n, nl, max_deg=32, signed=False)
+        layers = [(a, b_, w * np.float32(0.5), np.full(n, -0.3, np.float32)) for (a, b_, w, _) in layers]
+    dens = rng.uniform(0.2, 0.8, size=(m, 1))
+    y0 = (rng.random((m, n)) < dens).astype(np.float32)
+    y0[5] = 0.0
+    if kind == "signed-zero":
+        y0[y0 == 0] = -0.0
+    if kind == "not-binary":
+        y0[3, 7] = 0.5
+    log(f"bit route n={n} kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert_parity(gpu, o, cats)
