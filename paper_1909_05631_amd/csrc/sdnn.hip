@@ -60,7 +60,7 @@ constexpr int kMaxNeurons = 65536;
 constexpr int kMaxLayers = 1000000;
 constexpr int kMaxDegree = 4096;
 constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
-constexpr int kGfmOutputs = 32;            // outputs per work item of k_layer_gfm
+constexpr int kGfmOutputs = 64;            // outputs per work item of k_layer_gfm
 constexpr int kPollEvery = 4;              // layers between live-count read-backs
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -92,14 +92,33 @@ __device__ __forceinline__ float activate(float z, float b, float ymax) {
   return t > ymax ? ymax : (t > 0.0f ? t : 0.0f);
 }
 
+// Keeps the compiler from moving memory accesses across this point (no instruction is emitted):
+// pins the issue order of software-pipelined loads.
+__device__ __forceinline__ void mem_fence_compiler() { asm volatile("" ::: "memory"); }
+
+// Ties four values to this point of the instruction stream (no instruction is emitted): the
+// computations producing them are scheduled before it.
+__device__ __forceinline__ void pin4(float &a, float &b, float &c, float &d) {
+  asm volatile("" : "+v"(a), "+v"(b), "+v"(c), "+v"(d));
+}
+
+// 16-byte store that streams past the L2 (the data is read by the next kernel, not this one).
+__device__ __forceinline__ void store_stream(float4 *p, float4 v) {
+  typedef float v4f __attribute__((ext_vector_type(4)));
+  const v4f x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<v4f *>(p));
+}
+
 __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
 }
 
+// misc[0]: a layer-0 input is not 0 or 1; misc[kNposSlot + i]: positions in live list i.
+constexpr int kNposSlot = 4;
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, int *__restrict__ rownz,
                        int *__restrict__ counts, int *__restrict__ misc, int M, int L) {
   const int st = gridDim.x * blockDim.x;
-  if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = 0;
+  if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = (threadIdx.x == kNposSlot) ? M : 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
     masks[i] = 0u;
@@ -119,13 +138,15 @@ __device__ __forceinline__ int wave_inclusive_sum(int v, int lane) {
 }
 
 // Stable compaction over per-tile liveness masks: bit b of masks[t] says that list position
-// t*B + b is live. ids_out = the live ids in list order, count_out = their number. The masks are
-// cleared for the next layer. One workgroup of 1024 threads; tiles are taken 4096 at a time: an
-// exclusive scan of their popcounts gives each tile's output offset, then every position is placed.
+// t*B + b is live. ids_out = the live ids in list order, src_out (unless null) = their positions in
+// the input list, *count_out (and *count_out2 unless null) = their number. The masks are cleared for
+// the next layer. One workgroup of 1024 threads; tiles are taken 4096 at a time: an exclusive scan
+// of their popcounts gives each tile's output offset, then every position is placed.
 constexpr int kCompactTiles = 4096;
 __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, int B, const int *__restrict__ ids_in,
-                                                  int *__restrict__ ids_out, const int *__restrict__ count_in,
-                                                  int *__restrict__ count_out) {
+                                                  int *__restrict__ ids_out, int *__restrict__ src_out,
+                                                  const int *__restrict__ count_in, int *__restrict__ count_out,
+                                                  int *__restrict__ count_out2) {
   __shared__ int toff[kCompactTiles];
   __shared__ unsigned tmask[kCompactTiles];
   __shared__ int wsum[16];
@@ -170,13 +191,58 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
       const unsigned mk = tmask[tl];
       if ((mk >> b) & 1u) {
         const unsigned below = b == 0 ? 0u : (mk & (0xffffffffu >> (32 - b)));
-        ids_out[toff[tl] + __popc(below)] = ids_in[p];
+        const int o = toff[tl] + __popc(below);
+        ids_out[o] = ids_in[p];
+        if (src_out) src_out[o] = p;
       }
     }
     base += total;
     __syncthreads();
   }
-  if (tid == 0) *count_out = base;
+  if (tid == 0) {
+    *count_out = base;
+    if (count_out2) *count_out2 = base;
+  }
+}
+
+// After a compaction of the global-tile path: move the live positions of a layer's output tiles
+// into fresh tiles, dst[t][k][b] = the value at list position src[32t + b] of the source tiles
+// (tile src / 32, slot src % 32), for positions below *npos; zero past it. 8 threads per 128-byte
+// segment, 4 slots each.
+__global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
+                                                const int *__restrict__ src, const int *__restrict__ npos) {
+  const int R = *npos;
+  const int ntiles = (R + 31) / 32;
+  const size_t items = (size_t)ntiles * N * 8;
+  for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
+    const int qd = (int)(it & 7);
+    const size_t rest = it >> 3;
+    const int k = (int)(rest % N);
+    const int t = (int)(rest / N);
+    float v[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int p = t * 32 + qd * 4 + c;
+      v[c] = 0.0f;
+      if (p < R) {
+        const int sp = src[p];
+        v[c] = sfm[((size_t)(sp >> 5) * N + k) * 32 + (sp & 31)];
+      }
+    }
+    *reinterpret_cast<float4 *>(dfm + ((size_t)t * N + k) * 32 + qd * 4) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+}
+
+// Copy list positions pos[0..n) of feature-major tiles out as rows: out[i][k] = fm at position
+// pos[i], source k.
+__global__ __launch_bounds__(256) void k_gather_rows(const float *__restrict__ fm, int N, const int *__restrict__ pos,
+                                                     int n, float *__restrict__ out) {
+  const size_t items = (size_t)n * N;
+  for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
+    const int i = (int)(it / N), k = (int)(it % N);
+    const int p = pos[i];
+    out[it] = fm[((size_t)(p >> 5) * N + k) * 32 + (p & 31)];
+  }
 }
 
 __global__ void k_final_ids(const int *__restrict__ ids, const int *__restrict__ count, long long *__restrict__ out) {
@@ -399,31 +465,34 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
   }
 }
 
-// One round of a layer gathering from global feature-major tiles of FMR rows: tiles
-// [tile0, tile0 + 8) of the live list, one per XCD. blockDim 256 (4 waves); a work item is a chunk
-// of kGfmOutputs outputs. Lane = (row b = lane % FMR, output slot h = lane / FMR), so a wave
-// instruction reads 64 / FMR segments of FMR * 4 bytes. gridDim must be a multiple of 8:
-// workgroup x runs on XCD x % 8, and the workgroups of XCD x share the output chunks of one tile,
-// which therefore stays in that XCD's L2 (or, for the widest layers, in the Infinity Cache) for
-// the whole launch. With fewer than 8 tiles left, each tile's chunks are split over 8 / ntiles
-// XCDs. For KC > 0 the item's ELL rows are staged in LDS first, so the gathers are the only
-// vector-memory requests of the inner loop.
+// One round of a layer on global feature-major tiles of FMR = 32 rows: input tiles fin[t][k][b]
+// (source k of list position 32t + b), output tiles fout in the same layout and positions; tiles
+// [tile0, tile0 + 8) of the list, one per XCD. blockDim 256 (4 waves); a work item is a chunk of
+// kGfmOutputs = 64 outputs. Lane = (row quad q = lane % 8, output slot h = lane / 8): each gather is
+// one 16-byte load of rows 4q..4q+3 of one source, so a wave instruction fetches the 128-byte
+// source segments of 8 outputs, and every lane runs two outputs' chains (slots h and h + 32 of the
+// chunk's halves) to keep 16 loads in flight; results go out as one 16-byte store per output, so a
+// wave writes 1 KiB of consecutive output segments. gridDim must be a multiple of 8: workgroup x
+// runs on XCD x % 8, and the workgroups of XCD x share the output chunks of one tile, which
+// therefore stays in that XCD's L2 (or, for the widest layers, in the Infinity Cache) for the whole
+// launch. With fewer than 8 tiles left, each tile's chunks are split over 8 / ntiles XCDs. For
+// KC > 0 the chunk's ELL rows are staged in LDS first, so the gathers are the only vector-memory
+// reads of the inner loop. Slots past the list's end hold zeros in fin and get zeros in fout.
 template <int FMR, int KC>
-__global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm, float *__restrict__ yout, int N,
+__global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
                                                    const float *__restrict__ bias, float ymax,
-                                                   const int *__restrict__ ids, const int *__restrict__ count,
-                                                   unsigned *__restrict__ masks, int tile0) {
+                                                   const int *__restrict__ npos, unsigned *__restrict__ masks,
+                                                   int tile0) {
+  static_assert(FMR == 32, "the lane layout covers 32 rows with 8 lanes of float4");
+  static_assert(KC % 8 == 0, "KC must be a multiple of 8");
   constexpr int KS = KC > 0 ? KC : 1;
-  constexpr int OPI = 64 / FMR;             // outputs per wave instruction
-  constexpr int PER_ROUND = 4 * OPI;        // outputs per workgroup round
-  static_assert(KC % 16 == 0, "KC must be a multiple of 16");
-  static_assert(kGfmOutputs % PER_ROUND == 0, "chunk must be whole rounds");
-  __shared__ float stage[FMR][kGfmOutputs + 1];
+  constexpr int HALF = 32;  // outputs per pass of the 4 waves (8 each)
+  static_assert(kGfmOutputs == 2 * HALF, "two outputs per lane");
   __shared__ int2 ells2[kGfmOutputs * KS];
   __shared__ float bstage[kGfmOutputs];
-  __shared__ int rowlive[FMR];
-  const int R = *count;
+  __shared__ unsigned rowmask;
+  const int R = *npos;
   const int nt = min(8, (R + FMR - 1) / FMR - tile0);  // tiles in this round
   if (nt <= 0) return;
   const int parts = 8 / nt;
@@ -434,17 +503,17 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = min(nchunks, cbeg + cpp);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int b = lane % FMR, h = lane / FMR;
+  const int q = lane & 7, h = lane >> 3;
   const int per_xcd = gridDim.x >> 3;
-  if (tid < FMR) rowlive[tid] = 0;
-  __syncthreads();
+  const int nvalid = min(FMR, R - t * FMR);
+  const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
+  float *obase = fout + (size_t)t * N * FMR + q * 4;
+  const int jA = wave * 8 + h, jB = jA + HALF;
+  if (tid == 0) rowmask = 0u;
+  unsigned lm = 0u;  // live rows seen by this lane: bit 4q + c
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
-    const int p0 = t * FMR;
-    const int nvalid = min(FMR, R - p0);
     const int c0 = chunk * kGfmOutputs;
     const int nout = min(kGfmOutputs, N - c0);
-    const char *tbase = reinterpret_cast<const char *>(fm + (size_t)t * N * FMR);
-    const unsigned boff = (unsigned)b * 4u;
     // stage this chunk's biases (and, for KC > 0, its ELL entries as [slot][output]); the ELL is
     // read once per tile, streamed so it does not displace the tile from L2
     for (int i = tid; i < kGfmOutputs; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
@@ -457,84 +526,82 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fm,
       }
     }
     __syncthreads();
-    bool live = false;
+    float aA[4] = {0.0f, 0.0f, 0.0f, 0.0f}, aB[4] = {0.0f, 0.0f, 0.0f, 0.0f};
     if constexpr (KC > 0) {
-      // two outputs per lane at a time: 32 gathers in flight, each chain in ascending order
-      static_assert((kGfmOutputs / PER_ROUND) % 2 == 0, "rounds come in pairs");
-      for (int i = 0; i < kGfmOutputs / PER_ROUND; i += 2) {
-        const int jA = i * PER_ROUND + wave * OPI + h, jB = jA + PER_ROUND;
-        const bool okA = c0 + jA < N, okB = c0 + jB < N;
-        const int2 *eA = ells2 + jA, *eB = ells2 + jB;
-        float aA = 0.0f, aB = 0.0f;
 #pragma unroll 1
-        for (int g = 0; g < KC; g += 16) {
-          int2 evA[16], evB[16];
+      for (int g = 0; g < KC; g += 8) {
+        int2 evA[8], evB[8];
 #pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            evA[q] = eA[(g + q) * kGfmOutputs];
-            evB[q] = eB[(g + q) * kGfmOutputs];
-          }
-          float gA[16], gB[16];
-#pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            gA[q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)evA[q].x));
-            gB[q] = *reinterpret_cast<const float *>(tbase + (boff + (unsigned)evB[q].x));
-          }
-#pragma unroll
-          for (int q = 0; q < 16; ++q) {
-            aA = fmaf(gA[q], __int_as_float(evA[q].y), aA);
-            aB = fmaf(gB[q], __int_as_float(evB[q].y), aB);
-          }
+        for (int i = 0; i < 8; ++i) {
+          evA[i] = ells2[(g + i) * kGfmOutputs + jA];
+          evB[i] = ells2[(g + i) * kGfmOutputs + jB];
         }
-        if (okA) {
-          const float y = activate(aA, bstage[jA], ymax);
-          stage[b][jA] = y;
-          live |= (y > 0.0f);
+        float4 gA[8], gB[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          gA[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)evA[i].x);
+          gB[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)evB[i].x);
         }
-        if (okB) {
-          const float y = activate(aB, bstage[jB], ymax);
-          stage[b][jB] = y;
-          live |= (y > 0.0f);
+        // keep all 16 gathers in flight before the first fma waits on one
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float wA = __int_as_float(evA[i].y), wB = __int_as_float(evB[i].y);
+          aA[0] = fmaf(gA[i].x, wA, aA[0]);
+          aA[1] = fmaf(gA[i].y, wA, aA[1]);
+          aA[2] = fmaf(gA[i].z, wA, aA[2]);
+          aA[3] = fmaf(gA[i].w, wA, aA[3]);
+          aB[0] = fmaf(gB[i].x, wB, aB[0]);
+          aB[1] = fmaf(gB[i].y, wB, aB[1]);
+          aB[2] = fmaf(gB[i].z, wB, aB[2]);
+          aB[3] = fmaf(gB[i].w, wB, aB[3]);
         }
       }
     } else {
-      for (int i = 0; i < kGfmOutputs / PER_ROUND; ++i) {
-        const int jj = i * PER_ROUND + wave * OPI + h;
-        const int j = c0 + jj;
-        if (j < N) {
-          float a = 0.0f;
-          for (int s2 = 0; s2 < K; ++s2) {
-            const int2 p = ell[(size_t)s2 * N + j];
-            a = fmaf(*reinterpret_cast<const float *>(tbase + (boff + (unsigned)p.x)), __int_as_float(p.y), a);
-          }
-          const float y = activate(a, bstage[jj], ymax);
-          stage[b][jj] = y;
-          live |= (y > 0.0f);
-        }
+      const int2 *eA = ell + c0 + min(jA, nout - 1), *eB = ell + c0 + min(jB, nout - 1);
+      for (int sl = 0; sl < K; ++sl) {
+        const int2 pA = eA[(size_t)sl * N], pB = eB[(size_t)sl * N];
+        const float4 vA = *reinterpret_cast<const float4 *>(tbase + (unsigned)pA.x);
+        const float4 vB = *reinterpret_cast<const float4 *>(tbase + (unsigned)pB.x);
+        const float wA = __int_as_float(pA.y), wB = __int_as_float(pB.y);
+        aA[0] = fmaf(vA.x, wA, aA[0]);
+        aA[1] = fmaf(vA.y, wA, aA[1]);
+        aA[2] = fmaf(vA.z, wA, aA[2]);
+        aA[3] = fmaf(vA.w, wA, aA[3]);
+        aB[0] = fmaf(vB.x, wB, aB[0]);
+        aB[1] = fmaf(vB.y, wB, aB[1]);
+        aB[2] = fmaf(vB.z, wB, aB[2]);
+        aB[3] = fmaf(vB.w, wB, aB[3]);
       }
     }
-    if (live && b < nvalid) rowlive[b] = 1;
-    __syncthreads();
-    // write the staged block row by row: 256 / FMR threads per row
-    {
-      constexpr int TPR = 256 / FMR, PER = kGfmOutputs / TPR;
-      const int rb = tid / TPR, seg = (tid % TPR) * PER;
-      if (rb < nvalid) {
-        float *dst = yout + (size_t)ids[p0 + rb] * N + c0 + seg;
-#pragma unroll
-        for (int x = 0; x < PER; ++x)
-          if (seg + x < nout) __builtin_nontemporal_store(stage[rb][seg + x], dst + x);
-      }
+    if (jA < nout) {
+      const float b = bstage[jA];
+      const float4 y = make_float4(activate(aA[0], b, ymax), activate(aA[1], b, ymax), activate(aA[2], b, ymax),
+                                   activate(aA[3], b, ymax));
+      store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jA) * FMR), y);
+      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u)) << (4 * q);
     }
-    if (tid < 64) {
-      const unsigned long long m = __ballot(tid < nvalid && rowlive[tid] != 0);
-      if (tid == 0 && m) atomicOr(&masks[t], (unsigned)m);
+    if (jB < nout) {
+      const float b = bstage[jB];
+      const float4 y = make_float4(activate(aB[0], b, ymax), activate(aB[1], b, ymax), activate(aB[2], b, ymax),
+                                   activate(aB[3], b, ymax));
+      store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jB) * FMR), y);
+      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u)) << (4 * q);
     }
-    __syncthreads();
-    if (tid < FMR) rowlive[tid] = 0;
     __syncthreads();
   }
+  // rows of this tile that stayed live in any of this workgroup's chunks
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+  if (lane == 0 && lm) atomicOr(&rowmask, lm);
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
+    if (rowmask & valid) atomicOr(&masks[t], rowmask & valid);
+  }
 }
+
+constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 128 registers each
 
 template <int T>
 struct BitWord;
@@ -600,17 +667,19 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
 }
 
 // Layer 0 from bit tiles of T rows (T = 16 or 32): every term is fma(bit, w, acc) with bit 0 or 1,
-// the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim 1024. LDS holds
+// the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim kBitsThreads. LDS holds
 // the tile's N words and a 16-entry table that turns 4 bits into 4 floats. Lane = output j; each
-// lane carries the T rows of its output, so one ELL entry and one word serve T edge-rows, and the
-// stores of one row are 64 consecutive outputs.
-template <int T>
-__global__ __launch_bounds__(1024) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
-                                                     float *__restrict__ yout, int N, const int2 *__restrict__ ell,
-                                                     int K, int ell_shift, const float *__restrict__ bias,
-                                                     float ymax, const int *__restrict__ ids,
-                                                     const int *__restrict__ count, unsigned *__restrict__ masks,
-                                                     int B) {
+// lane carries the T rows of its output, so one ELL entry and one word serve T edge-rows. Results
+// go to feature-major tiles of 32 rows (list position p at tile p / 32, slot p % 32): a lane writes
+// its T rows of output j as T / 4 16-byte stores. Slots past the list's end get zeros.
+// word_shift turns an ELL source offset into the byte offset of the source's word in the tile.
+// KC = 32: the 32 ELL entries of a lane's output are all loaded before the first term is used.
+template <int T, int KC>
+__global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
+                                                     float *__restrict__ fout, int N, const int2 *__restrict__ ell,
+                                                     int K, int word_shift, const float *__restrict__ bias,
+                                                     float ymax, const int *__restrict__ count,
+                                                     unsigned *__restrict__ masks) {
   using W = typename BitWord<T>::type;
   // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), then the tile
   extern __shared__ float4 smem[];
@@ -653,29 +722,87 @@ __global__ __launch_bounds__(1024) void k_layer_bits(const typename BitWord<T>::
       float acc[T];
 #pragma unroll
       for (int b = 0; b < T; ++b) acc[b] = 0.0f;
-#pragma unroll 4
-      for (int sl = 0; sl < K; ++sl) {
-        const int2 e = ej[(size_t)sl * N];
-        const unsigned word = *reinterpret_cast<const W *>(tb + (size_t)(e.x >> ell_shift) * sizeof(W));
-        const float wv = __int_as_float(e.y);
+      // one term: the source's word gives the T input bits; each nibble picks 4 floats (0 or 1)
+      auto term = [&](unsigned word, float wv) {
+        float4 v[T / 4];
+#pragma unroll
+        for (int n = 0; n < T / 4; ++n) v[n] = lut[(word >> (4 * n)) & 15u];
 #pragma unroll
         for (int n = 0; n < T / 4; ++n) {
-          const float4 v = lut[(word >> (4 * n)) & 15u];
-          acc[4 * n] = fmaf(v.x, wv, acc[4 * n]);
-          acc[4 * n + 1] = fmaf(v.y, wv, acc[4 * n + 1]);
-          acc[4 * n + 2] = fmaf(v.z, wv, acc[4 * n + 2]);
-          acc[4 * n + 3] = fmaf(v.w, wv, acc[4 * n + 3]);
+          acc[4 * n] = fmaf(v[n].x, wv, acc[4 * n]);
+          acc[4 * n + 1] = fmaf(v[n].y, wv, acc[4 * n + 1]);
+          acc[4 * n + 2] = fmaf(v[n].z, wv, acc[4 * n + 2]);
+          acc[4 * n + 3] = fmaf(v[n].w, wv, acc[4 * n + 3]);
+        }
+      };
+      if constexpr (KC > 0) {
+        // slots go in groups of 16 with the issue order pinned by scheduling barriers: a group's
+        // tile words are read while the next group's ELL entries load, then its terms run
+        static_assert(KC % 16 == 0, "KC must be a multiple of 16");
+        int2 e[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) e[i] = ej[(size_t)i * N];
+#pragma unroll
+        for (int h = 0; h < KC; h += 16) {
+          mem_fence_compiler();
+          unsigned wd[16];
+          float wv[16];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            wd[i] = *reinterpret_cast<const W *>(tb + (e[i].x >> word_shift));
+            wv[i] = __int_as_float(e[i].y);
+          }
+          if (h + 16 < KC) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) e[i] = ej[(size_t)(h + 16 + i) * N];
+          }
+          mem_fence_compiler();
+          // table reads run one term ahead of the fmas
+          float4 vc[T / 4], vn[T / 4];
+#pragma unroll
+          for (int n = 0; n < T / 4; ++n) vc[n] = lut[(wd[0] >> (4 * n)) & 15u];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            if (i + 1 < 16) {
+#pragma unroll
+              for (int n = 0; n < T / 4; ++n) vn[n] = lut[(wd[i + 1] >> (4 * n)) & 15u];
+            }
+#pragma unroll
+            for (int n = 0; n < T / 4; ++n) {
+              acc[4 * n] = fmaf(vc[n].x, wv[i], acc[4 * n]);
+              acc[4 * n + 1] = fmaf(vc[n].y, wv[i], acc[4 * n + 1]);
+              acc[4 * n + 2] = fmaf(vc[n].z, wv[i], acc[4 * n + 2]);
+              acc[4 * n + 3] = fmaf(vc[n].w, wv[i], acc[4 * n + 3]);
+              vc[n] = vn[n];
+            }
+            // this term's fmas complete here, and the next table reads are issued after them
+#pragma unroll
+            for (int b = 0; b < T; b += 4) pin4(acc[b], acc[b + 1], acc[b + 2], acc[b + 3]);
+            mem_fence_compiler();
+          }
+        }
+      } else {
+        for (int sl = 0; sl < K; ++sl) {
+          const int2 e = ej[(size_t)sl * N];
+          term(*reinterpret_cast<const W *>(tb + (e.x >> word_shift)), __int_as_float(e.y));
         }
       }
       if (jin) {
+        // rows past nvalid have all-zero bits, so their outputs are zeros
         const float bj = bias[j];
+        float4 *dst = reinterpret_cast<float4 *>(fout + ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
 #pragma unroll
-        for (int b = 0; b < T; ++b) {
-          if (b < nvalid) {
-            const float y = activate(acc[b], bj, ymax);
-            yout[(size_t)ids[p0 + b] * N + j] = y;
-            live |= (y > 0.0f ? 1u : 0u) << b;
-          }
+        for (int n = 0; n < T / 4; ++n) {
+          const float4 y = make_float4(activate(acc[4 * n], bj, ymax), activate(acc[4 * n + 1], bj, ymax),
+                                       activate(acc[4 * n + 2], bj, ymax), activate(acc[4 * n + 3], bj, ymax));
+          dst[n] = y;
+          live |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u))
+                  << (4 * n);
+        }
+        if (T == 16 && (p0 & 31) == 0 && t + 1 == ntiles) {
+          // the last 32-row tile has no second half: zero its slots 16..31
+#pragma unroll
+          for (int n = 0; n < 4; ++n) dst[4 + n] = make_float4(0.f, 0.f, 0.f, 0.f);
         }
       }
     }
@@ -684,11 +811,8 @@ __global__ __launch_bounds__(1024) void k_layer_bits(const typename BitWord<T>::
     if (tid == 0) {
       unsigned m = tilemask;
       tilemask = 0u;
-      while (m) {
-        const int bb = __ffs(m) - 1;
-        m &= m - 1u;
-        atomicOr(&masks[(p0 + bb) / B], 1u << ((p0 + bb) % B));
-      }
+      m &= nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
+      if (m) atomicOr(&masks[p0 >> 5], m << (p0 & 31));
     }
     __syncthreads();
   }
@@ -722,16 +846,18 @@ struct sdnn_net {
   int64_t M = 0;
   hipStream_t stream = nullptr;
   char *ws = nullptr;
-  float *ybuf[2] = {nullptr, nullptr};
-  float *fm = nullptr;
-  int *ids[2] = {nullptr, nullptr};
+  float *ybuf[2] = {nullptr, nullptr};  // path 0: row-major activations
+  float *fm[2] = {nullptr, nullptr};    // path 1: feature-major tiles of 32 list positions
+  int *ids[2] = {nullptr, nullptr};     // live lists: row id per position
+  int *src[2] = {nullptr, nullptr};     // path 1: position in the previous list, per position
   unsigned *masks = nullptr;  // per-tile liveness bits
   int *rownz = nullptr, *counts = nullptr;
-  int *misc = nullptr;  // device flags: [0] a layer-0 input is not 0 or 1
+  int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [4 + i] positions in list i
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
-  const float *final_y = nullptr;
+  const float *final_y = nullptr;   // path 0: final activations, row-major by row id
+  const float *final_fm = nullptr;  // path 1: final activation tiles; live row i is at position src[final_list][i]
   int32_t *pinned = nullptr; // read-back slots (0-3: polling ring, 6: input-not-binary flag, 7: exact count)
   std::vector<hipEvent_t> events;
   // profiling
@@ -754,21 +880,23 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t ybuf[2], fm, ids[2], masks, rownz, counts, misc, final_ids, total;
+  size_t act[2], ids[2], src[2], masks, rownz, counts, misc, final_ids, total;
 };
 
+// Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
 WsLayout layout_for(const sdnn_net *net, int64_t M) {
   WsLayout w{};
   const size_t a = 256;
   size_t off = 0;
-  const size_t ybytes = align_up((size_t)M * (size_t)net->N * sizeof(float), a);
-  w.ybuf[0] = off; off += ybytes;
-  w.ybuf[1] = off; off += ybytes;
-  w.fm = off;
-  if (net->path == 1) off += align_up((size_t)((M + net->B - 1) / net->B) * net->B * (size_t)net->N * sizeof(float), a);
+  const size_t rows = net->path == 1 ? (size_t)((M + 31) / 32) * 32 : (size_t)M;
+  const size_t ybytes = align_up(rows * (size_t)net->N * sizeof(float), a);
+  w.act[0] = off; off += ybytes;
+  w.act[1] = off; off += ybytes;
   const size_t ib = align_up((size_t)std::max<int64_t>(M, 1) * sizeof(int), a);
   w.ids[0] = off; off += ib;
   w.ids[1] = off; off += ib;
+  w.src[0] = off; off += ib;
+  w.src[1] = off; off += ib;
   w.masks = off; off += ib;
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
@@ -808,74 +936,80 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
   return launch_lds<B, 0>(net, yin, yout, ld, ids, count, rownz);
 }
 
-template <int FMR>
-hipError_t launch_gfm(sdnn_net *net, const float *yin, float *yout, const LayerDev &ld, const int *ids,
-                      const int *count, int *rownz, int rounds) {
-  hipLaunchKernelGGL(k_to_fm<FMR>, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, net->fm, net->N, ids, count,
-                     rownz);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+// One layer of the global-tile path: ceil(tiles / 8) launches of 8 tiles each (rounds), reading fin
+// and writing fout at the same list positions; *npos is the list length.
+hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos, int rounds) {
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm<FMR, 32>), dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout, net->N,
-                         ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm<32, 32>), dim3(net->cus * 8), dim3(256), 0, net->stream, fin, fout, net->N,
+                         ld.ell, ld.K, ld.bias, net->ymax, npos, net->masks, r * 8);
     else
-      hipLaunchKernelGGL((k_layer_gfm<FMR, 0>), dim3(net->cus * 8), dim3(256), 0, net->stream, net->fm, yout,
-                         net->N, ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, r * 8);
-    e = hipGetLastError();
+      hipLaunchKernelGGL((k_layer_gfm<32, 0>), dim3(net->cus * 8), dim3(256), 0, net->stream, fin, fout, net->N,
+                         ld.ell, ld.K, ld.bias, net->ymax, npos, net->masks, r * 8);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
+hipError_t launch_to_fm(sdnn_net *net, const float *y, float *fm, const int *ids, const int *count, int *rownz) {
+  hipLaunchKernelGGL(k_to_fm<32>, dim3(net->cus * 8), dim3(256), 0, net->stream, y, fm, net->N, ids, count, rownz);
+  return hipGetLastError();
+}
+
 template <int T>
-size_t bits_lds_bytes(const sdnn_net *net, int) {
+size_t bits_lds_bytes(const sdnn_net *net) {
   using W = typename BitWord<T>::type;
   return 17 * 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
 }
 
 template <int T>
-hipError_t launch_pack_bits(sdnn_net *net, const float *yin, const int *ids, const int *count) {
+hipError_t launch_pack_bits(sdnn_net *net, const float *yin, void *bits, const int *ids, const int *count) {
   using W = typename BitWord<T>::type;
-  hipLaunchKernelGGL(k_pack_bits<T>, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, reinterpret_cast<W *>(net->fm),
+  hipLaunchKernelGGL(k_pack_bits<T>, dim3(net->cus * 8), dim3(256), 0, net->stream, yin, reinterpret_cast<W *>(bits),
                      net->N, ids, count, net->rownz, net->misc);
   return hipGetLastError();
 }
 
-template <int T>
-hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, float *yout, const int *ids, const int *count) {
+template <int T, int KC>
+hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count) {
   using W = typename BitWord<T>::type;
   static bool configured = false;
   if (!configured) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T, KC>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     configured = true;
   }
-  const size_t lds = bits_lds_bytes<T>(net, ld.K);
-  const int per_cu = lds <= 72 * 1024 ? 2 : 1;
+  // one workgroup per CU: 16 waves at up to 128 registers fill the register file
+  const size_t lds = bits_lds_bytes<T>(net);
+  const int per_cu = 1;
+  // ELL source offsets are k * 32 * 4 bytes (32-row fp32 tiles); a word sits at k * sizeof(W)
   int shift = 0;
-  while ((1 << shift) < net->B * (int)sizeof(float)) ++shift;
-  hipLaunchKernelGGL(k_layer_bits<T>, dim3(net->cus * per_cu), dim3(1024), lds, net->stream,
-                     reinterpret_cast<const W *>(net->fm), yout, net->N, ld.ell, ld.K, shift, ld.bias, net->ymax, ids,
-                     count, net->masks, net->B);
+  while ((1 << shift) < 32 * (int)sizeof(float)) ++shift;
+  int wshift = 0;
+  while ((1 << wshift) < (int)sizeof(W)) ++wshift;
+  hipLaunchKernelGGL((k_layer_bits<T, KC>), dim3(net->cus * per_cu), dim3(kBitsThreads), lds, net->stream,
+                     reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, shift - wshift, ld.bias, net->ymax,
+                     count, net->masks);
   return hipGetLastError();
 }
 
-// rounds: launches of the global-tile kernel (8 tiles each) the live count needs; 1 when the
-// count is known to fit in one round.
+template <int T>
+hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count) {
+  if (ld.K == 32) return launch_layer_bits_k<T, 32>(net, ld, bits, fout, count);
+  return launch_layer_bits_k<T, 0>(net, ld, bits, fout, count);
+}
+
+// One layer of the LDS-tile path.
 hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count,
-                        int rounds, int *rownz) {
+                        int *rownz) {
   const LayerDev &ld = net->layers[l];
-  if (net->path == 0) {
-    switch (net->B) {
-      case 32: return launch_lds_k<32>(net, yin, yout, ld, ids, count, rownz);
-      case 16: return launch_lds_k<16>(net, yin, yout, ld, ids, count, rownz);
-      default: return launch_lds_k<8>(net, yin, yout, ld, ids, count, rownz);
-    }
+  switch (net->B) {
+    case 32: return launch_lds_k<32>(net, yin, yout, ld, ids, count, rownz);
+    case 16: return launch_lds_k<16>(net, yin, yout, ld, ids, count, rownz);
+    default: return launch_lds_k<8>(net, yin, yout, ld, ids, count, rownz);
   }
-  if (net->B == 16) return launch_gfm<16>(net, yin, yout, ld, ids, count, rownz, rounds);
-  return launch_gfm<32>(net, yin, yout, ld, ids, count, rownz, rounds);
 }
 
 }  // namespace
@@ -1020,6 +1154,152 @@ size_t sdnn_workspace_bytes(const sdnn_net *net, int64_t n_rows) {
   return layout_for(net, n_rows).total;
 }
 
+namespace {
+
+// Read-back ring for the live count: every kPollEvery layers the count is copied to pinned host
+// memory behind an event; the host checks it two chunks later, so the stream never drains while
+// the host waits.
+struct PollRing {
+  int slot[4], bound[4], n = 0, head = 0, next = 0;
+};
+
+// Enqueue a poll of counts[l + 1] after layer l (every kPollEvery layers) and consume polls that are
+// two chunks old. *live_bound receives the smallest count seen; returns false on a HIP error.
+hipError_t poll_step(sdnn_net *net, PollRing &ring, int32_t l, int64_t *live_bound) {
+  hipStream_t s = net->stream;
+  if ((l + 1) % kPollEvery != 0 || l + 1 >= net->L) return hipSuccess;
+  const int slot = ring.next;
+  ring.next = (ring.next + 1) % 4;
+  hipError_t e = hipMemcpyAsync(net->pinned + slot, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return e;
+  e = hipEventRecord(net->events[(size_t)slot], s);
+  if (e != hipSuccess) return e;
+  ring.slot[(ring.head + ring.n) % 4] = slot;
+  ring.bound[(ring.head + ring.n) % 4] = l + 1;
+  ++ring.n;
+  while (ring.n > 2) {
+    const int sl = ring.slot[ring.head];
+    e = hipEventSynchronize(net->events[(size_t)sl]);
+    if (e != hipSuccess) return e;
+    ring.head = (ring.head + 1) % 4;
+    --ring.n;
+    *live_bound = std::min<int64_t>(*live_bound, net->pinned[sl]);
+  }
+  return hipSuccess;
+}
+
+// LDS-tile path: row-major activations ping-pong between two buffers; the live list is compacted
+// after every layer.
+sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
+  hipStream_t s = net->stream;
+  const float *yin = y0;
+  int cur = 0;
+  int32_t l = 0;
+  int64_t live_bound = M;
+  PollRing ring;
+  for (; l < net->L && live_bound > 0; ++l) {
+    float *yout = net->ybuf[l & 1];
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B, net->ids[cur], net->ids[cur ^ 1],
+                       (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr);
+    HIP_OR_POISON(net, hipGetLastError());
+    cur ^= 1;
+    yin = yout;
+    HIP_OR_POISON(net, poll_step(net, ring, l, &live_bound));
+  }
+  net->layers_run = l;
+  net->final_list = cur;
+  net->final_y = (l == net->L && net->L > 0) ? net->ybuf[(net->L - 1) & 1] : nullptr;
+  net->final_fm = nullptr;
+  return SDNN_OK;
+}
+
+// Global-tile path: activations stay in feature-major tiles of 32 list positions from layer to
+// layer. After every layer the live list is compacted (ids plus each live row's old position); the
+// tiles are repacked to the compacted list only when that saves tiles, otherwise the next layer
+// runs on the old positions, where rows that died hold zeros and stay zero.
+sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
+  hipStream_t s = net->stream;
+  int *npos = net->misc + kNposSlot;  // npos[i]: positions in list i
+  const int64_t one_round = 8 * 32;
+  auto tiles = [](int64_t r) { return (r + 31) / 32; };
+  int cur = 0;
+  int64_t P = M;           // host bound on the positions of list cur (exact after a read-back)
+  int64_t live_bound = M;  // host bound on the live rows
+  const float *fin = nullptr;
+  float *fout = nullptr;
+  int last_list = 0;
+  PollRing ring;
+  int32_t l = 0;
+  for (; l < net->L && live_bound > 0; ++l) {
+    const int rounds = (int)((tiles(P) + 7) / 8);
+    fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
+    if (l == 0) {
+      // layer 0 reads the caller's rows; binary inputs go through bit tiles (built in fm[0]),
+      // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
+      const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 &&
+                            (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <= 160 * 1024;
+      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[0], s));
+      bool bits_route = false;
+      if (try_bits) {
+        HIP_OR_POISON(net, net->bitsT == 32 ? launch_pack_bits<32>(net, y0, net->fm[0], net->ids[cur], npos + cur)
+                                            : launch_pack_bits<16>(net, y0, net->fm[0], net->ids[cur], npos + cur));
+        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 6, net->misc, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        HIP_OR_POISON(net, hipStreamSynchronize(s));
+        bits_route = net->pinned[6] == 0;
+      }
+      if (bits_route) {
+        HIP_OR_POISON(net, net->bitsT == 32 ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur)
+                                            : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur));
+      } else {
+        HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, try_bits ? nullptr : net->rownz));
+        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, rounds));
+      }
+    } else {
+      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+      HIP_OR_POISON(net, launch_gfm(net, net->layers[(size_t)l], fin, fout, npos + cur, rounds));
+    }
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, 32, net->ids[cur], net->ids[cur ^ 1],
+                       net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
+    HIP_OR_POISON(net, hipGetLastError());
+    last_list = cur ^ 1;
+    // adopt the compacted list? With many positions the exact count is read back (the next layer
+    // is large, so the wait is short relative to it); with few, the polled bound decides.
+    bool adopt;
+    if (P > one_round) {
+      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      HIP_OR_POISON(net, hipStreamSynchronize(s));
+      live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
+      adopt = live_bound == 0 || tiles(live_bound) * 20 <= tiles(P) * 19;
+    } else {
+      adopt = tiles(live_bound) < tiles(P);
+    }
+    if (adopt && live_bound > 0 && l + 1 < net->L) {
+      float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
+      const int64_t items = tiles(live_bound) * net->N * 8;
+      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+      hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1));
+      HIP_OR_POISON(net, hipGetLastError());
+      fin = dst;
+      cur ^= 1;
+      P = live_bound;
+    } else {
+      fin = fout;
+    }
+    HIP_OR_POISON(net, poll_step(net, ring, l, &live_bound));
+  }
+  net->layers_run = l;
+  net->final_list = last_list;
+  net->final_y = nullptr;
+  net->final_fm = (l == net->L && net->L > 0) ? fout : nullptr;
+  return SDNN_OK;
+}
+
+}  // namespace
+
 sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
                        void *hip_stream) {
   sdnn_status st = check_usable(net);
@@ -1045,11 +1325,13 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->M = n_rows;
   net->stream = reinterpret_cast<hipStream_t>(hip_stream);
   net->ws = ws;
-  net->ybuf[0] = reinterpret_cast<float *>(ws + w.ybuf[0]);
-  net->ybuf[1] = reinterpret_cast<float *>(ws + w.ybuf[1]);
-  net->fm = reinterpret_cast<float *>(ws + w.fm);
-  net->ids[0] = reinterpret_cast<int *>(ws + w.ids[0]);
-  net->ids[1] = reinterpret_cast<int *>(ws + w.ids[1]);
+  for (int i = 0; i < 2; ++i) {
+    float *act = reinterpret_cast<float *>(ws + w.act[i]);
+    net->ybuf[i] = net->path == 0 ? act : nullptr;
+    net->fm[i] = net->path == 1 ? act : nullptr;
+    net->ids[i] = reinterpret_cast<int *>(ws + w.ids[i]);
+    net->src[i] = reinterpret_cast<int *>(ws + w.src[i]);
+  }
   net->masks = reinterpret_cast<unsigned *>(ws + w.masks);
   net->rownz = reinterpret_cast<int *>(ws + w.rownz);
   net->counts = reinterpret_cast<int *>(ws + w.counts);
@@ -1062,82 +1344,10 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
                      net->ids[0], net->masks, net->rownz, net->counts, net->misc, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
-
-  const float *yin = y0;
-  int cur = 0;
-  int32_t l = 0;
-  // Upper bound of the live count known on the host (rows only die). The global-tile path needs
-  // the exact count before a layer with more than one round of tiles: it reads it back then,
-  // which costs one stream synchronization per such (large) layer.
-  int64_t known = M;
-  const int64_t one_round = 8 * (int64_t)net->B;
-  // read-back ring: (event slot, layer boundary) of chunks not yet checked
-  int ring_slot[4], ring_bound[4], ring_n = 0, ring_head = 0, next_slot = 0;
-  bool all_dead = (M == 0);
-  for (; l < net->L && !all_dead; ++l) {
-    float *yout = net->ybuf[l & 1];
-    int *rownz = (l == 0) ? net->rownz : nullptr;
-    int rounds = 1;
-    bool bits_route = false;
-    const bool try_bits = l == 0 && net->bitsT > 0 && net->layers[0].K <= 32 &&
-                          (net->bitsT == 32 ? bits_lds_bytes<32>(net, 32) : bits_lds_bytes<16>(net, 32)) <= 160 * 1024;
-    if (try_bits) {
-      // layer 0 of a wide network: pack the inputs to bits (this also finds the nonzero rows), then
-      // read back whether every input was 0 or 1
-      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-      HIP_OR_POISON(net, net->bitsT == 32 ? launch_pack_bits<32>(net, yin, net->ids[cur], net->counts)
-                                          : launch_pack_bits<16>(net, yin, net->ids[cur], net->counts));
-      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 6, net->misc, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-      HIP_OR_POISON(net, hipStreamSynchronize(s));
-      bits_route = net->pinned[6] == 0;
-      rownz = nullptr;
-      if (bits_route) {
-        HIP_OR_POISON(net, net->bitsT == 32 ? launch_layer_bits<32>(net, net->layers[0], yout, net->ids[cur], net->counts)
-                                            : launch_layer_bits<16>(net, net->layers[0], yout, net->ids[cur], net->counts));
-      } else {
-        rounds = (int)((((int64_t)M + net->B - 1) / net->B + 7) / 8);
-        HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds, rownz));
-      }
-    } else {
-      if (net->path == 1 && known > one_round) {
-        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-        HIP_OR_POISON(net, hipStreamSynchronize(s));
-        const int32_t r = net->pinned[7];
-        known = r;
-        if (r == 0) { all_dead = true; break; }
-        rounds = (int)((((int64_t)r + net->B - 1) / net->B + 7) / 8);
-      }
-      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-      HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, rounds, rownz));
-    }
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B,
-                       net->ids[cur], net->ids[cur ^ 1], net->counts + l, net->counts + l + 1);
-    HIP_OR_POISON(net, hipGetLastError());
-    cur ^= 1;
-    yin = yout;
-    if ((l + 1) % kPollEvery == 0 && l + 1 < net->L) {
-      const int slot = next_slot;
-      next_slot = (next_slot + 1) % 4;
-      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + slot, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-      HIP_OR_POISON(net, hipEventRecord(net->events[(size_t)slot], s));
-      ring_slot[(ring_head + ring_n) % 4] = slot;
-      ring_bound[(ring_head + ring_n) % 4] = l + 1;
-      ++ring_n;
-      while (ring_n > 2) {
-        const int sl = ring_slot[ring_head];
-        HIP_OR_POISON(net, hipEventSynchronize(net->events[(size_t)sl]));
-        ring_head = (ring_head + 1) % 4;
-        --ring_n;
-        if (net->pinned[sl] == 0) { all_dead = true; break; }
-      }
-    }
-  }
-  net->layers_run = l;
-  net->final_list = cur;
-  net->final_y = (l == net->L && net->L > 0) ? net->ybuf[(net->L - 1) & 1] : nullptr;
+  st = net->path == 0 ? infer_lds(net, y0, M) : infer_gfm(net, y0, M);
+  if (st != SDNN_OK) return st;
   hipLaunchKernelGGL(k_final_ids, dim3(std::max(1, std::min(net->cus, (M + 255) / 256 + 1))), dim3(256), 0, s,
-                     net->ids[cur], net->counts + l, net->final_ids);
+                     net->ids[net->final_list], net->counts + net->layers_run, net->final_ids);
   HIP_OR_POISON(net, hipGetLastError());
   net->ran = true;
   net->pending_times = net->profiling;
@@ -1200,11 +1410,47 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
   std::vector<long long> live((size_t)std::max(c, 1));
   if (c > 0) HIP_OR_POISON(net, hipMemcpy(live.data(), net->final_ids, (size_t)c * sizeof(long long), hipMemcpyDeviceToHost));
   const size_t rowb = (size_t)net->N * sizeof(float);
+  if (net->path == 0) {
+    for (int64_t q = 0; q < n; ++q) {
+      float *dst = out_host + (size_t)q * net->N;
+      const bool is_live = c > 0 && net->final_y && std::binary_search(live.begin(), live.begin() + c, (long long)ids[q]);
+      if (is_live) HIP_OR_POISON(net, hipMemcpy(dst, net->final_y + (size_t)ids[q] * net->N, rowb, hipMemcpyDeviceToHost));
+      else std::memset(dst, 0, rowb);
+    }
+    g_err.clear();
+    return SDNN_OK;
+  }
+  // global-tile path: live row i sits at position src[final_list][i] of the final tiles; rows are
+  // gathered on the device into the other activation buffer (free after the run), in batches
+  std::vector<int32_t> srcpos((size_t)std::max(c, 1));
+  if (c > 0)
+    HIP_OR_POISON(net, hipMemcpy(srcpos.data(), net->src[net->final_list], (size_t)c * sizeof(int32_t), hipMemcpyDeviceToHost));
+  std::vector<int32_t> pos;
+  std::vector<int64_t> which;
   for (int64_t q = 0; q < n; ++q) {
     float *dst = out_host + (size_t)q * net->N;
-    const bool is_live = c > 0 && net->final_y && std::binary_search(live.begin(), live.begin() + c, (long long)ids[q]);
-    if (is_live) HIP_OR_POISON(net, hipMemcpy(dst, net->final_y + (size_t)ids[q] * net->N, rowb, hipMemcpyDeviceToHost));
-    else std::memset(dst, 0, rowb);
+    std::memset(dst, 0, rowb);
+    if (c == 0 || !net->final_fm) continue;
+    auto it = std::lower_bound(live.begin(), live.begin() + c, (long long)ids[q]);
+    if (it == live.begin() + c || *it != ids[q]) continue;
+    pos.push_back(srcpos[(size_t)(it - live.begin())]);
+    which.push_back(q);
+  }
+  float *scratch = (net->final_fm == net->fm[0]) ? net->fm[1] : net->fm[0];
+  int *dpos = net->ids[net->final_list ^ 1];
+  const int64_t batch = std::max<int64_t>(1, net->M);
+  for (size_t b0 = 0; b0 < pos.size(); b0 += (size_t)batch) {
+    const int nb = (int)std::min<size_t>((size_t)batch, pos.size() - b0);
+    HIP_OR_POISON(net, hipMemcpy(dpos, pos.data() + b0, (size_t)nb * sizeof(int32_t), hipMemcpyHostToDevice));
+    const int64_t items = (int64_t)nb * net->N;
+    const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid), dim3(256), 0, net->stream, net->final_fm, net->N, dpos, nb, scratch);
+    HIP_OR_POISON(net, hipGetLastError());
+    HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
+    std::vector<float> rows((size_t)nb * net->N);
+    HIP_OR_POISON(net, hipMemcpy(rows.data(), scratch, (size_t)nb * rowb, hipMemcpyDeviceToHost));
+    for (int i = 0; i < nb; ++i)
+      std::memcpy(out_host + (size_t)which[b0 + (size_t)i] * net->N, rows.data() + (size_t)i * net->N, rowb);
   }
   g_err.clear();
   return SDNN_OK;

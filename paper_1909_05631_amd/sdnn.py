@@ -90,6 +90,7 @@ class Net:
         L = load_library()
         h = ctypes.c_void_p()
         _check(L.sdnn_create(ctypes.byref(h), n_neurons, n_layers, ymax))
+        self._lib = L  # held so that close() still works while the interpreter shuts down
         self._h = h
         self.n = n_neurons
         self.n_layers = n_layers
@@ -98,7 +99,7 @@ class Net:
 
     def close(self):
         if getattr(self, "_h", None):
-            load_library().sdnn_destroy(self._h)
+            self._lib.sdnn_destroy(self._h)
             self._h = None
 
     def __del__(self):
