@@ -115,13 +115,16 @@ __device__ __forceinline__ bool any_nonzero(float4 v) {
 
 // misc[0]: a layer-0 input is not 0 or 1; misc[kNposSlot + i]: positions in live list i.
 constexpr int kNposSlot = 4;
-__global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, int *__restrict__ rownz,
-                       int *__restrict__ counts, int *__restrict__ misc, int M, int L) {
+__global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsigned *__restrict__ masks2,
+                       unsigned *__restrict__ masks3, int *__restrict__ rownz, int *__restrict__ counts,
+                       int *__restrict__ misc, int M, int L) {
   const int st = gridDim.x * blockDim.x;
   if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = (threadIdx.x == kNposSlot) ? M : 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
     masks[i] = 0u;
+    masks2[i] = 0u;
+    masks3[i] = 0u;
     rownz[i] = 0;
   }
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i <= L; i += st) counts[i] = (i == 0) ? M : 0;
@@ -478,12 +481,18 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
 // launch. With fewer than 8 tiles left, each tile's chunks are split over 8 / ntiles XCDs. For
 // KC > 0 the chunk's ELL rows are staged in LDS first, so the gathers are the only vector-memory
 // reads of the inner loop. Slots past the list's end hold zeros in fin and get zeros in fout.
+//
+// Workgroup 0 of the first round also does the list bookkeeping of the layer sequence: with
+// count_out set (a layer that follows one without compaction) it counts the previous layer's live
+// rows (masks_prev, complete since that kernel ended) into *count_out, and with masks_clear set it
+// clears that buffer, the one the next layer will use (three buffers rotate by layer).
 template <int FMR, int KC>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
-                                                   int tile0) {
+                                                   int tile0, const unsigned *__restrict__ masks_prev,
+                                                   unsigned *__restrict__ masks_clear, int *__restrict__ count_out) {
   static_assert(FMR == 32, "the lane layout covers 32 rows with 8 lanes of float4");
   static_assert(KC % 8 == 0, "KC must be a multiple of 8");
   constexpr int KS = KC > 0 ? KC : 1;
@@ -494,22 +503,34 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   __shared__ unsigned rowmask;
   const int R = *npos;
   const int nt = min(8, (R + FMR - 1) / FMR - tile0);  // tiles in this round
-  if (nt <= 0) return;
-  const int parts = 8 / nt;
+  const int parts = nt > 0 ? 8 / nt : 1;
   const int xcd = blockIdx.x & 7;
-  if (xcd >= nt * parts) return;
+  const bool active = nt > 0 && xcd < nt * parts;  // uniform over the workgroup
   const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
   const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
   const int t = tile0 + xcd / parts;
-  const int cbeg = (xcd % parts) * cpp, cend = min(nchunks, cbeg + cpp);
+  const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q = lane & 7, h = lane >> 3;
   const int per_xcd = gridDim.x >> 3;
-  const int nvalid = min(FMR, R - t * FMR);
+  const int nvalid = active ? min(FMR, R - t * FMR) : 0;
   const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
   float *obase = fout + (size_t)t * N * FMR + q * 4;
   const int jA = wave * 8 + h, jB = jA + HALF;
   if (tid == 0) rowmask = 0u;
+  if (blockIdx.x == 0 && tid < 64 && (count_out || masks_clear)) {
+    const int ntiles = (R + FMR - 1) / FMR;
+    int c = 0;
+    for (int i = tid; i < ntiles; i += 64) {
+      if (count_out) c += __popc(masks_prev[i]);
+      if (masks_clear) masks_clear[i] = 0u;
+    }
+    if (count_out) {
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+      if (tid == 0) *count_out = c;
+    }
+  }
   unsigned lm = 0u;  // live rows seen by this lane: bit 4q + c
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int c0 = chunk * kGfmOutputs;
@@ -596,8 +617,8 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   if (lane == 0 && lm) atomicOr(&rowmask, lm);
   __syncthreads();
   if (tid == 0) {
-    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
-    if (rowmask & valid) atomicOr(&masks[t], rowmask & valid);
+    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);  // 0 when inactive
+    if (active && (rowmask & valid)) atomicOr(&masks[t], rowmask & valid);
   }
 }
 
@@ -850,7 +871,8 @@ struct sdnn_net {
   float *fm[2] = {nullptr, nullptr};    // path 1: feature-major tiles of 32 list positions
   int *ids[2] = {nullptr, nullptr};     // live lists: row id per position
   int *src[2] = {nullptr, nullptr};     // path 1: position in the previous list, per position
-  unsigned *masks = nullptr;  // per-tile liveness bits
+  unsigned *masks = nullptr;               // per-tile liveness bits (path 1: layers l % 3 == 0)
+  unsigned *masks_rot[3] = {nullptr, nullptr, nullptr};  // path 1: layer l uses masks_rot[l % 3]
   int *rownz = nullptr, *counts = nullptr;
   int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [4 + i] positions in list i
   long long *final_ids = nullptr;
@@ -880,7 +902,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks, rownz, counts, misc, final_ids, total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, final_ids, total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -897,7 +919,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.ids[1] = off; off += ib;
   w.src[0] = off; off += ib;
   w.src[1] = off; off += ib;
-  w.masks = off; off += ib;
+  for (int i = 0; i < 3; ++i) { w.masks[i] = off; off += ib; }
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
@@ -937,15 +959,26 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
 }
 
 // One layer of the global-tile path: ceil(tiles / 8) launches of 8 tiles each (rounds), reading fin
-// and writing fout at the same list positions; *npos is the list length.
-hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos, int rounds) {
+// and writing fout at the same list positions; *npos is the list length and max_tiles a host bound
+// on its tiles. With count_out set (one round only) the launch first counts the previous layer's
+// live rows from masks_prev and clears masks_clear.
+hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
+                      int64_t max_tiles, unsigned *masks, const unsigned *masks_prev = nullptr,
+                      unsigned *masks_clear = nullptr, int *count_out = nullptr) {
+  const int rounds = (int)((max_tiles + 7) / 8);
+  // one workgroup per output chunk of a tile's share when the round has fewer than 8 tiles
+  const int nchunks = (net->N + kGfmOutputs - 1) / kGfmOutputs;
+  const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
+  const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
+  const dim3 grid(8 * std::max(1, per_xcd));
   for (int r = 0; r < rounds; ++r) {
+    int *cnt = r == 0 ? count_out : nullptr;
     if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm<32, 32>), dim3(net->cus * 8), dim3(256), 0, net->stream, fin, fout, net->N,
-                         ld.ell, ld.K, ld.bias, net->ymax, npos, net->masks, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm<32, 32>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
     else
-      hipLaunchKernelGGL((k_layer_gfm<32, 0>), dim3(net->cus * 8), dim3(256), 0, net->stream, fin, fout, net->N,
-                         ld.ell, ld.K, ld.bias, net->ymax, npos, net->masks, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm<32, 0>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1163,14 +1196,15 @@ struct PollRing {
   int slot[4], bound[4], n = 0, head = 0, next = 0;
 };
 
-// Enqueue a poll of counts[l + 1] after layer l (every kPollEvery layers) and consume polls that are
-// two chunks old. *live_bound receives the smallest count seen; returns false on a HIP error.
-hipError_t poll_step(sdnn_net *net, PollRing &ring, int32_t l, int64_t *live_bound) {
+// After layer l (every kPollEvery layers), enqueue a poll of counts[idx], a live count known once
+// layer l has finished, and consume polls that are two chunks old. *live_bound receives the
+// smallest count seen.
+hipError_t poll_step(sdnn_net *net, PollRing &ring, int32_t l, int32_t idx, int64_t *live_bound) {
   hipStream_t s = net->stream;
   if ((l + 1) % kPollEvery != 0 || l + 1 >= net->L) return hipSuccess;
   const int slot = ring.next;
   ring.next = (ring.next + 1) % 4;
-  hipError_t e = hipMemcpyAsync(net->pinned + slot, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+  hipError_t e = hipMemcpyAsync(net->pinned + slot, net->counts + idx, sizeof(int32_t), hipMemcpyDeviceToHost, s);
   if (e != hipSuccess) return e;
   e = hipEventRecord(net->events[(size_t)slot], s);
   if (e != hipSuccess) return e;
@@ -1207,7 +1241,7 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;
     yin = yout;
-    HIP_OR_POISON(net, poll_step(net, ring, l, &live_bound));
+    HIP_OR_POISON(net, poll_step(net, ring, l, l + 1, &live_bound));
   }
   net->layers_run = l;
   net->final_list = cur;
@@ -1217,31 +1251,37 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
 }
 
 // Global-tile path: activations stay in feature-major tiles of 32 list positions from layer to
-// layer. After every layer the live list is compacted (ids plus each live row's old position); the
-// tiles are repacked to the compacted list only when that saves tiles, otherwise the next layer
-// runs on the old positions, where rows that died hold zeros and stay zero.
+// layer. Large layers are followed by a compaction of the live list (ids plus each live row's old
+// position); the tiles are repacked to the compacted list only when that saves tiles, otherwise the
+// next layer runs on the old positions, where rows that died hold zeros and stay zero. Small layers
+// (one round of tiles) count their live rows themselves, so a layer is one launch; they are
+// compacted only when the live bound says that fewer tiles would do, and after the last layer.
+// Liveness masks alternate between two buffers by layer parity.
 sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   hipStream_t s = net->stream;
   int *npos = net->misc + kNposSlot;  // npos[i]: positions in list i
   const int64_t one_round = 8 * 32;
   auto tiles = [](int64_t r) { return (r + 31) / 32; };
+  auto masks_for = [net](int32_t layer) { return net->masks_rot[layer % 3]; };
   int cur = 0;
   int64_t P = M;           // host bound on the positions of list cur (exact after a read-back)
   int64_t live_bound = M;  // host bound on the live rows
   const float *fin = nullptr;
   float *fout = nullptr;
   int last_list = 0;
+  bool compacted = true;   // the last layer run has been followed by a compaction
   PollRing ring;
   int32_t l = 0;
   for (; l < net->L && live_bound > 0; ++l) {
-    const int rounds = (int)((tiles(P) + 7) / 8);
+    const bool small = l > 0 && P <= one_round;
+    unsigned *mk = masks_for(l);
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
+    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     if (l == 0) {
       // layer 0 reads the caller's rows; binary inputs go through bit tiles (built in fm[0]),
       // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
       const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 &&
                             (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <= 160 * 1024;
-      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[0], s));
       bool bits_route = false;
       if (try_bits) {
         HIP_OR_POISON(net, net->bitsT == 32 ? launch_pack_bits<32>(net, y0, net->fm[0], net->ids[cur], npos + cur)
@@ -1255,21 +1295,27 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                                             : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur));
       } else {
         HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, try_bits ? nullptr : net->rownz));
-        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, rounds));
+        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk));
       }
     } else {
-      if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-      HIP_OR_POISON(net, launch_gfm(net, net->layers[(size_t)l], fin, fout, npos + cur, rounds));
+      // after a layer without compaction, this launch counts that layer's live rows
+      HIP_OR_POISON(net, launch_gfm(net, net->layers[(size_t)l], fin, fout, npos + cur, tiles(P), mk,
+                                    masks_for(l - 1), masks_for(l + 1), compacted ? nullptr : net->counts + l));
     }
     if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, 32, net->ids[cur], net->ids[cur ^ 1],
-                       net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
-    HIP_OR_POISON(net, hipGetLastError());
-    last_list = cur ^ 1;
-    // adopt the compacted list? With many positions the exact count is read back (the next layer
-    // is large, so the wait is short relative to it); with few, the polled bound decides.
+    auto compact = [&]() -> hipError_t {
+      hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, mk, 32, net->ids[cur], net->ids[cur ^ 1],
+                         net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
+      last_list = cur ^ 1;
+      return hipGetLastError();
+    };
+    compacted = false;
     bool adopt;
-    if (P > one_round) {
+    if (!small) {
+      // a large layer: compact, and read the exact count back (the next layer is large, so the
+      // wait is short relative to it)
+      HIP_OR_POISON(net, compact());
+      compacted = true;
       HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
       HIP_OR_POISON(net, hipStreamSynchronize(s));
       live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
@@ -1278,6 +1324,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       adopt = tiles(live_bound) < tiles(P);
     }
     if (adopt && live_bound > 0 && l + 1 < net->L) {
+      if (!compacted) HIP_OR_POISON(net, compact());
+      compacted = true;
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
       const int64_t items = tiles(live_bound) * net->N * 8;
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
@@ -1289,7 +1337,16 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     } else {
       fin = fout;
     }
-    HIP_OR_POISON(net, poll_step(net, ring, l, &live_bound));
+    // counts[l] is final once layer l has run (written by a compaction or by layer l's launch)
+    HIP_OR_POISON(net, poll_step(net, ring, l, l, &live_bound));
+  }
+  if (!compacted) {
+    // the final list: compaction of the last layer's masks
+    const int32_t last = l - 1;
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, masks_for(last), 32, net->ids[cur], net->ids[cur ^ 1],
+                       net->src[cur ^ 1], npos + cur, net->counts + last + 1, npos + (cur ^ 1));
+    HIP_OR_POISON(net, hipGetLastError());
+    last_list = cur ^ 1;
   }
   net->layers_run = l;
   net->final_list = last_list;
@@ -1332,7 +1389,8 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
     net->ids[i] = reinterpret_cast<int *>(ws + w.ids[i]);
     net->src[i] = reinterpret_cast<int *>(ws + w.src[i]);
   }
-  net->masks = reinterpret_cast<unsigned *>(ws + w.masks);
+  for (int i = 0; i < 3; ++i) net->masks_rot[i] = reinterpret_cast<unsigned *>(ws + w.masks[i]);
+  net->masks = net->masks_rot[0];
   net->rownz = reinterpret_cast<int *>(ws + w.rownz);
   net->counts = reinterpret_cast<int *>(ws + w.counts);
   net->misc = reinterpret_cast<int *>(ws + w.misc);
@@ -1342,7 +1400,8 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   const int M = (int)n_rows;
   hipStream_t s = net->stream;
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
-                     net->ids[0], net->masks, net->rownz, net->counts, net->misc, M, net->L);
+                     net->ids[0], net->masks_rot[0], net->masks_rot[1], net->masks_rot[2], net->rownz, net->counts,
+                     net->misc, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
   st = net->path == 0 ? infer_lds(net, y0, M) : infer_gfm(net, y0, M);
   if (st != SDNN_OK) return st;
