@@ -179,7 +179,9 @@ def main() -> int:
         cats = step()
         log(f"warmup {i}: {cats.size} categories")
     if not args.no_profile:
-        net.set_profiling(True)
+        # events around the large layers only: recording them around every layer of the long tail
+        # would slow the step it measures
+        net.set_profiling(True, large_only=True)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):

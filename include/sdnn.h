@@ -108,14 +108,17 @@ sdnn_status sdnn_live_counts(sdnn_net *net, int64_t *counts);
  * zero. SDNN_EINVAL for an id out of range. */
 sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float *out_host);
 
-/* Diagnostics. enable != 0: every later sdnn_infer records a HIP event pair on its stream around
+/* Diagnostics. enable == 1: every later sdnn_infer records a HIP event pair on its stream around
  * each layer's kernels (the layer SpMM with its fused epilogue; not the compaction), and
- * sdnn_categories adds the elapsed times to per-layer totals. enable == 0 stops recording.
+ * sdnn_categories adds the elapsed times to per-layer totals. enable == 2: the same for large
+ * layers only (layers whose live rows take more than one round of tiles, or, for widths staged in
+ * LDS, while more than 256 rows may be live), so that the event records do not slow the long tail
+ * of layers with few rows. enable == 0 stops recording; other values are SDNN_EINVAL.
  * Creates its events here (needs the device); enabling again resets the totals. */
 sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable);
 
 /* Diagnostics. Per-layer totals since profiling was enabled: ms[l] milliseconds over runs[l] timed
- * launches of layer l. ms, runs: host arrays of n_layers entries. */
+ * runs of layer l (0 for layers not recorded). ms, runs: host arrays of n_layers entries. */
 sdnn_status sdnn_layer_times(sdnn_net *net, double *ms, int64_t *runs);
 
 /* Free the handle and its device memory. NULL is a no-op. */

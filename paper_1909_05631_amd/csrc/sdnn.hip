@@ -61,7 +61,7 @@ constexpr int kMaxLayers = 1000000;
 constexpr int kMaxDegree = 4096;
 constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
 constexpr int kGfmOutputs = 64;            // outputs per work item of k_layer_gfm
-constexpr int kPollEvery = 4;              // layers between live-count read-backs
+constexpr int kPollEvery = 16;             // layers between live-count read-backs
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -622,6 +622,96 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   }
 }
 
+// Layers of few rows (at most 8 tiles, so each XCD works on one tile's share of outputs): the tile
+// layout and lane mapping of k_layer_gfm with one output per lane and a whole chain's loads in
+// flight at once: the KC ELL entries straight from memory (the 8 lanes of an output read the same
+// entry), then all KC gathers, then the fma chain. A work item is a chunk of 32 outputs. The
+// bookkeeping of the layer sequence is that of k_layer_gfm; in addition, when the previous layer
+// left no live row (a row that died stays dead), the layer writes nothing: its masks stay zero, so
+// every later layer does the same.
+template <int KC>
+__global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict__ fin, float *__restrict__ fout,
+                                                         int N, const int2 *__restrict__ ell,
+                                                         const float *__restrict__ bias, float ymax,
+                                                         const int *__restrict__ npos, unsigned *__restrict__ masks,
+                                                         const unsigned *__restrict__ masks_prev,
+                                                         unsigned *__restrict__ masks_clear,
+                                                         int *__restrict__ count_out) {
+  constexpr int FMR = 32, CH = 32;
+  __shared__ unsigned rowmask;
+  __shared__ int prev_live;
+  const int R = *npos;
+  const int ntiles = min(8, (R + FMR - 1) / FMR);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 64) {
+    int c = 0;
+    for (int i = tid; i < ntiles; i += 64) {
+      if (count_out) c += __popc(masks_prev[i]);
+      if (masks_clear && blockIdx.x == 0) masks_clear[i] = 0u;
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+    if (tid == 0) {
+      if (count_out && blockIdx.x == 0) *count_out = c;
+      prev_live = count_out ? c : 1;
+      rowmask = 0u;
+    }
+  }
+  __syncthreads();
+  if (prev_live == 0 || ntiles == 0) return;
+  const int parts = 8 / ntiles;
+  const int xcd = blockIdx.x & 7;
+  if (xcd >= ntiles * parts) return;
+  const int nchunks = (N + CH - 1) / CH;
+  const int cpp = (nchunks + parts - 1) / parts;
+  const int t = xcd / parts;
+  const int cbeg = (xcd % parts) * cpp, cend = min(nchunks, cbeg + cpp);
+  const int q = lane & 7, h = lane >> 3;
+  const int per_xcd = gridDim.x >> 3;
+  const int nvalid = min(FMR, R - t * FMR);
+  const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
+  float *obase = fout + (size_t)t * N * FMR + q * 4;
+  unsigned lm = 0u;
+  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+    const int j = chunk * CH + wave * 8 + h;
+    const int jj = min(j, N - 1);
+    int2 e[KC];
+#pragma unroll
+    for (int i = 0; i < KC; ++i) e[i] = ell[(size_t)i * N + jj];
+    const float b = bias[jj];
+    float4 g[KC];
+#pragma unroll
+    for (int i = 0; i < KC; ++i) g[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)e[i].x);
+    // every gather is issued before the first fma waits on one
+    mem_fence_compiler();
+    __builtin_amdgcn_sched_barrier(0);
+    float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int i = 0; i < KC; ++i) {
+      const float w = __int_as_float(e[i].y);
+      a[0] = fmaf(g[i].x, w, a[0]);
+      a[1] = fmaf(g[i].y, w, a[1]);
+      a[2] = fmaf(g[i].z, w, a[2]);
+      a[3] = fmaf(g[i].w, w, a[3]);
+    }
+    // the chain is computed for every lane (outputs past N repeat output N - 1), so the loads stay
+    // ahead of the branch that stores
+    const float4 y = make_float4(activate(a[0], b, ymax), activate(a[1], b, ymax), activate(a[2], b, ymax),
+                                 activate(a[3], b, ymax));
+    const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
+    lm |= (j < N ? bits : 0u) << (4 * q);
+    if (j < N) store_stream(reinterpret_cast<float4 *>(obase + (size_t)j * FMR), y);
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+  if (lane == 0 && lm) atomicOr(&rowmask, lm);
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
+    if (rowmask & valid) atomicOr(&masks[t], rowmask & valid);
+  }
+}
+
 constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 128 registers each
 
 template <int T>
@@ -884,6 +974,8 @@ struct sdnn_net {
   std::vector<hipEvent_t> events;
   // profiling
   bool profiling = false;
+  int prof_mode = 0;              // 1: every layer, 2: large layers only
+  std::vector<char> prof_rec;     // layers recorded by the last infer
   bool pending_times = false;
   std::vector<hipEvent_t> prof_start, prof_end;
   std::vector<double> prof_ms;
@@ -956,6 +1048,18 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
                         const int *count, int *rownz) {
   if (ld.K == 32) return launch_lds<B, 32>(net, yin, yout, ld, ids, count, rownz);
   return launch_lds<B, 0>(net, yin, yout, ld, ids, count, rownz);
+}
+
+// A layer of at most 8 tiles with K == 32 (see k_layer_gfm_small).
+hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
+                            int64_t max_tiles, unsigned *masks, const unsigned *masks_prev, unsigned *masks_clear,
+                            int *count_out) {
+  const int nchunks = (net->N + 31) / 32;
+  const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
+  const int per_xcd = (int)std::min<int64_t>(2 * net->cus, (nchunks + parts - 1) / parts);
+  hipLaunchKernelGGL(k_layer_gfm_small<32>, dim3(8 * std::max(1, per_xcd)), dim3(256), 0, net->stream, fin, fout,
+                     net->N, ld.ell, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
+  return hipGetLastError();
 }
 
 // One layer of the global-tile path: ceil(tiles / 8) launches of 8 tiles each (rounds), reading fin
@@ -1233,9 +1337,11 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
   PollRing ring;
   for (; l < net->L && live_bound > 0; ++l) {
     float *yout = net->ybuf[l & 1];
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+    const bool rec = net->profiling && (net->prof_mode == 1 || live_bound > 256);
+    if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    if (net->profiling) net->prof_rec[(size_t)l] = rec;
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B, net->ids[cur], net->ids[cur ^ 1],
                        (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr);
     HIP_OR_POISON(net, hipGetLastError());
@@ -1276,7 +1382,9 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     const bool small = l > 0 && P <= one_round;
     unsigned *mk = masks_for(l);
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+    const bool rec = net->profiling && (net->prof_mode == 1 || !small);
+    if (net->profiling) net->prof_rec[(size_t)l] = rec;
+    if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     if (l == 0) {
       // layer 0 reads the caller's rows; binary inputs go through bit tiles (built in fm[0]),
       // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
@@ -1299,10 +1407,16 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       }
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
-      HIP_OR_POISON(net, launch_gfm(net, net->layers[(size_t)l], fin, fout, npos + cur, tiles(P), mk,
-                                    masks_for(l - 1), masks_for(l + 1), compacted ? nullptr : net->counts + l));
+      const LayerDev &ld = net->layers[(size_t)l];
+      int *cnt = compacted ? nullptr : net->counts + l;
+      if (small && ld.K == 32)
+        HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
+                                            masks_for(l + 1), cnt));
+      else
+        HIP_OR_POISON(net, launch_gfm(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
+                                      masks_for(l + 1), cnt));
     }
-    if (net->profiling) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
     auto compact = [&]() -> hipError_t {
       hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, mk, 32, net->ids[cur], net->ids[cur ^ 1],
                          net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
@@ -1403,6 +1517,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
                      net->ids[0], net->masks_rot[0], net->masks_rot[1], net->masks_rot[2], net->rownz, net->counts,
                      net->misc, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
+  if (net->profiling) net->prof_rec.assign((size_t)net->L, 0);
   st = net->path == 0 ? infer_lds(net, y0, M) : infer_gfm(net, y0, M);
   if (st != SDNN_OK) return st;
   hipLaunchKernelGGL(k_final_ids, dim3(std::max(1, std::min(net->cus, (M + 255) / 256 + 1))), dim3(256), 0, s,
@@ -1422,6 +1537,7 @@ sdnn_status sdnn_categories(sdnn_net *net, int64_t *ids, int64_t capacity, int64
   HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
   if (net->pending_times) {
     for (int32_t l = 0; l < net->layers_run; ++l) {
+      if (!net->prof_rec[(size_t)l]) continue;
       float ms = 0.0f;
       HIP_OR_POISON(net, hipEventElapsedTime(&ms, net->prof_start[(size_t)l], net->prof_end[(size_t)l]));
       net->prof_ms[(size_t)l] += ms;
@@ -1518,6 +1634,7 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
 sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable) {
   sdnn_status st = check_usable(net);
   if (st != SDNN_OK) return st;
+  if (enable < 0 || enable > 2) return fail(SDNN_EINVAL, "profiling mode %d is not 0, 1 or 2", enable);
   net->pending_times = false;
   if (!enable) {
     net->profiling = false;
@@ -1535,6 +1652,7 @@ sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable) {
   net->prof_ms.assign((size_t)net->L, 0.0);
   net->prof_runs.assign((size_t)net->L, 0);
   net->profiling = true;
+  net->prof_mode = enable;
   g_err.clear();
   return SDNN_OK;
 }

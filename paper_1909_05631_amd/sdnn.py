@@ -148,8 +148,9 @@ class Net:
         _check(load_library().sdnn_live_counts(self._h, _p(out)))
         return out
 
-    def set_profiling(self, enable: bool) -> None:
-        _check(load_library().sdnn_set_profiling(self._h, 1 if enable else 0))
+    def set_profiling(self, enable, large_only: bool = False) -> None:
+        """Per-layer HIP-event timing of later runs: off, every layer, or large layers only."""
+        _check(load_library().sdnn_set_profiling(self._h, 0 if not enable else (2 if large_only else 1)))
 
     def layer_times(self) -> tuple[np.ndarray, np.ndarray]:
         ms = np.zeros(self.n_layers, dtype=np.float64)

@@ -118,3 +118,11 @@ def test_workspace_bytes_grows_with_rows():
     assert b >= 2 * 1000 * 1024 * 4
     # the global-tile path keeps two buffers of 32-row tiles: 65 rows round up to 96
     assert sdnn.Net(65536, 2).workspace_bytes(65) >= 2 * 96 * 65536 * 4
+
+
+def test_profiling_mode_out_of_range_is_einval():
+    net = sdnn.Net(1024, 2)
+    with pytest.raises(sdnn.SdnnError) as ei:
+        _check = sdnn.load_library().sdnn_set_profiling(net._h, 3)
+        sdnn._check(_check)
+    assert ei.value.name == "SDNN_EINVAL"

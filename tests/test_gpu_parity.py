@@ -164,3 +164,51 @@ def test_layer0_bit_route(n, kind):
     log(f"bit route n={n} kind={kind}")
     gpu, o, cats = run_both(n, layers, y0)
     assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("n,m,bias,lo,hi,kind", [
+    (6000, 1100, -0.40, 0.10, 0.40, "binary"),     # 1100 -> 561 -> 213 -> ... -> 7: large, then small layers
+    (6000, 1100, -0.35, 0.10, 0.30, "binary"),     # every row dies by layer 4
+    (6000, 1100, -0.40, 0.10, 0.40, "scaled"),     # non-binary inputs: fp32 layer 0 over 35 tiles (5 rounds)
+    (9000, 900, -0.45, 0.10, 0.40, "binary"),
+])
+def test_global_tile_large_lists(n, m, bias, lo, hi, kind):
+    """Hundreds of live rows on the global-tile path: layers of several rounds of 8 tiles, compaction
+    with exact read-back, repacking of the tiles when rows die, the switch to single-round layers that
+    count their own live rows, and an early exit once no row is left."""
+    nl = 12
+    rng = np.random.default_rng(7)
+    dens = rng.uniform(lo, hi, size=(m, 1))
+    y0 = (rng.random((m, n)) < dens).astype(np.float32)
+    if kind == "scaled":
+        y0 *= np.float32(1.25)
+    cp, ri, v = synth.layers_csc(12, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    log(f"large lists n={n} m={m} bias={bias} kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert gpu.net.kernel_path == 1
+    assert_parity(gpu, o, cats)
+
+
+def test_profiling_modes():
+    """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
+    than 256 live rows, on the global-tile path)."""
+    n, m, nl, bias = 6000, 1100, 12, -0.40
+    rng = np.random.default_rng(7)
+    y0 = (rng.random((m, n)) < rng.uniform(0.10, 0.40, size=(m, 1))).astype(np.float32)
+    cp, ri, v = synth.layers_csc(12, 0, nl, n)
+    gpu = GpuRun(n, nl)
+    gpu.load(0, cp, ri, v, np.full((nl, n), bias, np.float32))
+    gpu.net.set_profiling(True)
+    gpu.run(y0)
+    ms, runs = gpu.net.layer_times()
+    assert (runs == 1).all() and (ms > 0).all()
+    gpu.net.set_profiling(True, large_only=True)
+    gpu.run(y0)
+    gpu.run(y0)
+    ms, runs = gpu.net.layer_times()
+    counts = gpu.net.live_counts()
+    large = [l for l in range(nl) if l == 0 or counts[l] > 256]
+    assert runs[large].tolist() == [2] * len(large) and (ms[large] > 0).all()
+    assert (runs[[l for l in range(nl) if l not in large]] == 0).all()
+    gpu.net.set_profiling(False)
