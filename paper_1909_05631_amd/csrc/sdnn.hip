@@ -113,12 +113,17 @@ __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
 }
 
-// misc[0]: a layer-0 input is not 0 or 1; misc[kNposSlot + i]: positions in live list i.
+// misc[0]: a layer-0 input is not 0 or 1; misc[kOverflowSlot]: the value dictionary is full;
+// misc[kNposSlot + i]: positions in live list i.
+constexpr int kOverflowSlot = 2;
 constexpr int kNposSlot = 4;
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsigned *__restrict__ masks2,
                        unsigned *__restrict__ masks3, int *__restrict__ rownz, int *__restrict__ counts,
-                       int *__restrict__ misc, int M, int L) {
+                       int *__restrict__ misc, unsigned *__restrict__ dict, int M, int L) {
   const int st = gridDim.x * blockDim.x;
+  // value dictionary: slot 0 holds +0.0 (bit pattern 0), every other slot is free
+  if (blockIdx.x == 0)
+    for (int i = threadIdx.x; i < 256; i += blockDim.x) dict[i] = i == 0 ? 0u : 0x7fc00000u;
   if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = (threadIdx.x == kNposSlot) ? M : 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
@@ -714,6 +719,169 @@ __global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict
 
 constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 128 registers each
 
+// Value dictionary for one-byte activation codes: a 256-slot open-addressing table of fp32 bit
+// patterns in device memory; a value's code is its slot, so decoding is dict[code]. Slot 0 holds
+// +0.0 from the start (its hash is 0), so zero bytes decode to zero. kDictEmpty (a NaN pattern,
+// never an activation) marks free slots. Slots are claimed with compare-and-swap and never change
+// afterwards, so a workgroup may cache them in LDS.
+constexpr unsigned kDictEmpty = 0x7fc00000u;
+constexpr int kDictSlots = 256;
+
+__device__ __forceinline__ unsigned dict_hash(unsigned key) {
+  return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
+}
+
+// Code of y: probe the workgroup's LDS copy, then the global table (claiming a free slot on the
+// way). A full table sets *overflow and returns 0; the caller's output is then not used.
+__device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow) {
+  const unsigned key = __float_as_uint(y);
+  unsigned h = dict_hash(key);
+  for (int i = 0; i < kDictSlots; ++i) {
+    const unsigned cur = dl[h];
+    if (cur == key) return h;
+    if (cur == kDictEmpty) break;
+    h = (h + 1) & (kDictSlots - 1);
+  }
+  h = dict_hash(key);
+  for (int i = 0; i < kDictSlots; ++i) {
+    unsigned cur = __hip_atomic_load(&gd[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (cur == kDictEmpty) {
+      const unsigned prev = atomicCAS(&gd[h], kDictEmpty, key);
+      cur = prev == kDictEmpty ? key : prev;
+    }
+    dl[h] = cur;
+    if (cur == key) return h;
+    h = (h + 1) & (kDictSlots - 1);
+  }
+  *overflow = 1;
+  return 0;
+}
+
+// One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
+// (source k of list position 32t + b), decoded as dict[code]; the output is fp32 tiles as in
+// k_layer_gfm, with the same XCD mapping of tiles. A code segment is 32 bytes, so a tile of 65536
+// sources takes 2 MiB of its XCD's L2. Lane = (half = lane % 2: rows 16*half..+15, o = lane / 2):
+// each gather is one 16-byte load of 16 codes, a wave instruction serves 32 outputs, and a work
+// item is a chunk of 128 outputs. The dictionary sits in LDS; the ELL entries are read directly,
+// the next group's while the current group's gathers are in flight.
+template <int KC>
+__global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
+                                                      int N, const int2 *__restrict__ ell, int K,
+                                                      const float *__restrict__ bias, float ymax,
+                                                      const float *__restrict__ dict, const int *__restrict__ npos,
+                                                      unsigned *__restrict__ masks, int tile0) {
+  constexpr int FMR = 32, CH = 128;
+  __shared__ float dl[kDictSlots];
+  __shared__ unsigned rowmask;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = dict[i];
+  if (tid == 0) rowmask = 0u;
+  __syncthreads();
+  const int R = *npos;
+  const int nt = min(8, (R + FMR - 1) / FMR - tile0);
+  const int parts = nt > 0 ? 8 / nt : 1;
+  const int xcd = blockIdx.x & 7;
+  const bool active = nt > 0 && xcd < nt * parts;
+  const int nchunks = (N + CH - 1) / CH;
+  const int cpp = (nchunks + parts - 1) / parts;
+  const int t = tile0 + xcd / parts;
+  const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
+  const int half = lane & 1, o = lane >> 1;
+  const int per_xcd = gridDim.x >> 3;
+  const int nvalid = active ? min(FMR, R - t * FMR) : 0;
+  const unsigned char *tb = cin + (size_t)t * N * FMR + half * 16;
+  float *obase = fout + (size_t)t * N * FMR + half * 16;
+  unsigned lm = 0u;
+  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+    const int j = chunk * CH + wave * 32 + o;
+    const int2 *ej = ell + min(j, N - 1);
+    float acc[16];
+#pragma unroll
+    for (int b = 0; b < 16; ++b) acc[b] = 0.0f;
+    auto term = [&](uint4 c, float w) {
+      const unsigned cw[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+      for (int b = 0; b < 16; ++b) acc[b] = fmaf(dl[(cw[b >> 2] >> (8 * (b & 3))) & 255u], w, acc[b]);
+    };
+    if constexpr (KC > 0) {
+      static_assert(KC % 8 == 0, "KC must be a multiple of 8");
+      int2 e[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) e[i] = ej[(size_t)i * N];
+#pragma unroll
+      for (int g = 0; g < KC; g += 8) {
+        uint4 c[8];
+        float w[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          c[i] = *reinterpret_cast<const uint4 *>(tb + (e[i].x >> 2));
+          w[i] = __int_as_float(e[i].y);
+        }
+        if (g + 8 < KC) {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) e[i] = ej[(size_t)(g + 8 + i) * N];
+        }
+        mem_fence_compiler();
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) term(c[i], w[i]);
+      }
+    } else {
+      for (int sl = 0; sl < K; ++sl) {
+        const int2 e = ej[(size_t)sl * N];
+        term(*reinterpret_cast<const uint4 *>(tb + (e.x >> 2)), __int_as_float(e.y));
+      }
+    }
+    // every lane finishes its chain (outputs past N repeat output N - 1), only real outputs store
+    const float b = bias[min(j, N - 1)];
+    unsigned bits = 0u;
+    float y[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      y[r] = activate(acc[r], b, ymax);
+      bits |= (y[r] > 0.0f ? 1u : 0u) << r;
+    }
+    lm |= (j < N ? bits : 0u) << (16 * half);
+    if (j < N) {
+      float4 *dst = reinterpret_cast<float4 *>(obase + (size_t)j * FMR);
+#pragma unroll
+      for (int n = 0; n < 4; ++n) store_stream(dst + n, make_float4(y[4 * n], y[4 * n + 1], y[4 * n + 2], y[4 * n + 3]));
+    }
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+  if (lane == 0 && lm) atomicOr(&rowmask, lm);
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
+    if (active && (rowmask & valid)) atomicOr(&masks[t], rowmask & valid);
+  }
+}
+
+// k_repack for one-byte code tiles: positions past *npos get code 0 (+0.0).
+__global__ __launch_bounds__(256) void k_repack_u8(const unsigned char *__restrict__ sfm, unsigned char *__restrict__ dfm,
+                                                   int N, const int *__restrict__ src, const int *__restrict__ npos) {
+  const int R = *npos;
+  const int ntiles = (R + 31) / 32;
+  const size_t items = (size_t)ntiles * N * 8;
+  for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
+    const int qd = (int)(it & 7);
+    const size_t rest = it >> 3;
+    const int k = (int)(rest % N);
+    const int t = (int)(rest / N);
+    unsigned word = 0u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int p = t * 32 + qd * 4 + c;
+      if (p < R) {
+        const int sp = src[p];
+        word |= (unsigned)sfm[((size_t)(sp >> 5) * N + k) * 32 + (sp & 31)] << (8 * c);
+      }
+    }
+    *reinterpret_cast<unsigned *>(dfm + ((size_t)t * N + k) * 32 + qd * 4) = word;
+  }
+}
+
 template <int T>
 struct BitWord;
 template <>
@@ -785,18 +953,23 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
 // its T rows of output j as T / 4 16-byte stores. Slots past the list's end get zeros.
 // word_shift turns an ELL source offset into the byte offset of the source's word in the tile.
 // KC = 32: the 32 ELL entries of a lane's output are all loaded before the first term is used.
-template <int T, int KC>
+// CODES: instead of fp32 values, write each output's one-byte code in the value dictionary gd
+// (same tile layout, one byte per row); a full dictionary sets *overflow.
+template <int T, int KC, bool CODES>
 __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
                                                      float *__restrict__ fout, int N, const int2 *__restrict__ ell,
                                                      int K, int word_shift, const float *__restrict__ bias,
                                                      float ymax, const int *__restrict__ count,
-                                                     unsigned *__restrict__ masks) {
+                                                     unsigned *__restrict__ masks, unsigned *__restrict__ gd,
+                                                     int *__restrict__ overflow) {
   using W = typename BitWord<T>::type;
-  // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), then the tile
+  // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), the dictionary copy
+  // (1 KiB), then the tile
   extern __shared__ float4 smem[];
   float4 *lut = smem;
   unsigned &tilemask = *reinterpret_cast<unsigned *>(smem + 16);
-  W *tile = reinterpret_cast<W *>(smem + 17);
+  unsigned *dl = reinterpret_cast<unsigned *>(smem + 17);
+  W *tile = reinterpret_cast<W *>(smem + 17 + kDictSlots / 4);
   const int R = *count;
   const int ntiles = (R + T - 1) / T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
@@ -806,6 +979,8 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   const int items = ntiles * ch.nchunks;
   if (tid < 16) lut[tid] = make_float4((float)(tid & 1), (float)((tid >> 1) & 1), (float)((tid >> 2) & 1), (float)((tid >> 3) & 1));
   if (tid == 0) tilemask = 0u;
+  if (CODES)
+    for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = kDictEmpty;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
     const int t = w / ch.nchunks, c = w % ch.nchunks;
     const int p0 = t * T;
@@ -901,19 +1076,40 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
       if (jin) {
         // rows past nvalid have all-zero bits, so their outputs are zeros
         const float bj = bias[j];
-        float4 *dst = reinterpret_cast<float4 *>(fout + ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
+        if constexpr (CODES) {
+          uint4 *dst = reinterpret_cast<uint4 *>(reinterpret_cast<unsigned char *>(fout) +
+                                                 ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
+          unsigned cw[T / 4];
 #pragma unroll
-        for (int n = 0; n < T / 4; ++n) {
-          const float4 y = make_float4(activate(acc[4 * n], bj, ymax), activate(acc[4 * n + 1], bj, ymax),
-                                       activate(acc[4 * n + 2], bj, ymax), activate(acc[4 * n + 3], bj, ymax));
-          dst[n] = y;
-          live |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u))
-                  << (4 * n);
-        }
-        if (T == 16 && (p0 & 31) == 0 && t + 1 == ntiles) {
-          // the last 32-row tile has no second half: zero its slots 16..31
+          for (int n = 0; n < T / 4; ++n) {
+            unsigned word = 0u;
 #pragma unroll
-          for (int n = 0; n < 4; ++n) dst[4 + n] = make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int u = 0; u < 4; ++u) {
+              const float y = activate(acc[4 * n + u], bj, ymax);
+              live |= (y > 0.0f ? 1u : 0u) << (4 * n + u);
+              word |= dict_code(y, dl, gd, overflow) << (8 * u);
+            }
+            cw[n] = word;
+          }
+#pragma unroll
+          for (int n = 0; n < T / 16; ++n) dst[n] = make_uint4(cw[4 * n], cw[4 * n + 1], cw[4 * n + 2], cw[4 * n + 3]);
+          // the last 32-row tile has no second half: its slots 16..31 get code 0 (+0.0)
+          if (T == 16 && (p0 & 31) == 0 && t + 1 == ntiles) dst[1] = make_uint4(0u, 0u, 0u, 0u);
+        } else {
+          float4 *dst = reinterpret_cast<float4 *>(fout + ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
+#pragma unroll
+          for (int n = 0; n < T / 4; ++n) {
+            const float4 y = make_float4(activate(acc[4 * n], bj, ymax), activate(acc[4 * n + 1], bj, ymax),
+                                         activate(acc[4 * n + 2], bj, ymax), activate(acc[4 * n + 3], bj, ymax));
+            dst[n] = y;
+            live |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u))
+                    << (4 * n);
+          }
+          if (T == 16 && (p0 & 31) == 0 && t + 1 == ntiles) {
+            // the last 32-row tile has no second half: zero its slots 16..31
+#pragma unroll
+            for (int n = 0; n < 4; ++n) dst[4 + n] = make_float4(0.f, 0.f, 0.f, 0.f);
+          }
         }
       }
     }
@@ -964,7 +1160,9 @@ struct sdnn_net {
   unsigned *masks = nullptr;               // per-tile liveness bits (path 1: layers l % 3 == 0)
   unsigned *masks_rot[3] = {nullptr, nullptr, nullptr};  // path 1: layer l uses masks_rot[l % 3]
   int *rownz = nullptr, *counts = nullptr;
-  int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [4 + i] positions in list i
+  int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [2] dictionary full,
+                        // [4 + i] positions in list i
+  unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (256 fp32 bit patterns)
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
@@ -994,7 +1192,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, final_ids, total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, final_ids, total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -1015,6 +1213,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
+  w.dict = off; off += 256 * sizeof(unsigned);
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
   w.total = off;
   return w;
@@ -1097,7 +1296,7 @@ hipError_t launch_to_fm(sdnn_net *net, const float *y, float *fm, const int *ids
 template <int T>
 size_t bits_lds_bytes(const sdnn_net *net) {
   using W = typename BitWord<T>::type;
-  return 17 * 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+  return 17 * 16 + kDictSlots * 4 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
 }
 
 template <int T>
@@ -1108,12 +1307,12 @@ hipError_t launch_pack_bits(sdnn_net *net, const float *yin, void *bits, const i
   return hipGetLastError();
 }
 
-template <int T, int KC>
+template <int T, int KC, bool CODES>
 hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count) {
   using W = typename BitWord<T>::type;
   static bool configured = false;
   if (!configured) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T, KC>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T, KC, CODES>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     configured = true;
@@ -1126,16 +1325,44 @@ hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bi
   while ((1 << shift) < 32 * (int)sizeof(float)) ++shift;
   int wshift = 0;
   while ((1 << wshift) < (int)sizeof(W)) ++wshift;
-  hipLaunchKernelGGL((k_layer_bits<T, KC>), dim3(net->cus * per_cu), dim3(kBitsThreads), lds, net->stream,
+  hipLaunchKernelGGL((k_layer_bits<T, KC, CODES>), dim3(net->cus * per_cu), dim3(kBitsThreads), lds, net->stream,
                      reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, shift - wshift, ld.bias, net->ymax,
-                     count, net->masks);
+                     count, net->masks, net->dict, net->misc + kOverflowSlot);
   return hipGetLastError();
 }
 
+// codes: write one-byte dictionary codes instead of fp32 values
 template <int T>
-hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count) {
-  if (ld.K == 32) return launch_layer_bits_k<T, 32>(net, ld, bits, fout, count);
-  return launch_layer_bits_k<T, 0>(net, ld, bits, fout, count);
+hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count,
+                             bool codes) {
+  if (codes) {
+    if (ld.K == 32) return launch_layer_bits_k<T, 32, true>(net, ld, bits, fout, count);
+    return launch_layer_bits_k<T, 0, true>(net, ld, bits, fout, count);
+  }
+  if (ld.K == 32) return launch_layer_bits_k<T, 32, false>(net, ld, bits, fout, count);
+  return launch_layer_bits_k<T, 0, false>(net, ld, bits, fout, count);
+}
+
+// A layer whose input tiles hold dictionary codes (see k_layer_gfm_u8); rounds of 8 tiles.
+hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
+                         int64_t max_tiles, unsigned *masks) {
+  const int rounds = (int)((max_tiles + 7) / 8);
+  const int nchunks = (net->N + 127) / 128;
+  const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
+  const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
+  const dim3 grid(8 * std::max(1, per_xcd));
+  const float *dict = reinterpret_cast<const float *>(net->dict);
+  for (int r = 0; r < rounds; ++r) {
+    if (ld.K == 32)
+      hipLaunchKernelGGL(k_layer_gfm_u8<32>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
+                         net->ymax, dict, npos, masks, r * 8);
+    else
+      hipLaunchKernelGGL(k_layer_gfm_u8<0>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
+                         net->ymax, dict, npos, masks, r * 8);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // One layer of the LDS-tile path.
@@ -1374,12 +1601,14 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   int64_t live_bound = M;  // host bound on the live rows
   const float *fin = nullptr;
   float *fout = nullptr;
+  bool fin_codes = false, fout_codes = false;  // the tiles hold one-byte dictionary codes
   int last_list = 0;
   bool compacted = true;   // the last layer run has been followed by a compaction
   PollRing ring;
   int32_t l = 0;
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
+    fout_codes = false;
     unsigned *mk = masks_for(l);
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
     const bool rec = net->profiling && (net->prof_mode == 1 || !small);
@@ -1399,12 +1628,20 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         bits_route = net->pinned[6] == 0;
       }
       if (bits_route) {
-        HIP_OR_POISON(net, net->bitsT == 32 ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur)
-                                            : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur));
+        // outputs of a layer on binary inputs take few distinct values: a large layer 0 writes them
+        // as one-byte dictionary codes, which the next layer gathers four times denser
+        fout_codes = P > one_round && net->L > 1;
+        HIP_OR_POISON(net, net->bitsT == 32
+                               ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur, fout_codes)
+                               : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, fout_codes));
       } else {
         HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, try_bits ? nullptr : net->rownz));
         HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk));
       }
+    } else if (fin_codes) {
+      // follows layer 0, which is always compacted: no count to take over
+      HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
+                                       npos + cur, tiles(P), mk));
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -1431,7 +1668,20 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       HIP_OR_POISON(net, compact());
       compacted = true;
       HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      if (fout_codes)
+        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 5, net->misc + kOverflowSlot, sizeof(int32_t),
+                                          hipMemcpyDeviceToHost, s));
       HIP_OR_POISON(net, hipStreamSynchronize(s));
+      if (fout_codes && net->pinned[5] != 0) {
+        // more than 256 distinct values: redo layer 0 with fp32 outputs (same liveness)
+        fout_codes = false;
+        HIP_OR_POISON(net, net->bitsT == 32
+                               ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur, false)
+                               : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, false));
+        HIP_OR_POISON(net, compact());
+        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+        HIP_OR_POISON(net, hipStreamSynchronize(s));
+      }
       live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
       adopt = live_bound == 0 || tiles(live_bound) * 20 <= tiles(P) * 19;
     } else {
@@ -1443,7 +1693,11 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
       const int64_t items = tiles(live_bound) * net->N * 8;
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
-      hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1));
+      if (fout_codes)
+        hipLaunchKernelGGL(k_repack_u8, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
+                           reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
+      else
+        hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1));
       HIP_OR_POISON(net, hipGetLastError());
       fin = dst;
       cur ^= 1;
@@ -1451,6 +1705,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     } else {
       fin = fout;
     }
+    fin_codes = fout_codes;
     // counts[l] is final once layer l has run (written by a compaction or by layer l's launch)
     HIP_OR_POISON(net, poll_step(net, ring, l, l, &live_bound));
   }
@@ -1508,6 +1763,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->rownz = reinterpret_cast<int *>(ws + w.rownz);
   net->counts = reinterpret_cast<int *>(ws + w.counts);
   net->misc = reinterpret_cast<int *>(ws + w.misc);
+  net->dict = reinterpret_cast<unsigned *>(ws + w.dict);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
   net->ran = false;
 
@@ -1515,7 +1771,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   hipStream_t s = net->stream;
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
                      net->ids[0], net->masks_rot[0], net->masks_rot[1], net->masks_rot[2], net->rownz, net->counts,
-                     net->misc, M, net->L);
+                     net->misc, net->dict, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
   if (net->profiling) net->prof_rec.assign((size_t)net->L, 0);
   st = net->path == 0 ? infer_lds(net, y0, M) : infer_gfm(net, y0, M);
