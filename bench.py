@@ -98,16 +98,16 @@ def kernel_source_sha() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def committed_traffic(workload: str):
-    """HBM bytes per layer launch measured with rocprofv3 counters for this workload, if the record
-    in profiles/ was taken with the current kernel source; None otherwise."""
+def committed_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` measured with rocprofv3 counters for this workload, if the
+    record in profiles/ was taken with the current kernel source; None otherwise."""
     path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
     try:
         with open(path) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256") != kernel_source_sha():
+    if rec.get("kernel_source_sha256") != kernel_source_sha() or rec.get("kernel") != kernel:
         return None
     return rec.get("bytes_per_launch")
 
@@ -200,25 +200,29 @@ def main() -> int:
 
     roofline = None
     if not args.no_profile:
+        # the dominant kernel: the large layer with the most event time; its launches are the rounds
+        # (or the pack + layer pair) that the event pair of that layer spans
         ms, runs = net.layer_times()
-        tot_bytes = sum(algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1])) * int(runs[l])
-                        for l in range(L))
-        tot_ms = float(ms.sum())
-        launches = int(runs.sum())
-        achieved = tot_bytes / (tot_ms * 1e-3) / 1e9 if tot_ms > 0 else 0.0
-        nz = [l for l in range(L) if runs[l] > 0]
-        per = ms / np.maximum(runs, 1)
-        head = ", ".join(f"{l}:{per[l] * 1e3:.1f}us(R={int(counts[l])})" for l in nz[:6])
-        tail = [l for l in nz if int(counts[l]) < 64]
-        tail_avg = float(np.mean(per[tail]) * 1e3) if tail else 0.0
-        log(f"layer kernel times: {head}; {len(tail)} layers with <64 live rows average {tail_avg:.1f}us")
-        kname = f"k_layer_lds<{32 if n <= 1024 else 16 if n <= 2048 else 8}>" if net.kernel_path == 0 \
-            else "k_to_fm+k_layer_gfm"
+        kind, launches = net.layer_info()
+        per_run = ms / np.maximum(runs, 1)
+        timed = [l for l in range(L) if runs[l] > 0]
+        lay = max(timed, key=lambda l: per_run[l])
+        algo = algorithmic_layer_bytes(n, nnz, int(counts[lay]), int(counts[lay + 1]))
+        nl = max(int(launches[lay]), 1)
+        avg_launch_ms = float(per_run[lay]) / nl
+        achieved = algo / nl / (avg_launch_ms * 1e-3) / 1e9
+        kname = sdnn.KERNEL_KINDS.get(int(kind[lay]), str(int(kind[lay])))
+        head = ", ".join(f"{l}:{per_run[l] * 1e3:.1f}us({sdnn.KERNEL_KINDS.get(int(kind[l]))} x{int(launches[l])}, "
+                         f"R={int(counts[l])})" for l in timed[:6])
+        log(f"large-layer kernel times: {head}")
+        tot_bytes = sum(algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1])) * int(runs[l]) for l in timed)
+        tot_ms = float(ms[timed].sum())
         roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(cfg.name),
-                    "kernel": kname,
-                    "launches": launches, "avg_launch_ms": round(tot_ms / max(launches, 1), 5),
-                    "algorithmic_bytes_per_launch": int(tot_bytes / max(launches, 1))}
+                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(cfg.name, kname),
+                    "kernel": kname, "layer": lay, "launches_per_step": nl,
+                    "avg_launch_ms": round(avg_launch_ms, 5), "algorithmic_bytes_per_launch": int(algo / nl),
+                    "large_layers": {"layers": len(timed),
+                                     "achieved": round(tot_bytes / (tot_ms * 1e-3) / 1e9, 2) if tot_ms > 0 else None}}
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -121,6 +121,22 @@ sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable);
  * runs of layer l (0 for layers not recorded). ms, runs: host arrays of n_layers entries. */
 sdnn_status sdnn_layer_times(sdnn_net *net, double *ms, int64_t *runs);
 
+/* Kernel families reported by sdnn_layer_info. */
+typedef enum {
+  SDNN_KERNEL_NONE = 0,                 /* layer not run (every row had died) */
+  SDNN_KERNEL_LDS_TILE = 1,             /* activation tiles staged in LDS (k_layer_lds) */
+  SDNN_KERNEL_GLOBAL_TILE = 2,          /* fp32 feature-major tiles in global memory (k_layer_gfm) */
+  SDNN_KERNEL_GLOBAL_TILE_CODES = 3,    /* one-byte dictionary codes of the inputs (k_layer_gfm_u8) */
+  SDNN_KERNEL_GLOBAL_TILE_FEW_ROWS = 4, /* at most 8 tiles, whole chains in flight (k_layer_gfm_small) */
+  SDNN_KERNEL_BITS = 5,                 /* layer 0 from bit-packed binary inputs (k_pack_bits, k_layer_bits) */
+  SDNN_KERNEL_BITS_TO_CODES = 6         /* the same, writing one-byte dictionary codes */
+} sdnn_kernel_kind;
+
+/* Diagnostics (untimed). For each layer of the last sdnn_infer: the kernel family that ran it
+ * (sdnn_kernel_kind) and its number of kernel launches (for layers timed with events, the event
+ * pair spans these launches). kernel, launches: host arrays of n_layers entries. */
+sdnn_status sdnn_layer_info(sdnn_net *net, int32_t *kernel, int32_t *launches);
+
 /* Free the handle and its device memory. NULL is a no-op. */
 void sdnn_destroy(sdnn_net *net);
 

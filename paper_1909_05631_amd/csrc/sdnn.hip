@@ -1166,6 +1166,7 @@ struct sdnn_net {
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
+  std::vector<int32_t> layer_kernel, layer_launches;  // per layer of the last infer (sdnn_layer_info)
   const float *final_y = nullptr;   // path 0: final activations, row-major by row id
   const float *final_fm = nullptr;  // path 1: final activation tiles; live row i is at position src[final_list][i]
   int32_t *pinned = nullptr; // read-back slots (0-3: polling ring, 6: input-not-binary flag, 7: exact count)
@@ -1568,6 +1569,8 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+    net->layer_kernel[(size_t)l] = SDNN_KERNEL_LDS_TILE;
+    net->layer_launches[(size_t)l] = 1;
     if (net->profiling) net->prof_rec[(size_t)l] = rec;
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B, net->ids[cur], net->ids[cur ^ 1],
                        (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr);
@@ -1631,27 +1634,38 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         // outputs of a layer on binary inputs take few distinct values: a large layer 0 writes them
         // as one-byte dictionary codes, which the next layer gathers four times denser
         fout_codes = P > one_round && net->L > 1;
+        net->layer_kernel[0] = fout_codes ? SDNN_KERNEL_BITS_TO_CODES : SDNN_KERNEL_BITS;
+        net->layer_launches[0] = 2;  // pack + layer
         HIP_OR_POISON(net, net->bitsT == 32
                                ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur, fout_codes)
                                : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, fout_codes));
       } else {
         HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, try_bits ? nullptr : net->rownz));
         HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk));
+        net->layer_kernel[0] = SDNN_KERNEL_GLOBAL_TILE;
+        net->layer_launches[0] = (int32_t)(1 + (tiles(P) + 7) / 8) + (try_bits ? 1 : 0);
       }
     } else if (fin_codes) {
       // follows layer 0, which is always compacted: no count to take over
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
                                        npos + cur, tiles(P), mk));
+      net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
+      net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
       int *cnt = compacted ? nullptr : net->counts + l;
-      if (small && ld.K == 32)
+      if (small && ld.K == 32) {
         HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
                                             masks_for(l + 1), cnt));
-      else
+        net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_FEW_ROWS;
+        net->layer_launches[(size_t)l] = 1;
+      } else {
         HIP_OR_POISON(net, launch_gfm(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
                                       masks_for(l + 1), cnt));
+        net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
+        net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
+      }
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
     auto compact = [&]() -> hipError_t {
@@ -1774,6 +1788,8 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
                      net->misc, net->dict, M, net->L);
   HIP_OR_POISON(net, hipGetLastError());
   if (net->profiling) net->prof_rec.assign((size_t)net->L, 0);
+  net->layer_kernel.assign((size_t)net->L, SDNN_KERNEL_NONE);
+  net->layer_launches.assign((size_t)net->L, 0);
   st = net->path == 0 ? infer_lds(net, y0, M) : infer_gfm(net, y0, M);
   if (st != SDNN_OK) return st;
   hipLaunchKernelGGL(k_final_ids, dim3(std::max(1, std::min(net->cus, (M + 255) / 256 + 1))), dim3(256), 0, s,
@@ -1909,6 +1925,19 @@ sdnn_status sdnn_set_profiling(sdnn_net *net, int32_t enable) {
   net->prof_runs.assign((size_t)net->L, 0);
   net->profiling = true;
   net->prof_mode = enable;
+  g_err.clear();
+  return SDNN_OK;
+}
+
+sdnn_status sdnn_layer_info(sdnn_net *net, int32_t *kernel, int32_t *launches) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (!net->ran) return fail(SDNN_ESTATE, "no inference has run");
+  if (!kernel || !launches) return fail(SDNN_EINVAL, "null array");
+  for (int32_t l = 0; l < net->L; ++l) {
+    kernel[l] = net->layer_kernel[(size_t)l];
+    launches[l] = net->layer_launches[(size_t)l];
+  }
   g_err.clear();
   return SDNN_OK;
 }

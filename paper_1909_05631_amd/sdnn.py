@@ -15,8 +15,10 @@ STATUS = {0: "SDNN_OK", 1: "SDNN_EINVAL", 2: "SDNN_ENOMEM", 3: "SDNN_EDEVICE", 4
 EXPORTED_SYMBOLS = [
     "sdnn_create", "sdnn_load_layers", "sdnn_workspace_bytes", "sdnn_infer", "sdnn_categories",
     "sdnn_live_counts", "sdnn_final_rows", "sdnn_destroy", "sdnn_last_error", "sdnn_kernel_path",
-    "sdnn_set_profiling", "sdnn_layer_times",
+    "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info",
 ]
+KERNEL_KINDS = {0: "none", 1: "k_layer_lds", 2: "k_layer_gfm", 3: "k_layer_gfm_u8", 4: "k_layer_gfm_small",
+                5: "k_pack_bits+k_layer_bits", 6: "k_pack_bits+k_layer_bits(codes)"}
 
 
 class SdnnError(RuntimeError):
@@ -54,8 +56,9 @@ def load_library():
         L.sdnn_kernel_path.restype = i32
         L.sdnn_set_profiling.argtypes = [vp, i32]
         L.sdnn_layer_times.argtypes = [vp, vp, vp]
+        L.sdnn_layer_info.argtypes = [vp, vp, vp]
         for name in ("sdnn_create", "sdnn_load_layers", "sdnn_infer", "sdnn_categories", "sdnn_live_counts",
-                     "sdnn_final_rows", "sdnn_set_profiling", "sdnn_layer_times"):
+                     "sdnn_final_rows", "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -151,6 +154,13 @@ class Net:
     def set_profiling(self, enable, large_only: bool = False) -> None:
         """Per-layer HIP-event timing of later runs: off, every layer, or large layers only."""
         _check(load_library().sdnn_set_profiling(self._h, 0 if not enable else (2 if large_only else 1)))
+
+    def layer_info(self) -> tuple[np.ndarray, np.ndarray]:
+        """Per layer of the last run: kernel family (KERNEL_KINDS) and number of launches."""
+        kind = np.zeros(self.n_layers, dtype=np.int32)
+        launches = np.zeros(self.n_layers, dtype=np.int32)
+        _check(load_library().sdnn_layer_info(self._h, _p(kind), _p(launches)))
+        return kind, launches
 
     def layer_times(self) -> tuple[np.ndarray, np.ndarray]:
         ms = np.zeros(self.n_layers, dtype=np.float64)
