@@ -129,7 +129,9 @@ typedef enum {
   SDNN_KERNEL_GLOBAL_TILE_CODES = 3,    /* one-byte dictionary codes of the inputs (k_layer_gfm_u8) */
   SDNN_KERNEL_GLOBAL_TILE_FEW_ROWS = 4, /* at most 8 tiles, whole chains in flight (k_layer_gfm_small) */
   SDNN_KERNEL_BITS = 5,                 /* layer 0 from bit-packed binary inputs (k_pack_bits, k_layer_bits) */
-  SDNN_KERNEL_BITS_TO_CODES = 6         /* the same, writing one-byte dictionary codes */
+  SDNN_KERNEL_BITS_TO_CODES = 6,        /* the same, writing one-byte dictionary codes */
+  SDNN_KERNEL_BITS_COUNT = 7            /* layer 0 of a uniform layer on binary inputs, by bit-sliced counts
+                                           (k_pack_bits, k_count_dict, k_layer_count) */
 } sdnn_kernel_kind;
 
 /* Diagnostics (untimed). For each layer of the last sdnn_infer: the kernel family that ran it

@@ -109,12 +109,31 @@ __device__ __forceinline__ void store_stream(float4 *p, float4 v) {
   __builtin_nontemporal_store(x, reinterpret_cast<v4f *>(p));
 }
 
+__device__ __forceinline__ void store_stream(uint4 *p, uint4 v) {
+  typedef unsigned v4u __attribute__((ext_vector_type(4)));
+  const v4u x = {v.x, v.y, v.z, v.w};
+  __builtin_nontemporal_store(x, reinterpret_cast<v4u *>(p));
+}
+
+__device__ __forceinline__ float4 load_stream_f4(const float4 *p) {
+  typedef float v4f __attribute__((ext_vector_type(4)));
+  const v4f x = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(p));
+  return make_float4(x[0], x[1], x[2], x[3]);
+}
+
+// 16-byte load that streams past the L2 (read once per pass, keeps the L2 for data that is reused).
+__device__ __forceinline__ int4 load_stream(const int4 *p) {
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  const v4i x = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(p));
+  return make_int4(x[0], x[1], x[2], x[3]);
+}
+
 __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
 }
 
 // misc[0]: a layer-0 input is not 0 or 1; misc[kOverflowSlot]: the value dictionary is full;
-// misc[kNposSlot + i]: positions in live list i.
+// misc[3]: first live count of a uniform layer 0; misc[kNposSlot + i]: positions in live list i.
 constexpr int kOverflowSlot = 2;
 constexpr int kNposSlot = 4;
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsigned *__restrict__ masks2,
@@ -896,8 +915,9 @@ struct BitWord<32> {
 // Layer-0 inputs as bits (the challenge inputs are binary images, Sec. IV): pack the live rows into
 // feature-major bit tiles, bits[t][k] bit b = (Y[ids[t*T + b]][k] != 0). Any entry other than 0
 // and 1 (or not finite) sets *nonbinary, and the bit route is then not used. Rows with a nonzero
-// entry are recorded in rownz. One wave per (tile, run of kPackBlocks blocks of 64 sources),
-// lane = source; the rows' nonzero bits are gathered over the run and stored once.
+// entry are recorded in rownz. One wave per (tile, run of kPackBlocks blocks of sources): with
+// N % 4 == 0 a lane takes 4 consecutive sources per block (16-byte loads, 256 sources per block),
+// otherwise one (64 per block). The rows' nonzero bits are gathered over the run and stored once.
 constexpr int kPackBlocks = 16;
 template <int T>
 __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin, typename BitWord<T>::type *__restrict__ bits,
@@ -906,7 +926,9 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
   using W = typename BitWord<T>::type;
   const int R = *count;
   const int ntiles = (R + T - 1) / T;
-  const int kblocks = (N + 63) / 64;
+  const bool vec = (N & 3) == 0;
+  const int per_lane = vec ? 4 : 1;
+  const int kblocks = (N + 64 * per_lane - 1) / (64 * per_lane);
   const int runs = (kblocks + kPackBlocks - 1) / kPackBlocks;
   const int lane = threadIdx.x & 63;
   const long long nwaves = (long long)gridDim.x * (blockDim.x >> 6);
@@ -915,26 +937,61 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
        item < (long long)ntiles * runs; item += nwaves) {
     const int t = (int)(item / runs), run = (int)(item % runs);
     const int nvalid = min(T, R - t * T);
-    const float *rowp[T];
+    // row starts in units of 4 floats (vec) or floats: below 2^32 for any row id and width
+    unsigned rowq[T];
 #pragma unroll
-    for (int b = 0; b < T; ++b) rowp[b] = yin + (size_t)ids[t * T + min(b, nvalid - 1)] * N;
+    for (int b = 0; b < T; ++b) rowq[b] = (unsigned)ids[t * T + min(b, nvalid - 1)] * (unsigned)(vec ? N / 4 : N);
+    const float4 *y4 = reinterpret_cast<const float4 *>(yin);
     unsigned rows_nz = 0u;
     const int kb_end = min(kblocks, (run + 1) * kPackBlocks);
     for (int kb = run * kPackBlocks; kb < kb_end; ++kb) {
-      const int k = kb * 64 + lane;
-      const bool kin = k < N;
-      float v[T];
+      if (vec) {
+        const int k = (kb * 64 + lane) * 4;
+        const bool kin = k < N;
+        unsigned word[4] = {0u, 0u, 0u, 0u};
+        // rows in groups of 16 keep the loads in flight within the register budget
 #pragma unroll
-      for (int b = 0; b < T; ++b) v[b] = (b < nvalid && kin) ? rowp[b][k] : 0.0f;
-      unsigned word = 0u;
+        for (int b0 = 0; b0 < T; b0 += 16) {
+          float4 v[16];
 #pragma unroll
-      for (int b = 0; b < T; ++b) {
-        const bool nz = v[b] != 0.0f;
-        bad |= nz && v[b] != 1.0f;
-        word |= (unsigned)nz << b;
+          for (int b = 0; b < 16; ++b)
+            v[b] = (b0 + b < nvalid && kin) ? load_stream_f4(y4 + rowq[b0 + b] + (k >> 2)) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int b = 0; b < 16; ++b) {
+            const float e[4] = {v[b].x, v[b].y, v[b].z, v[b].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              const bool nz = e[c] != 0.0f;
+              bad |= nz && e[c] != 1.0f;
+              word[c] |= (unsigned)nz << (b0 + b);
+            }
+          }
+        }
+        rows_nz |= word[0] | word[1] | word[2] | word[3];
+        if (kin) {
+          W *dst = bits + (size_t)t * N + k;
+          if constexpr (sizeof(W) == 2) {
+            *reinterpret_cast<uint2 *>(dst) = make_uint2(word[0] | (word[1] << 16), word[2] | (word[3] << 16));
+          } else {
+            *reinterpret_cast<uint4 *>(dst) = make_uint4(word[0], word[1], word[2], word[3]);
+          }
+        }
+      } else {
+        const int k = kb * 64 + lane;
+        const bool kin = k < N;
+        float v[T];
+#pragma unroll
+        for (int b = 0; b < T; ++b) v[b] = (b < nvalid && kin) ? yin[(size_t)rowq[b] + k] : 0.0f;
+        unsigned word = 0u;
+#pragma unroll
+        for (int b = 0; b < T; ++b) {
+          const bool nz = v[b] != 0.0f;
+          bad |= nz && v[b] != 1.0f;
+          word |= (unsigned)nz << b;
+        }
+        rows_nz |= word;
+        if (kin) bits[(size_t)t * N + k] = (W)word;
       }
-      rows_nz |= word;
-      if (kin) bits[(size_t)t * N + k] = (W)word;
     }
     // rows with a nonzero anywhere in this run: OR over the wave, then lane b stores row b's flag
     unsigned all = rows_nz;
@@ -1125,6 +1182,179 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   }
 }
 
+// Dictionary of a uniform layer on binary inputs (every column K sources, weight w, bias b): a
+// column with c sources at 1 has z = z_c, the fp32 chain of c fma(1, w, .) steps from +0 (the steps
+// with input 0 leave the accumulator unchanged: fma(0, w, acc) = acc since acc is never -0), so its
+// output is dict[c] = activate(z_c, b). Codes c in [0, K]; the other slots are left free.
+// misc[kCountMinSlot] receives the smallest c with dict[c] > 0 (K + 1 if none; with w > 0 the
+// outputs grow with c, so a row is live exactly when one of its counts reaches it).
+constexpr int kCountMinSlot = 3;
+__global__ void k_count_dict(unsigned *__restrict__ dict, int *__restrict__ misc, int K, float w, float b,
+                             float ymax) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  float z = 0.0f;
+  int cmin = K + 1;
+  for (int c = 0; c <= K; ++c) {
+    const float y = activate(z, b, ymax);
+    dict[c] = __float_as_uint(y);
+    if (y > 0.0f && cmin > K) cmin = c;
+    z = fmaf(1.0f, w, z);
+  }
+  misc[kCountMinSlot] = cmin;
+}
+
+// Carry-save adder on bit-sliced words: per bit position, a + b + c = sum + 2 * carry.
+__device__ __forceinline__ void csa(unsigned &carry, unsigned &sum, unsigned a, unsigned b, unsigned c) {
+  carry = __builtin_amdgcn_bitop3_b32(a, b, c, 0xE8);  // majority
+  sum = __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);    // three-way xor
+}
+
+// Layer 0 of a uniform layer (K = 32, w > 0) on bit tiles of T rows: for each output, the counts
+// of set input bits among its 32 sources, for all rows of a word at once. The 32 source words go
+// through a carry-save adder tree (two 16-word blocks), giving the six bit planes of the counts
+// (0..32); a bit-sliced comparison with the first live count gives the live rows, and a transpose
+// turns the planes into one byte per row: the output's code, decoded by the dictionary of
+// k_count_dict. blockDim 1024; lane = output (T = 32) or outputs j and j + 64 in the low and high
+// halves of each word (T = 16). LDS holds the tile's N words; the source indices are read 8 per
+// 16-byte load from the [4][N][8] u16 table. Codes go to tiles of 32 rows, one byte per row.
+template <int T>
+__global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>::type *__restrict__ bits,
+                                                      unsigned char *__restrict__ cout, int N,
+                                                      const uint4 *__restrict__ ell16, const int *__restrict__ misc,
+                                                      const int *__restrict__ count, unsigned *__restrict__ masks) {
+  using W = typename BitWord<T>::type;
+  constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
+  extern __shared__ float4 smem[];
+  unsigned &tilemask = *reinterpret_cast<unsigned *>(smem);
+  W *tile = reinterpret_cast<W *>(smem + 1);
+  const int R = *count;
+  const int cmin = misc[kCountMinSlot];
+  const int ntiles = (R + T - 1) / T;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  const int blocks = (N + 64 * OPL - 1) / (64 * OPL);  // output blocks of one wave
+  const int rounds = (blocks + nw - 1) / nw;
+  const Chunking ch = chunking(ntiles, rounds);
+  const int items = ntiles * ch.nchunks;
+  if (tid == 0) tilemask = 0u;
+  for (int w = blockIdx.x; w < items; w += gridDim.x) {
+    const int t = w / ch.nchunks, c = w % ch.nchunks;
+    const int p0 = t * T;
+    const int nvalid = min(T, R - p0);
+    {
+      const W *src = bits + (size_t)t * N;
+      if ((reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+        const int n16 = (int)(((size_t)N * sizeof(W)) / 16);
+        for (int i = tid; i < n16; i += blockDim.x) reinterpret_cast<int4 *>(tile)[i] = load_stream(reinterpret_cast<const int4 *>(src) + i);
+        for (int k = n16 * (int)(16 / sizeof(W)) + tid; k < N; k += blockDim.x) tile[k] = src[k];
+      } else {
+        for (int k = tid; k < N; k += blockDim.x) tile[k] = src[k];
+      }
+    }
+    __syncthreads();
+    unsigned live = 0u;
+    const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
+    for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
+      const int blk = r * nw + wave;
+      if (blk >= blocks) break;
+      int jo[OPL];
+      bool jin[OPL];
+#pragma unroll
+      for (int u = 0; u < OPL; ++u) {
+        jo[u] = blk * 64 * OPL + u * 64 + lane;
+        jin[u] = jo[u] < N;
+      }
+      // the 32 source indices of each output, 8 per load (outputs past N read output N - 1)
+      uint4 ix[OPL][4];
+#pragma unroll
+      for (int u = 0; u < OPL; ++u)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) ix[u][g] = ell16[(size_t)g * N + min(jo[u], N - 1)];
+      auto word = [&](int sl) -> unsigned {
+        unsigned x = 0u;
+#pragma unroll
+        for (int u = 0; u < OPL; ++u) {
+          const uint4 q = ix[u][sl >> 3];
+          const unsigned pr = ((sl & 7) < 4) ? ((sl & 7) < 2 ? q.x : q.y) : ((sl & 7) < 6 ? q.z : q.w);
+          const unsigned k = (sl & 1) ? (pr >> 16) : (pr & 0xffffu);
+          x |= (unsigned)tile[k] << (16 * u);
+        }
+        return x;
+      };
+      // carry-save adder tree over two blocks of 16 source words
+      unsigned ones = 0u, twos = 0u, fours = 0u, eights = 0u, s16[2];
+#pragma unroll
+      for (int blk16 = 0; blk16 < 2; ++blk16) {
+        const int b0 = 16 * blk16;
+        unsigned twosA, twosB, foursA, foursB, eightsA, eightsB;
+        csa(twosA, ones, ones, word(b0 + 0), word(b0 + 1));
+        csa(twosB, ones, ones, word(b0 + 2), word(b0 + 3));
+        csa(foursA, twos, twos, twosA, twosB);
+        csa(twosA, ones, ones, word(b0 + 4), word(b0 + 5));
+        csa(twosB, ones, ones, word(b0 + 6), word(b0 + 7));
+        csa(foursB, twos, twos, twosA, twosB);
+        csa(eightsA, fours, fours, foursA, foursB);
+        csa(twosA, ones, ones, word(b0 + 8), word(b0 + 9));
+        csa(twosB, ones, ones, word(b0 + 10), word(b0 + 11));
+        csa(foursA, twos, twos, twosA, twosB);
+        csa(twosA, ones, ones, word(b0 + 12), word(b0 + 13));
+        csa(twosB, ones, ones, word(b0 + 14), word(b0 + 15));
+        csa(foursB, twos, twos, twosA, twosB);
+        csa(eightsB, fours, fours, foursA, foursB);
+        csa(s16[blk16], eights, eights, eightsA, eightsB);
+      }
+      const unsigned pl[6] = {ones, twos, fours, eights, s16[0] ^ s16[1], s16[0] & s16[1]};
+      // rows whose count reaches cmin (bit-sliced comparison from the top plane down)
+      unsigned gt = 0u, eq = 0xffffffffu;
+#pragma unroll
+      for (int i = 5; i >= 0; --i) {
+        if ((cmin >> i) & 1) {
+          eq &= pl[i];
+        } else {
+          gt |= eq & pl[i];
+          eq &= ~pl[i];
+        }
+      }
+      const unsigned ge = cmin > 63 ? 0u : (gt | eq);
+      // transpose the planes into one byte per row: dword d holds rows 4d..4d+3
+      unsigned cw[8];
+#pragma unroll
+      for (int d = 0; d < 8; ++d) {
+        unsigned acc = 0u;
+#pragma unroll
+        for (int i = 0; i < 6; ++i) {
+          const unsigned nib = (pl[i] >> (4 * d)) & 15u;
+          acc |= ((nib * 0x00204081u) & 0x01010101u) << i;
+        }
+        cw[d] = acc;
+      }
+#pragma unroll
+      for (int u = 0; u < OPL; ++u) {
+        if (!jin[u]) continue;
+        const unsigned rows = T == 16 ? ((ge >> (16 * u)) & 0xffffu) : ge;
+        live |= rows;
+        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 >> 5) * N + jo[u]) * 32 + (p0 & 31));
+        if (T == 32) {
+          store_stream(dst, make_uint4(cw[0], cw[1], cw[2], cw[3]));
+          store_stream(dst + 1, make_uint4(cw[4], cw[5], cw[6], cw[7]));
+        } else {
+          store_stream(dst, make_uint4(cw[4 * u], cw[4 * u + 1], cw[4 * u + 2], cw[4 * u + 3]));
+          // the last 32-row tile has no second half: its slots 16..31 get code 0 (+0.0)
+          if ((p0 & 31) == 0 && t + 1 == ntiles) store_stream(dst + 1, make_uint4(0u, 0u, 0u, 0u));
+        }
+      }
+    }
+    if (live) atomicOr(&tilemask, live);
+    __syncthreads();
+    if (tid == 0) {
+      unsigned m = tilemask;
+      tilemask = 0u;
+      m &= nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
+      if (m) atomicOr(&masks[p0 >> 5], m << (p0 & 31));
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------------------------------------------------------
 // Host side
 
@@ -1132,6 +1362,10 @@ struct LayerDev {
   const int2 *ell = nullptr;
   const float *bias = nullptr;
   int K = 0;
+  // uniform layer: every column holds exactly K sources, all weights are w and all biases b
+  bool uniform = false;
+  float w = 0.0f, b = 0.0f;
+  const uint4 *ell16 = nullptr;  // layer 0 of a uniform layer with K == 32: [K/8][N][8] u16 source indices
 };
 
 }  // namespace
@@ -1344,6 +1578,27 @@ hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits
   return launch_layer_bits_k<T, 0, false>(net, ld, bits, fout, count);
 }
 
+// Layer 0 of a uniform layer by counting (see k_layer_count): dictionary, then the counts as codes.
+template <int T>
+hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bits, unsigned char *cout,
+                              const int *count) {
+  using W = typename BitWord<T>::type;
+  static bool configured = false;
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_count<T>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  hipLaunchKernelGGL(k_count_dict, dim3(1), dim3(64), 0, net->stream, net->dict, net->misc, ld.K, ld.w, ld.b, net->ymax);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds = 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+  hipLaunchKernelGGL(k_layer_count<T>, dim3(net->cus), dim3(1024), lds, net->stream, reinterpret_cast<const W *>(bits),
+                     cout, net->N, ld.ell16, net->misc, count, net->masks);
+  return hipGetLastError();
+}
+
 // A layer whose input tiles hold dictionary codes (see k_layer_gfm_u8); rounds of 8 tiles.
 hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
                          int64_t max_tiles, unsigned *masks) {
@@ -1433,11 +1688,14 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   if (col_ptr[0] < 0) return fail(SDNN_EINVAL, "negative column offset");
   // ---- validate every layer before touching the device (layers in parallel on host threads)
   std::vector<int> K((size_t)nl, 0);
+  std::vector<char> uniform((size_t)nl, 0);
   std::vector<std::string> err((size_t)nl);
   parallel_for(nl, [&](int32_t i) {
     const int64_t *cp = col_ptr + (size_t)i * (N + 1);
     char buf[256];
-    int kmax = 0;
+    int kmax = 0, kmin = kMaxDegree + 1;
+    bool same_w = true;
+    const int64_t e0 = cp[0];
     for (int32_t j = 0; j < N; ++j) {
       const int64_t a = cp[j], b = cp[j + 1];
       if (b < a) { snprintf(buf, sizeof buf, "layer %d column %d: decreasing offsets", l0 + i, j); err[(size_t)i] = buf; return; }
@@ -1447,12 +1705,18 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         if (k < 0 || k >= N) { snprintf(buf, sizeof buf, "layer %d column %d: source %d out of range", l0 + i, j, k); err[(size_t)i] = buf; return; }
         if (e > a && k <= row_idx[e - 1]) { snprintf(buf, sizeof buf, "layer %d column %d: sources not strictly ascending", l0 + i, j); err[(size_t)i] = buf; return; }
         if (!std::isfinite(val[e])) { snprintf(buf, sizeof buf, "layer %d column %d: non-finite weight", l0 + i, j); err[(size_t)i] = buf; return; }
+        same_w = same_w && std::memcmp(&val[e], &val[e0], sizeof(float)) == 0;
       }
       kmax = std::max<int>(kmax, (int)(b - a));
+      kmin = std::min<int>(kmin, (int)(b - a));
     }
-    for (int32_t j = 0; j < N; ++j)
+    bool same_b = true;
+    for (int32_t j = 0; j < N; ++j) {
       if (!std::isfinite(bias[(size_t)i * N + j])) { snprintf(buf, sizeof buf, "layer %d: non-finite bias", l0 + i); err[(size_t)i] = buf; return; }
+      same_b = same_b && std::memcmp(&bias[(size_t)i * N + j], &bias[(size_t)i * N], sizeof(float)) == 0;
+    }
     K[(size_t)i] = std::max(kmax, 1);
+    uniform[(size_t)i] = kmax > 0 && kmin == kmax && same_w && same_b;
   });
   for (int32_t i = 0; i < nl; ++i)
     if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
@@ -1508,6 +1772,30 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     ld.ell = reinterpret_cast<const int2 *>(mem) + layer_off[(size_t)i];
     ld.bias = reinterpret_cast<const float *>(mem + ell_bytes) + (size_t)i * N;
     ld.K = K[(size_t)i];
+    ld.uniform = uniform[(size_t)i] != 0;
+    if (ld.uniform) {
+      ld.w = val[col_ptr[(size_t)i * (N + 1)]];
+      ld.b = bias[(size_t)i * N];
+    }
+  }
+  if (l0 == 0 && net->path == 1 && net->layers[0].uniform && net->layers[0].K == 32) {
+    // layer 0 of a uniform network: 16-bit source indices, 8 slots per 16-byte group, for the
+    // counting kernel
+    const int Kq = 32;
+    std::vector<uint16_t> h16((size_t)N * Kq);
+    const int64_t *cp = col_ptr;
+    for (int32_t j = 0; j < N; ++j)
+      for (int sl = 0; sl < Kq; ++sl)
+        h16[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)row_idx[cp[j] + sl];
+    char *m16 = nullptr;
+    e = hipMalloc(reinterpret_cast<void **>(&m16), h16.size() * sizeof(uint16_t));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", h16.size() * sizeof(uint16_t), hipGetErrorString(e));
+    }
+    net->allocations.push_back(m16);
+    HIP_OR_POISON(net, hipMemcpy(m16, h16.data(), h16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+    net->layers[0].ell16 = reinterpret_cast<const uint4 *>(m16);
   }
   net->n_loaded += nl;
   g_err.clear();
@@ -1620,7 +1908,9 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     if (l == 0) {
       // layer 0 reads the caller's rows; binary inputs go through bit tiles (built in fm[0]),
       // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
-      const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 &&
+      // the pack pass addresses rows with 32-bit offsets (in floats, or float4 when N % 4 == 0)
+      const uint64_t units = (uint64_t)M * (uint64_t)net->N / ((net->N & 3) == 0 ? 4 : 1);
+      const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 && units < (1ull << 32) &&
                             (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <= 160 * 1024;
       bool bits_route = false;
       if (try_bits) {
@@ -1630,7 +1920,17 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         HIP_OR_POISON(net, hipStreamSynchronize(s));
         bits_route = net->pinned[6] == 0;
       }
-      if (bits_route) {
+      const LayerDev &ld0 = net->layers[0];
+      if (bits_route && P > one_round && net->L > 1 && ld0.uniform && ld0.ell16 && ld0.w > 0.0f) {
+        // a uniform layer: the output of a column is a function of how many of its sources are 1,
+        // so the counts are the codes (see k_layer_count)
+        fout_codes = true;
+        net->layer_kernel[0] = SDNN_KERNEL_BITS_COUNT;
+        net->layer_launches[0] = 3;  // pack + dictionary + count
+        unsigned char *cout = reinterpret_cast<unsigned char *>(fout);
+        HIP_OR_POISON(net, net->bitsT == 32 ? launch_layer_count<32>(net, ld0, net->fm[0], cout, npos + cur)
+                                            : launch_layer_count<16>(net, ld0, net->fm[0], cout, npos + cur));
+      } else if (bits_route) {
         // outputs of a layer on binary inputs take few distinct values: a large layer 0 writes them
         // as one-byte dictionary codes, which the next layer gathers four times denser
         fout_codes = P > one_round && net->L > 1;
