@@ -234,29 +234,66 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
 
 // After a compaction of the global-tile path: move the live positions of a layer's output tiles
 // into fresh tiles, dst[t][k][b] = the value at list position src[32t + b] of the source tiles
-// (tile src / 32, slot src % 32), for positions below *npos; zero past it. 8 threads per 128-byte
-// segment, 4 slots each.
+// (tile src / 32, slot src % 32), for positions below *npos; zero past it. A work item is one new
+// tile and kRepackSources sources. The new tile's rows come from at most 32 old tiles (src is
+// ascending); for each of them, 8 lanes read a source's whole 128-byte segment (one 16-byte load
+// each), keep the rows the new tile takes, and place them in an LDS stage from which the new
+// segments are written whole. So each needed old segment is read once, coalesced.
+constexpr int kRepackSources = 256;
 __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
                                                 const int *__restrict__ src, const int *__restrict__ npos) {
+  __shared__ int otile[32];            // distinct old tiles of this new tile
+  __shared__ unsigned omask[32];       // their slots that this new tile takes
+  __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
+  __shared__ int nold;
+  __shared__ float stage[32][33];
   const int R = *npos;
   const int ntiles = (R + 31) / 32;
-  const size_t items = (size_t)ntiles * N * 8;
-  for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
-    const int qd = (int)(it & 7);
-    const size_t rest = it >> 3;
-    const int k = (int)(rest % N);
-    const int t = (int)(rest / N);
-    float v[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      const int p = t * 32 + qd * 4 + c;
-      v[c] = 0.0f;
-      if (p < R) {
-        const int sp = src[p];
-        v[c] = sfm[((size_t)(sp >> 5) * N + k) * 32 + (sp & 31)];
+  const int nkc = (N + kRepackSources - 1) / kRepackSources;
+  const int tid = threadIdx.x, kk = tid >> 3, q = tid & 7;
+  for (int item = blockIdx.x; item < ntiles * nkc; item += gridDim.x) {
+    const int t = item / nkc, k0 = (item % nkc) * kRepackSources;
+    const int nb = min(32, R - t * 32);
+    if (tid == 0) {
+      int n = 0, last = -1;
+      for (int b = 0; b < nb; ++b) {
+        const int sp = src[t * 32 + b];
+        const int ot = sp >> 5;
+        if (ot != last) {
+          otile[n] = ot;
+          omask[n] = 0u;
+          ++n;
+          last = ot;
+        }
+        omask[n - 1] |= 1u << (sp & 31);
+        bslot[n - 1][sp & 31] = (unsigned char)b;
       }
+      nold = n;
     }
-    *reinterpret_cast<float4 *>(dfm + ((size_t)t * N + k) * 32 + qd * 4) = make_float4(v[0], v[1], v[2], v[3]);
+    __syncthreads();
+    const int n = nold;
+    for (int kb = 0; kb < kRepackSources; kb += 32) {
+      const int k = k0 + kb + kk;
+      // rows not taken from any old tile (past nb) stay zero
+      for (int i = tid; i < 32 * 32; i += blockDim.x) stage[i >> 5][i & 31] = 0.0f;
+      __syncthreads();
+      if (k < N) {
+        for (int i = 0; i < n; ++i) {
+          const unsigned m = (omask[i] >> (4 * q)) & 15u;
+          if (!m) continue;
+          const float4 v = load_stream_f4(reinterpret_cast<const float4 *>(sfm + ((size_t)otile[i] * N + k) * 32) + q);
+          const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if ((m >> c) & 1u) stage[kk][bslot[i][4 * q + c]] = e[c];
+        }
+      }
+      __syncthreads();
+      if (k < N)
+        *reinterpret_cast<float4 *>(dfm + ((size_t)t * N + k) * 32 + 4 * q) =
+            make_float4(stage[kk][4 * q], stage[kk][4 * q + 1], stage[kk][4 * q + 2], stage[kk][4 * q + 3]);
+      __syncthreads();
+    }
   }
 }
 
@@ -282,9 +319,10 @@ __global__ void k_final_ids(const int *__restrict__ ids, const int *__restrict__
 struct Chunking {
   int nchunks, rounds_per_chunk;
 };
-__device__ __forceinline__ Chunking chunking(int ntiles, int rounds) {
+__device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chunks = 1) {
   int nchunks = ntiles > 0 ? (int)gridDim.x / ntiles : 1;
-  nchunks = max(1, min(nchunks, rounds));
+  nchunks = max(min_chunks, min(nchunks, rounds));
+  nchunks = min(nchunks, rounds);
   const int rpc = (rounds + nchunks - 1) / nchunks;
   return {(rounds + rpc - 1) / rpc, rpc};
 }
@@ -2005,8 +2043,9 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (!compacted) HIP_OR_POISON(net, compact());
       compacted = true;
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
-      const int64_t items = tiles(live_bound) * net->N * 8;
-      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+      const int64_t items = fout_codes ? tiles(live_bound) * net->N * 8 / 256
+                                       : tiles(live_bound) * ((net->N + kRepackSources - 1) / kRepackSources);
+      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
       if (fout_codes)
         hipLaunchKernelGGL(k_repack_u8, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
                            reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
