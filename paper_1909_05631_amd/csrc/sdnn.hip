@@ -319,6 +319,18 @@ __global__ void k_final_ids(const int *__restrict__ ids, const int *__restrict__
 struct Chunking {
   int nchunks, rounds_per_chunk;
 };
+
+// Tile of item w when whole tiles are the items and tpg consecutive tiles share one code group:
+// the tpg tiles of a group go to workgroups of the same XCD (workgroup x runs on XCD x % 8), so the
+// parts that they write of each code segment meet in that XCD's L2. A bijection of
+// [0, gridDim * ceil(n / gridDim)) onto itself; needs gridDim % (8 * tpg) == 0.
+__device__ __forceinline__ int code_group_tile(int w, int tpg) {
+  const int per_iter = gridDim.x;
+  const int k = w / per_iter, x = w % per_iter;
+  const int xcd = x & 7, sl = x >> 3;
+  const int g = k * (per_iter / tpg) + xcd + 8 * (sl / tpg);
+  return tpg * g + sl % tpg;
+}
 __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chunks = 1) {
   int nchunks = ntiles > 0 ? (int)gridDim.x / ntiles : 1;
   nchunks = max(min_chunks, min(nchunks, rounds));
@@ -783,6 +795,8 @@ constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 1
 // afterwards, so a workgroup may cache them in LDS.
 constexpr unsigned kDictEmpty = 0x7fc00000u;
 constexpr int kDictSlots = 256;
+// Code tiles hold 64 list positions: [tile][N][64] bytes, list position p at tile p / 64, byte p % 64.
+constexpr int kCodeRows = 64;
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
@@ -815,27 +829,30 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 }
 
 // One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
-// (source k of list position 32t + b), decoded as dict[code]; the output is fp32 tiles as in
-// k_layer_gfm, with the same XCD mapping of tiles. A code segment is 32 bytes, so a tile of 65536
-// sources takes 2 MiB of its XCD's L2. Lane = (half = lane % 2: rows 16*half..+15, o = lane / 2):
-// each gather is one 16-byte load of 16 codes, a wave instruction serves 32 outputs, and a work
-// item is a chunk of 128 outputs. The dictionary sits in LDS; the ELL entries are read directly,
-// the next group's while the current group's gathers are in flight.
+// (source k of list position 64t + b), decoded as dict[code]; the output is fp32 tiles of 32 rows
+// as in k_layer_gfm (code tile t covers output tiles 2t and 2t + 1). Code tiles [tile0, tile0 + 8)
+// go one per XCD, as in k_layer_gfm; a tile of 65536 sources takes 4 MiB, one XCD's L2. A code
+// segment is 64 bytes: 16 lanes read it with 4-byte loads (4 codes each), so a wave instruction
+// serves 4 outputs (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane =
+// (r = lane % 16: rows 4r..4r+3, o = lane / 16); a wave takes 32 outputs, 8 per lane, and a work
+// item is a chunk of 128 outputs. The dictionary and the chunk's ELL rows sit in LDS.
 template <int KC>
 __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
                                                       const float *__restrict__ bias, float ymax,
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, int tile0) {
-  constexpr int FMR = 32, CH = 128;
+  constexpr int CR = kCodeRows, CH = 128, OPL = 8;
+  constexpr int KS = KC > 0 ? KC : 1;
   __shared__ float dl[kDictSlots];
-  __shared__ unsigned rowmask;
+  __shared__ int2 ells[KS * CH];
+  __shared__ float bstage[CH];
+  __shared__ unsigned long long rowmask;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = dict[i];
-  if (tid == 0) rowmask = 0u;
-  __syncthreads();
+  if (tid == 0) rowmask = 0ull;
   const int R = *npos;
-  const int nt = min(8, (R + FMR - 1) / FMR - tile0);
+  const int nt = min(8, (R + CR - 1) / CR - tile0);
   const int parts = nt > 0 ? 8 / nt : 1;
   const int xcd = blockIdx.x & 7;
   const bool active = nt > 0 && xcd < nt * parts;
@@ -843,99 +860,128 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
   const int cpp = (nchunks + parts - 1) / parts;
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
-  const int half = lane & 1, o = lane >> 1;
+  const int r = lane & 15, o = lane >> 4;
   const int per_xcd = gridDim.x >> 3;
-  const int nvalid = active ? min(FMR, R - t * FMR) : 0;
-  const unsigned char *tb = cin + (size_t)t * N * FMR + half * 16;
-  float *obase = fout + (size_t)t * N * FMR + half * 16;
-  unsigned lm = 0u;
+  const int nvalid = active ? min(CR, R - t * CR) : 0;
+  const unsigned char *tb = cin + (size_t)t * N * CR + 4 * r;
+  // output rows 4r..4r+3 of the code tile: fp32 tile 2t + (4r >= 32), slots (4r) % 32
+  float *obase = fout + ((size_t)(2 * t + (r >> 3)) * N) * 32 + (4 * r) % 32;
+  unsigned long long lm = 0ull;
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
-    const int j = chunk * CH + wave * 32 + o;
-    const int2 *ej = ell + min(j, N - 1);
-    float acc[16];
+    const int c0 = chunk * CH;
+    const int nout = min(CH, N - c0);
+    __syncthreads();  // the previous chunk is done with ells / bstage
+    for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
+    if constexpr (KC > 0) {
+      // stage [slot][128 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
+      for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
+        const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
+        const int2 *src = ell + (size_t)sl * N + c0 + pr;
+        int4 v = make_int4(0, 0, 0, 0);
+        if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+          v = load_stream(reinterpret_cast<const int4 *>(src));
+        } else {
+          if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
+          if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
+        }
+        *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
+      }
+    }
+    __syncthreads();
+    const int jl0 = wave * 32 + o;  // this lane's outputs: jl0 + 4i, i < OPL
+    float acc[OPL][4];
 #pragma unroll
-    for (int b = 0; b < 16; ++b) acc[b] = 0.0f;
-    auto term = [&](uint4 c, float w) {
-      const unsigned cw[4] = {c.x, c.y, c.z, c.w};
+    for (int i = 0; i < OPL; ++i)
 #pragma unroll
-      for (int b = 0; b < 16; ++b) acc[b] = fmaf(dl[(cw[b >> 2] >> (8 * (b & 3))) & 255u], w, acc[b]);
+      for (int c = 0; c < 4; ++c) acc[i][c] = 0.0f;
+    auto term = [&](int i, unsigned word, float w) {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dl[(word >> (8 * c)) & 255u], w, acc[i][c]);
     };
     if constexpr (KC > 0) {
-      static_assert(KC % 8 == 0, "KC must be a multiple of 8");
-      int2 e[8];
+      // software pipeline: the next slot's gathers are issued before this slot's fmas
+      unsigned wd[2][OPL];
+      float wv[2][OPL];
+      auto fetch = [&](int sl, int bf) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) e[i] = ej[(size_t)i * N];
-#pragma unroll
-      for (int g = 0; g < KC; g += 8) {
-        uint4 c[8];
-        float w[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          c[i] = *reinterpret_cast<const uint4 *>(tb + (e[i].x >> 2));
-          w[i] = __int_as_float(e[i].y);
+        for (int i = 0; i < OPL; ++i) {
+          const int2 e = ells[sl * CH + jl0 + 4 * i];
+          wd[bf][i] = *reinterpret_cast<const unsigned *>(tb + (e.x >> 1));
+          wv[bf][i] = __int_as_float(e.y);
         }
-        if (g + 8 < KC) {
+      };
+      fetch(0, 0);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) e[i] = ej[(size_t)(g + 8 + i) * N];
-        }
+      for (int sl = 0; sl < KC; ++sl) {
+        if (sl + 1 < KC) fetch(sl + 1, (sl + 1) & 1);
         mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) term(c[i], w[i]);
+        for (int i = 0; i < OPL; ++i) term(i, wd[sl & 1][i], wv[sl & 1][i]);
+        // this slot's fmas complete here, before the slot after next is fetched
+#pragma unroll
+        for (int i = 0; i < OPL; ++i) pin4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
       }
     } else {
       for (int sl = 0; sl < K; ++sl) {
-        const int2 e = ej[(size_t)sl * N];
-        term(*reinterpret_cast<const uint4 *>(tb + (e.x >> 2)), __int_as_float(e.y));
+#pragma unroll
+        for (int i = 0; i < OPL; ++i) {
+          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + 4 * i, N - 1)];
+          term(i, *reinterpret_cast<const unsigned *>(tb + (e.x >> 1)), __int_as_float(e.y));
+        }
       }
     }
-    // every lane finishes its chain (outputs past N repeat output N - 1), only real outputs store
-    const float b = bias[min(j, N - 1)];
-    unsigned bits = 0u;
-    float y[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      y[r] = activate(acc[r], b, ymax);
-      bits |= (y[r] > 0.0f ? 1u : 0u) << r;
-    }
-    lm |= (j < N ? bits : 0u) << (16 * half);
-    if (j < N) {
-      float4 *dst = reinterpret_cast<float4 *>(obase + (size_t)j * FMR);
-#pragma unroll
-      for (int n = 0; n < 4; ++n) store_stream(dst + n, make_float4(y[4 * n], y[4 * n + 1], y[4 * n + 2], y[4 * n + 3]));
+    for (int i = 0; i < OPL; ++i) {
+      const int jl = jl0 + 4 * i;
+      if (jl < nout) {
+        const float b = bstage[jl];
+        const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
+                                     activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
+        store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jl) * 32), y);
+        const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
+        lm |= (unsigned long long)bits << (4 * r);
+      }
     }
   }
+  // rows of this code tile that stayed live in any of this workgroup's chunks
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+  __syncthreads();
   if (lane == 0 && lm) atomicOr(&rowmask, lm);
   __syncthreads();
-  if (tid == 0) {
-    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
-    if (active && (rowmask & valid)) atomicOr(&masks[t], rowmask & valid);
+  if (tid == 0 && active) {
+    const unsigned long long valid = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1ull);
+    const unsigned long long m = rowmask & valid;
+    if (m & 0xffffffffull) atomicOr(&masks[2 * t], (unsigned)m);
+    if (m >> 32) atomicOr(&masks[2 * t + 1], (unsigned)(m >> 32));
   }
 }
 
-// k_repack for one-byte code tiles: positions past *npos get code 0 (+0.0).
+// Repack of one-byte code tiles (kCodeRows positions each) after a compaction: position p of the
+// new tiles takes the code at position src[p] of the old ones; positions past *npos get code 0
+// (+0.0). A thread writes 4 codes of one source.
 __global__ __launch_bounds__(256) void k_repack_u8(const unsigned char *__restrict__ sfm, unsigned char *__restrict__ dfm,
                                                    int N, const int *__restrict__ src, const int *__restrict__ npos) {
+  constexpr int QPS = kCodeRows / 4;  // 4-byte quads per source segment
   const int R = *npos;
-  const int ntiles = (R + 31) / 32;
-  const size_t items = (size_t)ntiles * N * 8;
+  const int ntiles = (R + kCodeRows - 1) / kCodeRows;
+  const size_t items = (size_t)ntiles * N * QPS;
   for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
-    const int qd = (int)(it & 7);
-    const size_t rest = it >> 3;
+    const int qd = (int)(it % QPS);
+    const size_t rest = it / QPS;
     const int k = (int)(rest % N);
     const int t = (int)(rest / N);
     unsigned word = 0u;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int p = t * 32 + qd * 4 + c;
+      const int p = t * kCodeRows + qd * 4 + c;
       if (p < R) {
         const int sp = src[p];
-        word |= (unsigned)sfm[((size_t)(sp >> 5) * N + k) * 32 + (sp & 31)] << (8 * c);
+        word |= (unsigned)sfm[((size_t)(sp / kCodeRows) * N + k) * kCodeRows + sp % kCodeRows] << (8 * c);
       }
     }
-    *reinterpret_cast<unsigned *>(dfm + ((size_t)t * N + k) * 32 + qd * 4) = word;
+    *reinterpret_cast<unsigned *>(dfm + ((size_t)t * N + k) * kCodeRows + qd * 4) = word;
   }
 }
 
@@ -1071,13 +1117,17 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   const int blocks = (N + 63) / 64;                 // output blocks of 64
   const int rounds = (blocks + nw - 1) / nw;        // rounds of one block per wave
   const Chunking ch = chunking(ntiles, rounds);
-  const int items = ntiles * ch.nchunks;
+  // codes with whole tiles as items: keep the tiles of one code group on one XCD
+  const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (kCodeRows / T)) == 0;
+  const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
   if (tid < 16) lut[tid] = make_float4((float)(tid & 1), (float)((tid >> 1) & 1), (float)((tid >> 2) & 1), (float)((tid >> 3) & 1));
   if (tid == 0) tilemask = 0u;
   if (CODES)
     for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = kDictEmpty;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
-    const int t = w / ch.nchunks, c = w % ch.nchunks;
+    const int t = grouped ? code_group_tile(w, kCodeRows / T) : w / ch.nchunks;
+    const int c = grouped ? 0 : w % ch.nchunks;
+    if (t >= ntiles) continue;  // uniform over the workgroup
     const int p0 = t * T;
     const int nvalid = min(T, R - p0);
     {
@@ -1173,7 +1223,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         const float bj = bias[j];
         if constexpr (CODES) {
           uint4 *dst = reinterpret_cast<uint4 *>(reinterpret_cast<unsigned char *>(fout) +
-                                                 ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
+                                                 ((size_t)(p0 / kCodeRows) * N + j) * kCodeRows + p0 % kCodeRows);
           unsigned cw[T / 4];
 #pragma unroll
           for (int n = 0; n < T / 4; ++n) {
@@ -1188,8 +1238,9 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
           }
 #pragma unroll
           for (int n = 0; n < T / 16; ++n) dst[n] = make_uint4(cw[4 * n], cw[4 * n + 1], cw[4 * n + 2], cw[4 * n + 3]);
-          // the last 32-row tile has no second half: its slots 16..31 get code 0 (+0.0)
-          if (T == 16 && (p0 & 31) == 0 && t + 1 == ntiles) dst[1] = make_uint4(0u, 0u, 0u, 0u);
+          // the rest of the last code tile gets code 0 (+0.0)
+          if (t + 1 == ntiles)
+            for (int n = T / 16; n < (kCodeRows - p0 % kCodeRows) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
         } else {
           float4 *dst = reinterpret_cast<float4 *>(fout + ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
 #pragma unroll
@@ -1272,10 +1323,14 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   const int blocks = (N + 64 * OPL - 1) / (64 * OPL);  // output blocks of one wave
   const int rounds = (blocks + nw - 1) / nw;
   const Chunking ch = chunking(ntiles, rounds);
-  const int items = ntiles * ch.nchunks;
+  // whole tiles as items: keep the tiles of one code group on one XCD
+  const bool grouped = ch.nchunks == 1 && gridDim.x % (8 * (kCodeRows / T)) == 0;
+  const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
   if (tid == 0) tilemask = 0u;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
-    const int t = w / ch.nchunks, c = w % ch.nchunks;
+    const int t = grouped ? code_group_tile(w, kCodeRows / T) : w / ch.nchunks;
+    const int c = grouped ? 0 : w % ch.nchunks;
+    if (t >= ntiles) continue;  // uniform over the workgroup
     const int p0 = t * T;
     const int nvalid = min(T, R - p0);
     {
@@ -1370,15 +1425,17 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
         if (!jin[u]) continue;
         const unsigned rows = T == 16 ? ((ge >> (16 * u)) & 0xffffu) : ge;
         live |= rows;
-        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 >> 5) * N + jo[u]) * 32 + (p0 & 31));
+        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / kCodeRows) * N + jo[u]) * kCodeRows + p0 % kCodeRows);
+        // plain stores: the tiles of one 64-row code group fill each segment in parts, merged in L2
         if (T == 32) {
-          store_stream(dst, make_uint4(cw[0], cw[1], cw[2], cw[3]));
-          store_stream(dst + 1, make_uint4(cw[4], cw[5], cw[6], cw[7]));
+          dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+          dst[1] = make_uint4(cw[4], cw[5], cw[6], cw[7]);
         } else {
-          store_stream(dst, make_uint4(cw[4 * u], cw[4 * u + 1], cw[4 * u + 2], cw[4 * u + 3]));
-          // the last 32-row tile has no second half: its slots 16..31 get code 0 (+0.0)
-          if ((p0 & 31) == 0 && t + 1 == ntiles) store_stream(dst + 1, make_uint4(0u, 0u, 0u, 0u));
+          dst[0] = make_uint4(cw[4 * u], cw[4 * u + 1], cw[4 * u + 2], cw[4 * u + 3]);
         }
+        // the rest of the last code tile gets code 0 (+0.0)
+        if (t + 1 == ntiles)
+          for (int n = T / 16; n < (kCodeRows - p0 % kCodeRows) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
       }
     }
     if (live) atomicOr(&tilemask, live);
@@ -1637,9 +1694,11 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
   return hipGetLastError();
 }
 
-// A layer whose input tiles hold dictionary codes (see k_layer_gfm_u8); rounds of 8 tiles.
+// A layer whose input tiles hold dictionary codes (see k_layer_gfm_u8); rounds of 8 code tiles.
+// max_tiles: host bound on the 32-row tiles of the list.
 hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
                          int64_t max_tiles, unsigned *masks) {
+  max_tiles = (max_tiles + 1) / 2;  // code tiles of 64 rows
   const int rounds = (int)((max_tiles + 7) / 8);
   const int nchunks = (net->N + 127) / 128;
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
@@ -1988,7 +2047,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
                                        npos + cur, tiles(P), mk));
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
-      net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
+      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + 1) / 2 + 7) / 8);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -2043,7 +2102,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (!compacted) HIP_OR_POISON(net, compact());
       compacted = true;
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
-      const int64_t items = fout_codes ? tiles(live_bound) * net->N * 8 / 256
+      const int64_t items = fout_codes ? (tiles(live_bound) + 1) / 2 * net->N * (kCodeRows / 4) / 256
                                        : tiles(live_bound) * ((net->N + kRepackSources - 1) / kRepackSources);
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
       if (fout_codes)
