@@ -545,21 +545,22 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
 // One round of a layer on global feature-major tiles of FMR = 32 rows: input tiles fin[t][k][b]
 // (source k of list position 32t + b), output tiles fout in the same layout and positions; tiles
 // [tile0, tile0 + 8) of the list, one per XCD. blockDim 256 (4 waves); a work item is a chunk of
-// kGfmOutputs = 64 outputs. Lane = (row quad q = lane % 8, output slot h = lane / 8): each gather is
-// one 16-byte load of rows 4q..4q+3 of one source, so a wave instruction fetches the 128-byte
-// source segments of 8 outputs, and every lane runs two outputs' chains (slots h and h + 32 of the
-// chunk's halves) to keep 16 loads in flight; results go out as one 16-byte store per output, so a
-// wave writes 1 KiB of consecutive output segments. gridDim must be a multiple of 8: workgroup x
-// runs on XCD x % 8, and the workgroups of XCD x share the output chunks of one tile, which
-// therefore stays in that XCD's L2 (or, for the widest layers, in the Infinity Cache) for the whole
-// launch. With fewer than 8 tiles left, each tile's chunks are split over 8 / ntiles XCDs. For
-// KC > 0 the chunk's ELL rows are staged in LDS first, so the gathers are the only vector-memory
-// reads of the inner loop. Slots past the list's end hold zeros in fin and get zeros in fout.
+// kGfmOutputs = 64 outputs. Lane = (row b = lane % 32, h = lane / 32): a source segment of 128
+// bytes is read by 32 lanes with 4-byte loads (on gfx950 4-byte lane loads gather a segment three
+// times faster than 16-byte ones), so a wave instruction serves 2 outputs; each lane runs the
+// chains of 8 outputs (16 per wave), one slot ahead, and the results go out as 128-byte row
+// segments. gridDim must be a multiple of 8: workgroup x runs on XCD x % 8, and the workgroups of
+// XCD x share the output chunks of one tile, which therefore stays in that XCD's L2 (or, for the
+// widest layers, in the Infinity Cache) for the whole launch. With fewer than 8 tiles left, each
+// tile's chunks are split over 8 / ntiles XCDs. For KC > 0 the chunk's ELL rows are staged in LDS
+// with 16-byte loads, so the gathers are the only per-output memory reads. Slots past the list's
+// end hold zeros in fin and get zeros in fout.
 //
 // Workgroup 0 of the first round also does the list bookkeeping of the layer sequence: with
 // count_out set (a layer that follows one without compaction) it counts the previous layer's live
 // rows (masks_prev, complete since that kernel ended) into *count_out, and with masks_clear set it
-// clears that buffer, the one the next layer will use (three buffers rotate by layer).
+// clears that buffer, the one the next layer will use (three buffers rotate by layer). With
+// count_out set and no live row left (rows that die stay dead), the layer writes nothing.
 template <int FMR, int KC>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
@@ -567,127 +568,122 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                    int tile0, const unsigned *__restrict__ masks_prev,
                                                    unsigned *__restrict__ masks_clear, int *__restrict__ count_out) {
-  static_assert(FMR == 32, "the lane layout covers 32 rows with 8 lanes of float4");
-  static_assert(KC % 8 == 0, "KC must be a multiple of 8");
+  static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
+  constexpr int CH = kGfmOutputs, OPL = 8;
+  static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
   constexpr int KS = KC > 0 ? KC : 1;
-  constexpr int HALF = 32;  // outputs per pass of the 4 waves (8 each)
-  static_assert(kGfmOutputs == 2 * HALF, "two outputs per lane");
-  __shared__ int2 ells2[kGfmOutputs * KS];
-  __shared__ float bstage[kGfmOutputs];
+  __shared__ int2 ells[KS * CH];
+  __shared__ float bstage[CH];
   __shared__ unsigned rowmask;
+  __shared__ int prev_live;
   const int R = *npos;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (tid < 64) {
+    const int ntl = (R + FMR - 1) / FMR;
+    int c = 0;
+    if (count_out || (masks_clear && blockIdx.x == 0))
+      for (int i = tid; i < ntl; i += 64) {
+        if (count_out) c += __popc(masks_prev[i]);
+        if (masks_clear && blockIdx.x == 0) masks_clear[i] = 0u;
+      }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+    if (tid == 0) {
+      if (count_out && blockIdx.x == 0) *count_out = c;
+      prev_live = count_out ? c : 1;
+      rowmask = 0u;
+    }
+  }
+  __syncthreads();
   const int nt = min(8, (R + FMR - 1) / FMR - tile0);  // tiles in this round
   const int parts = nt > 0 ? 8 / nt : 1;
   const int xcd = blockIdx.x & 7;
-  const bool active = nt > 0 && xcd < nt * parts;  // uniform over the workgroup
-  const int nchunks = (N + kGfmOutputs - 1) / kGfmOutputs;
+  const bool active = nt > 0 && xcd < nt * parts && prev_live != 0;  // uniform over the workgroup
+  const int nchunks = (N + CH - 1) / CH;
   const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int q = lane & 7, h = lane >> 3;
+  const int b = lane & 31, h = lane >> 5;
   const int per_xcd = gridDim.x >> 3;
   const int nvalid = active ? min(FMR, R - t * FMR) : 0;
-  const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
-  float *obase = fout + (size_t)t * N * FMR + q * 4;
-  const int jA = wave * 8 + h, jB = jA + HALF;
-  if (tid == 0) rowmask = 0u;
-  if (blockIdx.x == 0 && tid < 64 && (count_out || masks_clear)) {
-    const int ntiles = (R + FMR - 1) / FMR;
-    int c = 0;
-    for (int i = tid; i < ntiles; i += 64) {
-      if (count_out) c += __popc(masks_prev[i]);
-      if (masks_clear) masks_clear[i] = 0u;
-    }
-    if (count_out) {
-#pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
-      if (tid == 0) *count_out = c;
-    }
-  }
-  unsigned lm = 0u;  // live rows seen by this lane: bit 4q + c
+  const float *tb = fin + (size_t)t * N * FMR + b;
+  float *ob = fout + (size_t)t * N * FMR + b;
+  const int jw = wave * 2 * OPL + h;  // this lane's outputs in the chunk: jw + 2i, i < OPL
+  bool live = false;
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
-    const int c0 = chunk * kGfmOutputs;
-    const int nout = min(kGfmOutputs, N - c0);
-    // stage this chunk's biases (and, for KC > 0, its ELL entries as [slot][output]); the ELL is
-    // read once per tile, streamed so it does not displace the tile from L2
-    for (int i = tid; i < kGfmOutputs; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
+    const int c0 = chunk * CH;
+    const int nout = min(CH, N - c0);
+    __syncthreads();  // the previous chunk is done with ells / bstage
+    for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
     if constexpr (KC > 0) {
-      for (int i = tid; i < KC * kGfmOutputs; i += blockDim.x) {
-        const int sl = i / kGfmOutputs, jj = i % kGfmOutputs;
-        long long e = 0;
-        if (jj < nout) e = __builtin_nontemporal_load(reinterpret_cast<const long long *>(ell + (size_t)sl * N + c0 + jj));
-        reinterpret_cast<long long *>(ells2)[sl * kGfmOutputs + jj] = e;
+      // stage [slot][64 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
+      for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
+        const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
+        const int2 *src = ell + (size_t)sl * N + c0 + pr;
+        int4 v = make_int4(0, 0, 0, 0);
+        if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
+          v = load_stream(reinterpret_cast<const int4 *>(src));
+        } else {
+          if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
+          if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
+        }
+        *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
       }
     }
     __syncthreads();
-    float aA[4] = {0.0f, 0.0f, 0.0f, 0.0f}, aB[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    float acc[OPL];
+#pragma unroll
+    for (int i = 0; i < OPL; ++i) acc[i] = 0.0f;
     if constexpr (KC > 0) {
-#pragma unroll 1
-      for (int g = 0; g < KC; g += 8) {
-        int2 evA[8], evB[8];
+      // software pipeline kDepth slots deep: a slot's gathers are issued kDepth - 1 slots before
+      // its fmas (each gather is one row of one output, so the depth is what keeps enough
+      // segments in flight to cover the L2 latency)
+      constexpr int kDepth = 4;
+      float g[kDepth][OPL], wv[kDepth][OPL];
+      auto fetch = [&](int sl, int bf) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          evA[i] = ells2[(g + i) * kGfmOutputs + jA];
-          evB[i] = ells2[(g + i) * kGfmOutputs + jB];
+        for (int i = 0; i < OPL; ++i) {
+          const int2 e = ells[sl * CH + jw + 2 * i];
+          g[bf][i] = tb[(unsigned)e.x >> 2];
+          wv[bf][i] = __int_as_float(e.y);
         }
-        float4 gA[8], gB[8];
+      };
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          gA[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)evA[i].x);
-          gB[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)evB[i].x);
-        }
-        // keep all 16 gathers in flight before the first fma waits on one
+      for (int sl = 0; sl < kDepth - 1; ++sl) fetch(sl, sl);
+#pragma unroll
+      for (int sl = 0; sl < KC; ++sl) {
+        if (sl + kDepth - 1 < KC) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
+        mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const float wA = __int_as_float(evA[i].y), wB = __int_as_float(evB[i].y);
-          aA[0] = fmaf(gA[i].x, wA, aA[0]);
-          aA[1] = fmaf(gA[i].y, wA, aA[1]);
-          aA[2] = fmaf(gA[i].z, wA, aA[2]);
-          aA[3] = fmaf(gA[i].w, wA, aA[3]);
-          aB[0] = fmaf(gB[i].x, wB, aB[0]);
-          aB[1] = fmaf(gB[i].y, wB, aB[1]);
-          aB[2] = fmaf(gB[i].z, wB, aB[2]);
-          aB[3] = fmaf(gB[i].w, wB, aB[3]);
-        }
+        for (int i = 0; i < OPL; ++i) acc[i] = fmaf(g[sl % kDepth][i], wv[sl % kDepth][i], acc[i]);
+#pragma unroll
+        for (int i = 0; i < OPL; i += 4) pin4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
       }
     } else {
-      const int2 *eA = ell + c0 + min(jA, nout - 1), *eB = ell + c0 + min(jB, nout - 1);
       for (int sl = 0; sl < K; ++sl) {
-        const int2 pA = eA[(size_t)sl * N], pB = eB[(size_t)sl * N];
-        const float4 vA = *reinterpret_cast<const float4 *>(tbase + (unsigned)pA.x);
-        const float4 vB = *reinterpret_cast<const float4 *>(tbase + (unsigned)pB.x);
-        const float wA = __int_as_float(pA.y), wB = __int_as_float(pB.y);
-        aA[0] = fmaf(vA.x, wA, aA[0]);
-        aA[1] = fmaf(vA.y, wA, aA[1]);
-        aA[2] = fmaf(vA.z, wA, aA[2]);
-        aA[3] = fmaf(vA.w, wA, aA[3]);
-        aB[0] = fmaf(vB.x, wB, aB[0]);
-        aB[1] = fmaf(vB.y, wB, aB[1]);
-        aB[2] = fmaf(vB.z, wB, aB[2]);
-        aB[3] = fmaf(vB.w, wB, aB[3]);
+#pragma unroll
+        for (int i = 0; i < OPL; ++i) {
+          const int2 e = ell[(size_t)sl * N + min(c0 + jw + 2 * i, N - 1)];
+          acc[i] = fmaf(tb[(unsigned)e.x >> 2], __int_as_float(e.y), acc[i]);
+        }
       }
     }
-    if (jA < nout) {
-      const float b = bstage[jA];
-      const float4 y = make_float4(activate(aA[0], b, ymax), activate(aA[1], b, ymax), activate(aA[2], b, ymax),
-                                   activate(aA[3], b, ymax));
-      store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jA) * FMR), y);
-      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u)) << (4 * q);
-    }
-    if (jB < nout) {
-      const float b = bstage[jB];
-      const float4 y = make_float4(activate(aB[0], b, ymax), activate(aB[1], b, ymax), activate(aB[2], b, ymax),
-                                   activate(aB[3], b, ymax));
-      store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jB) * FMR), y);
-      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u)) << (4 * q);
-    }
-    __syncthreads();
-  }
-  // rows of this tile that stayed live in any of this workgroup's chunks
 #pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+    for (int i = 0; i < OPL; ++i) {
+      const int jl = jw + 2 * i;
+      if (jl < nout) {
+        const float y = activate(acc[i], bstage[jl], ymax);
+        __builtin_nontemporal_store(y, ob + (size_t)(c0 + jl) * FMR);
+        live |= y > 0.0f;
+      }
+    }
+  }
+  // rows of this tile that stayed live in any of this workgroup's chunks: lanes b and b + 32 are
+  // row b
+  const unsigned long long bl = __ballot(live);
+  const unsigned lm = (unsigned)bl | (unsigned)(bl >> 32);
+  __syncthreads();
   if (lane == 0 && lm) atomicOr(&rowmask, lm);
   __syncthreads();
   if (tid == 0) {
