@@ -115,18 +115,14 @@ __device__ __forceinline__ void store_stream(uint4 *p, uint4 v) {
   __builtin_nontemporal_store(x, reinterpret_cast<v4u *>(p));
 }
 
+// 16-byte nontemporal load, for data that is read exactly once (the input rows). Data that other
+// workgroups read again (weights, activation tiles) takes plain loads, which measure faster.
 __device__ __forceinline__ float4 load_stream_f4(const float4 *p) {
   typedef float v4f __attribute__((ext_vector_type(4)));
   const v4f x = __builtin_nontemporal_load(reinterpret_cast<const v4f *>(p));
   return make_float4(x[0], x[1], x[2], x[3]);
 }
 
-// 16-byte load that streams past the L2 (read once per pass, keeps the L2 for data that is reused).
-__device__ __forceinline__ int4 load_stream(const int4 *p) {
-  typedef int v4i __attribute__((ext_vector_type(4)));
-  const v4i x = __builtin_nontemporal_load(reinterpret_cast<const v4i *>(p));
-  return make_int4(x[0], x[1], x[2], x[3]);
-}
 
 __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
@@ -281,7 +277,7 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
         for (int i = 0; i < n; ++i) {
           const unsigned m = (omask[i] >> (4 * q)) & 15u;
           if (!m) continue;
-          const float4 v = load_stream_f4(reinterpret_cast<const float4 *>(sfm + ((size_t)otile[i] * N + k) * 32) + q);
+          const float4 v = *(reinterpret_cast<const float4 *>(sfm + ((size_t)otile[i] * N + k) * 32) + q);
           const float e[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
           for (int c = 0; c < 4; ++c)
@@ -622,7 +618,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
         const int2 *src = ell + (size_t)sl * N + c0 + pr;
         int4 v = make_int4(0, 0, 0, 0);
         if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
-          v = load_stream(reinterpret_cast<const int4 *>(src));
+          v = *reinterpret_cast<const int4 *>(src);
         } else {
           if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
           if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
@@ -875,11 +871,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
         const int2 *src = ell + (size_t)sl * N + c0 + pr;
         int4 v = make_int4(0, 0, 0, 0);
         if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
-          v = load_stream(reinterpret_cast<const int4 *>(src));
+          v = *reinterpret_cast<const int4 *>(src);
         } else {
           if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
           if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
         }
+        // source offsets: fp32 32-row segments are 128 bytes, code segments 64
+        v.x = (int)((unsigned)v.x >> 1);
+        v.z = (int)((unsigned)v.z >> 1);
         *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
       }
     }
@@ -895,25 +894,46 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
       for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dl[(word >> (8 * c)) & 255u], w, acc[i][c]);
     };
     if constexpr (KC > 0) {
-      // software pipeline: the next slot's gathers are issued before this slot's fmas
-      unsigned wd[2][OPL];
-      float wv[2][OPL];
+      // software pipeline: a slot's gathers are issued one slot before its fmas (deeper pipelines
+      // measure no faster: the gathers are limited by the vector-memory path, not by latency)
+      constexpr int kDepth = 2;
+      unsigned wd[kDepth][OPL];
+      float wv[kDepth][OPL];
+      // the tile base is uniform, so a gather is one 32-bit offset from it
+      const unsigned char *tbs = cin + (size_t)t * N * CR;
+      const unsigned lofs = 4u * r;
       auto fetch = [&](int sl, int bf) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
           const int2 e = ells[sl * CH + jl0 + 4 * i];
-          wd[bf][i] = *reinterpret_cast<const unsigned *>(tb + (e.x >> 1));
+          wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)e.x + lofs));
           wv[bf][i] = __int_as_float(e.y);
         }
       };
-      fetch(0, 0);
+#pragma unroll
+      for (int sl = 0; sl < kDepth - 1; ++sl) fetch(sl, sl);
 #pragma unroll
       for (int sl = 0; sl < KC; ++sl) {
-        if (sl + 1 < KC) fetch(sl + 1, (sl + 1) & 1);
+        if (sl + kDepth - 1 < KC) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
         mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
+        // dictionary lookups run LA words ahead of the fmas that use them
+        constexpr int LA = 2;
+        float dv[LA + 1][4];
+        auto lookup = [&](int i) {
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) term(i, wd[sl & 1][i], wv[sl & 1][i]);
+          for (int c = 0; c < 4; ++c) dv[i % (LA + 1)][c] = dl[(wd[sl % kDepth][i] >> (8 * c)) & 255u];
+        };
+#pragma unroll
+        for (int i = 0; i < LA; ++i) lookup(i);
+#pragma unroll
+        for (int i = 0; i < OPL; ++i) {
+          if (i + LA < OPL) lookup(i + LA);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dv[i % (LA + 1)][c], wv[sl % kDepth][i], acc[i][c]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         // this slot's fmas complete here, before the slot after next is fetched
 #pragma unroll
         for (int i = 0; i < OPL; ++i) pin4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
@@ -1333,7 +1353,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
       const W *src = bits + (size_t)t * N;
       if ((reinterpret_cast<uintptr_t>(src) & 15) == 0) {
         const int n16 = (int)(((size_t)N * sizeof(W)) / 16);
-        for (int i = tid; i < n16; i += blockDim.x) reinterpret_cast<int4 *>(tile)[i] = load_stream(reinterpret_cast<const int4 *>(src) + i);
+        for (int i = tid; i < n16; i += blockDim.x) reinterpret_cast<int4 *>(tile)[i] = reinterpret_cast<const int4 *>(src)[i];
         for (int k = n16 * (int)(16 / sizeof(W)) + tid; k < N; k += blockDim.x) tile[k] = src[k];
       } else {
         for (int k = tid; k < N; k += blockDim.x) tile[k] = src[k];
