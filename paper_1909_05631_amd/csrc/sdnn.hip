@@ -234,10 +234,13 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
 // tile and kRepackSources sources. The new tile's rows come from at most 32 old tiles (src is
 // ascending); for each of them, 8 lanes read a source's whole 128-byte segment (one 16-byte load
 // each), keep the rows the new tile takes, and place them in an LDS stage from which the new
-// segments are written whole. So each needed old segment is read once, coalesced.
+// segments are written whole. So each needed old segment is read once, coalesced. With seglive
+// set, an old segment whose bit there is clear was never stored (all its rows are zero) and is not
+// read.
 constexpr int kRepackSources = 256;
 __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
-                                                const int *__restrict__ src, const int *__restrict__ npos) {
+                                                const int *__restrict__ src, const int *__restrict__ npos,
+                                                const unsigned *__restrict__ seglive) {
   __shared__ int otile[32];            // distinct old tiles of this new tile
   __shared__ unsigned omask[32];       // their slots that this new tile takes
   __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
@@ -247,6 +250,7 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
   const int ntiles = (R + 31) / 32;
   const int nkc = (N + kRepackSources - 1) / kRepackSources;
   const int tid = threadIdx.x, kk = tid >> 3, q = tid & 7;
+  const int NW = (N + 31) / 32;
   for (int item = blockIdx.x; item < ntiles * nkc; item += gridDim.x) {
     const int t = item / nkc, k0 = (item % nkc) * kRepackSources;
     const int nb = min(32, R - t * 32);
@@ -277,6 +281,8 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
         for (int i = 0; i < n; ++i) {
           const unsigned m = (omask[i] >> (4 * q)) & 15u;
           if (!m) continue;
+          // k0 + kb is a multiple of 32: the bitmap word of sources k0 + kb + [0, 32), bit kk
+          if (seglive && !((seglive[(size_t)otile[i] * NW + ((k0 + kb) >> 5)] >> kk) & 1u)) continue;
           const float4 v = *(reinterpret_cast<const float4 *>(sfm + ((size_t)otile[i] * N + k) * 32) + q);
           const float e[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -290,6 +296,24 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
             make_float4(stage[kk][4 * q], stage[kk][4 * q + 1], stage[kk][4 * q + 2], stage[kk][4 * q + 3]);
       __syncthreads();
     }
+  }
+}
+
+// Zeros into the 128-byte segments of fp32 tiles [0, (*npos + 31) / 32) whose seglive bit is clear
+// (segments that a producer skipped because all their rows are zero), for readers that take the
+// tiles as they are. 8 lanes write one segment.
+__global__ __launch_bounds__(256) void k_fill_dead(float *__restrict__ fm, int N, const unsigned *__restrict__ seglive,
+                                                   const int *__restrict__ npos) {
+  const int ntiles = (*npos + 31) / 32;
+  const int NW = (N + 31) / 32;
+  const size_t items = (size_t)ntiles * N * 8;
+  for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
+    const int q = (int)(it & 7);
+    const size_t seg = it >> 3;
+    const int k = (int)(seg % N);
+    const size_t t = seg / N;
+    if (!((seglive[t * NW + (k >> 5)] >> (k & 31)) & 1u))
+      reinterpret_cast<float4 *>(fm + seg * 32)[q] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
   }
 }
 
@@ -833,7 +857,8 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
                                                       int N, const int2 *__restrict__ ell, int K,
                                                       const float *__restrict__ bias, float ymax,
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
-                                                      unsigned *__restrict__ masks, int tile0) {
+                                                      unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
+                                                      int tile0) {
   constexpr int CR = kCodeRows, CH = 128, OPL = 8;
   constexpr int KS = KC > 0 ? KC : 1;
   __shared__ float dl[kDictSlots];
@@ -856,8 +881,12 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
   const int per_xcd = gridDim.x >> 3;
   const int nvalid = active ? min(CR, R - t * CR) : 0;
   const unsigned char *tb = cin + (size_t)t * N * CR + 4 * r;
-  // output rows 4r..4r+3 of the code tile: fp32 tile 2t + (4r >= 32), slots (4r) % 32
+  // output rows 4r..4r+3 of the code tile: fp32 tile 2t + (4r >= 32), slots (4r) % 32; the list's
+  // fp32 tiles end at (R + 31) / 32, so the upper half of the last code tile may have no tile
   float *obase = fout + ((size_t)(2 * t + (r >> 3)) * N) * 32 + (4 * r) % 32;
+  const bool has_tile = (2 * t + (r >> 3)) * 32 < R;
+  const bool has_tile_b = (2 * t + 1) * 32 < R;
+  const int NW = (N + 31) / 32;
   unsigned long long lm = 0ull;
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int c0 = chunk * CH;
@@ -947,17 +976,32 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
         }
       }
     }
+    // a 32-row output segment (8 lanes: o, r & 8) that is zero in every row is not stored; its bit
+    // in seglive says so. The wave's outputs are the 32 of one bitmap word, bit o + 4i.
+    unsigned sega = 0u, segb = 0u;
 #pragma unroll
     for (int i = 0; i < OPL; ++i) {
       const int jl = jl0 + 4 * i;
-      if (jl < nout) {
-        const float b = bstage[jl];
-        const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
-                                     activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
+      const float b = bstage[jl];
+      const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
+                                   activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
+      const unsigned bits = jl < nout ? (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) |
+                                            (y.w > 0.0f ? 8u : 0u)
+                                      : 0u;
+      const unsigned long long bal = __ballot(bits != 0u);
+      if (jl < nout && has_tile && ((bal >> (lane & 56)) & 0xffull) != 0ull)
         store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jl) * 32), y);
-        const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
-        lm |= (unsigned long long)bits << (4 * r);
+      lm |= (unsigned long long)bits << (4 * r);
+#pragma unroll
+      for (int oo = 0; oo < 4; ++oo) {
+        sega |= (((bal >> (16 * oo)) & 0xffull) != 0ull ? 1u : 0u) << (oo + 4 * i);
+        segb |= (((bal >> (16 * oo + 8)) & 0xffull) != 0ull ? 1u : 0u) << (oo + 4 * i);
       }
+    }
+    if (lane == 0 && c0 + 32 * wave < N) {
+      const int wi = chunk * (CH / 32) + wave;
+      seglive[(size_t)(2 * t) * NW + wi] = sega;
+      if (has_tile_b) seglive[(size_t)(2 * t + 1) * NW + wi] = segb;
     }
   }
   // rows of this code tile that stayed live in any of this workgroup's chunks
@@ -1508,6 +1552,7 @@ struct sdnn_net {
   int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [2] dictionary full,
                         // [4 + i] positions in list i
   unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (256 fp32 bit patterns)
+  unsigned *seglive = nullptr;  // path 1: per fp32 tile, one bit per source: the segment was stored
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
@@ -1538,7 +1583,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, final_ids, total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, final_ids, total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -1560,6 +1605,8 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
   w.dict = off; off += 256 * sizeof(unsigned);
+  w.seglive = off;
+  if (net->path == 1) off += align_up(rows / 32 * (size_t)((net->N + 31) / 32) * sizeof(unsigned), a);
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
   w.total = off;
   return w;
@@ -1724,10 +1771,10 @@ hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char 
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32)
       hipLaunchKernelGGL(k_layer_gfm_u8<32>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
-                         net->ymax, dict, npos, masks, r * 8);
+                         net->ymax, dict, npos, masks, net->seglive, r * 8);
     else
       hipLaunchKernelGGL(k_layer_gfm_u8<0>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
-                         net->ymax, dict, npos, masks, r * 8);
+                         net->ymax, dict, npos, masks, net->seglive, r * 8);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2013,6 +2060,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
     fout_codes = false;
+    bool seglive_out = false;  // fout's all-zero segments were skipped (net->seglive says which)
     unsigned *mk = masks_for(l);
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
     const bool rec = net->profiling && (net->prof_mode == 1 || !small);
@@ -2062,6 +2110,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       // follows layer 0, which is always compacted: no count to take over
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
                                        npos + cur, tiles(P), mk));
+      seglive_out = true;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
       net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + 1) / 2 + 7) / 8);
     } else {
@@ -2125,12 +2174,20 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         hipLaunchKernelGGL(k_repack_u8, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
                            reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
       else
-        hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1));
+        hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1),
+                           seglive_out ? net->seglive : nullptr);
       HIP_OR_POISON(net, hipGetLastError());
       fin = dst;
       cur ^= 1;
       P = live_bound;
     } else {
+      if (seglive_out) {
+        // the next layer (or the final read-out) takes the tiles as they are
+        const int64_t items = tiles(P) * net->N * 8;
+        const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+        hipLaunchKernelGGL(k_fill_dead, dim3(grid), dim3(256), 0, s, fout, net->N, net->seglive, npos + cur);
+        HIP_OR_POISON(net, hipGetLastError());
+      }
       fin = fout;
     }
     fin_codes = fout_codes;
@@ -2192,6 +2249,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->counts = reinterpret_cast<int *>(ws + w.counts);
   net->misc = reinterpret_cast<int *>(ws + w.misc);
   net->dict = reinterpret_cast<unsigned *>(ws + w.dict);
+  net->seglive = reinterpret_cast<unsigned *>(ws + w.seglive);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
   net->ran = false;
 

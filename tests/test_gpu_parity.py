@@ -9,6 +9,11 @@ import oracle
 import synth
 from tests.gpu_util import GpuRun, assert_parity, log
 
+
+def sdnn_kind(k):
+    from paper_1909_05631_amd import sdnn
+    return sdnn.KERNEL_KINDS.get(int(k))
+
 pytestmark = pytest.mark.gpu
 
 
@@ -187,6 +192,37 @@ def test_global_tile_large_lists(n, m, bias, lo, hi, kind):
     log(f"large lists n={n} m={m} bias={bias} kind={kind}")
     gpu, o, cats = run_both(n, layers, y0)
     assert gpu.net.kernel_path == 1
+    assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("case", ["last", "fill", "adopt-odd"])
+def test_code_layer_outputs(case):
+    """The layer after a uniform layer 0 gathers one-byte codes and skips storing 32-row output segments
+    that are zero in every row. Its tiles are then either repacked (reading only the stored segments)
+    or, when the next layer or the final read-out takes them as they are, completed with zeros.
+    "last": it is the last layer; "fill": it keeps nearly every row, so no repack follows; "adopt-odd":
+    layer 0 leaves 1044 live rows (16 code tiles and a half, 33 fp32 tiles), so the upper half of the
+    last code tile has no fp32 tile to write."""
+    n, m = 6000, 1100
+    nl = {"last": 2, "fill": 4, "adopt-odd": 6}[case]
+    rng = np.random.default_rng(31)
+    y0 = (rng.random((m, n)) < rng.uniform(0.15, 0.40, size=(m, 1))).astype(np.float32)
+    if case == "adopt-odd":
+        y0[rng.choice(m, 56, replace=False)] = 0.0
+    cp, ri, v = synth.layers_csc(13, 0, nl, n)
+    bias = [np.full(n, -0.40, np.float32) for _ in range(nl)]
+    if case == "fill":
+        bias[1][:] = 0.10
+    layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
+    log(f"code layer outputs case={case}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kind, _ = gpu.net.layer_info()
+    assert gpu.net.kernel_path == 1 and sdnn_kind(kind[1]) == "k_layer_gfm_u8"
+    counts = oracle.padded_live_counts(o, nl)
+    if case == "adopt-odd":
+        assert counts[1] == 1044
+    if case == "fill":
+        assert counts[2] * 20 > counts[1] * 19
     assert_parity(gpu, o, cats)
 
 
