@@ -562,6 +562,35 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
   }
 }
 
+// Stages the sources of a chunk of outputs [c0, c0 + nout) of a layer with one weight (16-bit
+// source lists src16[slot][N]) into LDS as dst[slot][CH] = source * scale, eight per 16-byte load;
+// outputs past nout get 0.
+template <int KC, int CH>
+__device__ __forceinline__ void stage_src16(unsigned *dst, const unsigned short *__restrict__ src16, int N, int c0,
+                                            int nout, unsigned scale) {
+  static_assert(CH % 8 == 0, "eight sources per load");
+  for (int i = threadIdx.x; i < KC * CH / 8; i += blockDim.x) {
+    const int sl = i / (CH / 8), pr = (i % (CH / 8)) * 8;
+    const unsigned short *sp = src16 + (size_t)sl * N + c0 + pr;
+    unsigned o[8];
+    if (pr + 7 < nout && (reinterpret_cast<uintptr_t>(sp) & 15) == 0) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(sp);
+      const unsigned w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        o[2 * c] = w[c] & 0xffffu;
+        o[2 * c + 1] = w[c] >> 16;
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) o[c] = pr + c < nout ? (unsigned)sp[c] : 0u;
+    }
+    uint4 *d = reinterpret_cast<uint4 *>(dst + sl * CH + pr);
+    d[0] = make_uint4(o[0] * scale, o[1] * scale, o[2] * scale, o[3] * scale);
+    d[1] = make_uint4(o[4] * scale, o[5] * scale, o[6] * scale, o[7] * scale);
+  }
+}
+
 // One round of a layer on global feature-major tiles of FMR = 32 rows: input tiles fin[t][k][b]
 // (source k of list position 32t + b), output tiles fout in the same layout and positions; tiles
 // [tile0, tile0 + 8) of the list, one per XCD. blockDim 256 (4 waves); a work item is a chunk of
@@ -573,17 +602,19 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
 // XCD x share the output chunks of one tile, which therefore stays in that XCD's L2 (or, for the
 // widest layers, in the Infinity Cache) for the whole launch. With fewer than 8 tiles left, each
 // tile's chunks are split over 8 / ntiles XCDs. For KC > 0 the chunk's ELL rows are staged in LDS
-// with 16-byte loads, so the gathers are the only per-output memory reads. Slots past the list's
-// end hold zeros in fin and get zeros in fout.
+// with 16-byte loads, so the gathers are the only per-output memory reads; with CW (a layer whose
+// weights are all wc) the staged entries are 16-bit source lists, a quarter of the ELL's bytes.
+// Slots past the list's end hold zeros in fin and get zeros in fout.
 //
 // Workgroup 0 of the first round also does the list bookkeeping of the layer sequence: with
 // count_out set (a layer that follows one without compaction) it counts the previous layer's live
 // rows (masks_prev, complete since that kernel ended) into *count_out, and with masks_clear set it
 // clears that buffer, the one the next layer will use (three buffers rotate by layer). With
 // count_out set and no live row left (rows that die stay dead), the layer writes nothing.
-template <int FMR, int KC>
+template <int FMR, int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
+                                                   const unsigned short *__restrict__ src16, float wc,
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                    int tile0, const unsigned *__restrict__ masks_prev,
@@ -591,8 +622,10 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
   constexpr int CH = kGfmOutputs, OPL = 8;
   static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
+  static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
   constexpr int KS = KC > 0 ? KC : 1;
-  __shared__ int2 ells[KS * CH];
+  __shared__ int2 ells[CW ? 1 : KS * CH];
+  __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * FMR
   __shared__ float bstage[CH];
   __shared__ unsigned rowmask;
   __shared__ int prev_live;
@@ -635,7 +668,9 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
     const int nout = min(CH, N - c0);
     __syncthreads();  // the previous chunk is done with ells / bstage
     for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
-    if constexpr (KC > 0) {
+    if constexpr (CW) {
+      stage_src16<KC, CH>(offs, src16, N, c0, nout, FMR);
+    } else if constexpr (KC > 0) {
       // stage [slot][64 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
       for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
         const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
@@ -663,9 +698,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
       auto fetch = [&](int sl, int bf) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const int2 e = ells[sl * CH + jw + 2 * i];
-          g[bf][i] = tb[(unsigned)e.x >> 2];
-          wv[bf][i] = __int_as_float(e.y);
+          if constexpr (CW) {
+            g[bf][i] = tb[offs[sl * CH + jw + 2 * i]];
+            wv[bf][i] = wc;
+          } else {
+            const int2 e = ells[sl * CH + jw + 2 * i];
+            g[bf][i] = tb[(unsigned)e.x >> 2];
+            wv[bf][i] = __int_as_float(e.y);
+          }
         }
       };
 #pragma unroll
@@ -719,9 +759,10 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
 // bookkeeping of the layer sequence is that of k_layer_gfm; in addition, when the previous layer
 // left no live row (a row that died stays dead), the layer writes nothing: its masks stay zero, so
 // every later layer does the same.
-template <int KC>
+template <int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict__ fin, float *__restrict__ fout,
                                                          int N, const int2 *__restrict__ ell,
+                                                         const unsigned short *__restrict__ src16, float wc,
                                                          const float *__restrict__ bias, float ymax,
                                                          const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                          const unsigned *__restrict__ masks_prev,
@@ -765,20 +806,31 @@ __global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int j = chunk * CH + wave * 8 + h;
     const int jj = min(j, N - 1);
-    int2 e[KC];
+    // byte offsets of the sources' segments and the weights (CW: 16-bit source lists, weight wc)
+    unsigned eo[KC];
+    float ew[KC];
 #pragma unroll
-    for (int i = 0; i < KC; ++i) e[i] = ell[(size_t)i * N + jj];
+    for (int i = 0; i < KC; ++i) {
+      if constexpr (CW) {
+        eo[i] = (unsigned)src16[(size_t)i * N + jj] * (FMR * 4);
+        ew[i] = wc;
+      } else {
+        const int2 e = ell[(size_t)i * N + jj];
+        eo[i] = (unsigned)e.x;
+        ew[i] = __int_as_float(e.y);
+      }
+    }
     const float b = bias[jj];
     float4 g[KC];
 #pragma unroll
-    for (int i = 0; i < KC; ++i) g[i] = *reinterpret_cast<const float4 *>(tbase + (unsigned)e[i].x);
+    for (int i = 0; i < KC; ++i) g[i] = *reinterpret_cast<const float4 *>(tbase + eo[i]);
     // every gather is issued before the first fma waits on one
     mem_fence_compiler();
     __builtin_amdgcn_sched_barrier(0);
     float a[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
-      const float w = __int_as_float(e[i].y);
+      const float w = ew[i];
       a[0] = fmaf(g[i].x, w, a[0]);
       a[1] = fmaf(g[i].y, w, a[1]);
       a[2] = fmaf(g[i].z, w, a[2]);
@@ -852,17 +904,20 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 // serves 4 outputs (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane =
 // (r = lane % 16: rows 4r..4r+3, o = lane / 16); a wave takes 32 outputs, 8 per lane, and a work
 // item is a chunk of 128 outputs. The dictionary and the chunk's ELL rows sit in LDS.
-template <int KC>
+template <int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
+                                                      const unsigned short *__restrict__ src16, float wc,
                                                       const float *__restrict__ bias, float ymax,
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
                                                       int tile0) {
   constexpr int CR = kCodeRows, CH = 128, OPL = 8;
+  static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
   constexpr int KS = KC > 0 ? KC : 1;
   __shared__ float dl[kDictSlots];
-  __shared__ int2 ells[KS * CH];
+  __shared__ int2 ells[CW ? 1 : KS * CH];
+  __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * CR
   __shared__ float bstage[CH];
   __shared__ unsigned long long rowmask;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -893,7 +948,9 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
     const int nout = min(CH, N - c0);
     __syncthreads();  // the previous chunk is done with ells / bstage
     for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
-    if constexpr (KC > 0) {
+    if constexpr (CW) {
+      stage_src16<KC, CH>(offs, src16, N, c0, nout, CR);
+    } else if constexpr (KC > 0) {
       // stage [slot][128 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
       for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
         const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
@@ -934,9 +991,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
       auto fetch = [&](int sl, int bf) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const int2 e = ells[sl * CH + jl0 + 4 * i];
-          wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)e.x + lofs));
-          wv[bf][i] = __int_as_float(e.y);
+          if constexpr (CW) {
+            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + (offs[sl * CH + jl0 + 4 * i] + lofs));
+            wv[bf][i] = wc;
+          } else {
+            const int2 e = ells[sl * CH + jl0 + 4 * i];
+            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)e.x + lofs));
+            wv[bf][i] = __int_as_float(e.y);
+          }
         }
       };
 #pragma unroll
@@ -1521,6 +1583,9 @@ struct LayerDev {
   bool uniform = false;
   float w = 0.0f, b = 0.0f;
   const uint4 *ell16 = nullptr;  // layer 0 of a uniform layer with K == 32: [K/8][N][8] u16 source indices
+  // global-tile path, uniform layer with K == 32 and N <= 65536: [K][N] u16 source indices (the
+  // ELL's sources without the repeated weight)
+  const unsigned short *src16 = nullptr;
 };
 
 }  // namespace
@@ -1649,8 +1714,13 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   const int nchunks = (net->N + 31) / 32;
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = (int)std::min<int64_t>(2 * net->cus, (nchunks + parts - 1) / parts);
-  hipLaunchKernelGGL(k_layer_gfm_small<32>, dim3(8 * std::max(1, per_xcd)), dim3(256), 0, net->stream, fin, fout,
-                     net->N, ld.ell, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
+  const dim3 grid(8 * std::max(1, per_xcd));
+  if (ld.src16)
+    hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell,
+                       ld.src16, ld.w, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
+  else
+    hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell,
+                       ld.src16, ld.w, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
   return hipGetLastError();
 }
 
@@ -1669,12 +1739,15 @@ hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float
   const dim3 grid(8 * std::max(1, per_xcd));
   for (int r = 0; r < rounds; ++r) {
     int *cnt = r == 0 ? count_out : nullptr;
-    if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm<32, 32>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+    if (ld.K == 32 && ld.src16)
+      hipLaunchKernelGGL((k_layer_gfm<32, 32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+    else if (ld.K == 32)
+      hipLaunchKernelGGL((k_layer_gfm<32, 32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
     else
-      hipLaunchKernelGGL((k_layer_gfm<32, 0>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+      hipLaunchKernelGGL((k_layer_gfm<32, 0, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1769,12 +1842,15 @@ hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char 
   const dim3 grid(8 * std::max(1, per_xcd));
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
-    if (ld.K == 32)
-      hipLaunchKernelGGL(k_layer_gfm_u8<32>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
-                         net->ymax, dict, npos, masks, net->seglive, r * 8);
+    if (ld.K == 32 && ld.src16)
+      hipLaunchKernelGGL((k_layer_gfm_u8<32, true>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+    else if (ld.K == 32)
+      hipLaunchKernelGGL((k_layer_gfm_u8<32, false>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
     else
-      hipLaunchKernelGGL(k_layer_gfm_u8<0>, grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K, ld.bias,
-                         net->ymax, dict, npos, masks, net->seglive, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm_u8<0, false>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -1936,6 +2012,33 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     if (ld.uniform) {
       ld.w = val[col_ptr[(size_t)i * (N + 1)]];
       ld.b = bias[(size_t)i * N];
+    }
+  }
+  if (net->path == 1 && N <= 65536) {
+    // uniform layers with 32 sources per column: 16-bit source lists, [K][N] like the ELL
+    std::vector<int32_t> sel;
+    for (int32_t i = 0; i < nl; ++i)
+      if (net->layers[(size_t)l0 + i].uniform && net->layers[(size_t)l0 + i].K == 32) sel.push_back(i);
+    if (!sel.empty()) {
+      const size_t per = (size_t)32 * N;
+      std::vector<uint16_t> hs(per * sel.size());
+      parallel_for((int32_t)sel.size(), [&](int32_t q) {
+        const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
+        uint16_t *dst = hs.data() + per * (size_t)q;
+        for (int32_t j = 0; j < N; ++j)
+          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * N + j] = (uint16_t)row_idx[cp[j] + sl];
+      });
+      char *ms = nullptr;
+      e = hipMalloc(reinterpret_cast<void **>(&ms), hs.size() * sizeof(uint16_t));
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", hs.size() * sizeof(uint16_t), hipGetErrorString(e));
+      }
+      net->allocations.push_back(ms);
+      HIP_OR_POISON(net, hipMemcpyAsync(ms, hs.data(), hs.size() * sizeof(uint16_t), hipMemcpyHostToDevice, s));
+      HIP_OR_POISON(net, hipStreamSynchronize(s));
+      for (size_t q = 0; q < sel.size(); ++q)
+        net->layers[(size_t)l0 + sel[q]].src16 = reinterpret_cast<const unsigned short *>(ms) + per * q;
     }
   }
   if (l0 == 0 && net->path == 1 && net->layers[0].uniform && net->layers[0].K == 32) {
