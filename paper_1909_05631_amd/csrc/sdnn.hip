@@ -245,6 +245,7 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
   __shared__ unsigned omask[32];       // their slots that this new tile takes
   __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
   __shared__ int nold;
+  __shared__ unsigned segw[32];        // seglive words of the old tiles for the current 32 sources
   __shared__ float stage[32][33];
   const int R = *npos;
   const int ntiles = (R + 31) / 32;
@@ -276,18 +277,31 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
       const int k = k0 + kb + kk;
       // rows not taken from any old tile (past nb) stay zero
       for (int i = tid; i < 32 * 32; i += blockDim.x) stage[i >> 5][i & 31] = 0.0f;
+      // k0 + kb is a multiple of 32: one bitmap word per old tile covers these sources, bit kk
+      if (tid < n) segw[tid] = seglive ? seglive[(size_t)otile[tid] * NW + ((k0 + kb) >> 5)] : ~0u;
       __syncthreads();
       if (k < N) {
-        for (int i = 0; i < n; ++i) {
-          const unsigned m = (omask[i] >> (4 * q)) & 15u;
-          if (!m) continue;
-          // k0 + kb is a multiple of 32: the bitmap word of sources k0 + kb + [0, 32), bit kk
-          if (seglive && !((seglive[(size_t)otile[i] * NW + ((k0 + kb) >> 5)] >> kk) & 1u)) continue;
-          const float4 v = *(reinterpret_cast<const float4 *>(sfm + ((size_t)otile[i] * N + k) * 32) + q);
-          const float e[4] = {v.x, v.y, v.z, v.w};
+        // old tiles in batches of 8: the batch's loads are all issued before the first is used
+        for (int i0 = 0; i0 < n; i0 += 8) {
+          float4 v[8];
+          unsigned mm[8];
 #pragma unroll
-          for (int c = 0; c < 4; ++c)
-            if ((m >> c) & 1u) stage[kk][bslot[i][4 * q + c]] = e[c];
+          for (int u = 0; u < 8; ++u) {
+            const int i = min(i0 + u, n - 1);
+            mm[u] = i0 + u < n && ((segw[i] >> kk) & 1u) ? (omask[i] >> (4 * q)) & 15u : 0u;
+            // without a branch: a quad that is not needed reads the first one of the old tiles
+            // instead (a cache hit), so the eight loads issue back to back
+            const size_t at = mm[u] ? ((size_t)otile[i] * N + k) * 32 : 0;
+            v[u] = *(reinterpret_cast<const float4 *>(sfm + at) + q);
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (!mm[u]) continue;
+            const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              if ((mm[u] >> c) & 1u) stage[kk][bslot[i0 + u][4 * q + c]] = e[c];
+          }
         }
       }
       __syncthreads();
