@@ -207,7 +207,10 @@ def main() -> int:
         per_run = ms / np.maximum(runs, 1)
         timed = [l for l in range(L) if runs[l] > 0]
         lay = max(timed, key=lambda l: per_run[l])
-        algo = algorithmic_layer_bytes(n, nnz, int(counts[lay]), int(counts[lay + 1]))
+        # a launch that runs every remaining layer (kind 8) is timed at its first layer and covers
+        # the algorithmic bytes of all of them
+        covered = range(lay, L) if sdnn.KERNEL_KINDS.get(int(kind[lay])) == "k_layers_lds" else [lay]
+        algo = sum(algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1])) for l in covered)
         nl = max(int(launches[lay]), 1)
         avg_launch_ms = float(per_run[lay]) / nl
         achieved = algo / nl / (avg_launch_ms * 1e-3) / 1e9
@@ -215,7 +218,10 @@ def main() -> int:
         head = ", ".join(f"{l}:{per_run[l] * 1e3:.1f}us({sdnn.KERNEL_KINDS.get(int(kind[l]))} x{int(launches[l])}, "
                          f"R={int(counts[l])})" for l in timed[:6])
         log(f"large-layer kernel times: {head}")
-        tot_bytes = sum(algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1])) * int(runs[l]) for l in timed)
+        def timed_bytes(l):
+            cov = range(l, L) if sdnn.KERNEL_KINDS.get(int(kind[l])) == "k_layers_lds" else [l]
+            return sum(algorithmic_layer_bytes(n, nnz, int(counts[q]), int(counts[q + 1])) for q in cov)
+        tot_bytes = sum(timed_bytes(l) * int(runs[l]) for l in timed)
         tot_ms = float(ms[timed].sum())
         roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(cfg.name, kname),

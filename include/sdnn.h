@@ -130,8 +130,11 @@ typedef enum {
   SDNN_KERNEL_GLOBAL_TILE_FEW_ROWS = 4, /* at most 8 tiles, whole chains in flight (k_layer_gfm_small) */
   SDNN_KERNEL_BITS = 5,                 /* layer 0 from bit-packed binary inputs (k_pack_bits, k_layer_bits) */
   SDNN_KERNEL_BITS_TO_CODES = 6,        /* the same, writing one-byte dictionary codes */
-  SDNN_KERNEL_BITS_COUNT = 7            /* layer 0 of a uniform layer on binary inputs, by bit-sliced counts
+  SDNN_KERNEL_BITS_COUNT = 7,           /* layer 0 of a uniform layer on binary inputs, by bit-sliced counts
                                            (k_pack_bits, k_count_dict, k_layer_count) */
+  SDNN_KERNEL_LDS_FUSED = 8             /* every layer from this one on, in one launch that keeps each
+                                           workgroup's rows in LDS (k_layers_lds); the launch is counted
+                                           at its first layer, later layers report 0 launches */
 } sdnn_kernel_kind;
 
 /* Diagnostics (untimed). For each layer of the last sdnn_infer: the kernel family that ran it

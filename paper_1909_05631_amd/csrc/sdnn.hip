@@ -531,6 +531,126 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
   }
 }
 
+// Device view of one layer for kernels that run several layers in one launch.
+struct LayerPtr {
+  const int2 *ell;              // slot-major ELL, offsets in units of 1 << ell_shift bytes per source
+  const unsigned short *src16;  // one-weight layer with 32 sources per column: [32][N] sources, else null
+  const float *bias;
+  float w;                      // the weight of a one-weight layer
+  int K;
+};
+
+// Layers [l0, L) of the live rows listed in ids (count *count), in one launch: workgroup g keeps
+// list positions [gB, gB + B) in LDS across all the layers, as two tiles [k][B] (the layer's input
+// and its output), so between layers nothing goes through global memory and nothing waits for other
+// workgroups (rows are independent, Sec. V). Lane = (quad = lane % (B/4): rows 4quad..4quad+3,
+// output slot lane / (B/4)); each term is one 16-byte LDS read of 4 rows and 4 fmas, in ascending
+// source order as everywhere. After every layer the workgroup adds its live rows to counts[l + 1]
+// and stops once none is left (rows that die stay dead). Rows still live after layer L - 1 are
+// written to yout (row-major, by row id) and marked in masks (one bit per list position) for the
+// final compaction. Dynamic LDS: 2 * N * B floats.
+template <int B>
+__global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
+                                                     const LayerPtr *__restrict__ lp, int l0, int L, float ymax,
+                                                     const int *__restrict__ ids, const int *__restrict__ count,
+                                                     int *__restrict__ counts, unsigned *__restrict__ masks,
+                                                     int ell_shift) {
+  static_assert(B == 4 || B == 8 || B == 16, "lanes hold 4 rows each, at most 4 lanes per output");
+  extern __shared__ float4 smem[];
+  __shared__ unsigned livebits[2];
+  float *ta = reinterpret_cast<float *>(smem);
+  float *tc = ta + (size_t)N * B;
+  const int R = *count;
+  const int p0 = blockIdx.x * B;
+  if (p0 >= R) return;  // uniform over the workgroup
+  const int nvalid = min(B, R - p0);
+  const unsigned valid = (1u << nvalid) - 1u;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
+  constexpr int LPO = B / 4, OPW = 64 / LPO;
+  const int quad = lane % LPO, jl = lane / LPO;
+  const int per_round = nw * OPW;
+  const int rounds = (N + per_round - 1) / per_round;
+  // stage the rows as ta[k][b] (reads run along k); positions past the list are zero
+  for (int it = tid; it < N * B; it += blockDim.x) {
+    const int b = it / N, k = it % N;
+    ta[(size_t)k * B + b] = b < nvalid ? yin[(size_t)ids[p0 + b] * N + k] : 0.0f;
+  }
+  unsigned lb = valid;
+  int l = l0;
+  for (; l < L; ++l) {
+    const LayerPtr P = lp[l];
+    // livebits[l & 1] was last read before the barrier at the top of layer l - 1
+    if (tid == 0) livebits[l & 1] = 0u;
+    __syncthreads();  // ta is complete, and every read of tc (the layer before's input) is done
+    unsigned lm = 0u;
+    const char *tq = reinterpret_cast<const char *>(ta) + quad * 16;
+    for (int r = 0; r < rounds; ++r) {
+      const int j = r * per_round + wave * OPW + jl;
+      if (j >= N) break;
+      float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      if (P.src16) {
+        // 32 sources in groups of 8; the next group's indices load while this group's terms run
+        const unsigned short *sj = P.src16 + j;
+        unsigned cur[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) cur[q] = sj[(size_t)q * N];
+#pragma unroll
+        for (int g = 0; g < 32; g += 8) {
+          unsigned nxt[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) nxt[q] = g + 8 < 32 ? sj[(size_t)(g + 8 + q) * N] : 0u;
+          float4 v[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const float4 *>(tq + cur[q] * (unsigned)(B * 4));
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            a0 = fmaf(v[q].x, P.w, a0);
+            a1 = fmaf(v[q].y, P.w, a1);
+            a2 = fmaf(v[q].z, P.w, a2);
+            a3 = fmaf(v[q].w, P.w, a3);
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) cur[q] = nxt[q];
+        }
+      } else {
+        for (int sl = 0; sl < P.K; ++sl) {
+          const int2 e = P.ell[(size_t)sl * N + j];
+          const float4 v = *reinterpret_cast<const float4 *>(tq + ((unsigned)e.x >> ell_shift) * (unsigned)(B * 4));
+          const float wv = __int_as_float(e.y);
+          a0 = fmaf(v.x, wv, a0);
+          a1 = fmaf(v.y, wv, a1);
+          a2 = fmaf(v.z, wv, a2);
+          a3 = fmaf(v.w, wv, a3);
+        }
+      }
+      const float bj = P.bias[j];
+      const float4 y = make_float4(activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
+                                   activate(a3, bj, ymax));
+      *reinterpret_cast<float4 *>(tc + (size_t)j * B + quad * 4) = y;
+      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u))
+            << (4 * quad);
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+    if (lane == 0 && lm) atomicOr(&livebits[l & 1], lm);
+    __syncthreads();
+    lb = livebits[l & 1] & valid;
+    if (tid == 0 && lb) atomicAdd(&counts[l + 1], __popc(lb));
+    float *t = ta;
+    ta = tc;
+    tc = t;
+    if (!lb) break;
+  }
+  if (l == L && lb) {
+    // ta holds the output of layer L - 1
+    for (int it = tid; it < N * B; it += blockDim.x) {
+      const int b = it / N, k = it % N;
+      if ((lb >> b) & 1u) yout[(size_t)ids[p0 + b] * N + k] = ta[(size_t)k * B + b];
+    }
+    if (tid < B && ((lb >> tid) & 1u)) atomicOr(&masks[(p0 + tid) >> 5], 1u << ((p0 + tid) & 31));
+  }
+}
+
 // Copy live rows into feature-major tiles of FMR rows: fm[t][k][b] = Y[ids[t*FMR + b]][k], zero
 // for positions past the live count.
 template <int FMR>
@@ -1615,6 +1735,7 @@ struct sdnn_net {
   bool poisoned = false;
   std::vector<LayerDev> layers;
   std::vector<void *> allocations;
+  LayerPtr *lp_dev = nullptr;  // device table of the layers, for launches that run several layers
   int32_t n_loaded = 0;
   // last run
   bool ran = false;
@@ -1871,6 +1992,48 @@ hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char 
   return hipSuccess;
 }
 
+// Rows per workgroup of k_layers_lds: at most the largest of 16, 8, 4 whose two tiles fit 128 KiB
+// of LDS, halved while twice the workgroups still fit one per CU.
+int fused_rows_max(const sdnn_net *net) {
+  int b = 16;
+  while (b > 4 && (size_t)2 * b * net->N * sizeof(float) > (size_t)kLdsTileBytes) b /= 2;
+  return b;
+}
+int fused_rows(const sdnn_net *net, int64_t rows) {
+  int b = fused_rows_max(net);
+  while (b > 4 && 2 * ((rows + b - 1) / b) <= net->cus) b /= 2;
+  return b;
+}
+
+template <int B>
+hipError_t launch_layers_lds_b(sdnn_net *net, const float *yin, float *yout, int l0, const int *ids, const int *count,
+                               int64_t rows) {
+  static bool configured = false;
+  if (!configured) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layers_lds<B>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kLdsTileBytes);
+    if (e != hipSuccess) return e;
+    configured = true;
+  }
+  int shift = 0;
+  while ((1 << shift) < net->B * (int)sizeof(float)) ++shift;
+  const size_t lds = (size_t)2 * net->N * B * sizeof(float);
+  const int grid = (int)std::max<int64_t>(1, (rows + B - 1) / B);
+  hipLaunchKernelGGL(k_layers_lds<B>, dim3(grid), dim3(1024), lds, net->stream, yin, yout, net->N, net->lp_dev, l0,
+                     net->L, net->ymax, ids, count, net->counts, net->masks, shift);
+  return hipGetLastError();
+}
+
+// Layers [l0, L) of at most `rows` live rows (list ids, count *count) in one launch (k_layers_lds).
+hipError_t launch_layers_lds(sdnn_net *net, const float *yin, float *yout, int l0, const int *ids, const int *count,
+                             int64_t rows) {
+  switch (fused_rows(net, rows)) {
+    case 16: return launch_layers_lds_b<16>(net, yin, yout, l0, ids, count, rows);
+    case 8: return launch_layers_lds_b<8>(net, yin, yout, l0, ids, count, rows);
+    default: return launch_layers_lds_b<4>(net, yin, yout, l0, ids, count, rows);
+  }
+}
+
 // One layer of the LDS-tile path.
 hipError_t launch_layer(sdnn_net *net, int l, const float *yin, float *yout, const int *ids, const int *count,
                         int *rownz) {
@@ -2028,7 +2191,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       ld.b = bias[(size_t)i * N];
     }
   }
-  if (net->path == 1 && N <= 65536) {
+  if (N <= 65536) {
     // uniform layers with 32 sources per column: 16-bit source lists, [K][N] like the ELL
     std::vector<int32_t> sel;
     for (int32_t i = 0; i < nl; ++i)
@@ -2073,6 +2236,24 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     net->allocations.push_back(m16);
     HIP_OR_POISON(net, hipMemcpy(m16, h16.data(), h16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
     net->layers[0].ell16 = reinterpret_cast<const uint4 *>(m16);
+  }
+  // the device table of layers (for launches that run several layers)
+  if (!net->lp_dev) {
+    e = hipMalloc(reinterpret_cast<void **>(&net->lp_dev), (size_t)net->L * sizeof(LayerPtr));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      net->lp_dev = nullptr;
+      return fail(SDNN_ENOMEM, "hipMalloc of the layer table failed: %s", hipGetErrorString(e));
+    }
+    net->allocations.push_back(net->lp_dev);
+  }
+  {
+    std::vector<LayerPtr> hp((size_t)nl);
+    for (int32_t i = 0; i < nl; ++i) {
+      const LayerDev &ld = net->layers[(size_t)l0 + i];
+      hp[(size_t)i] = LayerPtr{ld.ell, ld.src16, ld.bias, ld.w, ld.K};
+    }
+    HIP_OR_POISON(net, hipMemcpy(net->lp_dev + l0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
   }
   net->n_loaded += nl;
   g_err.clear();
@@ -2127,9 +2308,38 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
   int cur = 0;
   int32_t l = 0;
   int64_t live_bound = M;
-  PollRing ring;
+  // One launch runs every remaining layer once the live rows fit one workgroup per CU and either
+  // take 4-row tiles or have stopped dying fast (the last two layers, not counting layer 0, each
+  // kept 90% of their rows): inside that launch dead rows still occupy their tile's slots, while
+  // layer-by-layer launches compact them away. Until the switch the count is read back after each
+  // layer (those layers are long).
+  const int bmax = fused_rows_max(net);
+  int kept = 0;  // consecutive layers after layer 0 that kept at least 90% of their rows
   for (; l < net->L && live_bound > 0; ++l) {
     float *yout = net->ybuf[l & 1];
+    const bool fits = (live_bound + bmax - 1) / bmax <= net->cus;
+    const bool settled = kept >= 2;
+    if (l > 0 && (live_bound <= 4 * (int64_t)net->cus || (fits && settled))) {
+      const bool rec = net->profiling;
+      if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+      HIP_OR_POISON(net, launch_layers_lds(net, yin, yout, l, net->ids[cur], net->counts + l, live_bound));
+      if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
+      if (net->profiling) net->prof_rec[(size_t)l] = rec;
+      for (int32_t q = l; q < net->L; ++q) {
+        net->layer_kernel[(size_t)q] = SDNN_KERNEL_LDS_FUSED;
+        net->layer_launches[(size_t)q] = q == l ? 1 : 0;
+      }
+      // the final list: positions still live after the last layer (bits per 32 positions)
+      hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, 32, net->ids[cur], net->ids[cur ^ 1],
+                         (int *)nullptr, net->counts + l, net->counts + net->L, (int *)nullptr);
+      HIP_OR_POISON(net, hipGetLastError());
+      cur ^= 1;
+      net->layers_run = net->L;
+      net->final_list = cur;
+      net->final_y = yout;
+      net->final_fm = nullptr;
+      return SDNN_OK;
+    }
     const bool rec = net->profiling && (net->prof_mode == 1 || live_bound > 256);
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
@@ -2142,7 +2352,11 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;
     yin = yout;
-    HIP_OR_POISON(net, poll_step(net, ring, l, l + 1, &live_bound));
+    HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+    HIP_OR_POISON(net, hipStreamSynchronize(s));
+    const int64_t before = live_bound;
+    live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
+    kept = (l > 0 && live_bound * 10 >= before * 9) ? kept + 1 : 0;
   }
   net->layers_run = l;
   net->final_list = cur;
