@@ -226,6 +226,36 @@ def test_code_layer_outputs(case):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("n,m,kind", [(1024, 3000, "uniform"), (2048, 1500, "uniform"), (4096, 700, "uniform"),
+                                      (1500, 900, "random"), (1024, 600, "dying")])
+def test_fused_layers(n, m, kind):
+    """Widths up to 4096: once few enough rows are live, one launch runs every remaining layer with each
+    workgroup's rows kept in LDS (16, 8 or 4 rows per workgroup by width and count). "uniform": one-weight
+    layers read through 16-bit source lists; "random": signed weights of random degree through the ELL;
+    "dying": every row dies inside the fused launch."""
+    nl = 10
+    rng = np.random.default_rng(n + m)
+    if kind == "random":
+        layers = random_layers(rng, n, nl, max_deg=24)
+        y0 = rng.random((m, n)).astype(np.float32) * (rng.random((m, n)) < 0.3)
+    else:
+        cp, ri, v = synth.layers_csc(14, 0, nl, n)
+        bias = -0.30 if kind != "dying" else -0.45
+        layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+        lo, hi = (0.45, 0.7) if kind != "dying" else (0.25, 0.35)
+        y0 = (rng.random((m, n)) < rng.uniform(lo, hi, size=(m, 1))).astype(np.float32)
+    log(f"fused layers n={n} m={m} kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, launches = gpu.net.layer_info()
+    assert gpu.net.kernel_path == 0
+    fused = [l for l in range(nl) if sdnn_kind(kinds[l]) == "k_layers_lds"]
+    assert fused and launches[fused[0]] == 1 and all(launches[l] == 0 for l in fused[1:])
+    assert fused == list(range(fused[0], nl))
+    if kind == "dying":
+        assert oracle.padded_live_counts(o, nl)[-1] == 0
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
