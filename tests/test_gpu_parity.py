@@ -256,6 +256,27 @@ def test_fused_layers(n, m, kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("n,kind", [(6000, "binary"), (5003, "binary"), (6000, "one-value")])
+def test_counting_layer0(n, kind):
+    """Layer 0 of a uniform network on more than 256 rows goes by counts of the bit-packed inputs, at
+    widths that are and are not multiples of 4. "one-value": a single input of 0.5 rules the bit route
+    out, and layer 0 runs on fp32 tiles."""
+    m, nl = 700, 4
+    rng = np.random.default_rng(n)
+    y0 = (rng.random((m, n)) < rng.uniform(0.2, 0.6, size=(m, 1))).astype(np.float32)
+    y0[11] = 0.0
+    if kind == "one-value":
+        y0[300, 17] = 0.5
+    cp, ri, v = synth.layers_csc(15, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, -0.35, np.float32)) for l in range(nl)]
+    log(f"counting layer 0 n={n} kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, _ = gpu.net.layer_info()
+    expect = "k_pack_bits+k_layer_count" if kind == "binary" else "k_layer_gfm"
+    assert sdnn_kind(kinds[0]) == expect
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
