@@ -999,6 +999,9 @@ constexpr unsigned kDictEmpty = 0x7fc00000u;
 constexpr int kDictSlots = 256;
 // Code tiles hold 64 list positions: [tile][N][64] bytes, list position p at tile p / 64, byte p % 64.
 constexpr int kCodeRows = 64;
+// outputs per work item of k_layer_gfm_u8: 4 waves x (64 / (kCodeRows / 4)) outputs per wave
+// instruction x 8 outputs per lane
+constexpr int kU8Outputs = 4 * (64 / (kCodeRows / 4)) * 8;
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
@@ -1031,13 +1034,15 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 }
 
 // One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
-// (source k of list position 64t + b), decoded as dict[code]; the output is fp32 tiles of 32 rows
-// as in k_layer_gfm (code tile t covers output tiles 2t and 2t + 1). Code tiles [tile0, tile0 + 8)
-// go one per XCD, as in k_layer_gfm; a tile of 65536 sources takes 4 MiB, one XCD's L2. A code
-// segment is 64 bytes: 16 lanes read it with 4-byte loads (4 codes each), so a wave instruction
-// serves 4 outputs (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane =
-// (r = lane % 16: rows 4r..4r+3, o = lane / 16); a wave takes 32 outputs, 8 per lane, and a work
-// item is a chunk of 128 outputs. The dictionary and the chunk's ELL rows sit in LDS.
+// (source k of list position CR t + b, CR = kCodeRows), decoded as dict[code]; the output is fp32
+// tiles of 32 rows as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST =
+// CR / 32). Code tiles [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR
+// bytes: RL = CR / 4 lanes read it with 4-byte loads (4 codes each), so a wave instruction serves
+// 64 / RL outputs (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane =
+// (r = lane % RL: rows 4r..4r+3, o = lane / RL); a lane runs OPL outputs, and a work item is a chunk
+// of 4 waves' outputs. The dictionary and the chunk's sources sit in LDS. A 32-row output segment
+// that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
+// says so.
 template <int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
@@ -1046,17 +1051,20 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
                                                       int tile0) {
-  constexpr int CR = kCodeRows, CH = 128, OPL = 8;
+  constexpr int CR = kCodeRows, RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
+  static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
+  static_assert(CH % 32 == 0 && CH == kU8Outputs, "a chunk covers whole bitmap words");
   static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
   constexpr int KS = KC > 0 ? KC : 1;
   __shared__ float dl[kDictSlots];
   __shared__ int2 ells[CW ? 1 : KS * CH];
   __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * CR
   __shared__ float bstage[CH];
-  __shared__ unsigned long long rowmask;
+  __shared__ unsigned segw[ST][CH / 32];
+  __shared__ unsigned long long rowmask[CR / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = dict[i];
-  if (tid == 0) rowmask = 0ull;
+  if (tid < CR / 64) rowmask[tid] = 0ull;
   const int R = *npos;
   const int nt = min(8, (R + CR - 1) / CR - tile0);
   const int parts = nt > 0 ? 8 / nt : 1;
@@ -1066,26 +1074,31 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
   const int cpp = (nchunks + parts - 1) / parts;
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
-  const int r = lane & 15, o = lane >> 4;
+  const int r = lane % RL, o = lane / RL;
   const int per_xcd = gridDim.x >> 3;
   const int nvalid = active ? min(CR, R - t * CR) : 0;
   const unsigned char *tb = cin + (size_t)t * N * CR + 4 * r;
-  // output rows 4r..4r+3 of the code tile: fp32 tile 2t + (4r >= 32), slots (4r) % 32; the list's
-  // fp32 tiles end at (R + 31) / 32, so the upper half of the last code tile may have no tile
-  float *obase = fout + ((size_t)(2 * t + (r >> 3)) * N) * 32 + (4 * r) % 32;
-  const bool has_tile = (2 * t + (r >> 3)) * 32 < R;
-  const bool has_tile_b = (2 * t + 1) * 32 < R;
+  // output rows 4r..4r+3 of the code tile: fp32 tile ST t + r / 8, slots (4r) % 32; the list's
+  // fp32 tiles end at (R + 31) / 32, so the last code tile may lack some of its fp32 tiles
+  const int otile = ST * t + (r >> 3);
+  float *obase = fout + ((size_t)otile * N) * 32 + (4 * r) % 32;
+  const bool has_tile = otile * 32 < R;
   const int NW = (N + 31) / 32;
-  unsigned long long lm = 0ull;
+  // live rows seen by this lane: bit 4 (r % 16) + c of word r / 16
+  unsigned long long lm[CR / 64];
+#pragma unroll
+  for (int h = 0; h < CR / 64; ++h) lm[h] = 0ull;
+  const int jw = wave * OPI * OPL;  // first output of this wave in the chunk
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int c0 = chunk * CH;
     const int nout = min(CH, N - c0);
-    __syncthreads();  // the previous chunk is done with ells / bstage
+    __syncthreads();  // the previous chunk is done with ells / bstage / segw
     for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
+    if (tid < ST * (CH / 32)) segw[tid / (CH / 32)][tid % (CH / 32)] = 0u;
     if constexpr (CW) {
       stage_src16<KC, CH>(offs, src16, N, c0, nout, CR);
     } else if constexpr (KC > 0) {
-      // stage [slot][128 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
+      // stage [slot][CH outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
       for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
         const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
         const int2 *src = ell + (size_t)sl * N + c0 + pr;
@@ -1096,14 +1109,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
           if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
           if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
         }
-        // source offsets: fp32 32-row segments are 128 bytes, code segments 64
-        v.x = (int)((unsigned)v.x >> 1);
-        v.z = (int)((unsigned)v.z >> 1);
+        // source offsets: fp32 32-row segments are 128 bytes, code segments CR
+        v.x = (int)(((unsigned)v.x >> 7) * CR);
+        v.z = (int)(((unsigned)v.z >> 7) * CR);
         *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
       }
     }
     __syncthreads();
-    const int jl0 = wave * 32 + o;  // this lane's outputs: jl0 + 4i, i < OPL
+    const int jl0 = jw + o;  // this lane's outputs: jl0 + OPI i, i < OPL
     float acc[OPL][4];
 #pragma unroll
     for (int i = 0; i < OPL; ++i)
@@ -1126,10 +1139,10 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
           if constexpr (CW) {
-            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + (offs[sl * CH + jl0 + 4 * i] + lofs));
+            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + (offs[sl * CH + jl0 + OPI * i] + lofs));
             wv[bf][i] = wc;
           } else {
-            const int2 e = ells[sl * CH + jl0 + 4 * i];
+            const int2 e = ells[sl * CH + jl0 + OPI * i];
             wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)e.x + lofs));
             wv[bf][i] = __int_as_float(e.y);
           }
@@ -1167,17 +1180,18 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
       for (int sl = 0; sl < K; ++sl) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + 4 * i, N - 1)];
-          term(i, *reinterpret_cast<const unsigned *>(tb + (e.x >> 1)), __int_as_float(e.y));
+          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + OPI * i, N - 1)];
+          term(i, *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR), __int_as_float(e.y));
         }
       }
     }
-    // a 32-row output segment (8 lanes: o, r & 8) that is zero in every row is not stored; its bit
-    // in seglive says so. The wave's outputs are the 32 of one bitmap word, bit o + 4i.
-    unsigned sega = 0u, segb = 0u;
+    // segment bits of this wave's outputs (jw .. jw + OPI OPL, within one bitmap word), per fp32 tile
+    unsigned seg[ST];
+#pragma unroll
+    for (int q = 0; q < ST; ++q) seg[q] = 0u;
 #pragma unroll
     for (int i = 0; i < OPL; ++i) {
-      const int jl = jl0 + 4 * i;
+      const int jl = jl0 + OPI * i;
       const float b = bstage[jl];
       const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
                                    activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
@@ -1185,32 +1199,47 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
                                             (y.w > 0.0f ? 8u : 0u)
                                       : 0u;
       const unsigned long long bal = __ballot(bits != 0u);
-      if (jl < nout && has_tile && ((bal >> (lane & 56)) & 0xffull) != 0ull)
+      // the 8 lanes of this lane's output segment: lanes (lane & ~7) .. + 7
+      if (jl < nout && has_tile && ((bal >> (lane & ~7)) & 0xffull) != 0ull)
         store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jl) * 32), y);
-      lm |= (unsigned long long)bits << (4 * r);
 #pragma unroll
-      for (int oo = 0; oo < 4; ++oo) {
-        sega |= (((bal >> (16 * oo)) & 0xffull) != 0ull ? 1u : 0u) << (oo + 4 * i);
-        segb |= (((bal >> (16 * oo + 8)) & 0xffull) != 0ull ? 1u : 0u) << (oo + 4 * i);
-      }
+      for (int h = 0; h < CR / 64; ++h)
+        if ((r >> 4) == h) lm[h] |= (unsigned long long)bits << (4 * (r & 15));
+#pragma unroll
+      for (int oo = 0; oo < OPI; ++oo)
+#pragma unroll
+        for (int q = 0; q < ST; ++q)
+          seg[q] |= (((bal >> (oo * RL + 8 * q)) & 0xffull) != 0ull ? 1u : 0u) << ((jw % 32) + oo + OPI * i);
     }
-    if (lane == 0 && c0 + 32 * wave < N) {
-      const int wi = chunk * (CH / 32) + wave;
-      seglive[(size_t)(2 * t) * NW + wi] = sega;
-      if (has_tile_b) seglive[(size_t)(2 * t + 1) * NW + wi] = segb;
+    if (lane == 0)
+#pragma unroll
+      for (int q = 0; q < ST; ++q)
+        if (seg[q]) atomicOr(&segw[q][jw / 32], seg[q]);
+    __syncthreads();
+    if (tid < ST * (CH / 32)) {
+      const int q = tid / (CH / 32), wi = tid % (CH / 32);
+      if ((ST * t + q) * 32 < R && c0 + 32 * wi < N) seglive[(size_t)(ST * t + q) * NW + c0 / 32 + wi] = segw[q][wi];
     }
   }
   // rows of this code tile that stayed live in any of this workgroup's chunks
 #pragma unroll
-  for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
+  for (int h = 0; h < CR / 64; ++h)
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) lm[h] |= __shfl_xor(lm[h], d, 64);
   __syncthreads();
-  if (lane == 0 && lm) atomicOr(&rowmask, lm);
+  if (lane == 0)
+#pragma unroll
+    for (int h = 0; h < CR / 64; ++h)
+      if (lm[h]) atomicOr(&rowmask[h], lm[h]);
   __syncthreads();
   if (tid == 0 && active) {
-    const unsigned long long valid = nvalid >= 64 ? ~0ull : ((1ull << nvalid) - 1ull);
-    const unsigned long long m = rowmask & valid;
-    if (m & 0xffffffffull) atomicOr(&masks[2 * t], (unsigned)m);
-    if (m >> 32) atomicOr(&masks[2 * t + 1], (unsigned)(m >> 32));
+#pragma unroll
+    for (int q = 0; q < ST; ++q) {
+      const int lo = 32 * q;  // rows lo .. lo + 31 of the code tile
+      const unsigned valid = nvalid - lo >= 32 ? 0xffffffffu : (nvalid > lo ? ((1u << (nvalid - lo)) - 1u) : 0u);
+      const unsigned m = (unsigned)(rowmask[q / 2] >> (32 * (q & 1))) & valid;
+      if (m) atomicOr(&masks[ST * t + q], m);
+    }
   }
 }
 
@@ -1969,9 +1998,9 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
 // max_tiles: host bound on the 32-row tiles of the list.
 hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
                          int64_t max_tiles, unsigned *masks) {
-  max_tiles = (max_tiles + 1) / 2;  // code tiles of 64 rows
+  max_tiles = (max_tiles + kCodeRows / 32 - 1) / (kCodeRows / 32);  // code tiles
   const int rounds = (int)((max_tiles + 7) / 8);
-  const int nchunks = (net->N + 127) / 128;
+  const int nchunks = (net->N + kU8Outputs - 1) / kU8Outputs;
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
   const dim3 grid(8 * std::max(1, per_xcd));
@@ -2443,7 +2472,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                                        npos + cur, tiles(P), mk));
       seglive_out = true;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
-      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + 1) / 2 + 7) / 8);
+      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + kCodeRows / 32 - 1) / (kCodeRows / 32) + 7) / 8);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -2498,7 +2527,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (!compacted) HIP_OR_POISON(net, compact());
       compacted = true;
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
-      const int64_t items = fout_codes ? (tiles(live_bound) + 1) / 2 * net->N * (kCodeRows / 4) / 256
+      const int64_t items = fout_codes ? (tiles(live_bound) + kCodeRows / 32 - 1) / (kCodeRows / 32) * net->N * (kCodeRows / 4) / 256
                                        : tiles(live_bound) * ((net->N + kRepackSources - 1) / kRepackSources);
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
       if (fout_codes)
