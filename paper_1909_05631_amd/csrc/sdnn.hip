@@ -998,10 +998,13 @@ constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 1
 constexpr unsigned kDictEmpty = 0x7fc00000u;
 constexpr int kDictSlots = 256;
 // Code tiles hold 64 list positions: [tile][N][64] bytes, list position p at tile p / 64, byte p % 64.
-constexpr int kCodeRows = 64;
-// outputs per work item of k_layer_gfm_u8: 4 waves x (64 / (kCodeRows / 4)) outputs per wave
-// instruction x 8 outputs per lane
-constexpr int kU8Outputs = 4 * (64 / (kCodeRows / 4)) * 8;
+// The code-tile height goes with the bit tiles that write them: 128 rows after 32-row bit tiles,
+// whose counting workgroups then fill each 128-byte segment in 4 parts; 64 rows after 16-row bit
+// tiles (4 parts each as well). Taller segments serve more rows per gather request.
+__host__ __device__ constexpr int code_rows(int T) { return T == 32 ? 128 : 64; }
+// outputs per work item of k_layer_gfm_u8: 4 waves x (64 / (CR / 4)) outputs per wave instruction
+// x 8 outputs per lane
+__host__ __device__ constexpr int u8_outputs(int CR) { return 4 * (64 / (CR / 4)) * 8; }
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
@@ -1034,7 +1037,7 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 }
 
 // One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
-// (source k of list position CR t + b, CR = kCodeRows), decoded as dict[code]; the output is fp32
+// (source k of list position CR t + b), decoded as dict[code]; the output is fp32
 // tiles of 32 rows as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST =
 // CR / 32). Code tiles [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR
 // bytes: RL = CR / 4 lanes read it with 4-byte loads (4 codes each), so a wave instruction serves
@@ -1043,7 +1046,7 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 // of 4 waves' outputs. The dictionary and the chunk's sources sit in LDS. A 32-row output segment
 // that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
 // says so.
-template <int KC, bool CW>
+template <int KC, bool CW, int CR>
 __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
                                                       const unsigned short *__restrict__ src16, float wc,
@@ -1051,9 +1054,9 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
                                                       int tile0) {
-  constexpr int CR = kCodeRows, RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
+  constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
-  static_assert(CH % 32 == 0 && CH == kU8Outputs, "a chunk covers whole bitmap words");
+  static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
   static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
   constexpr int KS = KC > 0 ? KC : 1;
   __shared__ float dl[kDictSlots];
@@ -1243,14 +1246,15 @@ __global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__res
   }
 }
 
-// Repack of one-byte code tiles (kCodeRows positions each) after a compaction: position p of the
+// Repack of one-byte code tiles (CR positions each) after a compaction: position p of the
 // new tiles takes the code at position src[p] of the old ones; positions past *npos get code 0
 // (+0.0). A thread writes 4 codes of one source.
+template <int CR>
 __global__ __launch_bounds__(256) void k_repack_u8(const unsigned char *__restrict__ sfm, unsigned char *__restrict__ dfm,
                                                    int N, const int *__restrict__ src, const int *__restrict__ npos) {
-  constexpr int QPS = kCodeRows / 4;  // 4-byte quads per source segment
+  constexpr int QPS = CR / 4;  // 4-byte quads per source segment
   const int R = *npos;
-  const int ntiles = (R + kCodeRows - 1) / kCodeRows;
+  const int ntiles = (R + CR - 1) / CR;
   const size_t items = (size_t)ntiles * N * QPS;
   for (size_t it = blockIdx.x * (size_t)blockDim.x + threadIdx.x; it < items; it += (size_t)gridDim.x * blockDim.x) {
     const int qd = (int)(it % QPS);
@@ -1260,13 +1264,13 @@ __global__ __launch_bounds__(256) void k_repack_u8(const unsigned char *__restri
     unsigned word = 0u;
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int p = t * kCodeRows + qd * 4 + c;
+      const int p = t * CR + qd * 4 + c;
       if (p < R) {
         const int sp = src[p];
-        word |= (unsigned)sfm[((size_t)(sp / kCodeRows) * N + k) * kCodeRows + sp % kCodeRows] << (8 * c);
+        word |= (unsigned)sfm[((size_t)(sp / CR) * N + k) * CR + sp % CR] << (8 * c);
       }
     }
-    *reinterpret_cast<unsigned *>(dfm + ((size_t)t * N + k) * kCodeRows + qd * 4) = word;
+    *reinterpret_cast<unsigned *>(dfm + ((size_t)t * N + k) * CR + qd * 4) = word;
   }
 }
 
@@ -1388,6 +1392,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
                                                      float ymax, const int *__restrict__ count,
                                                      unsigned *__restrict__ masks, unsigned *__restrict__ gd,
                                                      int *__restrict__ overflow) {
+  constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
   // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), the dictionary copy
   // (1 KiB), then the tile
@@ -1403,14 +1408,14 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   const int rounds = (blocks + nw - 1) / nw;        // rounds of one block per wave
   const Chunking ch = chunking(ntiles, rounds);
   // codes with whole tiles as items: keep the tiles of one code group on one XCD
-  const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (kCodeRows / T)) == 0;
+  const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (CR / T)) == 0;
   const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
   if (tid < 16) lut[tid] = make_float4((float)(tid & 1), (float)((tid >> 1) & 1), (float)((tid >> 2) & 1), (float)((tid >> 3) & 1));
   if (tid == 0) tilemask = 0u;
   if (CODES)
     for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = kDictEmpty;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
-    const int t = grouped ? code_group_tile(w, kCodeRows / T) : w / ch.nchunks;
+    const int t = grouped ? code_group_tile(w, CR / T) : w / ch.nchunks;
     const int c = grouped ? 0 : w % ch.nchunks;
     if (t >= ntiles) continue;  // uniform over the workgroup
     const int p0 = t * T;
@@ -1508,7 +1513,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         const float bj = bias[j];
         if constexpr (CODES) {
           uint4 *dst = reinterpret_cast<uint4 *>(reinterpret_cast<unsigned char *>(fout) +
-                                                 ((size_t)(p0 / kCodeRows) * N + j) * kCodeRows + p0 % kCodeRows);
+                                                 ((size_t)(p0 / CR) * N + j) * CR + p0 % CR);
           unsigned cw[T / 4];
 #pragma unroll
           for (int n = 0; n < T / 4; ++n) {
@@ -1525,7 +1530,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
           for (int n = 0; n < T / 16; ++n) dst[n] = make_uint4(cw[4 * n], cw[4 * n + 1], cw[4 * n + 2], cw[4 * n + 3]);
           // the rest of the last code tile gets code 0 (+0.0)
           if (t + 1 == ntiles)
-            for (int n = T / 16; n < (kCodeRows - p0 % kCodeRows) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
+            for (int n = T / 16; n < (CR - p0 % CR) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
         } else {
           float4 *dst = reinterpret_cast<float4 *>(fout + ((size_t)(p0 >> 5) * N + j) * 32 + (p0 & 31));
 #pragma unroll
@@ -1596,6 +1601,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
                                                       unsigned char *__restrict__ cout, int N,
                                                       const uint4 *__restrict__ ell16, const int *__restrict__ misc,
                                                       const int *__restrict__ count, unsigned *__restrict__ masks) {
+  constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
   constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
   extern __shared__ float4 smem[];
@@ -1609,11 +1615,11 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   const int rounds = (blocks + nw - 1) / nw;
   const Chunking ch = chunking(ntiles, rounds);
   // whole tiles as items: keep the tiles of one code group on one XCD
-  const bool grouped = ch.nchunks == 1 && gridDim.x % (8 * (kCodeRows / T)) == 0;
+  const bool grouped = ch.nchunks == 1 && gridDim.x % (8 * (CR / T)) == 0;
   const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
   if (tid == 0) tilemask = 0u;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
-    const int t = grouped ? code_group_tile(w, kCodeRows / T) : w / ch.nchunks;
+    const int t = grouped ? code_group_tile(w, CR / T) : w / ch.nchunks;
     const int c = grouped ? 0 : w % ch.nchunks;
     if (t >= ntiles) continue;  // uniform over the workgroup
     const int p0 = t * T;
@@ -1710,7 +1716,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
         if (!jin[u]) continue;
         const unsigned rows = T == 16 ? ((ge >> (16 * u)) & 0xffffu) : ge;
         live |= rows;
-        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / kCodeRows) * N + jo[u]) * kCodeRows + p0 % kCodeRows);
+        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / CR) * N + jo[u]) * CR + p0 % CR);
         // plain stores: the tiles of one 64-row code group fill each segment in parts, merged in L2
         if (T == 32) {
           dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);
@@ -1720,7 +1726,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
         }
         // the rest of the last code tile gets code 0 (+0.0)
         if (t + 1 == ntiles)
-          for (int n = T / 16; n < (kCodeRows - p0 % kCodeRows) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
+          for (int n = T / 16; n < (CR - p0 % CR) / 16; ++n) dst[n] = make_uint4(0u, 0u, 0u, 0u);
       }
     }
     if (live) atomicOr(&tilemask, live);
@@ -1994,31 +2000,37 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
   return hipGetLastError();
 }
 
-// A layer whose input tiles hold dictionary codes (see k_layer_gfm_u8); rounds of 8 code tiles.
-// max_tiles: host bound on the 32-row tiles of the list.
-hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
-                         int64_t max_tiles, unsigned *masks) {
-  max_tiles = (max_tiles + kCodeRows / 32 - 1) / (kCodeRows / 32);  // code tiles
+// A layer whose input tiles hold dictionary codes of CR rows (see k_layer_gfm_u8); rounds of 8 code
+// tiles. max_tiles: host bound on the 32-row tiles of the list.
+template <int CR>
+hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
+                            int64_t max_tiles, unsigned *masks) {
+  max_tiles = (max_tiles + CR / 32 - 1) / (CR / 32);  // code tiles
   const int rounds = (int)((max_tiles + 7) / 8);
-  const int nchunks = (net->N + kU8Outputs - 1) / kU8Outputs;
+  const int nchunks = (net->N + u8_outputs(CR) - 1) / u8_outputs(CR);
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
   const dim3 grid(8 * std::max(1, per_xcd));
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16)
-      hipLaunchKernelGGL((k_layer_gfm_u8<32, true>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm_u8<32, true, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
     else if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm_u8<32, false>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm_u8<32, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
     else
-      hipLaunchKernelGGL((k_layer_gfm_u8<0, false>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+      hipLaunchKernelGGL((k_layer_gfm_u8<0, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
+                         int64_t max_tiles, unsigned *masks) {
+  return code_rows(net->bitsT) == 128 ? launch_gfm_u8_cr<128>(net, ld, cin, fout, npos, max_tiles, masks)
+                                      : launch_gfm_u8_cr<64>(net, ld, cin, fout, npos, max_tiles, masks);
 }
 
 // Rows per workgroup of k_layers_lds: at most the largest of 16, 8, 4 whose two tiles fit 128 KiB
@@ -2472,7 +2484,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                                        npos + cur, tiles(P), mk));
       seglive_out = true;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
-      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + kCodeRows / 32 - 1) / (kCodeRows / 32) + 7) / 8);
+      const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
+      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + st - 1) / st + 7) / 8);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -2527,11 +2540,15 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (!compacted) HIP_OR_POISON(net, compact());
       compacted = true;
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
-      const int64_t items = fout_codes ? (tiles(live_bound) + kCodeRows / 32 - 1) / (kCodeRows / 32) * net->N * (kCodeRows / 4) / 256
+      const int cr = code_rows(net->bitsT);
+      const int64_t items = fout_codes ? (tiles(live_bound) + cr / 32 - 1) / (cr / 32) * net->N * (cr / 4) / 256
                                        : tiles(live_bound) * ((net->N + kRepackSources - 1) / kRepackSources);
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
-      if (fout_codes)
-        hipLaunchKernelGGL(k_repack_u8, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
+      if (fout_codes && cr == 128)
+        hipLaunchKernelGGL(k_repack_u8<128>, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
+                           reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
+      else if (fout_codes)
+        hipLaunchKernelGGL(k_repack_u8<64>, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
                            reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
       else
         hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1),
