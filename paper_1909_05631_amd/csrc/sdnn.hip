@@ -1045,9 +1045,9 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 // (r = lane % RL: rows 4r..4r+3, o = lane / RL); a lane runs OPL outputs, and a work item is a chunk
 // of 4 waves' outputs. The dictionary and the chunk's sources sit in LDS. A 32-row output segment
 // that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
-// says so.
+// says so. Registers are held to 5 waves per SIMD (more waves keep more gathers in flight; 6 spill).
 template <int KC, bool CW, int CR>
-__global__ __launch_bounds__(256) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
                                                       const unsigned short *__restrict__ src16, float wc,
                                                       const float *__restrict__ bias, float ymax,
