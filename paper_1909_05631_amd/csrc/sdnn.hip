@@ -1595,18 +1595,28 @@ __device__ __forceinline__ void csa(unsigned &carry, unsigned &sum, unsigned a, 
 // turns the planes into one byte per row: the output's code, decoded by the dictionary of
 // k_count_dict. blockDim 1024; lane = output (T = 32) or outputs j and j + 64 in the low and high
 // halves of each word (T = 16). LDS holds the tile's N words; the source indices are read 8 per
-// 16-byte load from the [4][N][8] u16 table. Codes go to tiles of 32 rows, one byte per row.
-template <int T>
+// 16-byte load from the [4][N][8] u16 table. Codes go to tiles of CR rows, one byte per row. With
+// ROWMAJOR (T = 32; widths staged in LDS) the outputs are decoded instead and written as fp32 rows,
+// yout[ids[p]][j] = dict[code] (the dictionary is copied after the tile in LDS).
+template <int T, bool ROWMAJOR>
 __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>::type *__restrict__ bits,
                                                       unsigned char *__restrict__ cout, int N,
                                                       const uint4 *__restrict__ ell16, const int *__restrict__ misc,
-                                                      const int *__restrict__ count, unsigned *__restrict__ masks) {
+                                                      const int *__restrict__ count, unsigned *__restrict__ masks,
+                                                      float *__restrict__ yout, const int *__restrict__ ids,
+                                                      const unsigned *__restrict__ dict) {
+  static_assert(!ROWMAJOR || T == 32, "rows of fp32 outputs from 32-row bit tiles");
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
   constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
   extern __shared__ float4 smem[];
   unsigned &tilemask = *reinterpret_cast<unsigned *>(smem);
   W *tile = reinterpret_cast<W *>(smem + 1);
+  // ROWMAJOR: the dictionary, then the tile's row ids, after the tile's words
+  float *dl = reinterpret_cast<float *>(tile + ((N + 3) / 4) * 4);
+  int *rid = reinterpret_cast<int *>(dl + kDictSlots);
+  if constexpr (ROWMAJOR)
+    for (int i = threadIdx.x; i < kDictSlots; i += blockDim.x) dl[i] = __uint_as_float(dict[i]);
   const int R = *count;
   const int cmin = misc[kCountMinSlot];
   const int ntiles = (R + T - 1) / T;
@@ -1634,6 +1644,8 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
         for (int k = tid; k < N; k += blockDim.x) tile[k] = src[k];
       }
     }
+    if constexpr (ROWMAJOR)
+      if (threadIdx.x < T) rid[threadIdx.x] = (int)threadIdx.x < nvalid ? ids[p0 + threadIdx.x] : -1;
     __syncthreads();
     unsigned live = 0u;
     const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
@@ -1716,6 +1728,15 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
         if (!jin[u]) continue;
         const unsigned rows = T == 16 ? ((ge >> (16 * u)) & 0xffffu) : ge;
         live |= rows;
+        if constexpr (ROWMAJOR) {
+          // row b's code is byte b % 4 of cw[b / 4]; rows past the list are not written
+#pragma unroll
+          for (int b = 0; b < T; ++b) {
+            const int row = rid[b];
+            if (row >= 0) yout[(size_t)row * N + jo[u]] = dl[(cw[b >> 2] >> (8 * (b & 3))) & 255u];
+          }
+          continue;
+        }
         uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / CR) * N + jo[u]) * CR + p0 % CR);
         // plain stores: the tiles of one 64-row code group fill each segment in parts, merged in L2
         if (T == 32) {
@@ -1979,14 +2000,15 @@ hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits
   return launch_layer_bits_k<T, 0, false>(net, ld, bits, fout, count);
 }
 
-// Layer 0 of a uniform layer by counting (see k_layer_count): dictionary, then the counts as codes.
-template <int T>
-hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bits, unsigned char *cout,
-                              const int *count) {
+// Layer 0 of a uniform layer by counting (see k_layer_count): dictionary, then the counts as codes
+// (cout) or, with yout set, as fp32 rows yout[ids[p]] (masks: one bit per list position).
+template <int T, bool ROWMAJOR>
+hipError_t launch_layer_count_k(sdnn_net *net, const LayerDev &ld, const void *bits, unsigned char *cout,
+                                const int *count, float *yout, const int *ids, unsigned *masks) {
   using W = typename BitWord<T>::type;
   static bool configured = false;
   if (!configured) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_count<T>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_count<T, ROWMAJOR>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
     if (e != hipSuccess) return e;
     configured = true;
@@ -1994,10 +2016,17 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
   hipLaunchKernelGGL(k_count_dict, dim3(1), dim3(64), 0, net->stream, net->dict, net->misc, ld.K, ld.w, ld.b, net->ymax);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t lds = 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
-  hipLaunchKernelGGL(k_layer_count<T>, dim3(net->cus), dim3(1024), lds, net->stream, reinterpret_cast<const W *>(bits),
-                     cout, net->N, ld.ell16, net->misc, count, net->masks);
+  size_t lds = 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+  if (ROWMAJOR) lds += kDictSlots * sizeof(float) + T * sizeof(int);
+  hipLaunchKernelGGL((k_layer_count<T, ROWMAJOR>), dim3(net->cus), dim3(1024), lds, net->stream,
+                     reinterpret_cast<const W *>(bits), cout, net->N, ld.ell16, net->misc, count, masks, yout, ids,
+                     reinterpret_cast<const unsigned *>(net->dict));
   return hipGetLastError();
+}
+template <int T>
+hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bits, unsigned char *cout,
+                              const int *count) {
+  return launch_layer_count_k<T, false>(net, ld, bits, cout, count, nullptr, nullptr, net->masks);
 }
 
 // A layer whose input tiles hold dictionary codes of CR rows (see k_layer_gfm_u8); rounds of 8 code
@@ -2259,7 +2288,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         net->layers[(size_t)l0 + sel[q]].src16 = reinterpret_cast<const unsigned short *>(ms) + per * q;
     }
   }
-  if (l0 == 0 && net->path == 1 && net->layers[0].uniform && net->layers[0].K == 32) {
+  if (l0 == 0 && net->layers[0].uniform && net->layers[0].K == 32) {
     // layer 0 of a uniform network: 16-bit source indices, 8 slots per 16-byte group, for the
     // counting kernel
     const int Kq = 32;
@@ -2383,12 +2412,31 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
     }
     const bool rec = net->profiling && (net->prof_mode == 1 || live_bound > 256);
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
-    HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
+    // layer 0 of a uniform layer on a large batch (from 2^24 inputs, where packing and a read-back
+    // cost less than they save): if every input is 0 or 1, by counts of the bit-packed rows (see
+    // k_layer_count), written back as fp32 rows; masks then hold one bit per list position
+    int mask_rows = net->B;
+    bool counted = false;
+    const LayerDev &ld0 = net->layers[0];
+    if (l == 0 && (int64_t)M * net->N >= (1 << 24) && ld0.uniform && ld0.ell16 && ld0.w > 0.0f && (net->N & 3) == 0 &&
+        (uint64_t)M * (uint64_t)net->N / 4 < (1ull << 32)) {
+      HIP_OR_POISON(net, launch_pack_bits<32>(net, y0, net->ybuf[1], net->ids[cur], net->counts));
+      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 6, net->misc, sizeof(int32_t), hipMemcpyDeviceToHost, s));
+      HIP_OR_POISON(net, hipStreamSynchronize(s));
+      if (net->pinned[6] == 0) {
+        HIP_OR_POISON(net, (launch_layer_count_k<32, true>(net, ld0, net->ybuf[1], nullptr, net->counts, yout,
+                                                           net->ids[cur], net->masks)));
+        counted = true;
+        mask_rows = 32;
+      }
+    }
+    if (!counted)
+      HIP_OR_POISON(net, launch_layer(net, l, yin, yout, net->ids[cur], net->counts + l, l == 0 ? net->rownz : nullptr));
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    net->layer_kernel[(size_t)l] = SDNN_KERNEL_LDS_TILE;
-    net->layer_launches[(size_t)l] = 1;
+    net->layer_kernel[(size_t)l] = counted ? SDNN_KERNEL_BITS_COUNT : SDNN_KERNEL_LDS_TILE;
+    net->layer_launches[(size_t)l] = counted ? 3 : 1;
     if (net->profiling) net->prof_rec[(size_t)l] = rec;
-    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, net->B, net->ids[cur], net->ids[cur ^ 1],
+    hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, mask_rows, net->ids[cur], net->ids[cur ^ 1],
                        (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr);
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;

@@ -277,6 +277,27 @@ def test_counting_layer0(n, kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("kind", ["binary", "one-value"])
+def test_counting_layer0_lds_widths(kind):
+    """Widths staged in LDS, from 2^24 inputs: layer 0 of a uniform network goes by counts of the
+    bit-packed rows and is written back as fp32 rows (one mask bit per list position), then the
+    row tiles take over. "one-value": an input of 0.5 keeps layer 0 on the fp32 kernel."""
+    n, m, nl = 1024, 16384, 4
+    rng = np.random.default_rng(77)
+    y0 = (rng.random((m, n)) < rng.uniform(0.15, 0.6, size=(m, 1))).astype(np.float32)
+    y0[5] = 0.0
+    if kind == "one-value":
+        y0[9000, 3] = 0.5
+    cp, ri, v = synth.layers_csc(16, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, -0.30, np.float32)) for l in range(nl)]
+    log(f"counting layer 0 on LDS widths kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, _ = gpu.net.layer_info()
+    assert gpu.net.kernel_path == 0
+    assert sdnn_kind(kinds[0]) == ("k_pack_bits+k_layer_count" if kind == "binary" else "k_layer_lds")
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
