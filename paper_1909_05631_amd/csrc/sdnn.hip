@@ -378,6 +378,7 @@ __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chu
 template <int B, int KC>
 __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                     const int2 *__restrict__ ell, int K,
+                                                    const uint4 *__restrict__ ell16, float wc,
                                                     const float *__restrict__ bias, float ymax,
                                                     const int *__restrict__ ids, const int *__restrict__ count,
                                                     unsigned *__restrict__ masks, int *__restrict__ rownz) {
@@ -457,7 +458,30 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
       // entries are loaded (unconditionally, so no branch delays the wait counts) while the
       // current group's LDS reads and fma chain run.
       const int2 *ej = ell + j;
-      if constexpr (KC > 0) {
+      if (ell16) {
+        // one weight wc and 32 sources per column, eight per 16-byte load ([4][N][8] u16); all
+        // four loads are in flight before the first group's LDS reads
+        uint4 ix[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) ix[g] = ell16[(size_t)g * N + j];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
+          float4 v[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const unsigned k = (q & 1) ? (pr[q >> 1] >> 16) : (pr[q >> 1] & 0xffffu);
+            v[q] = *reinterpret_cast<const float4 *>(tile + k * (unsigned)(B * 4) + qoff);
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            a0 = fmaf(v[q].x, wc, a0);
+            a1 = fmaf(v[q].y, wc, a1);
+            a2 = fmaf(v[q].z, wc, a2);
+            a3 = fmaf(v[q].w, wc, a3);
+          }
+        }
+      } else if constexpr (KC > 0) {
         static_assert(KC % 8 == 0, "KC must be a multiple of 8");
         int2 cur[8];
 #pragma unroll
@@ -533,8 +557,8 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
 
 // Device view of one layer for kernels that run several layers in one launch.
 struct LayerPtr {
-  const int2 *ell;              // slot-major ELL, offsets in units of 1 << ell_shift bytes per source
-  const unsigned short *src16;  // one-weight layer with 32 sources per column: [32][N] sources, else null
+  const int2 *ell;     // slot-major ELL, offsets in units of 1 << ell_shift bytes per source
+  const uint4 *ell16;  // one-weight layer with 32 sources per column: [4][N][8] u16 sources, else null
   const float *bias;
   float w;                      // the weight of a one-weight layer
   int K;
@@ -588,20 +612,20 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
       const int j = r * per_round + wave * OPW + jl;
       if (j >= N) break;
       float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
-      if (P.src16) {
-        // 32 sources in groups of 8; the next group's indices load while this group's terms run
-        const unsigned short *sj = P.src16 + j;
-        unsigned cur[8];
+      if (P.ell16) {
+        // 32 sources, eight per 16-byte load ([4][N][8] u16); all four loads in flight first
+        uint4 ix[4];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) cur[q] = sj[(size_t)q * N];
+        for (int g = 0; g < 4; ++g) ix[g] = P.ell16[(size_t)g * N + j];
 #pragma unroll
-        for (int g = 0; g < 32; g += 8) {
-          unsigned nxt[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) nxt[q] = g + 8 < 32 ? sj[(size_t)(g + 8 + q) * N] : 0u;
+        for (int g = 0; g < 4; ++g) {
+          const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
           float4 v[8];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) v[q] = *reinterpret_cast<const float4 *>(tq + cur[q] * (unsigned)(B * 4));
+          for (int q = 0; q < 8; ++q) {
+            const unsigned k = (q & 1) ? (pr[q >> 1] >> 16) : (pr[q >> 1] & 0xffffu);
+            v[q] = *reinterpret_cast<const float4 *>(tq + k * (unsigned)(B * 4));
+          }
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             a0 = fmaf(v[q].x, P.w, a0);
@@ -609,8 +633,6 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
             a2 = fmaf(v[q].z, P.w, a2);
             a3 = fmaf(v[q].w, P.w, a3);
           }
-#pragma unroll
-          for (int q = 0; q < 8; ++q) cur[q] = nxt[q];
         }
       } else {
         for (int sl = 0; sl < P.K; ++sl) {
@@ -1772,7 +1794,9 @@ struct LayerDev {
   // uniform layer: every column holds exactly K sources, all weights are w and all biases b
   bool uniform = false;
   float w = 0.0f, b = 0.0f;
-  const uint4 *ell16 = nullptr;  // layer 0 of a uniform layer with K == 32: [K/8][N][8] u16 source indices
+  // uniform layer with K == 32 on widths staged in LDS, and layer 0 of any width: [K/8][N][8] u16
+  // source indices, eight per 16-byte load
+  const uint4 *ell16 = nullptr;
   // global-tile path, uniform layer with K == 32 and N <= 65536: [K][N] u16 source indices (the
   // ELL's sources without the repeated weight)
   const unsigned short *src16 = nullptr;
@@ -1887,7 +1911,7 @@ hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerD
   }
   const int per_cu = lds <= 64 * 1024 ? 2 : 1;
   hipLaunchKernelGGL((k_layer_lds<B, KC>), dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
-                     ld.ell, ld.K, ld.bias, net->ymax, ids, count, net->masks, rownz);
+                     ld.ell, ld.K, ld.ell16, ld.w, ld.bias, net->ymax, ids, count, net->masks, rownz);
   return hipGetLastError();
 }
 
@@ -2261,7 +2285,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       ld.b = bias[(size_t)i * N];
     }
   }
-  if (N <= 65536) {
+  if (net->path == 1 && N <= 65536) {
     // uniform layers with 32 sources per column: 16-bit source lists, [K][N] like the ELL
     std::vector<int32_t> sel;
     for (int32_t i = 0; i < nl; ++i)
@@ -2288,24 +2312,35 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         net->layers[(size_t)l0 + sel[q]].src16 = reinterpret_cast<const unsigned short *>(ms) + per * q;
     }
   }
-  if (l0 == 0 && net->layers[0].uniform && net->layers[0].K == 32) {
-    // layer 0 of a uniform network: 16-bit source indices, 8 slots per 16-byte group, for the
-    // counting kernel
-    const int Kq = 32;
-    std::vector<uint16_t> h16((size_t)N * Kq);
-    const int64_t *cp = col_ptr;
-    for (int32_t j = 0; j < N; ++j)
-      for (int sl = 0; sl < Kq; ++sl)
-        h16[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)row_idx[cp[j] + sl];
-    char *m16 = nullptr;
-    e = hipMalloc(reinterpret_cast<void **>(&m16), h16.size() * sizeof(uint16_t));
-    if (e != hipSuccess) {
-      (void)hipGetLastError();
-      return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", h16.size() * sizeof(uint16_t), hipGetErrorString(e));
+  {
+    // 16-bit source indices in groups of 8 per output ([4][N][8] u16, one 16-byte load per group):
+    // every uniform layer with 32 sources per column on widths staged in LDS, and layer 0 of a
+    // uniform network of any width (for the counting kernel)
+    std::vector<int32_t> sel;
+    for (int32_t i = 0; i < nl; ++i) {
+      const LayerDev &ld = net->layers[(size_t)l0 + i];
+      if (ld.uniform && ld.K == 32 && N <= 65536 && (net->path == 0 || l0 + i == 0)) sel.push_back(i);
     }
-    net->allocations.push_back(m16);
-    HIP_OR_POISON(net, hipMemcpy(m16, h16.data(), h16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
-    net->layers[0].ell16 = reinterpret_cast<const uint4 *>(m16);
+    if (!sel.empty()) {
+      const size_t per = (size_t)32 * N;
+      std::vector<uint16_t> h16(per * sel.size());
+      parallel_for((int32_t)sel.size(), [&](int32_t q) {
+        const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
+        uint16_t *dst = h16.data() + per * (size_t)q;
+        for (int32_t j = 0; j < N; ++j)
+          for (int sl = 0; sl < 32; ++sl) dst[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)row_idx[cp[j] + sl];
+      });
+      char *m16 = nullptr;
+      e = hipMalloc(reinterpret_cast<void **>(&m16), h16.size() * sizeof(uint16_t));
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", h16.size() * sizeof(uint16_t), hipGetErrorString(e));
+      }
+      net->allocations.push_back(m16);
+      HIP_OR_POISON(net, hipMemcpy(m16, h16.data(), h16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      for (size_t q = 0; q < sel.size(); ++q)
+        net->layers[(size_t)l0 + sel[q]].ell16 = reinterpret_cast<const uint4 *>(m16) + (per / 8) * q;
+    }
   }
   // the device table of layers (for launches that run several layers)
   if (!net->lp_dev) {
@@ -2321,7 +2356,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     std::vector<LayerPtr> hp((size_t)nl);
     for (int32_t i = 0; i < nl; ++i) {
       const LayerDev &ld = net->layers[(size_t)l0 + i];
-      hp[(size_t)i] = LayerPtr{ld.ell, ld.src16, ld.bias, ld.w, ld.K};
+      hp[(size_t)i] = LayerPtr{ld.ell, ld.ell16, ld.bias, ld.w, ld.K};
     }
     HIP_OR_POISON(net, hipMemcpy(net->lp_dev + l0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
   }
