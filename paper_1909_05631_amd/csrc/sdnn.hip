@@ -1019,7 +1019,8 @@ constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 1
 // afterwards, so a workgroup may cache them in LDS.
 constexpr unsigned kDictEmpty = 0x7fc00000u;
 constexpr int kDictSlots = 256;
-// Code tiles hold 64 list positions: [tile][N][64] bytes, list position p at tile p / 64, byte p % 64.
+// Code tiles hold CR list positions (code_rows below): [tile][N][CR] bytes, list position p at tile
+// p / CR, byte p % CR.
 // The code-tile height goes with the bit tiles that write them: 128 rows after 32-row bit tiles,
 // whose counting workgroups then fill each 128-byte segment in 4 parts; 64 rows after 16-row bit
 // tiles (4 parts each as well). Taller segments serve more rows per gather request.
@@ -1760,7 +1761,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
           continue;
         }
         uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / CR) * N + jo[u]) * CR + p0 % CR);
-        // plain stores: the tiles of one 64-row code group fill each segment in parts, merged in L2
+        // plain stores: the tiles of one code group fill each segment in parts, merged in L2
         if (T == 32) {
           dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);
           dst[1] = make_uint4(cw[4], cw[5], cw[6], cw[7]);
@@ -2158,11 +2159,7 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
   net->ymax = ymax;
   net->layers.resize((size_t)n_layers);
   // LDS tile of B rows x N fp32 must fit the budget with B >= 8
-  int want = 32;
-  if (const char *e = std::getenv("SDNN_LDS_ROWS")) want = std::atoi(e);
-  if (want != 8 && want != 16 && want != 32) want = 32;
-  if ((size_t)want * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = want; }
-  else if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
+  if ((size_t)32 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 32; }
   else if ((size_t)16 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 16; }
   else if ((size_t)8 * n_neurons * sizeof(float) <= (size_t)kLdsTileBytes) { net->path = 0; net->B = 8; }
   else {
