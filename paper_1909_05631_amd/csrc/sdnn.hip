@@ -37,6 +37,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <type_traits>
 #include <thread>
 #include <vector>
 
@@ -95,6 +96,14 @@ __device__ __forceinline__ float activate(float z, float b, float ymax) {
 // Keeps the compiler from moving memory accesses across this point (no instruction is emitted):
 // pins the issue order of software-pipelined loads.
 __device__ __forceinline__ void mem_fence_compiler() { asm volatile("" ::: "memory"); }
+
+// Sets bits m in a liveness mask word that many workgroups report to. They report mostly the same
+// rows, and hundreds of atomics on one word from workgroups that finish together serialize (several
+// us per launch), so only bits not yet set go through an atomic. Within a layer bits are only ever
+// set, so a set bit read here is final; a stale read only costs an atomic.
+__device__ __forceinline__ void or_new_bits(unsigned *w, unsigned m) {
+  if (m & ~__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicOr(w, m);
+}
 
 // Ties four values to this point of the instruction stream (no instruction is emitted): the
 // computations producing them are scheduled before it.
@@ -908,58 +917,93 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   }
 }
 
+// Partial liveness words of a few-tile layer: worker workgroup (t, s) of a launch with S slots per
+// tile writes the rows of tile t that stayed live in its chunks to part[t * S + s], a plain store
+// (zero or not). The tile's mask word is the OR of its S slots. Hundreds of workgroups that finish
+// together would otherwise serialize on one atomic word (several us per launch).
+constexpr int kPartThreads = 256;
+constexpr int kPartLoads = 16;  // words per thread: kPartThreads x kPartLoads >= any launch's slots
+constexpr int kMaxPartWords = kPartThreads * kPartLoads;
+
+// Mask words m[t] = OR of the partial words of tile t (t < nt, S slots each), from the kPartLoads
+// words each thread of a kPartThreads workgroup loaded (word tid + kPartThreads k). Every thread of
+// the workgroup calls it; m: nt <= 8 words of LDS, returned after a barrier.
+__device__ void or_partials(const unsigned (&pp)[kPartLoads], int S, int nt, unsigned *m) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  if (tid < 8) m[tid] = 0u;
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    unsigned v = 0u;
+#pragma unroll
+    for (int k = 0; k < kPartLoads; ++k) v |= (tid + kPartThreads * k) / S == t ? pp[k] : 0u;
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) v |= __shfl_xor(v, d, 64);
+    if (lane == 0 && v) atomicOr(&m[t], v);
+  }
+  __syncthreads();
+}
+
+__device__ __forceinline__ void load_partials(unsigned (&pp)[kPartLoads], const unsigned *part, int words) {
+#pragma unroll
+  for (int k = 0; k < kPartLoads; ++k) {
+    const int i = threadIdx.x + kPartThreads * k;
+    pp[k] = i < words ? part[i] : 0u;
+  }
+}
+
+// The mask words of a few-tile layer from its partial words (before a compaction reads them).
+__global__ __launch_bounds__(kPartThreads) void k_finalize_masks(const unsigned *__restrict__ part, int S, int nt,
+                                                                 unsigned *__restrict__ masks) {
+  __shared__ unsigned m[8];
+  unsigned pp[kPartLoads];
+  load_partials(pp, part, S * nt);
+  or_partials(pp, S, nt, m);
+  if (threadIdx.x < nt) masks[threadIdx.x] = m[threadIdx.x];
+}
+
 // Layers of few rows (at most 8 tiles, so each XCD works on one tile's share of outputs): the tile
 // layout and lane mapping of k_layer_gfm with one output per lane and a whole chain's loads in
 // flight at once: the KC ELL entries straight from memory (the 8 lanes of an output read the same
-// entry), then all KC gathers, then the fma chain. A work item is a chunk of 32 outputs. The
-// bookkeeping of the layer sequence is that of k_layer_gfm; in addition, when the previous layer
-// left no live row (a row that died stays dead), the layer writes nothing: its masks stay zero, so
-// every later layer does the same.
+// entry), then all KC gathers, then the fma chain. A work item is a chunk of 32 outputs.
+// Such a layer is short, so its time is mostly the latency of dependent loads. The work split
+// follows ntiles_h, the host's bound on the tiles, so a lane issues its ELL loads and gathers before
+// it has read the list length, which only masks the liveness bits. Liveness goes to partial words part_out (S = per-XCD workgroups x parts slots per
+// tile); workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
+// tiles) into its mask words masks_prev, or, with part_prev null, reads those words; then it writes
+// their live count to count_out (if set) and clears masks_clear.
 template <int KC, bool CW>
-__global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict__ fin, float *__restrict__ fout,
-                                                         int N, const int2 *__restrict__ ell,
-                                                         const unsigned short *__restrict__ src16, float wc,
-                                                         const float *__restrict__ bias, float ymax,
-                                                         const int *__restrict__ npos, unsigned *__restrict__ masks,
-                                                         const unsigned *__restrict__ masks_prev,
-                                                         unsigned *__restrict__ masks_clear,
-                                                         int *__restrict__ count_out) {
+__global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
+    const float *__restrict__ fin, float *__restrict__ fout, int N, const int2 *__restrict__ ell,
+    const unsigned short *__restrict__ src16, float wc, const float *__restrict__ bias, float ymax,
+    const int *__restrict__ npos, int ntiles_h, unsigned *__restrict__ part_out,
+    const unsigned *__restrict__ part_prev, int prev_S, int prev_nt, unsigned *__restrict__ masks_prev,
+    unsigned *__restrict__ masks_clear, int *__restrict__ count_out) {
   constexpr int FMR = 32, CH = 32;
-  __shared__ unsigned rowmask;
-  __shared__ int prev_live;
-  const int R = *npos;
-  const int ntiles = min(8, (R + FMR - 1) / FMR);
+  __shared__ unsigned wmask[4];
+  __shared__ unsigned pmask[8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (tid < 64) {
-    int c = 0;
-    for (int i = tid; i < ntiles; i += 64) {
-      if (count_out) c += __popc(masks_prev[i]);
-      if (masks_clear && blockIdx.x == 0) masks_clear[i] = 0u;
-    }
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
-    if (tid == 0) {
-      if (count_out && blockIdx.x == 0) *count_out = c;
-      prev_live = count_out ? c : 1;
-      rowmask = 0u;
-    }
-  }
-  __syncthreads();
-  if (prev_live == 0 || ntiles == 0) return;
-  const int parts = 8 / ntiles;
+  const int parts = 8 / ntiles_h;
   const int xcd = blockIdx.x & 7;
-  if (xcd >= ntiles * parts) return;
   const int nchunks = (N + CH - 1) / CH;
   const int cpp = (nchunks + parts - 1) / parts;
   const int t = xcd / parts;
-  const int cbeg = (xcd % parts) * cpp, cend = min(nchunks, cbeg + cpp);
+  const bool worker = xcd < ntiles_h * parts;
+  const int cbeg = (xcd % parts) * cpp, cend = worker ? min(nchunks, cbeg + cpp) : 0;
   const int q = lane & 7, h = lane >> 3;
   const int per_xcd = gridDim.x >> 3;
-  const int nvalid = min(FMR, R - t * FMR);
   const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
   float *obase = fout + (size_t)t * N * FMR + q * 4;
+  const bool wg0 = blockIdx.x == 0;
+  // workgroup 0: the previous layer's partial words, in flight during its chunk
+  unsigned pp[kPartLoads];
+  if (wg0 && part_prev) load_partials(pp, part_prev, prev_S * prev_nt);
+  int R = 0;           // list length
+  unsigned pm = 0u;    // lane i < ntiles_h of workgroup 0: the previous layer's mask word of tile i
   unsigned lm = 0u;
-  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+  // FIRST: the workgroup's first chunk, which also issues the loads of the list length and the
+  // previous masks
+  auto run_chunk = [&](int chunk, auto first) {
+    constexpr bool FIRST = decltype(first)::value;
     const int j = chunk * CH + wave * 8 + h;
     const int jj = min(j, N - 1);
     // byte offsets of the sources' segments and the weights (CW: 16-bit source lists, weight wc)
@@ -980,6 +1024,13 @@ __global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict
     float4 g[KC];
 #pragma unroll
     for (int i = 0; i < KC; ++i) g[i] = *reinterpret_cast<const float4 *>(tbase + eo[i]);
+    if constexpr (FIRST) {
+      // after the gathers: vector loads complete in order, so waiting for these waits for nothing
+      // the fma chain does not need anyway
+      R = __hip_atomic_load(npos, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (wg0 && !part_prev && count_out)
+        pm = __hip_atomic_load(masks_prev + min(lane, ntiles_h - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     // every gather is issued before the first fma waits on one
     mem_fence_compiler();
     __builtin_amdgcn_sched_barrier(0);
@@ -998,15 +1049,39 @@ __global__ __launch_bounds__(256) void k_layer_gfm_small(const float *__restrict
                                  activate(a[3], b, ymax));
     const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
     lm |= (j < N ? bits : 0u) << (4 * q);
+    // positions past the list length (up to the host's tile bound) are stored too: nothing reads them
     if (j < N) store_stream(reinterpret_cast<float4 *>(obase + (size_t)j * FMR), y);
+  };
+  int chunk = cbeg + (int)(blockIdx.x >> 3);
+  if (chunk < cend) {
+    run_chunk(chunk, std::true_type{});
+    for (chunk += per_xcd; chunk < cend; chunk += per_xcd) run_chunk(chunk, std::false_type{});
+  }
+  if (wg0) {
+    // (workgroup 0 always runs chunk 0, so R is loaded)
+    const int ntiles = min(8, (R + FMR - 1) / FMR);
+    if (part_prev) {
+      or_partials(pp, prev_S, prev_nt, pmask);
+      if (tid < prev_nt) masks_prev[tid] = pmask[tid];
+      pm = lane < prev_nt ? pmask[lane] : 0u;
+    }
+    if (wave == 0) {
+      int c = __popc(lane < ntiles ? pm : 0u);
+#pragma unroll
+      for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
+      if (lane == 0 && count_out) *count_out = c;
+      if (masks_clear && lane < ntiles) masks_clear[lane] = 0u;
+    }
   }
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
-  if (lane == 0 && lm) atomicOr(&rowmask, lm);
+  if (lane == 0) wmask[wave] = lm;
   __syncthreads();
-  if (tid == 0) {
-    const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);
-    if (rowmask & valid) atomicOr(&masks[t], rowmask & valid);
+  if (tid == 0 && worker) {
+    const int nvalid = min(FMR, R - t * FMR);
+    const unsigned valid = nvalid >= 32 ? 0xffffffffu : (nvalid > 0 ? (1u << nvalid) - 1u : 0u);
+    const int S = per_xcd * parts;
+    part_out[t * S + (blockIdx.x >> 3) * parts + xcd % parts] = (wmask[0] | wmask[1] | wmask[2] | wmask[3]) & valid;
   }
 }
 
@@ -1834,6 +1909,7 @@ struct sdnn_net {
                         // [4 + i] positions in list i
   unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (256 fp32 bit patterns)
   unsigned *seglive = nullptr;  // path 1: per fp32 tile, one bit per source: the segment was stored
+  unsigned *part[2] = {nullptr, nullptr};  // path 1: partial liveness words of few-tile layers, by layer parity
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
@@ -1864,7 +1940,7 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, final_ids, total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, part[2], final_ids, total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -1888,6 +1964,10 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.dict = off; off += 256 * sizeof(unsigned);
   w.seglive = off;
   if (net->path == 1) off += align_up(rows / 32 * (size_t)((net->N + 31) / 32) * sizeof(unsigned), a);
+  for (int i = 0; i < 2; ++i) {
+    w.part[i] = off;
+    if (net->path == 1) off += align_up((size_t)kMaxPartWords * sizeof(unsigned), a);
+  }
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
   w.total = off;
   return w;
@@ -1923,20 +2003,27 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
   return launch_lds<B, 0>(net, yin, yout, ld, ids, count, rownz);
 }
 
-// A layer of at most 8 tiles with K == 32 (see k_layer_gfm_small).
+// A layer of at most 8 tiles with K == 32 (see k_layer_gfm_small). Liveness goes to the partial
+// words part_out; *S_out and *nt_out receive their slots per tile and tiles.
 hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
-                            int64_t max_tiles, unsigned *masks, const unsigned *masks_prev, unsigned *masks_clear,
-                            int *count_out) {
+                            int64_t max_tiles, unsigned *part_out, const unsigned *part_prev, int prev_S, int prev_nt,
+                            unsigned *masks_prev, unsigned *masks_clear, int *count_out, int *S_out, int *nt_out) {
   const int nchunks = (net->N + 31) / 32;
-  const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
-  const int per_xcd = (int)std::min<int64_t>(2 * net->cus, (nchunks + parts - 1) / parts);
-  const dim3 grid(8 * std::max(1, per_xcd));
+  const int ntiles_h = (int)std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
+  const int parts = 8 / ntiles_h;
+  // at most kMaxPartWords / 8 workgroups per XCD, so that the partial words fit their buffer
+  const int per_xcd = std::max(1, std::min({kMaxPartWords / 8, 2 * net->cus, (nchunks + parts - 1) / parts}));
+  const dim3 grid(8 * per_xcd);
+  *S_out = per_xcd * parts;
+  *nt_out = ntiles_h;
   if (ld.src16)
-    hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell,
-                       ld.src16, ld.w, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
+    hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
+                       ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
+                       masks_prev, masks_clear, count_out);
   else
-    hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell,
-                       ld.src16, ld.w, ld.bias, net->ymax, npos, masks, masks_prev, masks_clear, count_out);
+    hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
+                       ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
+                       masks_prev, masks_clear, count_out);
   return hipGetLastError();
 }
 
@@ -2508,6 +2595,18 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   int last_list = 0;
   bool compacted = true;   // the last layer run has been followed by a compaction
   PollRing ring;
+  // few-tile layers leave their liveness in partial words; the next few-tile launch turns them into
+  // mask words, any other reader of the masks needs k_finalize_masks first
+  bool parts_pending = false;
+  int32_t part_layer = -1;
+  int part_S = 0, part_nt = 0;
+  auto finalize_parts = [&]() -> hipError_t {
+    if (!parts_pending) return hipSuccess;
+    parts_pending = false;
+    hipLaunchKernelGGL(k_finalize_masks, dim3(1), dim3(kPartThreads), 0, s, net->part[part_layer & 1], part_S, part_nt,
+                       masks_for(part_layer));
+    return hipGetLastError();
+  };
   int32_t l = 0;
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
@@ -2571,11 +2670,18 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       const LayerDev &ld = net->layers[(size_t)l];
       int *cnt = compacted ? nullptr : net->counts + l;
       if (small && ld.K == 32) {
-        HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
-                                            masks_for(l + 1), cnt));
+        const unsigned *prev = cnt && parts_pending ? net->part[part_layer & 1] : nullptr;
+        int S = 0, nt = 0;
+        HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), net->part[l & 1], prev, part_S,
+                                            part_nt, masks_for(l - 1), masks_for(l + 1), cnt, &S, &nt));
+        parts_pending = true;
+        part_layer = l;
+        part_S = S;
+        part_nt = nt;
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_FEW_ROWS;
         net->layer_launches[(size_t)l] = 1;
       } else {
+        HIP_OR_POISON(net, finalize_parts());
         HIP_OR_POISON(net, launch_gfm(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
                                       masks_for(l + 1), cnt));
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
@@ -2584,6 +2690,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
     auto compact = [&]() -> hipError_t {
+      const hipError_t e = finalize_parts();
+      if (e != hipSuccess) return e;
       hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, mk, 32, net->ids[cur], net->ids[cur ^ 1],
                          net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
       last_list = cur ^ 1;
@@ -2654,6 +2762,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   if (!compacted) {
     // the final list: compaction of the last layer's masks
     const int32_t last = l - 1;
+    HIP_OR_POISON(net, finalize_parts());
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, masks_for(last), 32, net->ids[cur], net->ids[cur ^ 1],
                        net->src[cur ^ 1], npos + cur, net->counts + last + 1, npos + (cur ^ 1));
     HIP_OR_POISON(net, hipGetLastError());
@@ -2707,6 +2816,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->misc = reinterpret_cast<int *>(ws + w.misc);
   net->dict = reinterpret_cast<unsigned *>(ws + w.dict);
   net->seglive = reinterpret_cast<unsigned *>(ws + w.seglive);
+  for (int i = 0; i < 2; ++i) net->part[i] = reinterpret_cast<unsigned *>(ws + w.part[i]);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
   net->ran = false;
 
