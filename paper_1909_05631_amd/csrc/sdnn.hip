@@ -101,8 +101,17 @@ __device__ __forceinline__ void mem_fence_compiler() { asm volatile("" ::: "memo
 // rows, and hundreds of atomics on one word from workgroups that finish together serialize (several
 // us per launch), so only bits not yet set go through an atomic. Within a layer bits are only ever
 // set, so a set bit read here is final; a stale read only costs an atomic.
-__device__ __forceinline__ void or_new_bits(unsigned *w, unsigned m) {
-  if (m & ~__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) atomicOr(w, m);
+// Liveness words of large layers. Device-scope atomics on one 128-byte line serialize across
+// workgroups (2048 workgroups of a launch ORing into one line: tens of us), while atomics on
+// different lines proceed in parallel. So mask word t of such a layer is spread over kSpread words
+// in lines of their own, spread[(t * kSpread + g) * kLineWords] with g taken from the workgroup
+// index, and k_spread_to_masks ORs them into masks[t] before a compaction reads it.
+constexpr int kSpread = 8, kLineWords = 32;
+__device__ __forceinline__ void or_mask(unsigned *masks, unsigned *spread, int t, unsigned m) {
+  if (spread)
+    atomicOr(&spread[((size_t)t * kSpread + ((blockIdx.x >> 3) & (kSpread - 1))) * kLineWords], m);
+  else
+    atomicOr(&masks[t], m);
 }
 
 // Ties four values to this point of the instruction stream (no instruction is emitted): the
@@ -143,7 +152,8 @@ constexpr int kOverflowSlot = 2;
 constexpr int kNposSlot = 4;
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsigned *__restrict__ masks2,
                        unsigned *__restrict__ masks3, int *__restrict__ rownz, int *__restrict__ counts,
-                       int *__restrict__ misc, unsigned *__restrict__ dict, int M, int L) {
+                       int *__restrict__ misc, unsigned *__restrict__ dict, int M, int L,
+                       unsigned *__restrict__ spread, size_t spread_words) {
   const int st = gridDim.x * blockDim.x;
   // value dictionary: slot 0 holds +0.0 (bit pattern 0), every other slot is free
   if (blockIdx.x == 0)
@@ -157,6 +167,7 @@ __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsi
     rownz[i] = 0;
   }
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i <= L; i += st) counts[i] = (i == 0) ? M : 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < spread_words; i += st) spread[i] = 0u;
 }
 
 // Inclusive prefix sum over the 64 lanes of a wave.
@@ -175,6 +186,23 @@ __device__ __forceinline__ int wave_inclusive_sum(int v, int lane) {
 // the next layer. One workgroup of 1024 threads; tiles are taken 4096 at a time: an exclusive scan
 // of their popcounts gives each tile's output offset, then every position is placed.
 constexpr int kCompactTiles = 4096;
+// masks[t] = OR of the spread words of tile t (see or_mask) for the tiles of the first *npos list
+// positions; the spread words are zeroed for the next large layer.
+__global__ __launch_bounds__(256) void k_spread_to_masks(unsigned *__restrict__ spread, const int *__restrict__ npos,
+                                                         unsigned *__restrict__ masks) {
+  const int nt = (*npos + 31) / 32;
+  for (int t = blockIdx.x * blockDim.x + threadIdx.x; t < nt; t += gridDim.x * blockDim.x) {
+    unsigned m = 0u;
+#pragma unroll
+    for (int g = 0; g < kSpread; ++g) {
+      unsigned *w = &spread[((size_t)t * kSpread + g) * kLineWords];
+      m |= *w;
+      *w = 0u;
+    }
+    masks[t] = m;
+  }
+}
+
 __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, int B, const int *__restrict__ ids_in,
                                                   int *__restrict__ ids_out, int *__restrict__ src_out,
                                                   const int *__restrict__ count_in, int *__restrict__ count_out,
@@ -783,7 +811,8 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                    int tile0, const unsigned *__restrict__ masks_prev,
-                                                   unsigned *__restrict__ masks_clear, int *__restrict__ count_out) {
+                                                   unsigned *__restrict__ masks_clear, int *__restrict__ count_out,
+                                                   unsigned *__restrict__ spread) {
   static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
   constexpr int CH = kGfmOutputs, OPL = 8;
   static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
@@ -913,7 +942,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   __syncthreads();
   if (tid == 0) {
     const unsigned valid = nvalid >= 32 ? 0xffffffffu : ((1u << nvalid) - 1u);  // 0 when inactive
-    if (active && (rowmask & valid)) atomicOr(&masks[t], rowmask & valid);
+    if (active && (rowmask & valid)) or_mask(masks, spread, t, rowmask & valid);
   }
 }
 
@@ -967,8 +996,10 @@ __global__ __launch_bounds__(kPartThreads) void k_finalize_masks(const unsigned 
 // entry), then all KC gathers, then the fma chain. A work item is a chunk of 32 outputs.
 // Such a layer is short, so its time is mostly the latency of dependent loads. The work split
 // follows ntiles_h, the host's bound on the tiles, so a lane issues its ELL loads and gathers before
-// it has read the list length, which only masks the liveness bits. Liveness goes to partial words part_out (S = per-XCD workgroups x parts slots per
-// tile); workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
+// it has read the list length, which only masks the liveness bits. live_before is the live count two
+// layers back (final when the launch starts); at zero every input is zero and the layer neither
+// gathers nor stores. Liveness goes to partial words part_out (S = per-XCD workgroups x parts slots
+// per tile). Workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
 // tiles) into its mask words masks_prev, or, with part_prev null, reads those words; then it writes
 // their live count to count_out (if set) and clears masks_clear.
 template <int KC, bool CW>
@@ -977,7 +1008,7 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const unsigned short *__restrict__ src16, float wc, const float *__restrict__ bias, float ymax,
     const int *__restrict__ npos, int ntiles_h, unsigned *__restrict__ part_out,
     const unsigned *__restrict__ part_prev, int prev_S, int prev_nt, unsigned *__restrict__ masks_prev,
-    unsigned *__restrict__ masks_clear, int *__restrict__ count_out) {
+    unsigned *__restrict__ masks_clear, int *__restrict__ count_out, const int *__restrict__ live_before) {
   constexpr int FMR = 32, CH = 32;
   __shared__ unsigned wmask[4];
   __shared__ unsigned pmask[8];
@@ -994,6 +1025,12 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
   const char *tbase = reinterpret_cast<const char *>(fin + (size_t)t * N * FMR) + q * 16;
   float *obase = fout + (size_t)t * N * FMR + q * 4;
   const bool wg0 = blockIdx.x == 0;
+  // no row was live two layers back: every input is zero, so the layer gathers nothing and stores
+  // nothing, and its rows stay dead. The count is read through a per-lane (zero) offset, which keeps
+  // it a vector value: used as a scalar it would be waited for before the ELL loads are issued.
+  int zero;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+  const int count_before = __hip_atomic_load(live_before + zero, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   // workgroup 0: the previous layer's partial words, in flight during its chunk
   unsigned pp[kPartLoads];
   if (wg0 && part_prev) load_partials(pp, part_prev, prev_S * prev_nt);
@@ -1021,6 +1058,12 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
       }
     }
     const float b = bias[jj];
+    // taken here, after the ELL loads (the asm keeps the compare from being hoisted above them)
+    int cb = count_before;
+    asm volatile("" : "+v"(cb));
+    const bool dead = cb == 0;
+#pragma unroll
+    for (int i = 0; i < KC; ++i) eo[i] = dead ? 0u : eo[i];
     float4 g[KC];
 #pragma unroll
     for (int i = 0; i < KC; ++i) g[i] = *reinterpret_cast<const float4 *>(tbase + eo[i]);
@@ -1050,7 +1093,7 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
     lm |= (j < N ? bits : 0u) << (4 * q);
     // positions past the list length (up to the host's tile bound) are stored too: nothing reads them
-    if (j < N) store_stream(reinterpret_cast<float4 *>(obase + (size_t)j * FMR), y);
+    if (j < N && !dead) store_stream(reinterpret_cast<float4 *>(obase + (size_t)j * FMR), y);
   };
   int chunk = cbeg + (int)(blockIdx.x >> 3);
   if (chunk < cend) {
@@ -1081,7 +1124,8 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const int nvalid = min(FMR, R - t * FMR);
     const unsigned valid = nvalid >= 32 ? 0xffffffffu : (nvalid > 0 ? (1u << nvalid) - 1u : 0u);
     const int S = per_xcd * parts;
-    part_out[t * S + (blockIdx.x >> 3) * parts + xcd % parts] = (wmask[0] | wmask[1] | wmask[2] | wmask[3]) & valid;
+    part_out[t * S + (blockIdx.x >> 3) * parts + xcd % parts] =
+        count_before == 0 ? 0u : (wmask[0] | wmask[1] | wmask[2] | wmask[3]) & valid;
   }
 }
 
@@ -1151,7 +1195,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
                                                       const float *__restrict__ bias, float ymax,
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
-                                                      int tile0) {
+                                                      int tile0, unsigned *__restrict__ spread) {
   constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
@@ -1339,7 +1383,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
       const int lo = 32 * q;  // rows lo .. lo + 31 of the code tile
       const unsigned valid = nvalid - lo >= 32 ? 0xffffffffu : (nvalid > lo ? ((1u << (nvalid - lo)) - 1u) : 0u);
       const unsigned m = (unsigned)(rowmask[q / 2] >> (32 * (q & 1))) & valid;
-      if (m) atomicOr(&masks[ST * t + q], m);
+      if (m) or_mask(masks, spread, ST * t + q, m);
     }
   }
 }
@@ -1910,6 +1954,7 @@ struct sdnn_net {
   unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (256 fp32 bit patterns)
   unsigned *seglive = nullptr;  // path 1: per fp32 tile, one bit per source: the segment was stored
   unsigned *part[2] = {nullptr, nullptr};  // path 1: partial liveness words of few-tile layers, by layer parity
+  unsigned *spread = nullptr;              // path 1: liveness words of large layers, one 128-byte line each
   long long *final_ids = nullptr;
   int final_list = 0;        // which ids buffer holds the final list
   int32_t layers_run = 0;    // layers enqueued by the last infer
@@ -1940,7 +1985,8 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, part[2], final_ids, total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, part[2], spread, spread_words, final_ids,
+      total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -1968,6 +2014,9 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
     w.part[i] = off;
     if (net->path == 1) off += align_up((size_t)kMaxPartWords * sizeof(unsigned), a);
   }
+  w.spread = off;
+  w.spread_words = net->path == 1 ? rows / 32 * kSpread * kLineWords : 0;
+  off += align_up(w.spread_words * sizeof(unsigned), a);
   w.final_ids = off; off += align_up((size_t)std::max<int64_t>(M, 1) * sizeof(long long), a);
   w.total = off;
   return w;
@@ -2007,7 +2056,8 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
 // words part_out; *S_out and *nt_out receive their slots per tile and tiles.
 hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
                             int64_t max_tiles, unsigned *part_out, const unsigned *part_prev, int prev_S, int prev_nt,
-                            unsigned *masks_prev, unsigned *masks_clear, int *count_out, int *S_out, int *nt_out) {
+                            unsigned *masks_prev, unsigned *masks_clear, int *count_out, const int *live_before,
+                            int *S_out, int *nt_out) {
   const int nchunks = (net->N + 31) / 32;
   const int ntiles_h = (int)std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int parts = 8 / ntiles_h;
@@ -2019,11 +2069,11 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   if (ld.src16)
     hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out);
+                       masks_prev, masks_clear, count_out, live_before);
   else
     hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out);
+                       masks_prev, masks_clear, count_out, live_before);
   return hipGetLastError();
 }
 
@@ -2033,7 +2083,7 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
 // live rows from masks_prev and clears masks_clear.
 hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
                       int64_t max_tiles, unsigned *masks, const unsigned *masks_prev = nullptr,
-                      unsigned *masks_clear = nullptr, int *count_out = nullptr) {
+                      unsigned *masks_clear = nullptr, int *count_out = nullptr, unsigned *spread = nullptr) {
   const int rounds = (int)((max_tiles + 7) / 8);
   // one workgroup per output chunk of a tile's share when the round has fewer than 8 tiles
   const int nchunks = (net->N + kGfmOutputs - 1) / kGfmOutputs;
@@ -2044,13 +2094,13 @@ hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float
     int *cnt = r == 0 ? count_out : nullptr;
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
     else
       hipLaunchKernelGGL((k_layer_gfm<32, 0, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt);
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2156,13 +2206,16 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, true, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
+                         net->spread);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
+                         net->spread);
     else
       hipLaunchKernelGGL((k_layer_gfm_u8<0, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8);
+                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
+                         net->spread);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2611,6 +2664,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
     fout_codes = false;
+    bool spread_used = false;  // this layer's liveness is in the spread words
     bool seglive_out = false;  // fout's all-zero segments were skipped (net->seglive says which)
     unsigned *mk = masks_for(l);
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
@@ -2653,7 +2707,9 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                                : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, fout_codes));
       } else {
         HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, try_bits ? nullptr : net->rownz));
-        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk));
+        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk, nullptr, nullptr,
+                                      nullptr, net->spread));
+        spread_used = true;
         net->layer_kernel[0] = SDNN_KERNEL_GLOBAL_TILE;
         net->layer_launches[0] = (int32_t)(1 + (tiles(P) + 7) / 8) + (try_bits ? 1 : 0);
       }
@@ -2661,6 +2717,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       // follows layer 0, which is always compacted: no count to take over
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
                                        npos + cur, tiles(P), mk));
+      spread_used = true;
       seglive_out = true;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
       const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
@@ -2673,7 +2730,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         const unsigned *prev = cnt && parts_pending ? net->part[part_layer & 1] : nullptr;
         int S = 0, nt = 0;
         HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), net->part[l & 1], prev, part_S,
-                                            part_nt, masks_for(l - 1), masks_for(l + 1), cnt, &S, &nt));
+                                            part_nt, masks_for(l - 1), masks_for(l + 1), cnt, net->counts + (l - 1), &S, &nt));
         parts_pending = true;
         part_layer = l;
         part_S = S;
@@ -2682,16 +2739,25 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         net->layer_launches[(size_t)l] = 1;
       } else {
         HIP_OR_POISON(net, finalize_parts());
+        // a large layer's liveness goes through spread words (compacted right after)
         HIP_OR_POISON(net, launch_gfm(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
-                                      masks_for(l + 1), cnt));
+                                      masks_for(l + 1), cnt, small ? nullptr : net->spread));
+        spread_used = !small;
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
         net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
       }
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
     auto compact = [&]() -> hipError_t {
-      const hipError_t e = finalize_parts();
+      hipError_t e = finalize_parts();
       if (e != hipSuccess) return e;
+      if (spread_used) {
+        const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus, (tiles(P) + 255) / 256));
+        hipLaunchKernelGGL(k_spread_to_masks, dim3(grid), dim3(256), 0, s, net->spread, npos + cur, mk);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        spread_used = false;
+      }
       hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, mk, 32, net->ids[cur], net->ids[cur ^ 1],
                          net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
       last_list = cur ^ 1;
@@ -2817,6 +2883,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->dict = reinterpret_cast<unsigned *>(ws + w.dict);
   net->seglive = reinterpret_cast<unsigned *>(ws + w.seglive);
   for (int i = 0; i < 2; ++i) net->part[i] = reinterpret_cast<unsigned *>(ws + w.part[i]);
+  net->spread = reinterpret_cast<unsigned *>(ws + w.spread);
   net->final_ids = reinterpret_cast<long long *>(ws + w.final_ids);
   net->ran = false;
 
@@ -2824,7 +2891,7 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   hipStream_t s = net->stream;
   hipLaunchKernelGGL(k_init, dim3(std::max(1, std::min(net->cus * 4, (M + 255) / 256 + 1))), dim3(256), 0, s,
                      net->ids[0], net->masks_rot[0], net->masks_rot[1], net->masks_rot[2], net->rownz, net->counts,
-                     net->misc, net->dict, M, net->L);
+                     net->misc, net->dict, M, net->L, net->spread, w.spread_words);
   HIP_OR_POISON(net, hipGetLastError());
   if (net->profiling) net->prof_rec.assign((size_t)net->L, 0);
   net->layer_kernel.assign((size_t)net->L, SDNN_KERNEL_NONE);
