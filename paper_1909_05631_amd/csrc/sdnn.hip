@@ -30,6 +30,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -946,6 +947,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   }
 }
 
+// Progress word of few-tile layers, stored by workgroup 0 of each launch into coherent host memory:
+// run generation (16 bits) | layer of the launch (20 bits) | live count of the previous layer (28
+// bits; all ones when this launch did not count it). The host reads it to follow the device
+// without copies or events, and to stop enqueuing layers once no row is live.
+constexpr int kProgLayerShift = 28, kProgGenShift = 48;
+constexpr unsigned long long kProgCountMask = (1ull << kProgLayerShift) - 1;
+constexpr int kProgressAhead = 6;  // layers the host may enqueue ahead of the last reported one
+
 // Partial liveness words of a few-tile layer: worker workgroup (t, s) of a launch with S slots per
 // tile writes the rows of tile t that stayed live in its chunks to part[t * S + s], a plain store
 // (zero or not). The tile's mask word is the OR of its S slots. Hundreds of workgroups that finish
@@ -1001,14 +1010,15 @@ __global__ __launch_bounds__(kPartThreads) void k_finalize_masks(const unsigned 
 // gathers nor stores. Liveness goes to partial words part_out (S = per-XCD workgroups x parts slots
 // per tile). Workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
 // tiles) into its mask words masks_prev, or, with part_prev null, reads those words; then it writes
-// their live count to count_out (if set) and clears masks_clear.
+// their live count to count_out (if set) and to the progress word (if set), and clears masks_clear.
 template <int KC, bool CW>
 __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const float *__restrict__ fin, float *__restrict__ fout, int N, const int2 *__restrict__ ell,
     const unsigned short *__restrict__ src16, float wc, const float *__restrict__ bias, float ymax,
     const int *__restrict__ npos, int ntiles_h, unsigned *__restrict__ part_out,
     const unsigned *__restrict__ part_prev, int prev_S, int prev_nt, unsigned *__restrict__ masks_prev,
-    unsigned *__restrict__ masks_clear, int *__restrict__ count_out, const int *__restrict__ live_before) {
+    unsigned *__restrict__ masks_clear, int *__restrict__ count_out, const int *__restrict__ live_before,
+    unsigned long long *__restrict__ progress, unsigned long long progress_tag) {
   constexpr int FMR = 32, CH = 32;
   __shared__ unsigned wmask[4];
   __shared__ unsigned pmask[8];
@@ -1113,6 +1123,9 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
 #pragma unroll
       for (int d = 32; d >= 1; d >>= 1) c += __shfl_xor(c, d, 64);
       if (lane == 0 && count_out) *count_out = c;
+      if (lane == 0 && progress)
+        __hip_atomic_store(progress, progress_tag | (count_out ? (unsigned long long)c : kProgCountMask),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
       if (masks_clear && lane < ntiles) masks_clear[lane] = 0u;
     }
   }
@@ -1962,6 +1975,10 @@ struct sdnn_net {
   const float *final_y = nullptr;   // path 0: final activations, row-major by row id
   const float *final_fm = nullptr;  // path 1: final activation tiles; live row i is at position src[final_list][i]
   int32_t *pinned = nullptr; // read-back slots (0-3: polling ring, 6: input-not-binary flag, 7: exact count)
+  // progress word of few-tile layers, in coherent host memory written by the device (see
+  // progress_word); progress_dev is its device address
+  unsigned long long *progress = nullptr, *progress_dev = nullptr;
+  uint32_t run_gen = 0;      // generation of the current infer, in the progress word's top bits
   std::vector<hipEvent_t> events;
   // profiling
   bool profiling = false;
@@ -2057,7 +2074,7 @@ hipError_t launch_lds_k(sdnn_net *net, const float *yin, float *yout, const Laye
 hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
                             int64_t max_tiles, unsigned *part_out, const unsigned *part_prev, int prev_S, int prev_nt,
                             unsigned *masks_prev, unsigned *masks_clear, int *count_out, const int *live_before,
-                            int *S_out, int *nt_out) {
+                            unsigned long long *progress, unsigned long long progress_tag, int *S_out, int *nt_out) {
   const int nchunks = (net->N + 31) / 32;
   const int ntiles_h = (int)std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int parts = 8 / ntiles_h;
@@ -2069,11 +2086,11 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   if (ld.src16)
     hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out, live_before);
+                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag);
   else
     hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out, live_before);
+                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag);
   return hipGetLastError();
 }
 
@@ -2660,9 +2677,33 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                        masks_for(part_layer));
     return hipGetLastError();
   };
+  // few-tile layers: the host follows the device through the progress word, staying at most
+  // kProgressAhead layers ahead of it, so that it learns within a few layers that no row is left
+  const unsigned long long gen = net->run_gen & 0xffffu;
+  bool follow = net->progress != nullptr;
+  auto follow_progress = [&](int32_t layer) -> hipError_t {
+    const int32_t need = layer - kProgressAhead;
+    if (!follow || need < 0) return hipSuccess;
+    const auto t0 = std::chrono::steady_clock::now();
+    for (uint32_t it = 1;; ++it) {
+      const unsigned long long w = __atomic_load_n(net->progress, __ATOMIC_ACQUIRE);
+      if ((w >> kProgGenShift) == gen && (int32_t)((w >> kProgLayerShift) & 0xfffffu) >= need) {
+        const unsigned long long c = w & kProgCountMask;
+        if (c != kProgCountMask) live_bound = std::min<int64_t>(live_bound, (int64_t)c);
+        return hipSuccess;
+      }
+      if ((it & 4095u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) {
+        // no report from the device: wait for the stream, and poll by copies from now on
+        follow = false;
+        return hipStreamSynchronize(s);
+      }
+      __builtin_ia32_pause();
+    }
+  };
   int32_t l = 0;
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
+    bool reported = false;  // this layer's launch writes the progress word
     fout_codes = false;
     bool spread_used = false;  // this layer's liveness is in the spread words
     bool seglive_out = false;  // fout's all-zero segments were skipped (net->seglive says which)
@@ -2729,8 +2770,11 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (small && ld.K == 32) {
         const unsigned *prev = cnt && parts_pending ? net->part[part_layer & 1] : nullptr;
         int S = 0, nt = 0;
+        const unsigned long long tag = (gen << kProgGenShift) | ((unsigned long long)l << kProgLayerShift);
         HIP_OR_POISON(net, launch_gfm_small(net, ld, fin, fout, npos + cur, tiles(P), net->part[l & 1], prev, part_S,
-                                            part_nt, masks_for(l - 1), masks_for(l + 1), cnt, net->counts + (l - 1), &S, &nt));
+                                            part_nt, masks_for(l - 1), masks_for(l + 1), cnt, net->counts + (l - 1),
+                                            follow ? net->progress_dev : nullptr, tag, &S, &nt));
+        reported = follow;
         parts_pending = true;
         part_layer = l;
         part_S = S;
@@ -2823,7 +2867,10 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     }
     fin_codes = fout_codes;
     // counts[l] is final once layer l has run (written by a compaction or by layer l's launch)
-    HIP_OR_POISON(net, poll_step(net, ring, l, l, &live_bound));
+    if (reported)
+      HIP_OR_POISON(net, follow_progress(l));
+    else
+      HIP_OR_POISON(net, poll_step(net, ring, l, l, &live_bound));
   }
   if (!compacted) {
     // the final list: compaction of the last layer's masks
@@ -2863,9 +2910,14 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
     net->events.resize(4);
     for (auto &ev : net->events) HIP_OR_POISON(net, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
     HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 8 * sizeof(int32_t), hipHostMallocDefault));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->progress), sizeof(unsigned long long),
+                                     hipHostMallocCoherent));
+    *net->progress = 0ull;
+    HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->progress_dev), net->progress, 0));
   }
   char *ws = static_cast<char *>(workspace);
   net->M = n_rows;
+  ++net->run_gen;
   net->stream = reinterpret_cast<hipStream_t>(hip_stream);
   net->ws = ws;
   for (int i = 0; i < 2; ++i) {
@@ -3067,6 +3119,7 @@ void sdnn_destroy(sdnn_net *net) {
   for (void *p : net->allocations) (void)hipFree(p);
   for (auto &ev : net->events) (void)hipEventDestroy(ev);
   if (net->pinned) (void)hipHostFree(net->pinned);
+  if (net->progress) (void)hipHostFree(net->progress);
   delete net;
 }
 
