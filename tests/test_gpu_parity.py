@@ -298,6 +298,33 @@ def test_counting_layer0_lds_widths(kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("m", [40, 200])
+def test_few_tile_tail_dies(m):
+    """Widths gathered from global tiles with few rows (at most 8 tiles per layer): every row stays
+    live up to layer 20, whose bias kills them all. The few-tile launches report liveness through
+    per-workgroup partial words and the host follows them through the progress word, so it must stop
+    enqueuing within a few layers of the last live one; layers enqueued after it must store nothing
+    and report no row (their inputs are zero)."""
+    n, nl, die = 6000, 200, 20
+    rng = np.random.default_rng(m)
+    y0 = (rng.random((m, n)) < 0.5).astype(np.float32)
+    cp, ri, v = synth.layers_csc(17, 0, nl, n)
+    bias = [np.full(n, 0.10 if l != die else -100.0, np.float32) for l in range(nl)]
+    layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
+    log(f"few-tile tail dies m={m}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert cats.size == 0
+    counts = oracle.padded_live_counts(o, nl)
+    assert counts[die] == m and counts[die + 1] == 0
+    kinds, _ = gpu.net.layer_info()
+    ran = [l for l in range(nl) if sdnn_kind(kinds[l]) != "none"]
+    assert ran == list(range(len(ran)))
+    assert sdnn_kind(kinds[5]) == "k_layer_gfm_small"
+    # the host learns of the empty list a few layers after the device (6 layers of lead)
+    assert die + 1 < len(ran) <= die + 12, len(ran)
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
