@@ -41,11 +41,25 @@ def algorithmic_layer_bytes(n: int, nnz: int, r_in: int, r_out: int) -> int:
     return 4 * n * (r_in + r_out) + 8 * nnz + 4 * n
 
 
-def cpu_baseline(cfg, target_s: float, threads: int) -> dict:
+def layer_source(cfg, network: str):
+    """The weight layers of a workload: the configs' permutation-union layers, or structured
+    RadiX-Net style layers of the same width (synth.radix_layers_csc)."""
+    import synth
+    if network == "radix":
+        return lambda l0, nl: synth.radix_layers_csc(cfg.net_id, l0, nl, cfg.n_neurons, cfg.weight)
+    return lambda l0, nl: synth.layers_csc(cfg.net_id, l0, nl, cfg.n_neurons, cfg.k, cfg.weight)
+
+
+def workload_name(cfg, network: str) -> str:
+    return cfg.name if network == "union" else f"{network}-{cfg.name}"
+
+
+def cpu_baseline(cfg, target_s: float, threads: int, network: str = "union") -> dict:
     """The oracle as it is, on a bounded sample of the same workload (first rows of the input set),
     timing only its layer evaluations (weight generation is loading, untimed as on the GPU side)."""
     import oracle
     import synth
+    layers = layer_source(cfg, network)
 
     def run(rows: int) -> float:
         y0 = synth.config_inputs(cfg, 0, rows)
@@ -54,7 +68,7 @@ def cpu_baseline(cfg, target_s: float, threads: int) -> dict:
         spent, l, chunk = 0.0, 0, 8
         while l < cfg.n_layers and o.live > 0:
             nl = min(chunk, cfg.n_layers - l)
-            cp, ri, v = synth.layers_csc(cfg.net_id, l, nl, cfg.n_neurons, cfg.k, cfg.weight)
+            cp, ri, v = layers(l, nl)
             for i in range(nl):
                 t0 = time.perf_counter()
                 o.layer(cp[i], ri, v, bias, threads)
@@ -74,7 +88,7 @@ def cpu_baseline(cfg, target_s: float, threads: int) -> dict:
         t = run(rows)
     rate = rows * cfg.total_nnz / t
     return {"value": rate, "unit": "inputs*edges/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {rows} of {cfg.n_rows} input rows of {cfg.name}, all {cfg.n_layers} layers "
+            "sample": f"first {rows} of {cfg.n_rows} input rows of {workload_name(cfg, network)}, all {cfg.n_layers} layers "
                       f"(rows stop when dead, as on the GPU); {t:.2f} s of oracle layer evaluation on "
                       f"{threads} host threads"}
 
@@ -118,6 +132,9 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, help="index into synth.CONFIGS (0-4)")
+    ap.add_argument("--network", choices=["union", "radix"], default="union",
+                    help="weight layers: the configs' permutation unions, or structured RadiX-Net style "
+                         "layers (Kronecker-expanded radix-2 base DNN, Fig. 1 / Table 1) of the same width")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-layer events (no roofline)")
@@ -145,6 +162,8 @@ def main() -> int:
     torch.cuda.set_device(0)
     cfg = synth.CONFIGS[args.config]
     n, L, m = cfg.n_neurons, cfg.n_layers, cfg.n_rows
+    wname = workload_name(cfg, args.network)
+    layers = layer_source(cfg, args.network)
     stream = torch.cuda.current_stream()
 
     # ---------------- untimed: load the network and inputs into HBM (Sec. V, load steps)
@@ -155,13 +174,13 @@ def main() -> int:
         nr = min(chunk, m - r0)
         y0[r0:r0 + nr].copy_(torch.from_numpy(synth.config_inputs(cfg, r0, nr)))
     density = float(y0.mean().item())
-    log(f"{cfg.name}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
+    log(f"{wname}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
     t0 = time.time()
     net = sdnn.Net(n, L, cfg.ymax)
     lchunk = max(1, min(64, (1 << 27) // (n * cfg.k)))
     for l0 in range(0, L, lchunk):
         nl = min(lchunk, L - l0)
-        cp, ri, v = synth.layers_csc(cfg.net_id, l0, nl, n, cfg.k, cfg.weight)
+        cp, ri, v = layers(l0, nl)
         net.load_layers(l0, cp, ri, v, np.full((nl, n), cfg.bias, np.float32))
         if (l0 // lchunk) % 8 == 0:
             log(f"loaded layers {l0 + nl}/{L}")
@@ -224,7 +243,7 @@ def main() -> int:
         tot_bytes = sum(timed_bytes(l) * int(runs[l]) for l in timed)
         tot_ms = float(ms[timed].sum())
         roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(cfg.name, kname),
+                    "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(wname, kname),
                     "kernel": kname, "layer": lay, "launches_per_step": nl,
                     "avg_launch_ms": round(avg_launch_ms, 5), "algorithmic_bytes_per_launch": int(algo / nl),
                     "large_layers": {"layers": len(timed),
@@ -233,7 +252,7 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         threads = max(1, min(16, os.cpu_count() or 1))
-        cpu = cpu_baseline(cfg, args.cpu_seconds, threads)
+        cpu = cpu_baseline(cfg, args.cpu_seconds, threads, args.network)
 
     out = {
         "metric": "inference edges/sec (Ninputs*sum nnz(W)/t) + % HBM roofline, 1 MI355X",
@@ -248,7 +267,8 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "n_neurons": n, "n_layers": L, "n_rows": m, "bias": cfg.bias,
+        "config": {"workload": wname, "network": "permutation-union" if args.network == "union" else "radix-kronecker",
+                   "n_neurons": n, "n_layers": L, "n_rows": m, "bias": cfg.bias,
                    "ymax": cfg.ymax, "connections": cfg.total_nnz, "input_density": round(density, 4),
                    "parallelism": "none (1 GPU)"},
         "roofline": roofline,

@@ -45,6 +45,10 @@ def lib():
         L.synth_layers_csc.restype = ctypes.c_int
         L.synth_layer_perms.argtypes = [u64, u64, u64, i32, i32, vp]
         L.synth_layer_perms.restype = ctypes.c_int
+        L.synth_radix_layers_csc.argtypes = [u64, u64, i32, i32, i32, ctypes.c_float, vp, vp, vp, i32]
+        L.synth_radix_layers_csc.restype = ctypes.c_int
+        L.synth_radix_perm.argtypes = [u64, u64, u64, i32, vp]
+        L.synth_radix_perm.restype = ctypes.c_int
         L.synth_inputs.argtypes = [u64, u64, i32, i32, i64, i64, ctypes.c_double, ctypes.c_double, vp, i32]
         L.synth_inputs.restype = ctypes.c_int
         L.synth_stream_value.argtypes = [u64, u64]
@@ -124,6 +128,38 @@ def layer_perms(net_id: int, layer: int, n: int, k: int = 32, root: int = ROOT_S
     rc = lib().synth_layer_perms(root, net_id, layer, n, k, _ptr(perm))
     if rc != 0:
         raise RuntimeError(f"synth_layer_perms failed ({rc})")
+    return perm
+
+
+def radix_depth(n: int) -> int:
+    """D for a structured network of n = 16 * 2^D neurons (Table 1: D = 6, 8, 10, 12), else 0."""
+    d = 0
+    while n >= 32 and n % 16 == 0 and (1 << d) < n // 16:
+        d += 1
+    return d if n >= 32 and n % 16 == 0 and (1 << d) == n // 16 else 0
+
+
+def radix_layers_csc(net_id: int, l0: int, nl: int, n: int, weight: float = 1.0 / 16.0, root: int = ROOT_SEED,
+                     threads: int | None = None):
+    """Structured (RadiX-Net style) layers [l0, l0+nl) in the layout of layers_csc with k = 32: base layer
+    i of a radix-2 DNN on n / 16 nodes (node u links to u and u + 2^i), Kronecker-expanded by 16 x 16
+    blocks, copy c of the D base layers relabelled by the permutation radix_perm(net_id, c, n)."""
+    col_ptr = np.empty((nl, n + 1), dtype=np.int64)
+    row_idx = np.empty(nl * n * 32, dtype=np.int32)
+    val = np.empty(nl * n * 32, dtype=np.float32)
+    rc = lib().synth_radix_layers_csc(root, net_id, l0, nl, n, weight, _ptr(col_ptr), _ptr(row_idx), _ptr(val),
+                                      threads or default_threads())
+    if rc != 0:
+        raise RuntimeError(f"synth_radix_layers_csc failed ({rc})")
+    return col_ptr, row_idx, val
+
+
+def radix_perm(net_id: int, copy: int, n: int, root: int = ROOT_SEED) -> np.ndarray:
+    """P_c as an array: neuron x of the base labelling is neuron perm[x] of copy `copy`."""
+    perm = np.empty(n, dtype=np.int32)
+    rc = lib().synth_radix_perm(root, net_id, copy, n, _ptr(perm))
+    if rc != 0:
+        raise RuntimeError(f"synth_radix_perm failed ({rc})")
     return perm
 
 

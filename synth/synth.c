@@ -42,7 +42,7 @@
 
 #define GOLDEN 0x9E3779B97F4A7C15ULL
 
-enum { PURPOSE_PERM = 1, PURPOSE_REPAIR = 2, PURPOSE_INPUT = 3 };
+enum { PURPOSE_PERM = 1, PURPOSE_REPAIR = 2, PURPOSE_INPUT = 3, PURPOSE_RADIX = 4 };
 
 static inline uint64_t mix64(uint64_t z) {
   z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
@@ -196,6 +196,114 @@ int synth_layers_csc(uint64_t root, uint64_t net, int32_t l0, int32_t nl, int32_
   pthread_t th[256];
   if (nthreads > 256) nthreads = 256;
   for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, layers_worker, &J);
+  for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
+  return J.rc;
+}
+
+/* ---------------------------------------------------------------------------------------------- */
+/* Structured (RadiX-Net style) weight layers                                                      */
+/*
+ * Sec. III, Fig. 1 and Table 1 describe the challenge's networks: a base DNN from a radix set of D
+ * radices 2 (2^D nodes per layer, 2 connections per node), expanded by a Kronecker product with
+ * 16 x 16 blocks into N = 16 * 2^D neurons with 32 connections each, then made deep by appending
+ * randomly permuted copies of the base DNN. The construction of the base layers belongs to the
+ * RadiX-Net paper, which is not at hand; this generator takes the mixed-radix reading: base layer i
+ * links node u to u and to u + 2^i (mod 2^D), so that within one copy of D layers every input node
+ * reaches every output node by exactly one path. After the Kronecker product neuron 16u + a feeds
+ * neuron 16v + b for all a, b whenever u links to v. Copy c (layers cD .. cD + D - 1) is relabelled
+ * by a random permutation P_c of the N neurons: W_l(P_c(s), P_c(t)) = B_{l mod D}(s, t). P_c is drawn
+ * by Fisher-Yates from the stream of (root, PURPOSE_RADIX, net, c).
+ */
+
+/* D with N = 16 * 2^D, or -1 */
+static int radix_depth(int32_t N) {
+  if (N < 32 || (N & 15) != 0) return -1;
+  int32_t nodes = N / 16, d = 0;
+  while ((1 << d) < nodes) ++d;
+  return (1 << d) == nodes ? d : -1;
+}
+
+/* perm[x] = P_c(x) for copy c; returns 0, or -1 if N is not 16 * 2^D with D >= 1 */
+int synth_radix_perm(uint64_t root, uint64_t net, uint64_t copy, int32_t N, int32_t *perm) {
+  if (radix_depth(N) < 1) return -1;
+  uint64_t key = derive_key(root, PURPOSE_RADIX, net, copy, 0);
+  for (int32_t i = 0; i < N; ++i) perm[i] = i;
+  for (int32_t i = N - 1; i >= 1; --i) {
+    uint64_t ctr = (uint64_t)i << 8;
+    int32_t j = (int32_t)bounded(key, &ctr, (uint32_t)i + 1);
+    int32_t t = perm[i]; perm[i] = perm[j]; perm[j] = t;
+  }
+  return 0;
+}
+
+/* One structured layer in CSC form (sources ascending per column), col_ptr[j] = base + 32 j. perm and
+   inv are scratch of N int32 each. */
+static int radix_layer_csc(uint64_t root, uint64_t net, uint64_t layer, int32_t N, float wval, int64_t base,
+                           int64_t *col_ptr, int32_t *row_idx, float *val, int32_t *perm, int32_t *inv) {
+  const int D = radix_depth(N);
+  if (D < 1) return -1;
+  const uint64_t copy = layer / (uint64_t)D;
+  const int32_t i = (int32_t)(layer % (uint64_t)D), nodes = N / 16;
+  int rc = synth_radix_perm(root, net, copy, N, perm);
+  if (rc) return rc;
+  for (int32_t x = 0; x < N; ++x) inv[perm[x]] = x;
+  for (int32_t j = 0; j < N; ++j) {
+    /* column j is relabelled neuron t = 16 v + b; its base sources are nodes v and v - 2^i */
+    const int32_t t = inv[j], v = t / 16;
+    const int32_t u[2] = {v, (v - (1 << i) + nodes) % nodes};
+    int32_t *c = row_idx + (int64_t)j * 32;
+    for (int32_t k = 0; k < 2; ++k)
+      for (int32_t a = 0; a < 16; ++a) c[16 * k + a] = perm[16 * u[k] + a];
+    for (int32_t x = 1; x < 32; ++x) { /* insertion sort */
+      int32_t w = c[x], y = x - 1;
+      while (y >= 0 && c[y] > w) { c[y + 1] = c[y]; --y; }
+      c[y + 1] = w;
+    }
+    col_ptr[j] = base + (int64_t)j * 32;
+  }
+  col_ptr[N] = base + (int64_t)N * 32;
+  for (int64_t e = 0; e < (int64_t)N * 32; ++e) val[e] = wval;
+  return 0;
+}
+
+typedef struct {
+  uint64_t root, net; int32_t l0, nl, N; float wval;
+  int64_t *col_ptr; int32_t *row_idx; float *val;
+  int next; pthread_mutex_t mu; int rc;
+} radix_job;
+
+static void *radix_worker(void *arg) {
+  radix_job *J = (radix_job *)arg;
+  int32_t *perm = (int32_t *)malloc(sizeof(int32_t) * (size_t)J->N);
+  int32_t *inv = (int32_t *)malloc(sizeof(int32_t) * (size_t)J->N);
+  if (!perm || !inv) { pthread_mutex_lock(&J->mu); J->rc = -2; pthread_mutex_unlock(&J->mu); free(perm); free(inv); return NULL; }
+  for (;;) {
+    pthread_mutex_lock(&J->mu);
+    int i = J->next++;
+    int stop = J->rc != 0;
+    pthread_mutex_unlock(&J->mu);
+    if (stop || i >= J->nl) break;
+    int64_t nnz = (int64_t)J->N * 32;
+    int rc = radix_layer_csc(J->root, J->net, (uint64_t)(J->l0 + i), J->N, J->wval, (int64_t)i * nnz,
+                             J->col_ptr + (int64_t)i * (J->N + 1), J->row_idx + (int64_t)i * nnz, J->val + (int64_t)i * nnz,
+                             perm, inv);
+    if (rc) { pthread_mutex_lock(&J->mu); J->rc = rc; pthread_mutex_unlock(&J->mu); }
+  }
+  free(perm); free(inv);
+  return NULL;
+}
+
+/* Structured layers [l0, l0+nl) of network `net` (N = 16 * 2^D), in the layout of synth_layers_csc
+   with K = 32. Returns 0 on success. */
+int synth_radix_layers_csc(uint64_t root, uint64_t net, int32_t l0, int32_t nl, int32_t N, float wval,
+                           int64_t *col_ptr, int32_t *row_idx, float *val, int32_t nthreads) {
+  if (radix_depth(N) < 1 || nl < 0 || l0 < 0) return -1;
+  if (nthreads < 1) nthreads = 1;
+  if (nthreads > nl) nthreads = nl > 0 ? nl : 1;
+  radix_job J = {root, net, l0, nl, N, wval, col_ptr, row_idx, val, 0, PTHREAD_MUTEX_INITIALIZER, 0};
+  pthread_t th[256];
+  if (nthreads > 256) nthreads = 256;
+  for (int t = 0; t < nthreads; ++t) pthread_create(&th[t], NULL, radix_worker, &J);
   for (int t = 0; t < nthreads; ++t) pthread_join(th[t], NULL);
   return J.rc;
 }

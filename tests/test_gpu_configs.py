@@ -59,3 +59,38 @@ def test_full_config_sampled_rows(ci):
     if o.categories().size:
         np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
     log(f"{cfg.name}: sample live counts {oc[:6].tolist()}")
+
+
+@pytest.mark.parametrize("ci", [2, 3])
+def test_structured_full_config_sampled_rows(ci):
+    """The second workload: structured (RadiX-Net style) layers of the config's width and depth on the
+    config's inputs, full size on the GPU; a seeded sample of rows recomputed by the oracle."""
+    cfg = synth.CONFIGS[ci]
+    n, L = cfg.n_neurons, cfg.n_layers
+    y0 = synth.config_inputs(cfg)
+    gpu = GpuRun(n, L, cfg.ymax)
+    log(f"radix-{cfg.name}: loading {L} structured layers")
+    for l0 in range(0, L, 64):
+        nl = min(64, L - l0)
+        cp, ri, v = synth.radix_layers_csc(cfg.net_id, l0, nl, n, cfg.weight)
+        gpu.load(l0, cp, ri, v, np.full((nl, n), cfg.bias, np.float32))
+    cats = gpu.run(y0)
+    counts = gpu.net.live_counts()
+    log(f"radix-{cfg.name}: {cats.size} categories; live counts {counts[:8].tolist()}")
+    assert (np.diff(counts) <= 0).all() and cats.size == counts[-1]
+    rng = np.random.default_rng(100 + ci)
+    sample = np.sort(rng.choice(cfg.n_rows, size=600, replace=False))
+    o = oracle.Oracle(y0[sample], cfg.ymax)
+    bias = np.full(n, cfg.bias, np.float32)
+    l = 0
+    while l < L and o.live > 0:
+        nl = min(64, L - l)
+        cp, ri, v = synth.radix_layers_csc(cfg.net_id, l, nl, n, cfg.weight)
+        for i in range(nl):
+            o.layer(cp[i], ri, v, bias, THREADS)
+        l += nl
+    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
+    assert (oracle.padded_live_counts(o, L) <= counts).all()
+    if o.categories().size:
+        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
+    o.close()

@@ -325,6 +325,50 @@ def test_few_tile_tail_dies(m):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("kind", ["one-weight", "ell"])
+def test_few_tile_rows_die_one_by_one(kind):
+    """Rows that die at chosen layers: a dense row of value 1/4 - 2^-k / 4 under 32 weights of 1/16 and
+    bias -1/4 drifts from the fixed point 1/4 by a doubling amount and dies near layer k, while rows
+    of value 1/2 saturate and survive. The list shrinks a few rows per layer through the few-tile
+    layers, with compactions as the host's bound drops. "ell": one weight per layer differs, so the
+    layers go through the ELL instead of the 16-bit source lists."""
+    n, nl, bias = 6000, 40, -0.25
+    die = [1 + (7 * r) % 17 for r in range(42)]
+    vals = [0.25 - 0.25 * 2.0 ** -k for k in die] + [0.5] * 6
+    y0 = np.repeat(np.asarray(vals, np.float32)[:, None], n, axis=1)
+    cp, ri, v = synth.layers_csc(18, 0, nl, n)
+    if kind == "ell":
+        v = v.copy()
+        for l in range(nl):
+            v[cp[l][0]] = np.float32(0.125)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    log(f"few-tile rows die one by one kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    counts = oracle.padded_live_counts(o, nl)
+    assert counts[-1] >= 6 and any(8 < c <= 16 for c in counts) and any(c <= 8 for c in counts)
+    kinds, _ = gpu.net.layer_info()
+    assert sdnn_kind(kinds[nl - 1]) == "k_layer_gfm_small"
+    assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("n,m", [(1024, 400), (4096, 200), (16384, 80), (65536, 30)])
+def test_structured_networks(n, m):
+    """Structured (RadiX-Net style) layers: a radix-2 base DNN Kronecker-expanded by 16 x 16 blocks,
+    randomly relabelled per copy of the D base layers (Fig. 1, Table 1). Inputs of mixed density so
+    that some rows survive; two copies and a layer of the third, on both kernel paths."""
+    d = synth.radix_depth(n)
+    nl = 2 * d + 1
+    bias = {1024: -0.30, 4096: -0.35, 16384: -0.40, 65536: -0.45}[n]
+    side = int(round(n ** 0.5))
+    y0 = synth.inputs(40 + d, side, 0, m, "mixed", 0.3, 0.8)
+    cp, ri, v = synth.radix_layers_csc(21, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    log(f"structured n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert 0 < cats.size < m
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
