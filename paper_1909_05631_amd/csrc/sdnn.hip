@@ -805,6 +805,7 @@ __device__ __forceinline__ void stage_src16(unsigned *dst, const unsigned short 
 // rows (masks_prev, complete since that kernel ended) into *count_out, and with masks_clear set it
 // clears that buffer, the one the next layer will use (three buffers rotate by layer). With
 // count_out set and no live row left (rows that die stay dead), the layer writes nothing.
+// Live rows go to masks, or with spread set to the spread words of each tile (see or_mask).
 template <int FMR, int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
@@ -1201,6 +1202,7 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 // of 4 waves' outputs. The dictionary and the chunk's sources sit in LDS. A 32-row output segment
 // that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
 // says so. Registers are held to 5 waves per SIMD (more waves keep more gathers in flight; 6 spill).
+// Live rows go to masks, or with spread set to the spread words of each fp32 tile (see or_mask).
 template <int KC, bool CW, int CR>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
