@@ -40,6 +40,7 @@
 #include <string>
 #include <type_traits>
 #include <thread>
+#include <unordered_map>
 #include <vector>
 
 #include "sdnn.h"
@@ -805,7 +806,9 @@ __device__ __forceinline__ void stage_src16(unsigned *dst, const unsigned short 
 // rows (masks_prev, complete since that kernel ended) into *count_out, and with masks_clear set it
 // clears that buffer, the one the next layer will use (three buffers rotate by layer). With
 // count_out set and no live row left (rows that die stay dead), the layer writes nothing.
-// Live rows go to masks, or with spread set to the spread words of each tile (see or_mask).
+// Live rows go to masks, or with spread set to the spread words of each tile (see or_mask). With
+// cols set (CW only), the launch computes the ncols columns cols[p] alone, their source lists in
+// src16 as [K][ncols]; the other columns equal one of these and are neither computed nor stored.
 template <int FMR, int KC, bool CW>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
@@ -814,7 +817,8 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                    int tile0, const unsigned *__restrict__ masks_prev,
                                                    unsigned *__restrict__ masks_clear, int *__restrict__ count_out,
-                                                   unsigned *__restrict__ spread) {
+                                                   unsigned *__restrict__ spread, const int *__restrict__ cols,
+                                                   int ncols) {
   static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
   constexpr int CH = kGfmOutputs, OPL = 8;
   static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
@@ -823,6 +827,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   __shared__ int2 ells[CW ? 1 : KS * CH];
   __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * FMR
   __shared__ float bstage[CH];
+  __shared__ int cstage[CH];  // output column of each chunk position
   __shared__ unsigned rowmask;
   __shared__ int prev_live;
   const int R = *npos;
@@ -848,7 +853,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   const int parts = nt > 0 ? 8 / nt : 1;
   const int xcd = blockIdx.x & 7;
   const bool active = nt > 0 && xcd < nt * parts && prev_live != 0;  // uniform over the workgroup
-  const int nchunks = (N + CH - 1) / CH;
+  const int nchunks = (ncols + CH - 1) / CH;
   const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
@@ -861,11 +866,15 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   bool live = false;
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int c0 = chunk * CH;
-    const int nout = min(CH, N - c0);
-    __syncthreads();  // the previous chunk is done with ells / bstage
-    for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
+    const int nout = min(CH, ncols - c0);
+    __syncthreads();  // the previous chunk is done with ells / bstage / cstage
+    for (int i = tid; i < CH; i += blockDim.x) {
+      const int col = i < nout ? (cols ? cols[c0 + i] : c0 + i) : 0;
+      cstage[i] = col;
+      bstage[i] = i < nout ? bias[col] : 0.0f;
+    }
     if constexpr (CW) {
-      stage_src16<KC, CH>(offs, src16, N, c0, nout, FMR);
+      stage_src16<KC, CH>(offs, src16, ncols, c0, nout, FMR);
     } else if constexpr (KC > 0) {
       // stage [slot][64 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
       for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
@@ -930,7 +939,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
       const int jl = jw + 2 * i;
       if (jl < nout) {
         const float y = activate(acc[i], bstage[jl], ymax);
-        __builtin_nontemporal_store(y, ob + (size_t)(c0 + jl) * FMR);
+        __builtin_nontemporal_store(y, ob + (size_t)cstage[jl] * FMR);
         live |= y > 0.0f;
       }
     }
@@ -1012,6 +1021,7 @@ __global__ __launch_bounds__(kPartThreads) void k_finalize_masks(const unsigned 
 // per tile). Workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
 // tiles) into its mask words masks_prev, or, with part_prev null, reads those words; then it writes
 // their live count to count_out (if set) and to the progress word (if set), and clears masks_clear.
+// With cols set (CW only), only the ncols columns cols[p] are computed (see k_layer_gfm).
 template <int KC, bool CW>
 __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const float *__restrict__ fin, float *__restrict__ fout, int N, const int2 *__restrict__ ell,
@@ -1019,14 +1029,15 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const int *__restrict__ npos, int ntiles_h, unsigned *__restrict__ part_out,
     const unsigned *__restrict__ part_prev, int prev_S, int prev_nt, unsigned *__restrict__ masks_prev,
     unsigned *__restrict__ masks_clear, int *__restrict__ count_out, const int *__restrict__ live_before,
-    unsigned long long *__restrict__ progress, unsigned long long progress_tag) {
+    unsigned long long *__restrict__ progress, unsigned long long progress_tag, const int *__restrict__ cols,
+    int ncols) {
   constexpr int FMR = 32, CH = 32;
   __shared__ unsigned wmask[4];
   __shared__ unsigned pmask[8];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int parts = 8 / ntiles_h;
   const int xcd = blockIdx.x & 7;
-  const int nchunks = (N + CH - 1) / CH;
+  const int nchunks = (ncols + CH - 1) / CH;
   const int cpp = (nchunks + parts - 1) / parts;
   const int t = xcd / parts;
   const bool worker = xcd < ntiles_h * parts;
@@ -1053,14 +1064,15 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
   auto run_chunk = [&](int chunk, auto first) {
     constexpr bool FIRST = decltype(first)::value;
     const int j = chunk * CH + wave * 8 + h;
-    const int jj = min(j, N - 1);
+    const int jj = min(j, ncols - 1);
+    const int col = cols ? cols[jj] : jj;  // output column
     // byte offsets of the sources' segments and the weights (CW: 16-bit source lists, weight wc)
     unsigned eo[KC];
     float ew[KC];
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
       if constexpr (CW) {
-        eo[i] = (unsigned)src16[(size_t)i * N + jj] * (FMR * 4);
+        eo[i] = (unsigned)src16[(size_t)i * ncols + jj] * (FMR * 4);
         ew[i] = wc;
       } else {
         const int2 e = ell[(size_t)i * N + jj];
@@ -1068,7 +1080,7 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
         ew[i] = __int_as_float(e.y);
       }
     }
-    const float b = bias[jj];
+    const float b = bias[col];
     // taken here, after the ELL loads (the asm keeps the compare from being hoisted above them)
     int cb = count_before;
     asm volatile("" : "+v"(cb));
@@ -1102,9 +1114,9 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const float4 y = make_float4(activate(a[0], b, ymax), activate(a[1], b, ymax), activate(a[2], b, ymax),
                                  activate(a[3], b, ymax));
     const unsigned bits = (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u);
-    lm |= (j < N ? bits : 0u) << (4 * q);
+    lm |= (j < ncols ? bits : 0u) << (4 * q);
     // positions past the list length (up to the host's tile bound) are stored too: nothing reads them
-    if (j < N && !dead) store_stream(reinterpret_cast<float4 *>(obase + (size_t)j * FMR), y);
+    if (j < ncols && !dead) store_stream(reinterpret_cast<float4 *>(obase + (size_t)col * FMR), y);
   };
   int chunk = cbeg + (int)(blockIdx.x >> 3);
   if (chunk < cend) {
@@ -1935,6 +1947,14 @@ struct LayerDev {
   // global-tile path, uniform layer with K == 32 and N <= 65536: [K][N] u16 source indices (the
   // ELL's sources without the repeated weight)
   const unsigned short *src16 = nullptr;
+  // distinct columns (global-tile path, uniform layer with K == 32): columns with equal source lists
+  // have equal outputs, so only the D representatives cols[0..D) need computing, with their source
+  // lists in src16c ([K][D] u16). Usable (dedup_ok) once the next layer's sources point to
+  // representatives only (or for the last layer).
+  const int *cols = nullptr;
+  const unsigned short *src16c = nullptr;
+  int D = 0;
+  bool dedup_ok = false;
 };
 
 }  // namespace
@@ -1950,6 +1970,11 @@ struct sdnn_net {
   bool poisoned = false;
   std::vector<LayerDev> layers;
   std::vector<void *> allocations;
+  // duplicate columns: representatives of the last layer loaded (rep[j] = smallest column with j's
+  // source list), which the next layer's sources are mapped through when it is loaded right after
+  std::vector<int32_t> prev_rep;
+  int32_t prev_rep_layer = -1;
+  std::vector<int32_t> last_rep;  // the same for layer L - 1 (final rows are expanded through it)
   LayerPtr *lp_dev = nullptr;  // device table of the layers, for launches that run several layers
   int32_t n_loaded = 0;
   // last run
@@ -2077,7 +2102,9 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
                             int64_t max_tiles, unsigned *part_out, const unsigned *part_prev, int prev_S, int prev_nt,
                             unsigned *masks_prev, unsigned *masks_clear, int *count_out, const int *live_before,
                             unsigned long long *progress, unsigned long long progress_tag, int *S_out, int *nt_out) {
-  const int nchunks = (net->N + 31) / 32;
+  const bool dd = ld.src16 && ld.cols && ld.dedup_ok;  // distinct columns only
+  const int ncols = dd ? ld.D : net->N;
+  const int nchunks = (ncols + 31) / 32;
   const int ntiles_h = (int)std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int parts = 8 / ntiles_h;
   // at most kMaxPartWords / 8 workgroups per XCD, so that the partial words fit their buffer
@@ -2087,12 +2114,14 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   *nt_out = ntiles_h;
   if (ld.src16)
     hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
-                       ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag);
+                       ld.ell, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev,
+                       prev_S, prev_nt, masks_prev, masks_clear, count_out, live_before, progress, progress_tag,
+                       dd ? ld.cols : nullptr, ncols);
   else
     hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag);
+                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag, (const int *)nullptr,
+                       net->N);
   return hipGetLastError();
 }
 
@@ -2104,8 +2133,13 @@ hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float
                       int64_t max_tiles, unsigned *masks, const unsigned *masks_prev = nullptr,
                       unsigned *masks_clear = nullptr, int *count_out = nullptr, unsigned *spread = nullptr) {
   const int rounds = (int)((max_tiles + 7) / 8);
+  // distinct columns only, when the layer's duplicates need not be computed
+  const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
+  const int ncols = dd ? ld.D : net->N;
+  const int *cols = dd ? ld.cols : nullptr;
+  const unsigned short *s16 = dd ? ld.src16c : ld.src16;
   // one workgroup per output chunk of a tile's share when the round has fewer than 8 tiles
-  const int nchunks = (net->N + kGfmOutputs - 1) / kGfmOutputs;
+  const int nchunks = (ncols + kGfmOutputs - 1) / kGfmOutputs;
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
   const dim3 grid(8 * std::max(1, per_xcd));
@@ -2113,13 +2147,16 @@ hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float
     int *cnt = r == 0 ? count_out : nullptr;
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
+                         s16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread, cols,
+                         ncols);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
+                         (const int *)nullptr, net->N);
     else
       hipLaunchKernelGGL((k_layer_gfm<32, 0, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread);
+                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
+                         (const int *)nullptr, net->N);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2383,6 +2420,63 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   });
   for (int32_t i = 0; i < nl; ++i)
     if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
+  // ---- duplicate columns (global-tile path, uniform layers with 32 sources per column): columns
+  // with the same source list have the same output, so reps[i][j] = the smallest column with j's
+  // list (empty: no duplicates). Grouping uses the sources as given; equal lists stay equal once
+  // mapped (below). With the Kronecker-expanded networks of Sec. III every 16 columns of a block
+  // share their list.
+  std::vector<std::vector<int32_t>> reps((size_t)nl);
+  parallel_for(nl, [&](int32_t i) {
+    if (net->path != 1 || N > 65536 || !uniform[(size_t)i] || K[(size_t)i] != 32) return;
+    const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+    std::unordered_map<uint64_t, std::vector<int32_t>> seen;
+    seen.reserve((size_t)N);
+    std::vector<int32_t> r((size_t)N);
+    int32_t distinct = 0;
+    for (int32_t j = 0; j < N; ++j) {
+      const int32_t *src = row_idx + cp[j];
+      uint64_t h = 0x9E3779B97F4A7C15ull;
+      for (int k = 0; k < 32; ++k) {
+        h ^= (uint32_t)src[k] + 0x9E3779B97F4A7C15ull + (h << 6) + (h >> 2);
+        h *= 0xBF58476D1CE4E5B9ull;
+      }
+      std::vector<int32_t> &cand = seen[h];
+      int32_t found = -1;
+      for (int32_t c : cand)
+        if (std::memcmp(row_idx + cp[c], src, 32 * sizeof(int32_t)) == 0) { found = c; break; }
+      if (found < 0) {
+        cand.push_back(j);
+        found = j;
+        ++distinct;
+      }
+      r[(size_t)j] = found;
+    }
+    if (distinct < N) reps[(size_t)i] = std::move(r);
+  });
+  // ---- a layer loaded right after one with duplicates reads that layer's representatives only:
+  // its sources are mapped through them (values are equal), and the earlier layer may then skip
+  // its duplicate columns. mapped[i] holds layer i's mapped sources (empty: as given).
+  std::vector<std::vector<int32_t>> mapped((size_t)nl);
+  std::vector<char> maps_prev((size_t)nl, 0);  // layer l0 + i's sources go through layer l0 + i - 1's reps
+  {
+    const std::vector<int32_t> *prev = (net->prev_rep_layer == l0 - 1 && !net->prev_rep.empty()) ? &net->prev_rep : nullptr;
+    for (int32_t i = 0; i < nl; ++i) {
+      if (prev) {
+        const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+        const int64_t e0 = cp[0], e1 = cp[N];
+        std::vector<int32_t> &m = mapped[(size_t)i];
+        m.resize((size_t)(e1 - e0));
+        for (int64_t e = e0; e < e1; ++e) m[(size_t)(e - e0)] = (*prev)[(size_t)row_idx[e]];
+        maps_prev[(size_t)i] = 1;
+      }
+      prev = reps[(size_t)i].empty() ? nullptr : &reps[(size_t)i];
+    }
+  }
+  // source of entry e of layer i (absolute index into row_idx)
+  auto src_at = [&](int32_t i, int64_t e) -> int32_t {
+    const std::vector<int32_t> &m = mapped[(size_t)i];
+    return m.empty() ? row_idx[e] : m[(size_t)(e - col_ptr[(size_t)i * (N + 1)])];
+  };
   // ---- pack: slot-major ELL [K][N] of (byte offset of source row in the tile, weight bits)
   const int stride = net->B * (int)sizeof(float);
   std::vector<size_t> layer_off((size_t)nl + 1, 0);
@@ -2405,7 +2499,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       for (int64_t e = cp[j]; e < cp[j + 1]; ++e, ++s) {
         int wbits;
         std::memcpy(&wbits, &val[e], sizeof(int));
-        base[(size_t)s * N + j] = make_int2(row_idx[e] * stride, wbits);
+        base[(size_t)s * N + j] = make_int2(src_at(i, e) * stride, wbits);
       }
       for (; s < Ki; ++s) base[(size_t)s * N + j] = make_int2(0, 0);
     }
@@ -2453,7 +2547,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         uint16_t *dst = hs.data() + per * (size_t)q;
         for (int32_t j = 0; j < N; ++j)
-          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * N + j] = (uint16_t)row_idx[cp[j] + sl];
+          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * N + j] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
       });
       char *ms = nullptr;
       e = hipMalloc(reinterpret_cast<void **>(&ms), hs.size() * sizeof(uint16_t));
@@ -2484,7 +2578,8 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         uint16_t *dst = h16.data() + per * (size_t)q;
         for (int32_t j = 0; j < N; ++j)
-          for (int sl = 0; sl < 32; ++sl) dst[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)row_idx[cp[j] + sl];
+          for (int sl = 0; sl < 32; ++sl)
+            dst[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
       });
       char *m16 = nullptr;
       e = hipMalloc(reinterpret_cast<void **>(&m16), h16.size() * sizeof(uint16_t));
@@ -2497,6 +2592,63 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       for (size_t q = 0; q < sel.size(); ++q)
         net->layers[(size_t)l0 + sel[q]].ell16 = reinterpret_cast<const uint4 *>(m16) + (per / 8) * q;
     }
+  }
+  {
+    // distinct columns: the representatives and their (mapped) source lists, [32][D] u16
+    std::vector<int32_t> sel;
+    for (int32_t i = 0; i < nl; ++i)
+      if (!reps[(size_t)i].empty() && net->layers[(size_t)l0 + i].src16) sel.push_back(i);
+    if (!sel.empty()) {
+      std::vector<size_t> off(sel.size() + 1, 0);  // in columns
+      std::vector<std::vector<int32_t>> cols(sel.size());
+      for (size_t q = 0; q < sel.size(); ++q) {
+        const std::vector<int32_t> &r = reps[(size_t)sel[q]];
+        for (int32_t j = 0; j < N; ++j)
+          if (r[(size_t)j] == j) cols[q].push_back(j);
+        off[q + 1] = off[q] + cols[q].size();
+      }
+      const size_t tot = off[sel.size()];
+      std::vector<int32_t> hc(tot);
+      std::vector<uint16_t> hs((size_t)32 * tot);
+      parallel_for((int32_t)sel.size(), [&](int32_t q) {
+        const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
+        const size_t D = cols[(size_t)q].size();
+        uint16_t *dst = hs.data() + (size_t)32 * off[(size_t)q];
+        for (size_t p = 0; p < D; ++p) {
+          const int32_t j = cols[(size_t)q][p];
+          hc[off[(size_t)q] + p] = j;
+          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * D + p] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
+        }
+      });
+      const size_t cbytes = align_up(tot * sizeof(int32_t), 256);
+      char *mc = nullptr;
+      e = hipMalloc(reinterpret_cast<void **>(&mc), cbytes + hs.size() * sizeof(uint16_t));
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", cbytes + hs.size() * sizeof(uint16_t),
+                    hipGetErrorString(e));
+      }
+      net->allocations.push_back(mc);
+      HIP_OR_POISON(net, hipMemcpy(mc, hc.data(), tot * sizeof(int32_t), hipMemcpyHostToDevice));
+      HIP_OR_POISON(net, hipMemcpy(mc + cbytes, hs.data(), hs.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      for (size_t q = 0; q < sel.size(); ++q) {
+        LayerDev &ld = net->layers[(size_t)l0 + sel[q]];
+        ld.cols = reinterpret_cast<const int *>(mc) + off[q];
+        ld.src16c = reinterpret_cast<const unsigned short *>(mc + cbytes) + (size_t)32 * off[q];
+        ld.D = (int)cols[q].size();
+      }
+    }
+    // a layer whose successor reads its representatives only may skip its duplicates; so may the
+    // last layer (the final rows are expanded through its representatives)
+    for (int32_t i = 0; i < nl; ++i) {
+      if (maps_prev[(size_t)i]) net->layers[(size_t)l0 + i - 1].dedup_ok = true;
+      if (l0 + i == net->L - 1 && !reps[(size_t)i].empty()) {
+        net->layers[(size_t)l0 + i].dedup_ok = true;
+        net->last_rep = reps[(size_t)i];
+      }
+    }
+    net->prev_rep = std::move(reps[(size_t)nl - 1]);
+    net->prev_rep_layer = net->prev_rep.empty() ? -1 : l0 + nl - 1;
   }
   // the device table of layers (for launches that run several layers)
   if (!net->lp_dev) {
@@ -3056,8 +3208,13 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
     HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
     std::vector<float> rows((size_t)nb * net->N);
     HIP_OR_POISON(net, hipMemcpy(rows.data(), scratch, (size_t)nb * rowb, hipMemcpyDeviceToHost));
-    for (int i = 0; i < nb; ++i)
-      std::memcpy(out_host + (size_t)which[b0 + (size_t)i] * net->N, rows.data() + (size_t)i * net->N, rowb);
+    for (int i = 0; i < nb; ++i) {
+      float *dst = out_host + (size_t)which[b0 + (size_t)i] * net->N;
+      std::memcpy(dst, rows.data() + (size_t)i * net->N, rowb);
+      // the last layer may have computed only one column of each group of equal columns
+      if (!net->last_rep.empty())
+        for (int32_t j = 0; j < net->N; ++j) dst[j] = dst[net->last_rep[(size_t)j]];
+    }
   }
   g_err.clear();
   return SDNN_OK;

@@ -369,6 +369,35 @@ def test_structured_networks(n, m):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("order", ["one-by-one", "reversed", "mixed-bias"])
+def test_structured_duplicate_columns(order):
+    """In structured layers every 16 columns of a Kronecker block share their sources, weights and
+    bias, so their outputs are equal: the library computes one column per group once the next
+    layer's sources have been mapped to the representatives, which needs that layer loaded right
+    after. "one-by-one": layers loaded one per call, in order; "reversed": one per call from the last
+    layer back, so no layer's successor is mapped and every column is computed; "mixed-bias": one
+    column's bias differs, so that layer is not uniform and keeps all its columns."""
+    n, m = 16384, 80
+    d = synth.radix_depth(n)
+    nl = 2 * d + 1
+    side = int(round(n ** 0.5))
+    y0 = synth.inputs(40 + d, side, 0, m, "mixed", 0.3, 0.8)
+    cp, ri, v = synth.radix_layers_csc(22, 0, nl, n)
+    bias = [np.full(n, -0.40, np.float32) for _ in range(nl)]
+    if order == "mixed-bias":
+        bias[d][123] = np.float32(-0.41)
+    layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
+    gpu = GpuRun(n, nl)
+    seq = range(nl - 1, -1, -1) if order == "reversed" else range(nl)
+    for l in seq:
+        gpu.load(l, cp[l], ri, v, bias[l])
+    log(f"structured duplicate columns order={order}")
+    cats = gpu.run(y0)
+    o = oracle.run(y0, layers, 32.0, threads=4)
+    assert 0 < cats.size < m
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
