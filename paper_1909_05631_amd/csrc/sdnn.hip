@@ -275,11 +275,13 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
 // each), keep the rows the new tile takes, and place them in an LDS stage from which the new
 // segments are written whole. So each needed old segment is read once, coalesced. With seglive
 // set, an old segment whose bit there is clear was never stored (all its rows are zero) and is not
-// read.
+// read. With cols set (tiles of a layer that computed only the columns cols[0..ncols); seglive is
+// then null), only those sources are moved.
 constexpr int kRepackSources = 256;
 __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
                                                 const int *__restrict__ src, const int *__restrict__ npos,
-                                                const unsigned *__restrict__ seglive) {
+                                                const unsigned *__restrict__ seglive, const int *__restrict__ cols,
+                                                int ncols) {
   __shared__ int otile[32];            // distinct old tiles of this new tile
   __shared__ unsigned omask[32];       // their slots that this new tile takes
   __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
@@ -288,7 +290,7 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
   __shared__ float stage[32][33];
   const int R = *npos;
   const int ntiles = (R + 31) / 32;
-  const int nkc = (N + kRepackSources - 1) / kRepackSources;
+  const int nkc = (ncols + kRepackSources - 1) / kRepackSources;
   const int tid = threadIdx.x, kk = tid >> 3, q = tid & 7;
   const int NW = (N + 31) / 32;
   for (int item = blockIdx.x; item < ntiles * nkc; item += gridDim.x) {
@@ -313,7 +315,8 @@ __global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, f
     __syncthreads();
     const int n = nold;
     for (int kb = 0; kb < kRepackSources; kb += 32) {
-      const int k = k0 + kb + kk;
+      const int kp = k0 + kb + kk;  // source position; the source is cols[kp] with a column list
+      const int k = kp < ncols ? (cols ? cols[kp] : kp) : N;
       // rows not taken from any old tile (past nb) stay zero
       for (int i = tid; i < 32 * 32; i += blockDim.x) stage[i >> 5][i & 31] = 0.0f;
       // k0 + kb is a multiple of 32: one bitmap word per old tile covers these sources, bit kk
@@ -1215,6 +1218,8 @@ __device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow
 // that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
 // says so. Registers are held to 5 waves per SIMD (more waves keep more gathers in flight; 6 spill).
 // Live rows go to masks, or with spread set to the spread words of each fp32 tile (see or_mask).
+// With cols set (CW only), the launch computes the ncols columns cols[p] alone (see k_layer_gfm),
+// stores every segment of them and leaves seglive untouched.
 template <int KC, bool CW, int CR>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
                                                       int N, const int2 *__restrict__ ell, int K,
@@ -1222,7 +1227,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
                                                       const float *__restrict__ bias, float ymax,
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
-                                                      int tile0, unsigned *__restrict__ spread) {
+                                                      int tile0, unsigned *__restrict__ spread,
+                                                      const int *__restrict__ cols, int ncols) {
   constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
@@ -1232,6 +1238,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   __shared__ int2 ells[CW ? 1 : KS * CH];
   __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * CR
   __shared__ float bstage[CH];
+  __shared__ int cstage[CH];  // output column of each chunk position
   __shared__ unsigned segw[ST][CH / 32];
   __shared__ unsigned long long rowmask[CR / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -1242,7 +1249,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const int parts = nt > 0 ? 8 / nt : 1;
   const int xcd = blockIdx.x & 7;
   const bool active = nt > 0 && xcd < nt * parts;
-  const int nchunks = (N + CH - 1) / CH;
+  const int nchunks = (ncols + CH - 1) / CH;
   const int cpp = (nchunks + parts - 1) / parts;
   const int t = tile0 + xcd / parts;
   const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
@@ -1263,12 +1270,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const int jw = wave * OPI * OPL;  // first output of this wave in the chunk
   for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
     const int c0 = chunk * CH;
-    const int nout = min(CH, N - c0);
-    __syncthreads();  // the previous chunk is done with ells / bstage / segw
-    for (int i = tid; i < CH; i += blockDim.x) bstage[i] = i < nout ? bias[c0 + i] : 0.0f;
+    const int nout = min(CH, ncols - c0);
+    __syncthreads();  // the previous chunk is done with ells / bstage / cstage / segw
+    for (int i = tid; i < CH; i += blockDim.x) {
+      const int col = i < nout ? (cols ? cols[c0 + i] : c0 + i) : 0;
+      cstage[i] = col;
+      bstage[i] = i < nout ? bias[col] : 0.0f;
+    }
     if (tid < ST * (CH / 32)) segw[tid / (CH / 32)][tid % (CH / 32)] = 0u;
     if constexpr (CW) {
-      stage_src16<KC, CH>(offs, src16, N, c0, nout, CR);
+      stage_src16<KC, CH>(offs, src16, ncols, c0, nout, CR);
     } else if constexpr (KC > 0) {
       // stage [slot][CH outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
       for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
@@ -1372,8 +1383,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
                                       : 0u;
       const unsigned long long bal = __ballot(bits != 0u);
       // the 8 lanes of this lane's output segment: lanes (lane & ~7) .. + 7
-      if (jl < nout && has_tile && ((bal >> (lane & ~7)) & 0xffull) != 0ull)
-        store_stream(reinterpret_cast<float4 *>(obase + (size_t)(c0 + jl) * 32), y);
+      if (jl < nout && has_tile && (cols || ((bal >> (lane & ~7)) & 0xffull) != 0ull))
+        store_stream(reinterpret_cast<float4 *>(obase + (size_t)cstage[jl] * 32), y);
 #pragma unroll
       for (int h = 0; h < CR / 64; ++h)
         if ((r >> 4) == h) lm[h] |= (unsigned long long)bits << (4 * (r & 15));
@@ -1388,7 +1399,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
       for (int q = 0; q < ST; ++q)
         if (seg[q]) atomicOr(&segw[q][jw / 32], seg[q]);
     __syncthreads();
-    if (tid < ST * (CH / 32)) {
+    if (tid < ST * (CH / 32) && !cols) {
       const int q = tid / (CH / 32), wi = tid % (CH / 32);
       if ((ST * t + q) * 32 < R && c0 + 32 * wi < N) seglive[(size_t)(ST * t + q) * NW + c0 / 32 + wi] = segw[q][wi];
     }
@@ -2251,10 +2262,15 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
 // tiles. max_tiles: host bound on the 32-row tiles of the list.
 template <int CR>
 hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
-                            int64_t max_tiles, unsigned *masks) {
+                            int64_t max_tiles, unsigned *masks, bool *seglive_used) {
   max_tiles = (max_tiles + CR / 32 - 1) / (CR / 32);  // code tiles
   const int rounds = (int)((max_tiles + 7) / 8);
-  const int nchunks = (net->N + u8_outputs(CR) - 1) / u8_outputs(CR);
+  // distinct columns only, when the layer's duplicates need not be computed (every segment of them
+  // is then stored and seglive is not written)
+  const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
+  const int ncols = dd ? ld.D : net->N;
+  *seglive_used = !dd;
+  const int nchunks = (ncols + u8_outputs(CR) - 1) / u8_outputs(CR);
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
   const dim3 grid(8 * std::max(1, per_xcd));
@@ -2262,25 +2278,25 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, true, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread);
+                         ld.K, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive,
+                         r * 8, net->spread, dd ? ld.cols : nullptr, ncols);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread);
+                         net->spread, (const int *)nullptr, net->N);
     else
       hipLaunchKernelGGL((k_layer_gfm_u8<0, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread);
+                         net->spread, (const int *)nullptr, net->N);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
-                         int64_t max_tiles, unsigned *masks) {
-  return code_rows(net->bitsT) == 128 ? launch_gfm_u8_cr<128>(net, ld, cin, fout, npos, max_tiles, masks)
-                                      : launch_gfm_u8_cr<64>(net, ld, cin, fout, npos, max_tiles, masks);
+                         int64_t max_tiles, unsigned *masks, bool *seglive_used) {
+  return code_rows(net->bitsT) == 128 ? launch_gfm_u8_cr<128>(net, ld, cin, fout, npos, max_tiles, masks, seglive_used)
+                                      : launch_gfm_u8_cr<64>(net, ld, cin, fout, npos, max_tiles, masks, seglive_used);
 }
 
 // Rows per workgroup of k_layers_lds: at most the largest of 16, 8, 4 whose two tiles fit 128 KiB
@@ -2859,6 +2875,10 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     const bool small = l > 0 && P <= one_round;
     bool reported = false;  // this layer's launch writes the progress word
     fout_codes = false;
+    // the columns fout holds, when this layer computed one column per group of equal columns
+    const LayerDev &lcur = net->layers[(size_t)l];
+    const bool ocols_on = lcur.K == 32 && lcur.src16 && lcur.cols && lcur.dedup_ok;
+    const int *fout_cols = nullptr;  // set by the branches whose kernels take the column list
     bool spread_used = false;  // this layer's liveness is in the spread words
     bool seglive_out = false;  // fout's all-zero segments were skipped (net->seglive says which)
     unsigned *mk = masks_for(l);
@@ -2905,15 +2925,16 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk, nullptr, nullptr,
                                       nullptr, net->spread));
         spread_used = true;
+        fout_cols = ocols_on ? lcur.cols : nullptr;
         net->layer_kernel[0] = SDNN_KERNEL_GLOBAL_TILE;
         net->layer_launches[0] = (int32_t)(1 + (tiles(P) + 7) / 8) + (try_bits ? 1 : 0);
       }
     } else if (fin_codes) {
       // follows layer 0, which is always compacted: no count to take over
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
-                                       npos + cur, tiles(P), mk));
+                                       npos + cur, tiles(P), mk, &seglive_out));
       spread_used = true;
-      seglive_out = true;
+      fout_cols = ocols_on ? lcur.cols : nullptr;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
       const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
       net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + st - 1) / st + 7) / 8);
@@ -2929,6 +2950,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                                             part_nt, masks_for(l - 1), masks_for(l + 1), cnt, net->counts + (l - 1),
                                             follow ? net->progress_dev : nullptr, tag, &S, &nt));
         reported = follow;
+        fout_cols = ocols_on ? lcur.cols : nullptr;
         parts_pending = true;
         part_layer = l;
         part_S = S;
@@ -2941,6 +2963,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         HIP_OR_POISON(net, launch_gfm(net, ld, fin, fout, npos + cur, tiles(P), mk, masks_for(l - 1),
                                       masks_for(l + 1), cnt, small ? nullptr : net->spread));
         spread_used = !small;
+        fout_cols = ocols_on ? lcur.cols : nullptr;
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
         net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
       }
@@ -2994,7 +3017,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       float *dst = (fout == net->fm[1]) ? net->fm[0] : net->fm[1];
       const int cr = code_rows(net->bitsT);
       const int64_t items = fout_codes ? (tiles(live_bound) + cr / 32 - 1) / (cr / 32) * net->N * (cr / 4) / 256
-                                       : tiles(live_bound) * ((net->N + kRepackSources - 1) / kRepackSources);
+                                       : tiles(live_bound) * (((fout_cols ? lcur.D : net->N) + kRepackSources - 1) /
+                                                              kRepackSources);
       const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
       if (fout_codes && cr == 128)
         hipLaunchKernelGGL(k_repack_u8<128>, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
@@ -3004,7 +3028,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
                            reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
       else
         hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1),
-                           seglive_out ? net->seglive : nullptr);
+                           seglive_out ? net->seglive : nullptr, fout_cols, fout_cols ? lcur.D : net->N);
       HIP_OR_POISON(net, hipGetLastError());
       fin = dst;
       cur ^= 1;

@@ -398,6 +398,26 @@ def test_structured_duplicate_columns(order):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("nl", [2, 5])
+def test_structured_code_layer_columns(nl):
+    """A structured network on more than 256 rows: layer 0 by counts, layer 1 gathers one-byte codes
+    and, its successor's sources mapped to the representatives, computes one column per group of
+    equal columns and stores all of their segments. nl=2: layer 1 is the last layer, whose final rows
+    are expanded through its groups."""
+    n, m = 8192, 700
+    d = synth.radix_depth(n)
+    rng = np.random.default_rng(nl)
+    y0 = (rng.random((m, n)) < rng.uniform(0.1, 0.5, size=(m, 1))).astype(np.float32)
+    cp, ri, v = synth.radix_layers_csc(23, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, -0.40, np.float32)) for l in range(nl)]
+    log(f"structured code layer columns n={n} nl={nl} (D={d})")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, _ = gpu.net.layer_info()
+    assert sdnn_kind(kinds[1]) == "k_layer_gfm_u8"
+    assert 0 < cats.size < m
+    assert_parity(gpu, o, cats)
+
+
 def test_profiling_modes():
     """Mode 1 times every layer that ran; mode 2 only the large ones (here: the layers entered with more
     than 256 live rows, on the global-tile path)."""
