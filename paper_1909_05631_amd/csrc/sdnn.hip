@@ -1777,14 +1777,16 @@ __device__ __forceinline__ void csa(unsigned &carry, unsigned &sum, unsigned a, 
 // halves of each word (T = 16). LDS holds the tile's N words; the source indices are read 8 per
 // 16-byte load from the [4][N][8] u16 table. Codes go to tiles of CR rows, one byte per row. With
 // ROWMAJOR (T = 32; widths staged in LDS) the outputs are decoded instead and written as fp32 rows,
-// yout[ids[p]][j] = dict[code] (the dictionary is copied after the tile in LDS).
+// yout[ids[p]][j] = dict[code] (the dictionary is copied after the tile in LDS). With cols set, only
+// the ncols columns cols[p] are computed, their source lists in ell16 as [4][ncols][8].
 template <int T, bool ROWMAJOR>
 __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>::type *__restrict__ bits,
                                                       unsigned char *__restrict__ cout, int N,
                                                       const uint4 *__restrict__ ell16, const int *__restrict__ misc,
                                                       const int *__restrict__ count, unsigned *__restrict__ masks,
                                                       float *__restrict__ yout, const int *__restrict__ ids,
-                                                      const unsigned *__restrict__ dict) {
+                                                      const unsigned *__restrict__ dict, const int *__restrict__ cols,
+                                                      int ncols) {
   static_assert(!ROWMAJOR || T == 32, "rows of fp32 outputs from 32-row bit tiles");
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
@@ -1801,7 +1803,7 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   const int cmin = misc[kCountMinSlot];
   const int ntiles = (R + T - 1) / T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
-  const int blocks = (N + 64 * OPL - 1) / (64 * OPL);  // output blocks of one wave
+  const int blocks = (ncols + 64 * OPL - 1) / (64 * OPL);  // output blocks of one wave
   const int rounds = (blocks + nw - 1) / nw;
   const Chunking ch = chunking(ntiles, rounds);
   // whole tiles as items: keep the tiles of one code group on one XCD
@@ -1832,19 +1834,20 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
     for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
       const int blk = r * nw + wave;
       if (blk >= blocks) break;
-      int jo[OPL];
+      int jo[OPL], jc[OPL];  // output position and its column
       bool jin[OPL];
 #pragma unroll
       for (int u = 0; u < OPL; ++u) {
         jo[u] = blk * 64 * OPL + u * 64 + lane;
-        jin[u] = jo[u] < N;
+        jin[u] = jo[u] < ncols;
+        jc[u] = cols ? cols[min(jo[u], ncols - 1)] : jo[u];
       }
-      // the 32 source indices of each output, 8 per load (outputs past N read output N - 1)
+      // the 32 source indices of each output, 8 per load (positions past the last read the last)
       uint4 ix[OPL][4];
 #pragma unroll
       for (int u = 0; u < OPL; ++u)
 #pragma unroll
-        for (int g = 0; g < 4; ++g) ix[u][g] = ell16[(size_t)g * N + min(jo[u], N - 1)];
+        for (int g = 0; g < 4; ++g) ix[u][g] = ell16[(size_t)g * ncols + min(jo[u], ncols - 1)];
       auto word = [&](int sl) -> unsigned {
         unsigned x = 0u;
 #pragma unroll
@@ -1913,11 +1916,11 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
 #pragma unroll
           for (int b = 0; b < T; ++b) {
             const int row = rid[b];
-            if (row >= 0) yout[(size_t)row * N + jo[u]] = dl[(cw[b >> 2] >> (8 * (b & 3))) & 255u];
+            if (row >= 0) yout[(size_t)row * N + jc[u]] = dl[(cw[b >> 2] >> (8 * (b & 3))) & 255u];
           }
           continue;
         }
-        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / CR) * N + jo[u]) * CR + p0 % CR);
+        uint4 *dst = reinterpret_cast<uint4 *>(cout + ((size_t)(p0 / CR) * N + jc[u]) * CR + p0 % CR);
         // plain stores: the tiles of one code group fill each segment in parts, merged in L2
         if (T == 32) {
           dst[0] = make_uint4(cw[0], cw[1], cw[2], cw[3]);
@@ -1964,6 +1967,7 @@ struct LayerDev {
   // representatives only (or for the last layer).
   const int *cols = nullptr;
   const unsigned short *src16c = nullptr;
+  const uint4 *ell16c = nullptr;  // layer 0: the representatives' source lists as [K/8][D][8]
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2247,9 +2251,12 @@ hipError_t launch_layer_count_k(sdnn_net *net, const LayerDev &ld, const void *b
   if (e != hipSuccess) return e;
   size_t lds = 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
   if (ROWMAJOR) lds += kDictSlots * sizeof(float) + T * sizeof(int);
+  // distinct columns only, when the layer's duplicates need not be computed
+  const bool dd = !ROWMAJOR && ld.cols && ld.ell16c && ld.dedup_ok;
   hipLaunchKernelGGL((k_layer_count<T, ROWMAJOR>), dim3(net->cus), dim3(1024), lds, net->stream,
-                     reinterpret_cast<const W *>(bits), cout, net->N, ld.ell16, net->misc, count, masks, yout, ids,
-                     reinterpret_cast<const unsigned *>(net->dict));
+                     reinterpret_cast<const W *>(bits), cout, net->N, dd ? ld.ell16c : ld.ell16, net->misc, count, masks,
+                     yout, ids, reinterpret_cast<const unsigned *>(net->dict), dd ? ld.cols : nullptr,
+                     dd ? ld.D : net->N);
   return hipGetLastError();
 }
 template <int T>
@@ -2626,6 +2633,12 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       const size_t tot = off[sel.size()];
       std::vector<int32_t> hc(tot);
       std::vector<uint16_t> hs((size_t)32 * tot);
+      // layer 0 also in the counting kernel's grouped layout
+      std::vector<uint16_t> hg;
+      int32_t q0 = -1;
+      for (size_t q = 0; q < sel.size(); ++q)
+        if (l0 + sel[q] == 0 && net->layers[0].ell16) q0 = (int32_t)q;
+      if (q0 >= 0) hg.resize((size_t)32 * cols[(size_t)q0].size());
       parallel_for((int32_t)sel.size(), [&](int32_t q) {
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         const size_t D = cols[(size_t)q].size();
@@ -2633,7 +2646,11 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         for (size_t p = 0; p < D; ++p) {
           const int32_t j = cols[(size_t)q][p];
           hc[off[(size_t)q] + p] = j;
-          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * D + p] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
+          for (int sl = 0; sl < 32; ++sl) {
+            const uint16_t v = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
+            dst[(size_t)sl * D + p] = v;
+            if (q == q0) hg[((size_t)(sl / 8) * D + p) * 8 + sl % 8] = v;
+          }
         }
       });
       const size_t cbytes = align_up(tot * sizeof(int32_t), 256);
@@ -2652,6 +2669,17 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         ld.cols = reinterpret_cast<const int *>(mc) + off[q];
         ld.src16c = reinterpret_cast<const unsigned short *>(mc + cbytes) + (size_t)32 * off[q];
         ld.D = (int)cols[q].size();
+      }
+      if (q0 >= 0) {
+        char *mg = nullptr;
+        e = hipMalloc(reinterpret_cast<void **>(&mg), hg.size() * sizeof(uint16_t));
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", hg.size() * sizeof(uint16_t), hipGetErrorString(e));
+        }
+        net->allocations.push_back(mg);
+        HIP_OR_POISON(net, hipMemcpy(mg, hg.data(), hg.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+        net->layers[0].ell16c = reinterpret_cast<const uint4 *>(mg);
       }
     }
     // a layer whose successor reads its representatives only may skip its duplicates; so may the
