@@ -789,6 +789,40 @@ __device__ __forceinline__ void stage_src16(unsigned *dst, const unsigned short 
   }
 }
 
+// Work split of one round of a layer on global tiles, tpx tiles per XCD (workgroup x runs on XCD
+// x % 8; gridDim.x / 8 must be a multiple of tpx). ntl: tiles left from the round's first tile.
+// With more than 8 tiles in the round, XCD x takes its tiles x, x + 8, ..., x + 8 (tpx - 1), one per
+// group of its workgroups, each tile's chunks spread over the group; with at most 8 (always for
+// tpx = 1), group 0 alone works and each tile's chunks are split over 8 / nt XCDs.
+struct RoundSplit {
+  int t;             // tile, relative to the round's first
+  bool active;
+  int cbeg, cend;    // the tile's chunks this XCD (part) covers
+  int first, step;   // this workgroup's first chunk and stride
+};
+__device__ __forceinline__ RoundSplit round_split(int ntl, int tpx, int nchunks) {
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, per_xcd = gridDim.x >> 3;
+  const int g = slot % tpx, per_group = per_xcd / tpx;
+  const int nt = min(8 * tpx, ntl);
+  RoundSplit r;
+  if (nt > 8) {
+    r.t = xcd + 8 * g;
+    r.active = r.t < nt;
+    r.cbeg = 0;
+  } else {
+    const int parts = nt > 0 ? 8 / nt : 1;
+    r.t = xcd / parts;
+    r.active = nt > 0 && g == 0 && xcd < nt * parts;
+    r.cbeg = (xcd % parts) * ((nchunks + parts - 1) / parts);
+    r.cend = min(nchunks, r.cbeg + (nchunks + parts - 1) / parts);
+  }
+  if (nt > 8) r.cend = nchunks;
+  if (!r.active) r.cend = 0;
+  r.first = r.cbeg + slot / tpx;
+  r.step = per_group;
+  return r;
+}
+
 // One round of a layer on global feature-major tiles of FMR = 32 rows: input tiles fin[t][k][b]
 // (source k of list position 32t + b), output tiles fout in the same layout and positions; tiles
 // [tile0, tile0 + 8) of the list, one per XCD. blockDim 256 (4 waves); a work item is a chunk of
@@ -821,7 +855,7 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
                                                    int tile0, const unsigned *__restrict__ masks_prev,
                                                    unsigned *__restrict__ masks_clear, int *__restrict__ count_out,
                                                    unsigned *__restrict__ spread, const int *__restrict__ cols,
-                                                   int ncols) {
+                                                   int ncols, int tpx) {
   static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
   constexpr int CH = kGfmOutputs, OPL = 8;
   static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
@@ -852,22 +886,18 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
     }
   }
   __syncthreads();
-  const int nt = min(8, (R + FMR - 1) / FMR - tile0);  // tiles in this round
-  const int parts = nt > 0 ? 8 / nt : 1;
-  const int xcd = blockIdx.x & 7;
-  const bool active = nt > 0 && xcd < nt * parts && prev_live != 0;  // uniform over the workgroup
   const int nchunks = (ncols + CH - 1) / CH;
-  const int cpp = (nchunks + parts - 1) / parts;  // chunks per part
-  const int t = tile0 + xcd / parts;
-  const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
+  const RoundSplit rs = round_split((R + FMR - 1) / FMR - tile0, tpx, nchunks);
+  const bool active = rs.active && prev_live != 0;  // uniform over the workgroup
+  const int t = tile0 + rs.t;
+  const int cend = active ? rs.cend : 0;
   const int b = lane & 31, h = lane >> 5;
-  const int per_xcd = gridDim.x >> 3;
   const int nvalid = active ? min(FMR, R - t * FMR) : 0;
   const float *tb = fin + (size_t)t * N * FMR + b;
   float *ob = fout + (size_t)t * N * FMR + b;
   const int jw = wave * 2 * OPL + h;  // this lane's outputs in the chunk: jw + 2i, i < OPL
   bool live = false;
-  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+  for (int chunk = rs.first; chunk < cend; chunk += rs.step) {
     const int c0 = chunk * CH;
     const int nout = min(CH, ncols - c0);
     __syncthreads();  // the previous chunk is done with ells / bstage / cstage
@@ -1228,7 +1258,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
                                                       const float *__restrict__ dict, const int *__restrict__ npos,
                                                       unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
                                                       int tile0, unsigned *__restrict__ spread,
-                                                      const int *__restrict__ cols, int ncols) {
+                                                      const int *__restrict__ cols, int ncols, int tpx) {
   constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
@@ -1245,16 +1275,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = dict[i];
   if (tid < CR / 64) rowmask[tid] = 0ull;
   const int R = *npos;
-  const int nt = min(8, (R + CR - 1) / CR - tile0);
-  const int parts = nt > 0 ? 8 / nt : 1;
-  const int xcd = blockIdx.x & 7;
-  const bool active = nt > 0 && xcd < nt * parts;
   const int nchunks = (ncols + CH - 1) / CH;
-  const int cpp = (nchunks + parts - 1) / parts;
-  const int t = tile0 + xcd / parts;
-  const int cbeg = (xcd % parts) * cpp, cend = active ? min(nchunks, cbeg + cpp) : 0;
+  const RoundSplit rs = round_split((R + CR - 1) / CR - tile0, tpx, nchunks);
+  const bool active = rs.active;
+  const int t = tile0 + rs.t;
+  const int cend = rs.cend;
   const int r = lane % RL, o = lane / RL;
-  const int per_xcd = gridDim.x >> 3;
   const int nvalid = active ? min(CR, R - t * CR) : 0;
   const unsigned char *tb = cin + (size_t)t * N * CR + 4 * r;
   // output rows 4r..4r+3 of the code tile: fp32 tile ST t + r / 8, slots (4r) % 32; the list's
@@ -1268,7 +1294,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
 #pragma unroll
   for (int h = 0; h < CR / 64; ++h) lm[h] = 0ull;
   const int jw = wave * OPI * OPL;  // first output of this wave in the chunk
-  for (int chunk = cbeg + (int)(blockIdx.x >> 3); chunk < cend; chunk += per_xcd) {
+  for (int chunk = rs.first; chunk < cend; chunk += rs.step) {
     const int c0 = chunk * CH;
     const int nout = min(CH, ncols - c0);
     __syncthreads();  // the previous chunk is done with ells / bstage / cstage / segw
@@ -2144,34 +2170,52 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
 // and writing fout at the same list positions; *npos is the list length and max_tiles a host bound
 // on its tiles. With count_out set (one round only) the launch first counts the previous layer's
 // live rows from masks_prev and clears masks_clear.
+// Tiles per XCD and launch for a layer that reads `bytes` of each input tile: as many as fit 2 MiB of
+// the XCD's 4 MiB L2, at most 8.
+int tiles_per_xcd(size_t bytes) {
+  return (int)std::max<size_t>(1, std::min<size_t>(8, ((size_t)2 << 20) / std::max<size_t>(bytes, 1)));
+}
+// Launches of launch_gfm (fp32 tiles) or launch_gfm_u8 (code tiles of cr rows, cr > 0) for a layer
+// over max_tiles fp32 tiles.
+int32_t gfm_launches(const sdnn_net *net, const LayerDev &ld, int64_t max_tiles, int cr) {
+  const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
+  const int ncols = dd ? ld.D : net->N;
+  if (cr > 0) max_tiles = (max_tiles + cr / 32 - 1) / (cr / 32);
+  const int tpx = dd ? tiles_per_xcd((size_t)ncols * (cr > 0 ? cr : 32 * sizeof(float))) : 1;
+  return (int32_t)((max_tiles + 8 * tpx - 1) / (8 * tpx));
+}
+
 hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float *fout, const int *npos,
                       int64_t max_tiles, unsigned *masks, const unsigned *masks_prev = nullptr,
                       unsigned *masks_clear = nullptr, int *count_out = nullptr, unsigned *spread = nullptr) {
-  const int rounds = (int)((max_tiles + 7) / 8);
   // distinct columns only, when the layer's duplicates need not be computed
   const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
   const int ncols = dd ? ld.D : net->N;
   const int *cols = dd ? ld.cols : nullptr;
   const unsigned short *s16 = dd ? ld.src16c : ld.src16;
+  // the few columns of such a layer touch a small part of each tile, so an XCD can keep several
+  // tiles in its L2 and a launch covers 8 tpx of them
+  const int tpx = dd ? tiles_per_xcd((size_t)ncols * 32 * sizeof(float)) : 1;
+  const int rounds = (int)((max_tiles + 8 * tpx - 1) / (8 * tpx));
   // one workgroup per output chunk of a tile's share when the round has fewer than 8 tiles
   const int nchunks = (ncols + kGfmOutputs - 1) / kGfmOutputs;
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
-  const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
-  const dim3 grid(8 * std::max(1, per_xcd));
+  const int per_xcd = tpx * std::max(1, (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts));
+  const dim3 grid(8 * per_xcd);
   for (int r = 0; r < rounds; ++r) {
     int *cnt = r == 0 ? count_out : nullptr;
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         s16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread, cols,
-                         ncols);
+                         s16, ld.w, ld.bias, net->ymax, npos, masks, r * 8 * tpx, masks_prev, masks_clear, cnt, spread,
+                         cols, ncols, tpx);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm<32, 32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
                          ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
-                         (const int *)nullptr, net->N);
+                         (const int *)nullptr, net->N, 1);
     else
       hipLaunchKernelGGL((k_layer_gfm<32, 0, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
                          ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
-                         (const int *)nullptr, net->N);
+                         (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2271,30 +2315,31 @@ template <int CR>
 hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
                             int64_t max_tiles, unsigned *masks, bool *seglive_used) {
   max_tiles = (max_tiles + CR / 32 - 1) / (CR / 32);  // code tiles
-  const int rounds = (int)((max_tiles + 7) / 8);
   // distinct columns only, when the layer's duplicates need not be computed (every segment of them
   // is then stored and seglive is not written)
   const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
   const int ncols = dd ? ld.D : net->N;
   *seglive_used = !dd;
+  const int tpx = dd ? tiles_per_xcd((size_t)ncols * CR) : 1;  // see launch_gfm
   const int nchunks = (ncols + u8_outputs(CR) - 1) / u8_outputs(CR);
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
-  const int per_xcd = (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts);
-  const dim3 grid(8 * std::max(1, per_xcd));
+  const int per_xcd = tpx * std::max(1, (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts));
+  const dim3 grid(8 * per_xcd);
+  const int rounds = (int)((max_tiles + 8 * tpx - 1) / (8 * tpx));
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, true, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive,
-                         r * 8, net->spread, dd ? ld.cols : nullptr, ncols);
+                         r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
     else if (ld.K == 32)
       hipLaunchKernelGGL((k_layer_gfm_u8<32, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread, (const int *)nullptr, net->N);
+                         net->spread, (const int *)nullptr, net->N, 1);
     else
       hipLaunchKernelGGL((k_layer_gfm_u8<0, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread, (const int *)nullptr, net->N);
+                         net->spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2955,7 +3000,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         spread_used = true;
         fout_cols = ocols_on ? lcur.cols : nullptr;
         net->layer_kernel[0] = SDNN_KERNEL_GLOBAL_TILE;
-        net->layer_launches[0] = (int32_t)(1 + (tiles(P) + 7) / 8) + (try_bits ? 1 : 0);
+        net->layer_launches[0] = 1 + gfm_launches(net, net->layers[0], tiles(P), 0) + (try_bits ? 1 : 0);
       }
     } else if (fin_codes) {
       // follows layer 0, which is always compacted: no count to take over
@@ -2965,7 +3010,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       fout_cols = ocols_on ? lcur.cols : nullptr;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
       const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
-      net->layer_launches[(size_t)l] = (int32_t)(((tiles(P) + st - 1) / st + 7) / 8);
+      net->layer_launches[(size_t)l] = gfm_launches(net, net->layers[(size_t)l], tiles(P), st * 32);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -2993,7 +3038,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         spread_used = !small;
         fout_cols = ocols_on ? lcur.cols : nullptr;
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
-        net->layer_launches[(size_t)l] = (int32_t)((tiles(P) + 7) / 8);
+        net->layer_launches[(size_t)l] = gfm_launches(net, ld, tiles(P), 0);
       }
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
