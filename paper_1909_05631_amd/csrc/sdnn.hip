@@ -416,14 +416,17 @@ __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chu
 }
 
 // One layer with the activation tile staged in LDS. B rows per tile (4 <= B <= 32, a multiple of 4);
-// blockDim 1024. KC is the compile-time ELL width (0: use the runtime K).
+// blockDim 1024. KC is the compile-time ELL width (0: use the runtime K). With cols set (one-weight
+// layers through ell16 only), the ncols columns cols[p] alone are computed and written, their
+// source lists in ell16 as [4][ncols][8]; the other columns equal one of them (see k_layer_gfm).
 template <int B, int KC>
 __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                     const int2 *__restrict__ ell, int K,
                                                     const uint4 *__restrict__ ell16, float wc,
                                                     const float *__restrict__ bias, float ymax,
                                                     const int *__restrict__ ids, const int *__restrict__ count,
-                                                    unsigned *__restrict__ masks, int *__restrict__ rownz) {
+                                                    unsigned *__restrict__ masks, int *__restrict__ rownz,
+                                                    const int *__restrict__ cols, int ncols) {
   extern __shared__ float4 smem[];
   const char *tile = reinterpret_cast<const char *>(smem);
   float *tilef = reinterpret_cast<float *>(smem);
@@ -436,7 +439,7 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int quad = lane % LPO, jl = lane / LPO;
   const int per_round = nw * OPW;
-  const int rounds = (N + per_round - 1) / per_round;
+  const int rounds = (ncols + per_round - 1) / per_round;
   const Chunking ch = chunking(ntiles, rounds);
   const int items = ntiles * ch.nchunks;
   if (tid < B) {
@@ -492,8 +495,9 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
     int live_mask = 0;
     const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
     for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
-      const int j = r * per_round + wave * OPW + jl;
-      if (j >= N) continue;
+      const int j = r * per_round + wave * OPW + jl;  // output position (the column without cols)
+      if (j >= ncols) continue;
+      const int col = cols ? cols[j] : j;
       float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
       // ELL is slot-major ([s][j]): for a given slot the lanes of a wave read consecutive entries.
       // Terms go in groups of 8 in ascending source order; with KC known, the next group's
@@ -505,7 +509,7 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
         // four loads are in flight before the first group's LDS reads
         uint4 ix[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) ix[g] = ell16[(size_t)g * N + j];
+        for (int g = 0; g < 4; ++g) ix[g] = ell16[(size_t)g * ncols + j];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
@@ -569,13 +573,13 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
           a3 = fmaf(v.w, wv, a3);
         }
       }
-      const float bj = bias[j];
+      const float bj = bias[col];
       const float y[4] = {activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
                           activate(a3, bj, ymax)};
 #pragma unroll
       for (int c4 = 0; c4 < 4; ++c4) {
         if (row[c4] >= 0) {
-          yout[(size_t)row[c4] * N + j] = y[c4];
+          yout[(size_t)row[c4] * N + col] = y[c4];
           if (y[c4] > 0.0f) live_mask |= 1 << c4;
         }
       }
@@ -600,10 +604,12 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
 // Device view of one layer for kernels that run several layers in one launch.
 struct LayerPtr {
   const int2 *ell;     // slot-major ELL, offsets in units of 1 << ell_shift bytes per source
-  const uint4 *ell16;  // one-weight layer with 32 sources per column: [4][N][8] u16 sources, else null
+  const uint4 *ell16;  // one-weight layer with 32 sources per column: [4][D][8] u16 sources, else null
   const float *bias;
-  float w;                      // the weight of a one-weight layer
+  const int *cols;     // with ell16: the D columns computed (null: all N, D = N)
+  float w;             // the weight of a one-weight layer
   int K;
+  int D;
 };
 
 // Layers [l0, L) of the live rows listed in ids (count *count), in one launch: workgroup g keeps
@@ -614,7 +620,9 @@ struct LayerPtr {
 // source order as everywhere. After every layer the workgroup adds its live rows to counts[l + 1]
 // and stops once none is left (rows that die stay dead). Rows still live after layer L - 1 are
 // written to yout (row-major, by row id) and marked in masks (one bit per list position) for the
-// final compaction. Dynamic LDS: 2 * N * B floats.
+// final compaction. A layer with cols computes only those columns (the others are never read: the
+// next layer's sources are representatives, and final rows are expanded on the host). Dynamic LDS:
+// 2 * N * B floats.
 template <int B>
 __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                      const LayerPtr *__restrict__ lp, int l0, int L, float ymax,
@@ -635,7 +643,6 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
   constexpr int LPO = B / 4, OPW = 64 / LPO;
   const int quad = lane % LPO, jl = lane / LPO;
   const int per_round = nw * OPW;
-  const int rounds = (N + per_round - 1) / per_round;
   // stage the rows as ta[k][b] (reads run along k); positions past the list are zero
   for (int it = tid; it < N * B; it += blockDim.x) {
     const int b = it / N, k = it % N;
@@ -650,15 +657,18 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
     __syncthreads();  // ta is complete, and every read of tc (the layer before's input) is done
     unsigned lm = 0u;
     const char *tq = reinterpret_cast<const char *>(ta) + quad * 16;
+    const int ncols = P.ell16 ? P.D : N;
+    const int rounds = (ncols + per_round - 1) / per_round;
     for (int r = 0; r < rounds; ++r) {
-      const int j = r * per_round + wave * OPW + jl;
-      if (j >= N) break;
+      const int jp = r * per_round + wave * OPW + jl;
+      if (jp >= ncols) break;
+      const int j = P.cols ? P.cols[jp] : jp;
       float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
       if (P.ell16) {
-        // 32 sources, eight per 16-byte load ([4][N][8] u16); all four loads in flight first
+        // 32 sources, eight per 16-byte load ([4][D][8] u16); all four loads in flight first
         uint4 ix[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) ix[g] = P.ell16[(size_t)g * N + j];
+        for (int g = 0; g < 4; ++g) ix[g] = P.ell16[(size_t)g * ncols + jp];
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
@@ -1987,13 +1997,13 @@ struct LayerDev {
   // global-tile path, uniform layer with K == 32 and N <= 65536: [K][N] u16 source indices (the
   // ELL's sources without the repeated weight)
   const unsigned short *src16 = nullptr;
-  // distinct columns (global-tile path, uniform layer with K == 32): columns with equal source lists
-  // have equal outputs, so only the D representatives cols[0..D) need computing, with their source
-  // lists in src16c ([K][D] u16). Usable (dedup_ok) once the next layer's sources point to
-  // representatives only (or for the last layer).
+  // distinct columns (uniform layer with K == 32): columns with equal source lists have equal
+  // outputs, so only the D representatives cols[0..D) need computing, with their source lists in
+  // src16c ([K][D] u16, beside src16) and ell16c ([K/8][D][8], beside ell16). Usable (dedup_ok) once
+  // the next layer's sources point to representatives only (or for the last layer).
   const int *cols = nullptr;
   const unsigned short *src16c = nullptr;
-  const uint4 *ell16c = nullptr;  // layer 0: the representatives' source lists as [K/8][D][8]
+  const uint4 *ell16c = nullptr;
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2125,8 +2135,11 @@ hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerD
     configured = true;
   }
   const int per_cu = lds <= 64 * 1024 ? 2 : 1;
+  // distinct columns only, when the layer's duplicates need not be computed
+  const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
   hipLaunchKernelGGL((k_layer_lds<B, KC>), dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
-                     ld.ell, ld.K, ld.ell16, ld.w, ld.bias, net->ymax, ids, count, net->masks, rownz);
+                     ld.ell, ld.K, dd ? ld.ell16c : ld.ell16, ld.w, ld.bias, net->ymax, ids, count, net->masks, rownz,
+                     dd ? ld.cols : nullptr, dd ? ld.D : net->N);
   return hipGetLastError();
 }
 
@@ -2296,7 +2309,7 @@ hipError_t launch_layer_count_k(sdnn_net *net, const LayerDev &ld, const void *b
   size_t lds = 16 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
   if (ROWMAJOR) lds += kDictSlots * sizeof(float) + T * sizeof(int);
   // distinct columns only, when the layer's duplicates need not be computed
-  const bool dd = !ROWMAJOR && ld.cols && ld.ell16c && ld.dedup_ok;
+  const bool dd = ld.cols && ld.ell16c && ld.dedup_ok;
   hipLaunchKernelGGL((k_layer_count<T, ROWMAJOR>), dim3(net->cus), dim3(1024), lds, net->stream,
                      reinterpret_cast<const W *>(bits), cout, net->N, dd ? ld.ell16c : ld.ell16, net->misc, count, masks,
                      yout, ids, reinterpret_cast<const unsigned *>(net->dict), dd ? ld.cols : nullptr,
@@ -2488,14 +2501,14 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   });
   for (int32_t i = 0; i < nl; ++i)
     if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
-  // ---- duplicate columns (global-tile path, uniform layers with 32 sources per column): columns
+  // ---- duplicate columns (uniform layers with 32 sources per column): columns
   // with the same source list have the same output, so reps[i][j] = the smallest column with j's
   // list (empty: no duplicates). Grouping uses the sources as given; equal lists stay equal once
   // mapped (below). With the Kronecker-expanded networks of Sec. III every 16 columns of a block
   // share their list.
   std::vector<std::vector<int32_t>> reps((size_t)nl);
   parallel_for(nl, [&](int32_t i) {
-    if (net->path != 1 || N > 65536 || !uniform[(size_t)i] || K[(size_t)i] != 32) return;
+    if (N > 65536 || !uniform[(size_t)i] || K[(size_t)i] != 32) return;
     const int64_t *cp = col_ptr + (size_t)i * (N + 1);
     std::unordered_map<uint64_t, std::vector<int32_t>> seen;
     seen.reserve((size_t)N);
@@ -2662,10 +2675,13 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     }
   }
   {
-    // distinct columns: the representatives and their (mapped) source lists, [32][D] u16
+    // distinct columns: the representatives and their (mapped) source lists, as [32][D] u16 for the
+    // global-tile kernels and as [4][D][8] u16 for the LDS-tile and counting kernels
     std::vector<int32_t> sel;
-    for (int32_t i = 0; i < nl; ++i)
-      if (!reps[(size_t)i].empty() && net->layers[(size_t)l0 + i].src16) sel.push_back(i);
+    for (int32_t i = 0; i < nl; ++i) {
+      const LayerDev &ld = net->layers[(size_t)l0 + i];
+      if (!reps[(size_t)i].empty() && (ld.src16 || ld.ell16)) sel.push_back(i);
+    }
     if (!sel.empty()) {
       std::vector<size_t> off(sel.size() + 1, 0);  // in columns
       std::vector<std::vector<int32_t>> cols(sel.size());
@@ -2677,54 +2693,40 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       }
       const size_t tot = off[sel.size()];
       std::vector<int32_t> hc(tot);
-      std::vector<uint16_t> hs((size_t)32 * tot);
-      // layer 0 also in the counting kernel's grouped layout
-      std::vector<uint16_t> hg;
-      int32_t q0 = -1;
-      for (size_t q = 0; q < sel.size(); ++q)
-        if (l0 + sel[q] == 0 && net->layers[0].ell16) q0 = (int32_t)q;
-      if (q0 >= 0) hg.resize((size_t)32 * cols[(size_t)q0].size());
+      std::vector<uint16_t> hs((size_t)32 * tot), hg((size_t)32 * tot);
       parallel_for((int32_t)sel.size(), [&](int32_t q) {
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         const size_t D = cols[(size_t)q].size();
-        uint16_t *dst = hs.data() + (size_t)32 * off[(size_t)q];
+        uint16_t *ds = hs.data() + (size_t)32 * off[(size_t)q];
+        uint16_t *dg = hg.data() + (size_t)32 * off[(size_t)q];
         for (size_t p = 0; p < D; ++p) {
           const int32_t j = cols[(size_t)q][p];
           hc[off[(size_t)q] + p] = j;
           for (int sl = 0; sl < 32; ++sl) {
             const uint16_t v = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
-            dst[(size_t)sl * D + p] = v;
-            if (q == q0) hg[((size_t)(sl / 8) * D + p) * 8 + sl % 8] = v;
+            ds[(size_t)sl * D + p] = v;
+            dg[((size_t)(sl / 8) * D + p) * 8 + sl % 8] = v;
           }
         }
       });
       const size_t cbytes = align_up(tot * sizeof(int32_t), 256);
+      const size_t sbytes = align_up(hs.size() * sizeof(uint16_t), 256);
       char *mc = nullptr;
-      e = hipMalloc(reinterpret_cast<void **>(&mc), cbytes + hs.size() * sizeof(uint16_t));
+      e = hipMalloc(reinterpret_cast<void **>(&mc), cbytes + 2 * sbytes);
       if (e != hipSuccess) {
         (void)hipGetLastError();
-        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", cbytes + hs.size() * sizeof(uint16_t),
-                    hipGetErrorString(e));
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", cbytes + 2 * sbytes, hipGetErrorString(e));
       }
       net->allocations.push_back(mc);
       HIP_OR_POISON(net, hipMemcpy(mc, hc.data(), tot * sizeof(int32_t), hipMemcpyHostToDevice));
       HIP_OR_POISON(net, hipMemcpy(mc + cbytes, hs.data(), hs.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      HIP_OR_POISON(net, hipMemcpy(mc + cbytes + sbytes, hg.data(), hg.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
       for (size_t q = 0; q < sel.size(); ++q) {
         LayerDev &ld = net->layers[(size_t)l0 + sel[q]];
         ld.cols = reinterpret_cast<const int *>(mc) + off[q];
-        ld.src16c = reinterpret_cast<const unsigned short *>(mc + cbytes) + (size_t)32 * off[q];
+        ld.src16c = ld.src16 ? reinterpret_cast<const unsigned short *>(mc + cbytes) + (size_t)32 * off[q] : nullptr;
+        ld.ell16c = ld.ell16 ? reinterpret_cast<const uint4 *>(mc + cbytes + sbytes) + (size_t)4 * off[q] : nullptr;
         ld.D = (int)cols[q].size();
-      }
-      if (q0 >= 0) {
-        char *mg = nullptr;
-        e = hipMalloc(reinterpret_cast<void **>(&mg), hg.size() * sizeof(uint16_t));
-        if (e != hipSuccess) {
-          (void)hipGetLastError();
-          return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", hg.size() * sizeof(uint16_t), hipGetErrorString(e));
-        }
-        net->allocations.push_back(mg);
-        HIP_OR_POISON(net, hipMemcpy(mg, hg.data(), hg.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
-        net->layers[0].ell16c = reinterpret_cast<const uint4 *>(mg);
       }
     }
     // a layer whose successor reads its representatives only may skip its duplicates; so may the
@@ -2750,12 +2752,16 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     net->allocations.push_back(net->lp_dev);
   }
   {
-    std::vector<LayerPtr> hp((size_t)nl);
-    for (int32_t i = 0; i < nl; ++i) {
-      const LayerDev &ld = net->layers[(size_t)l0 + i];
-      hp[(size_t)i] = LayerPtr{ld.ell, ld.ell16, ld.bias, ld.w, ld.K};
+    // from layer l0 - 1 when this load let it skip its duplicate columns
+    const int32_t t0 = (l0 > 0 && net->layers[(size_t)l0 - 1].dedup_ok) ? l0 - 1 : l0;
+    std::vector<LayerPtr> hp((size_t)(l0 + nl - t0));
+    for (int32_t l = t0; l < l0 + nl; ++l) {
+      const LayerDev &ld = net->layers[(size_t)l];
+      const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
+      hp[(size_t)(l - t0)] = LayerPtr{ld.ell, dd ? ld.ell16c : ld.ell16, ld.bias, dd ? ld.cols : nullptr, ld.w, ld.K,
+                                      dd ? ld.D : N};
     }
-    HIP_OR_POISON(net, hipMemcpy(net->lp_dev + l0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
+    HIP_OR_POISON(net, hipMemcpy(net->lp_dev + t0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
   }
   net->n_loaded += nl;
   g_err.clear();
@@ -3270,8 +3276,14 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
     for (int64_t q = 0; q < n; ++q) {
       float *dst = out_host + (size_t)q * net->N;
       const bool is_live = c > 0 && net->final_y && std::binary_search(live.begin(), live.begin() + c, (long long)ids[q]);
-      if (is_live) HIP_OR_POISON(net, hipMemcpy(dst, net->final_y + (size_t)ids[q] * net->N, rowb, hipMemcpyDeviceToHost));
-      else std::memset(dst, 0, rowb);
+      if (is_live) {
+        HIP_OR_POISON(net, hipMemcpy(dst, net->final_y + (size_t)ids[q] * net->N, rowb, hipMemcpyDeviceToHost));
+        // the last layer may have computed only one column of each group of equal columns
+        if (!net->last_rep.empty())
+          for (int32_t j = 0; j < net->N; ++j) dst[j] = dst[net->last_rep[(size_t)j]];
+      } else {
+        std::memset(dst, 0, rowb);
+      }
     }
     g_err.clear();
     return SDNN_OK;

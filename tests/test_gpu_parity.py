@@ -398,6 +398,34 @@ def test_structured_duplicate_columns(order):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("case", ["tiles", "counted", "last-fused"])
+def test_structured_lds_columns(case):
+    """Structured networks on widths staged in LDS: one column per group of equal columns in the
+    one-layer LDS kernel, in layer 0 by counts (written as fp32 rows) and in the launch that runs
+    every remaining layer; the final rows are expanded through the last layer's groups.
+    "tiles": more live rows than the fused launch takes, so several layers run one by one;
+    "counted": 2^24 binary inputs, layer 0 by counts; "last-fused": the fused launch ends the run."""
+    n, m, nl, bias = {"tiles": (1024, 3000, 6, -0.30), "counted": (4096, 4200, 4, -0.35),
+                      "last-fused": (1024, 600, 21, -0.30)}[case]
+    d = synth.radix_depth(n)
+    side = int(round(n ** 0.5))
+    y0 = synth.inputs(50 + d, side, 0, m, "mixed", 0.05, 0.35)
+    cp, ri, v = synth.radix_layers_csc(24, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
+    log(f"structured LDS columns case={case} n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
+    log(f"kinds {kinds}")
+    if case == "tiles":
+        assert kinds[1] == "k_layer_lds"
+    if case == "counted":
+        assert kinds[0] == "k_pack_bits+k_layer_count"
+    if case == "last-fused":
+        assert kinds[-1] == "k_layers_lds"
+    assert 0 < cats.size < m
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("nl", [2, 5])
 def test_structured_code_layer_columns(nl):
     """A structured network on more than 256 rows: layer 0 by counts, layer 1 gathers one-byte codes
