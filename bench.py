@@ -141,6 +141,23 @@ def committed_traffic(workload: str, kernel: str):
     return rec.get("bytes_per_launch")
 
 
+def committed_lds(workload: str, kernel: str):
+    """LDS bank-conflict share (bank-conflict stall cycles over LDS-active cycles, rocprofv3
+    SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE) of each kernel of `kernel` (names joined by '+'), from
+    the same record as committed_traffic; None if absent or taken with another kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    try:
+        with open(path) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256") != kernel_source_sha() or "lds" not in rec:
+        return None
+    parts = kernel.split("+")
+    out = {k: v["conflict_cycle_frac"] for k, v in rec["lds"]["kernels"].items() if k.split("<")[0] in parts}
+    return out or None
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -272,6 +289,7 @@ def main() -> int:
         tot_ms = float(ms[timed].sum())
         roofline = {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                     "frac": round(achieved / HBM_PEAK_GBS, 5), "traffic": committed_traffic(wname, kname),
+                    "lds_bank_conflict": committed_lds(wname, kname),
                     "kernel": kname, "layer": lay, "launches_per_step": nl,
                     "avg_launch_ms": round(avg_launch_ms, 5), "algorithmic_bytes_per_launch": int(algo / nl),
                     "large_layers": {"layers": len(timed),

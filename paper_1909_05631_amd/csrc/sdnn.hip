@@ -612,24 +612,46 @@ struct LayerPtr {
   int D;
 };
 
+// RPL consecutive fp32 rows of one source, read or written as one LDS access
+template <int RPL>
+__device__ __forceinline__ void lds_rows_load(const char *p, float (&v)[RPL]) {
+  if constexpr (RPL == 4) {
+    const float4 t = *reinterpret_cast<const float4 *>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else if constexpr (RPL == 2) {
+    const float2 t = *reinterpret_cast<const float2 *>(p);
+    v[0] = t.x; v[1] = t.y;
+  } else {
+    v[0] = *reinterpret_cast<const float *>(p);
+  }
+}
+template <int RPL>
+__device__ __forceinline__ void lds_rows_store(float *p, const float (&v)[RPL]) {
+  if constexpr (RPL == 4) *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  else if constexpr (RPL == 2) *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+  else *p = v[0];
+}
+
 // Layers [l0, L) of the live rows listed in ids (count *count), in one launch: workgroup g keeps
 // list positions [gB, gB + B) in LDS across all the layers, as two tiles [k][B] (the layer's input
 // and its output), so between layers nothing goes through global memory and nothing waits for other
-// workgroups (rows are independent, Sec. V). Lane = (quad = lane % (B/4): rows 4quad..4quad+3,
-// output slot lane / (B/4)); each term is one 16-byte LDS read of 4 rows and 4 fmas, in ascending
-// source order as everywhere. After every layer the workgroup adds its live rows to counts[l + 1]
-// and stops once none is left (rows that die stay dead). Rows still live after layer L - 1 are
-// written to yout (row-major, by row id) and marked in masks (one bit per list position) for the
-// final compaction. A layer with cols computes only those columns (the others are never read: the
-// next layer's sources are representatives, and final rows are expanded on the host). Dynamic LDS:
-// 2 * N * B floats.
+// workgroups (rows are independent, Sec. V). A lane holds RPL = min(B, 4) rows: lane = (quad = lane
+// % (B/RPL): rows RPL quad .. RPL quad + RPL - 1, output slot lane / (B/RPL)); each term is one LDS
+// read of RPL rows (16, 8 or 4 bytes) and RPL fmas, in ascending source order as everywhere. Small
+// B spreads a short list over more CUs. After every layer the workgroup adds its live rows to
+// counts[l + 1] and stops once none is left (rows that die stay dead). Rows still live after layer
+// L - 1 are written to yout (row-major, by row id) and marked in masks (one bit per list position)
+// for the final compaction. A layer with cols computes only those columns (the others are never
+// read: the next layer's sources are representatives, and final rows are expanded on the host).
+// Dynamic LDS: 2 * N * B floats.
 template <int B>
 __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                      const LayerPtr *__restrict__ lp, int l0, int L, float ymax,
                                                      const int *__restrict__ ids, const int *__restrict__ count,
                                                      int *__restrict__ counts, unsigned *__restrict__ masks,
                                                      int ell_shift) {
-  static_assert(B == 4 || B == 8 || B == 16, "lanes hold 4 rows each, at most 4 lanes per output");
+  static_assert(B == 1 || B == 2 || B == 4 || B == 8 || B == 16, "lanes hold up to 4 rows, at most 4 lanes per output");
+  constexpr int RPL = B < 4 ? B : 4;
   extern __shared__ float4 smem[];
   __shared__ unsigned livebits[2];
   float *ta = reinterpret_cast<float *>(smem);
@@ -640,7 +662,7 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
   const int nvalid = min(B, R - p0);
   const unsigned valid = (1u << nvalid) - 1u;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
-  constexpr int LPO = B / 4, OPW = 64 / LPO;
+  constexpr int LPO = B / RPL, OPW = 64 / LPO;
   const int quad = lane % LPO, jl = lane / LPO;
   const int per_round = nw * OPW;
   // stage the rows as ta[k][b] (reads run along k); positions past the list are zero
@@ -656,14 +678,16 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
     if (tid == 0) livebits[l & 1] = 0u;
     __syncthreads();  // ta is complete, and every read of tc (the layer before's input) is done
     unsigned lm = 0u;
-    const char *tq = reinterpret_cast<const char *>(ta) + quad * 16;
+    const char *tq = reinterpret_cast<const char *>(ta) + quad * (RPL * 4);
     const int ncols = P.ell16 ? P.D : N;
     const int rounds = (ncols + per_round - 1) / per_round;
     for (int r = 0; r < rounds; ++r) {
       const int jp = r * per_round + wave * OPW + jl;
       if (jp >= ncols) break;
       const int j = P.cols ? P.cols[jp] : jp;
-      float a0 = 0.0f, a1 = 0.0f, a2 = 0.0f, a3 = 0.0f;
+      float a[RPL];
+#pragma unroll
+      for (int c = 0; c < RPL; ++c) a[c] = 0.0f;
       if (P.ell16) {
         // 32 sources, eight per 16-byte load ([4][D][8] u16); all four loads in flight first
         uint4 ix[4];
@@ -672,37 +696,37 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
-          float4 v[8];
+          float v[8][RPL];
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
             const unsigned k = (q & 1) ? (pr[q >> 1] >> 16) : (pr[q >> 1] & 0xffffu);
-            v[q] = *reinterpret_cast<const float4 *>(tq + k * (unsigned)(B * 4));
+            lds_rows_load<RPL>(tq + k * (unsigned)(B * 4), v[q]);
           }
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            a0 = fmaf(v[q].x, P.w, a0);
-            a1 = fmaf(v[q].y, P.w, a1);
-            a2 = fmaf(v[q].z, P.w, a2);
-            a3 = fmaf(v[q].w, P.w, a3);
-          }
+          for (int q = 0; q < 8; ++q)
+#pragma unroll
+            for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[q][c], P.w, a[c]);
         }
       } else {
         for (int sl = 0; sl < P.K; ++sl) {
           const int2 e = P.ell[(size_t)sl * N + j];
-          const float4 v = *reinterpret_cast<const float4 *>(tq + ((unsigned)e.x >> ell_shift) * (unsigned)(B * 4));
+          float v[RPL];
+          lds_rows_load<RPL>(tq + ((unsigned)e.x >> ell_shift) * (unsigned)(B * 4), v);
           const float wv = __int_as_float(e.y);
-          a0 = fmaf(v.x, wv, a0);
-          a1 = fmaf(v.y, wv, a1);
-          a2 = fmaf(v.z, wv, a2);
-          a3 = fmaf(v.w, wv, a3);
+#pragma unroll
+          for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[c], wv, a[c]);
         }
       }
       const float bj = P.bias[j];
-      const float4 y = make_float4(activate(a0, bj, ymax), activate(a1, bj, ymax), activate(a2, bj, ymax),
-                                   activate(a3, bj, ymax));
-      *reinterpret_cast<float4 *>(tc + (size_t)j * B + quad * 4) = y;
-      lm |= ((y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) | (y.w > 0.0f ? 8u : 0u))
-            << (4 * quad);
+      float y[RPL];
+      unsigned bits = 0u;
+#pragma unroll
+      for (int c = 0; c < RPL; ++c) {
+        y[c] = activate(a[c], bj, ymax);
+        bits |= (y[c] > 0.0f ? 1u : 0u) << c;
+      }
+      lds_rows_store<RPL>(tc + (size_t)j * B + quad * RPL, y);
+      lm |= bits << (RPL * quad);
     }
 #pragma unroll
     for (int d = 32; d >= 1; d >>= 1) lm |= __shfl_xor(lm, d, 64);
@@ -2004,6 +2028,9 @@ struct LayerDev {
   const int *cols = nullptr;
   const unsigned short *src16c = nullptr;
   const uint4 *ell16c = nullptr;
+  // layer 0 of a uniform layer with K == 32: the lists of ell16 (and ell16c) with each column's
+  // sources reordered for the counting kernel, whose counts do not depend on the order
+  const uint4 *ell16s = nullptr, *ell16cs = nullptr;
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2290,6 +2317,59 @@ hipError_t launch_layer_bits(sdnn_net *net, const LayerDev &ld, const void *bits
   return launch_layer_bits_k<T, 0, false>(net, ld, bits, fout, count);
 }
 
+// Source order for the counting kernel. A wave's LDS read of one source slot serves 64 outputs, in
+// two halves of 32 lanes (32 consecutive output positions); within a half, reads of different
+// 4-byte words in the same one of the 32 banks are served one after another. The count does not
+// depend on the order of a column's sources, so for each half the sources are dealt to the 32
+// slots greedily: slot by slot, lanes with the fewest distinct remaining banks choose first, each
+// taking a remaining source whose bank this slot has used least. src: [4][D][8] u16 lists; wbytes:
+// bytes per LDS word of the bit tile (the word of source k is k * wbytes / 4).
+std::vector<uint16_t> bank_balanced_lists(const uint16_t *src, int D, int wbytes) {
+  std::vector<uint16_t> out((size_t)32 * D);
+  const int groups = (D + 31) / 32;
+  parallel_for(groups, [&](int32_t g) {
+    const int p0 = g * 32, np = std::min(32, D - p0);
+    uint16_t rem[32][32];
+    int nrem[32];
+    for (int i = 0; i < np; ++i) {
+      for (int sl = 0; sl < 32; ++sl) rem[i][sl] = src[((size_t)(sl / 8) * D + p0 + i) * 8 + sl % 8];
+      nrem[i] = 32;
+    }
+    auto word = [&](unsigned k) { return (unsigned)((k * (unsigned)wbytes) / 4u); };
+    for (int sl = 0; sl < 32; ++sl) {
+      int load[32] = {0};
+      unsigned used[32][32];  // words of each bank read in this slot
+      int order[32], key[32];
+      for (int i = 0; i < np; ++i) {
+        unsigned seen = 0u;
+        for (int q = 0; q < nrem[i]; ++q) seen |= 1u << (word(rem[i][q]) & 31u);
+        key[i] = __builtin_popcount(seen);
+        order[i] = i;
+      }
+      std::stable_sort(order, order + np, [&](int a, int b) { return key[a] < key[b]; });
+      for (int oi = 0; oi < np; ++oi) {
+        const int i = order[oi];
+        int best = 0, bcost = 1 << 30;
+        for (int q = 0; q < nrem[i]; ++q) {
+          const unsigned w = word(rem[i][q]), b = w & 31u;
+          bool same = false;
+          for (int u = 0; u < load[b]; ++u) same = same || used[b][u] == w;
+          const int cost = same ? 0 : load[b] + 1;
+          if (cost < bcost) { bcost = cost; best = q; }
+        }
+        const uint16_t k = rem[i][best];
+        rem[i][best] = rem[i][--nrem[i]];
+        const unsigned w = word(k), b = w & 31u;
+        bool same = false;
+        for (int u = 0; u < load[b]; ++u) same = same || used[b][u] == w;
+        if (!same) used[b][load[b]++] = w;
+        out[((size_t)(sl / 8) * D + p0 + i) * 8 + sl % 8] = k;
+      }
+    }
+  });
+  return out;
+}
+
 // Layer 0 of a uniform layer by counting (see k_layer_count): dictionary, then the counts as codes
 // (cout) or, with yout set, as fp32 rows yout[ids[p]] (masks: one bit per list position).
 template <int T, bool ROWMAJOR>
@@ -2311,7 +2391,8 @@ hipError_t launch_layer_count_k(sdnn_net *net, const LayerDev &ld, const void *b
   // distinct columns only, when the layer's duplicates need not be computed
   const bool dd = ld.cols && ld.ell16c && ld.dedup_ok;
   hipLaunchKernelGGL((k_layer_count<T, ROWMAJOR>), dim3(net->cus), dim3(1024), lds, net->stream,
-                     reinterpret_cast<const W *>(bits), cout, net->N, dd ? ld.ell16c : ld.ell16, net->misc, count, masks,
+                     reinterpret_cast<const W *>(bits), cout, net->N,
+                     dd ? (ld.ell16cs ? ld.ell16cs : ld.ell16c) : (ld.ell16s ? ld.ell16s : ld.ell16), net->misc, count, masks,
                      yout, ids, reinterpret_cast<const unsigned *>(net->dict), dd ? ld.cols : nullptr,
                      dd ? ld.D : net->N);
   return hipGetLastError();
@@ -2365,7 +2446,7 @@ hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char 
 }
 
 // Rows per workgroup of k_layers_lds: at most the largest of 16, 8, 4 whose two tiles fit 128 KiB
-// of LDS, halved while twice the workgroups still fit one per CU.
+// of LDS, halved (down to 1) while twice the workgroups still fit one per CU.
 int fused_rows_max(const sdnn_net *net) {
   int b = 16;
   while (b > 4 && (size_t)2 * b * net->N * sizeof(float) > (size_t)kLdsTileBytes) b /= 2;
@@ -2373,7 +2454,7 @@ int fused_rows_max(const sdnn_net *net) {
 }
 int fused_rows(const sdnn_net *net, int64_t rows) {
   int b = fused_rows_max(net);
-  while (b > 4 && 2 * ((rows + b - 1) / b) <= net->cus) b /= 2;
+  while (b > 1 && 2 * ((rows + b - 1) / b) <= net->cus) b /= 2;
   return b;
 }
 
@@ -2402,7 +2483,9 @@ hipError_t launch_layers_lds(sdnn_net *net, const float *yin, float *yout, int l
   switch (fused_rows(net, rows)) {
     case 16: return launch_layers_lds_b<16>(net, yin, yout, l0, ids, count, rows);
     case 8: return launch_layers_lds_b<8>(net, yin, yout, l0, ids, count, rows);
-    default: return launch_layers_lds_b<4>(net, yin, yout, l0, ids, count, rows);
+    case 4: return launch_layers_lds_b<4>(net, yin, yout, l0, ids, count, rows);
+    case 2: return launch_layers_lds_b<2>(net, yin, yout, l0, ids, count, rows);
+    default: return launch_layers_lds_b<1>(net, yin, yout, l0, ids, count, rows);
   }
 }
 
@@ -2728,6 +2811,38 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         ld.ell16c = ld.ell16 ? reinterpret_cast<const uint4 *>(mc + cbytes + sbytes) + (size_t)4 * off[q] : nullptr;
         ld.D = (int)cols[q].size();
       }
+    }
+    // layer 0: the lists in the counting kernel's order (words of 4 bytes on the LDS-tile path, of
+    // bitsT / 8 bytes on the global-tile path)
+    if (l0 == 0 && net->layers[0].ell16 && net->layers[0].w > 0.0f) {
+      LayerDev &ld = net->layers[0];
+      const int wbytes = net->path == 0 ? 4 : std::max(net->bitsT, 16) / 8;
+      const int64_t *cp = col_ptr;
+      std::vector<int32_t> c0;
+      if (ld.cols)
+        for (int32_t j = 0; j < N; ++j)
+          if (reps[0][(size_t)j] == j) c0.push_back(j);
+      std::vector<uint16_t> full((size_t)32 * N), part((size_t)32 * c0.size());
+      for (int32_t j = 0; j < N; ++j)
+        for (int sl = 0; sl < 32; ++sl) full[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)src_at(0, cp[j] + sl);
+      const int D0 = (int)c0.size();
+      for (int p = 0; p < D0; ++p)
+        for (int sl = 0; sl < 32; ++sl)
+          part[((size_t)(sl / 8) * D0 + p) * 8 + sl % 8] = (uint16_t)src_at(0, cp[c0[(size_t)p]] + sl);
+      const std::vector<uint16_t> bf = bank_balanced_lists(full.data(), N, wbytes);
+      const std::vector<uint16_t> bp = D0 ? bank_balanced_lists(part.data(), D0, wbytes) : std::vector<uint16_t>();
+      const size_t fb = align_up(bf.size() * sizeof(uint16_t), 256);
+      char *mb = nullptr;
+      e = hipMalloc(reinterpret_cast<void **>(&mb), fb + bp.size() * sizeof(uint16_t));
+      if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", fb + bp.size() * sizeof(uint16_t), hipGetErrorString(e));
+      }
+      net->allocations.push_back(mb);
+      HIP_OR_POISON(net, hipMemcpy(mb, bf.data(), bf.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      if (D0) HIP_OR_POISON(net, hipMemcpy(mb + fb, bp.data(), bp.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+      ld.ell16s = reinterpret_cast<const uint4 *>(mb);
+      ld.ell16cs = D0 ? reinterpret_cast<const uint4 *>(mb + fb) : nullptr;
     }
     // a layer whose successor reads its representatives only may skip its duplicates; so may the
     // last layer (the final rows are expanded through its representatives)

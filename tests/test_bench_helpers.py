@@ -1,0 +1,47 @@
+"""Host-side pieces of bench.py: the algorithmic byte count of a layer (dense fp32 live rows, weights
+once, bias) and the lookup of committed rocprofv3 records, which must ignore records taken with
+another kernel source."""
+import json
+
+import numpy as np
+
+import bench
+
+
+def test_algorithmic_layer_bytes_counts_rows_weights_and_bias():
+    # 4 neurons, 8 weights, 2 rows in, 1 row out: 4*4*(2+1) + 8*8 + 4*4
+    assert bench.algorithmic_layer_bytes(4, 8, 2, 1) == 48 + 64 + 16
+    # nothing enters: nothing moves
+    assert bench.algorithmic_layer_bytes(4, 8, 0, 0) == 0
+    # equal columns: 16 columns in groups of 4 read 4 distinct input columns and write 4 outputs;
+    # the weights of 4 of the 16 columns are read
+    assert bench.algorithmic_layer_bytes(16, 16 * 32, 10, 5, 4, 4) == 4 * (4 * 10 + 4 * 5) + 8 * 4 * 32 + 4 * 4
+    # every column distinct: the same as the plain count
+    assert bench.algorithmic_layer_bytes(16, 512, 10, 5, 16, 16) == bench.algorithmic_layer_bytes(16, 512, 10, 5)
+
+
+def test_distinct_columns():
+    n, k = 8, 2
+    # columns 0..3 read (0, 1); columns 4..7 read (2, 3): two distinct lists
+    ri = np.array([0, 1] * 4 + [2, 3] * 4, np.int32)
+    cp = [np.arange(0, n * k + 1, k, dtype=np.int64)]
+    assert bench.distinct_columns(lambda l0, nl: (cp, ri, None), 0, n) == 2
+
+
+def test_committed_records_follow_the_kernel_source(tmp_path, monkeypatch):
+    (tmp_path / "profiles").mkdir()
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda: "abc")
+    rec = {"kernel": "k_layer_gfm_u8", "kernel_source_sha256": "abc", "bytes_per_launch": 123,
+           "lds": {"command": "", "kernels": {"k_layer_gfm_u8<32, true, 64>": {"conflict_cycle_frac": 0.012},
+                                              "k_layer_count<16, false>": {"conflict_cycle_frac": 0.48},
+                                              "k_layer_gfm<32, 32, true>": {"conflict_cycle_frac": 0.03}}}}
+    (tmp_path / "profiles" / "traffic_w.json").write_text(json.dumps(rec))
+    assert bench.committed_traffic("w", "k_layer_gfm_u8") == 123
+    assert bench.committed_traffic("w", "k_layer_gfm") is None  # another kernel's record
+    assert bench.committed_lds("w", "k_layer_gfm_u8") == {"k_layer_gfm_u8<32, true, 64>": 0.012}
+    assert bench.committed_lds("w", "k_pack_bits+k_layer_count") == {"k_layer_count<16, false>": 0.48}
+    assert bench.committed_traffic("x", "k_layer_gfm_u8") is None  # no record
+    monkeypatch.setattr(bench, "kernel_source_sha", lambda: "def")  # source changed since
+    assert bench.committed_traffic("w", "k_layer_gfm_u8") is None
+    assert bench.committed_lds("w", "k_layer_gfm_u8") is None
