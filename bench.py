@@ -69,15 +69,38 @@ def workload_name(cfg, network: str) -> str:
     return cfg.name if network == "union" else f"{network}-{cfg.name}"
 
 
-def cpu_baseline(cfg, target_s: float, threads: int, network: str = "union") -> dict:
+# The supplementary all-live input set: Bernoulli(0.6) rows. Each column sums 32 weights of 1/16,
+# so a row grows while its mean exceeds -b; at density 0.6 every row stays live at every width and
+# saturates at YMAX within a few layers, so each layer runs at its full shape (R_l = M).
+ALL_LIVE_DENSITY = 0.6
+
+
+def workload(cfg, inputs: str, layers: int | None):
+    """The config, cut to its first `layers` layers and, for the all-live set, renamed."""
+    import dataclasses
+    L = layers or cfg.n_layers
+    if L == cfg.n_layers and inputs == "strokes":
+        return cfg
+    name = f"n{cfg.n_neurons}-l{L}-m{cfg.n_rows}"
+    return dataclasses.replace(cfg, n_layers=L, name=("alllive-" + name) if inputs == "alllive" else name)
+
+
+def input_rows(cfg, inputs: str, r0: int, nr: int) -> np.ndarray:
+    """Rows [r0, r0 + nr) of the workload's inputs: the config's stroke images, or Bernoulli rows."""
+    import synth
+    if inputs == "alllive":
+        return synth.inputs(cfg.input_set, cfg.side, r0, nr, "bernoulli", ALL_LIVE_DENSITY)
+    return synth.config_inputs(cfg, r0, nr)
+
+
+def cpu_baseline(cfg, target_s: float, threads: int, network: str = "union", inputs: str = "strokes") -> dict:
     """The oracle as it is, on a bounded sample of the same workload (first rows of the input set),
     timing only its layer evaluations (weight generation is loading, untimed as on the GPU side)."""
     import oracle
-    import synth
     layers = layer_source(cfg, network)
 
     def run(rows: int) -> float:
-        y0 = synth.config_inputs(cfg, 0, rows)
+        y0 = input_rows(cfg, inputs, 0, rows)
         o = oracle.Oracle(y0, cfg.ymax)
         bias = np.full(cfg.n_neurons, cfg.bias, np.float32)
         spent, l, chunk = 0.0, 0, 8
@@ -167,6 +190,10 @@ def main() -> int:
     ap.add_argument("--network", choices=["union", "radix"], default="union",
                     help="weight layers: the configs' permutation unions, or structured RadiX-Net style "
                          "layers (Kronecker-expanded radix-2 base DNN, Fig. 1 / Table 1) of the same width")
+    ap.add_argument("--inputs", choices=["strokes", "alllive"], default="strokes",
+                    help="the config's stroke images (~19%% ones), or the supplementary all-live set "
+                         "(Bernoulli(0.6) rows: every row stays live, so every layer runs at full shape)")
+    ap.add_argument("--layers", type=int, default=0, help="run only the first LAYERS layers (0: all)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-layer events (no roofline)")
@@ -192,7 +219,7 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 2
     torch.cuda.set_device(0)
-    cfg = synth.CONFIGS[args.config]
+    cfg = workload(synth.CONFIGS[args.config], args.inputs, args.layers)
     n, L, m = cfg.n_neurons, cfg.n_layers, cfg.n_rows
     wname = workload_name(cfg, args.network)
     layers = layer_source(cfg, args.network)
@@ -204,7 +231,7 @@ def main() -> int:
     chunk = max(1, (1 << 28) // (4 * n))
     for r0 in range(0, m, chunk):
         nr = min(chunk, m - r0)
-        y0[r0:r0 + nr].copy_(torch.from_numpy(synth.config_inputs(cfg, r0, nr)))
+        y0[r0:r0 + nr].copy_(torch.from_numpy(input_rows(cfg, args.inputs, r0, nr)))
     density = float(y0.mean().item())
     log(f"{wname}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
     t0 = time.time()
@@ -298,7 +325,7 @@ def main() -> int:
     cpu = None
     if not args.no_cpu_baseline:
         threads = max(1, min(16, os.cpu_count() or 1))
-        cpu = cpu_baseline(cfg, args.cpu_seconds, threads, args.network)
+        cpu = cpu_baseline(cfg, args.cpu_seconds, threads, args.network, args.inputs)
 
     out = {
         "metric": "inference edges/sec (Ninputs*sum nnz(W)/t) + % HBM roofline, 1 MI355X",
@@ -316,6 +343,8 @@ def main() -> int:
         "config": {"workload": wname, "network": "permutation-union" if args.network == "union" else "radix-kronecker",
                    "n_neurons": n, "n_layers": L, "n_rows": m, "bias": cfg.bias,
                    "ymax": cfg.ymax, "connections": cfg.total_nnz, "input_density": round(density, 4),
+                   "inputs": "binary stroke images" if args.inputs == "strokes" else
+                             f"binary Bernoulli({ALL_LIVE_DENSITY}) rows, all live (supplementary set)",
                    "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "cpu_baseline": cpu,

@@ -94,3 +94,27 @@ def test_structured_full_config_sampled_rows(ci):
     if o.categories().size:
         np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
     o.close()
+
+
+@pytest.mark.parametrize("ci,nl", [(2, 12), (4, 6)])
+def test_all_live_sampled_rows(ci, nl):
+    """The supplementary all-live set: Bernoulli(0.6) rows on the config's network, which keep every
+    row live at every layer, so each layer runs at its full shape (60,000 rows); the first nl layers.
+    A seeded sample of 64 rows is recomputed by the oracle."""
+    import bench
+    cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
+    n, m = cfg.n_neurons, cfg.n_rows
+    y0 = bench.input_rows(cfg, "alllive", 0, m)
+    gpu = GpuRun(n, nl, cfg.ymax)
+    log(f"{cfg.name}: loading {nl} layers")
+    gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
+    cats = gpu.run(y0)
+    counts = gpu.net.live_counts()
+    log(f"{cfg.name}: {cats.size} categories; live counts {counts.tolist()}")
+    assert (counts == m).all() and cats.size == m
+    rng = np.random.default_rng(200 + ci)
+    sample = np.sort(rng.choice(m, size=64, replace=False))
+    o = oracle.run_config_layers(y0[sample], cfg.net_id, nl, n, cfg.k, cfg.weight, cfg.bias, cfg.ymax,
+                                 threads=THREADS)
+    assert o.categories().size == sample.size
+    np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
