@@ -68,7 +68,10 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
  * A column may hold at most 4096 sources. Each layer may be loaded once. The call copies the data
  * into device memory it owns (allocated here, on the current device) and packs it into the layout
  * the kernels read; it synchronizes `hip_stream` (a hipStream_t, or NULL for the default stream)
- * before returning. */
+ * before returning. Columns of a one-weight layer with 32 sources that share their source list (and
+ * so their output) are computed once when the next layer is loaded right after it, in the same call
+ * or the next one; loading layers in ascending order therefore never costs speed, and any order
+ * gives the same results. */
 sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_t *col_ptr,
                              const int32_t *row_idx, const float *val, const float *bias,
                              void *hip_stream);
