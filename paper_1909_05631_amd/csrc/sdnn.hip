@@ -2031,6 +2031,10 @@ struct LayerDev {
   // layer 0 of a uniform layer with K == 32: the lists of ell16 (and ell16c) with each column's
   // sources reordered for the counting kernel, whose counts do not depend on the order
   const uint4 *ell16s = nullptr, *ell16cs = nullptr;
+  // widths staged in LDS: the positions of ell16 (and of ell16c) reordered for the fused kernel
+  // (see conflict_grouped_order): gcols[p] is the column at position p, gell16 its sources
+  const int *gcols = nullptr, *gcolsc = nullptr;
+  const uint4 *gell16 = nullptr, *gell16c = nullptr;
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2368,6 +2372,53 @@ std::vector<uint16_t> bank_balanced_lists(const uint16_t *src, int D, int wbytes
     }
   });
   return out;
+}
+
+// Column order for the fused LDS kernel with 4-row tiles: a wave's 16-byte LDS read of one source
+// slot is served 16 lanes (16 consecutive positions) at a time, and reads of different rows in the
+// same 16-byte bank group (source mod 16 for 16-byte rows) are served one after another. The fp32
+// chain fixes the order of a column's sources, but which columns share a read is free, so positions
+// are filled in groups of 16: each group starts from a remaining column and repeatedly takes, among
+// 128 sampled remaining columns, the one whose sources add the fewest collisions over the 32 slots.
+// lists: D x 32 sources by position; returns the positions' new order.
+std::vector<int32_t> conflict_grouped_order(const std::vector<uint16_t> &lists, int D) {
+  std::vector<int32_t> order, rem((size_t)D);
+  order.reserve((size_t)D);
+  for (int i = 0; i < D; ++i) rem[(size_t)i] = i;
+  uint64_t st = 0x5DEECE66Dull + (uint64_t)D;
+  auto next = [&]() {  // SplitMix64
+    uint64_t z = (st += 0x9E3779B97F4A7C15ull);
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  };
+  auto take = [&](size_t idx) {
+    const int32_t c = rem[idx];
+    rem[idx] = rem.back();
+    rem.pop_back();
+    return c;
+  };
+  while (!rem.empty()) {
+    uint8_t load[32][16] = {};
+    auto add = [&](int32_t c) {
+      for (int sl = 0; sl < 32; ++sl) ++load[sl][lists[(size_t)c * 32 + sl] & 15u];
+      order.push_back(c);
+    };
+    add(take((size_t)(next() % rem.size())));
+    for (int g = 1; g < 16 && !rem.empty(); ++g) {
+      size_t best = 0;
+      int bcost = 1 << 30;
+      for (int t = 0; t < 128; ++t) {
+        const size_t idx = (size_t)(next() % rem.size());
+        const uint16_t *l = lists.data() + (size_t)rem[idx] * 32;
+        int cost = 0;
+        for (int sl = 0; sl < 32; ++sl) cost += load[sl][l[sl] & 15u];
+        if (cost < bcost) { bcost = cost; best = idx; }
+      }
+      add(take(best));
+    }
+  }
+  return order;
 }
 
 // Layer 0 of a uniform layer by counting (see k_layer_count): dictionary, then the counts as codes
@@ -2844,6 +2895,71 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       ld.ell16s = reinterpret_cast<const uint4 *>(mb);
       ld.ell16cs = D0 ? reinterpret_cast<const uint4 *>(mb + fb) : nullptr;
     }
+    // widths staged in LDS: positions in groups for the fused kernel, over all columns and over the
+    // distinct columns
+    if (net->path == 0) {
+      std::vector<int32_t> gsel;
+      for (int32_t i = 0; i < nl; ++i)
+        if (net->layers[(size_t)l0 + i].ell16) gsel.push_back(i);
+      const size_t ng = gsel.size();
+      std::vector<std::vector<int32_t>> gcol(2 * ng);   // [2q]: all columns, [2q + 1]: distinct ones
+      std::vector<std::vector<uint16_t>> gl(2 * ng);    // their [4][D][8] lists
+      parallel_for((int32_t)(2 * ng), [&](int32_t u) {
+        const int32_t i = gsel[(size_t)u / 2];
+        const LayerDev &ld = net->layers[(size_t)l0 + i];
+        std::vector<int32_t> pos;
+        if (u % 2 == 0) {
+          pos.resize((size_t)N);
+          for (int32_t j = 0; j < N; ++j) pos[(size_t)j] = j;
+        } else if (ld.cols) {
+          for (int32_t j = 0; j < N; ++j)
+            if (reps[(size_t)i][(size_t)j] == j) pos.push_back(j);
+        }
+        if (pos.empty()) return;
+        const int64_t *cp = col_ptr + (size_t)i * (N + 1);
+        const int D = (int)pos.size();
+        std::vector<uint16_t> lists((size_t)D * 32);
+        for (int p = 0; p < D; ++p)
+          for (int sl = 0; sl < 32; ++sl) lists[(size_t)p * 32 + sl] = (uint16_t)src_at(i, cp[pos[(size_t)p]] + sl);
+        const std::vector<int32_t> ord = conflict_grouped_order(lists, D);
+        std::vector<int32_t> &gc = gcol[(size_t)u];
+        std::vector<uint16_t> &g16 = gl[(size_t)u];
+        gc.resize((size_t)D);
+        g16.resize((size_t)D * 32);
+        for (int p = 0; p < D; ++p) {
+          const int32_t q = ord[(size_t)p];
+          gc[(size_t)p] = pos[(size_t)q];
+          for (int sl = 0; sl < 32; ++sl) g16[((size_t)(sl / 8) * D + p) * 8 + sl % 8] = lists[(size_t)q * 32 + sl];
+        }
+      });
+      size_t bytes = 0;
+      std::vector<size_t> co(2 * ng), lo(2 * ng);
+      for (size_t u = 0; u < 2 * ng; ++u) {
+        co[u] = bytes;
+        bytes += align_up(gcol[u].size() * sizeof(int32_t), 256);
+        lo[u] = bytes;
+        bytes += align_up(gl[u].size() * sizeof(uint16_t), 256);
+      }
+      if (bytes) {
+        char *mg = nullptr;
+        e = hipMalloc(reinterpret_cast<void **>(&mg), bytes);
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+        }
+        net->allocations.push_back(mg);
+        for (size_t u = 0; u < 2 * ng; ++u) {
+          if (gcol[u].empty()) continue;
+          HIP_OR_POISON(net, hipMemcpy(mg + co[u], gcol[u].data(), gcol[u].size() * sizeof(int32_t), hipMemcpyHostToDevice));
+          HIP_OR_POISON(net, hipMemcpy(mg + lo[u], gl[u].data(), gl[u].size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+          LayerDev &ld = net->layers[(size_t)l0 + gsel[u / 2]];
+          const int *gc = reinterpret_cast<const int *>(mg + co[u]);
+          const uint4 *g16 = reinterpret_cast<const uint4 *>(mg + lo[u]);
+          if (u % 2 == 0) { ld.gcols = gc; ld.gell16 = g16; }
+          else { ld.gcolsc = gc; ld.gell16c = g16; }
+        }
+      }
+    }
     // a layer whose successor reads its representatives only may skip its duplicates; so may the
     // last layer (the final rows are expanded through its representatives)
     for (int32_t i = 0; i < nl; ++i) {
@@ -2873,8 +2989,10 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     for (int32_t l = t0; l < l0 + nl; ++l) {
       const LayerDev &ld = net->layers[(size_t)l];
       const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
-      hp[(size_t)(l - t0)] = LayerPtr{ld.ell, dd ? ld.ell16c : ld.ell16, ld.bias, dd ? ld.cols : nullptr, ld.w, ld.K,
-                                      dd ? ld.D : N};
+      // the fused kernel reads the positions in their grouped order where there is one
+      const uint4 *e16 = dd ? (ld.gell16c ? ld.gell16c : ld.ell16c) : (ld.gell16 ? ld.gell16 : ld.ell16);
+      const int *cl = dd ? (ld.gell16c ? ld.gcolsc : ld.cols) : (ld.gell16 ? ld.gcols : nullptr);
+      hp[(size_t)(l - t0)] = LayerPtr{ld.ell, e16, ld.bias, cl, ld.w, ld.K, dd ? ld.D : N};
     }
     HIP_OR_POISON(net, hipMemcpy(net->lp_dev + t0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
   }
