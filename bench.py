@@ -225,7 +225,7 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU share of the "
+        print("bench.py runs on one GPU only: it measures the single-GPU share of the "
               "data-parallel path (inputs split across GPUs, weights replicated); use --gpus 1.",
               file=sys.stderr)
         return 2
