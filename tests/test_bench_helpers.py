@@ -45,3 +45,23 @@ def test_committed_records_follow_the_kernel_source(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "kernel_source_sha", lambda: "def")  # source changed since
     assert bench.committed_traffic("w", "k_layer_gfm_u8") is None
     assert bench.committed_lds("w", "k_layer_gfm_u8") is None
+
+
+def test_more_than_one_gpu_is_refused():
+    """The benchmark measures one GPU's share; asking for more exits with a message, touching no GPU."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU only" in r.stderr and r.stdout == ""
+
+
+def test_workload_names():
+    import synth
+    c4 = synth.CONFIGS[4]
+    assert bench.workload(c4, "strokes", 0) is c4
+    assert bench.workload(c4, "alllive", 16).name == "alllive-n65536-l16-m60000"
+    assert bench.workload(c4, "alllive", 16).total_nnz == 16 * c4.nnz_per_layer
+    assert bench.workload_name(bench.workload(synth.CONFIGS[2], "strokes", 40), "radix") == "radix-n4096-l40-m60000"
