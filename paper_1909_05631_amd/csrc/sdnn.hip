@@ -2032,9 +2032,10 @@ struct LayerDev {
   // sources reordered for the counting kernel, whose counts do not depend on the order
   const uint4 *ell16s = nullptr, *ell16cs = nullptr;
   // widths staged in LDS: the positions of ell16 (and of ell16c) reordered for the fused kernel
-  // (see conflict_grouped_order): gcols[p] is the column at position p, gell16 its sources
-  const int *gcols = nullptr, *gcolsc = nullptr;
-  const uint4 *gell16 = nullptr, *gell16c = nullptr;
+  // with tiles of 4 << c rows (c = 0 also serves 1 and 2; see conflict_grouped_order): gcols[c][p]
+  // is the column at position p, gell16[c] its sources
+  const int *gcols[3] = {}, *gcolsc[3] = {};
+  const uint4 *gell16[3] = {}, *gell16c[3] = {};
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2057,7 +2058,9 @@ struct sdnn_net {
   std::vector<int32_t> prev_rep;
   int32_t prev_rep_layer = -1;
   std::vector<int32_t> last_rep;  // the same for layer L - 1 (final rows are expanded through it)
-  LayerPtr *lp_dev = nullptr;  // device table of the layers, for launches that run several layers
+  // device tables of the layers, for launches that run several layers: one per fused tile height
+  // class (4 << c rows; class 0 also for 1 and 2 rows)
+  LayerPtr *lp_dev[3] = {};
   int32_t n_loaded = 0;
   // last run
   bool ran = false;
@@ -2374,14 +2377,16 @@ std::vector<uint16_t> bank_balanced_lists(const uint16_t *src, int D, int wbytes
   return out;
 }
 
-// Column order for the fused LDS kernel with 4-row tiles: a wave's 16-byte LDS read of one source
-// slot is served 16 lanes (16 consecutive positions) at a time, and reads of different rows in the
-// same 16-byte bank group (source mod 16 for 16-byte rows) are served one after another. The fp32
-// chain fixes the order of a column's sources, but which columns share a read is free, so positions
-// are filled in groups of 16: each group starts from a remaining column and repeatedly takes, among
-// 128 sampled remaining columns, the one whose sources add the fewest collisions over the 32 slots.
+// Column order for the fused LDS kernel: a wave's 16-byte LDS reads of one source slot are served
+// 16 lanes at a time, and reads of different rows in the same 16-byte bank group are served one
+// after another. With B-row tiles (B = 4, 8, 16) an output takes B / 4 lanes, so a cycle serves
+// G = 64 / B consecutive positions, and row k covers bank groups (B / 4) k .. (B / 4) k + B / 4 - 1
+// mod 16: two of the G columns collide when their sources agree mod G. The fp32 chain fixes the
+// order of a column's sources, but which columns share a read is free, so positions are filled in
+// groups of G: each group starts from a remaining column and repeatedly takes, among 128 sampled
+// remaining columns, the one whose sources add the fewest collisions over the 32 slots.
 // lists: D x 32 sources by position; returns the positions' new order.
-std::vector<int32_t> conflict_grouped_order(const std::vector<uint16_t> &lists, int D) {
+std::vector<int32_t> conflict_grouped_order(const std::vector<uint16_t> &lists, int D, int G) {
   std::vector<int32_t> order, rem((size_t)D);
   order.reserve((size_t)D);
   for (int i = 0; i < D; ++i) rem[(size_t)i] = i;
@@ -2401,18 +2406,18 @@ std::vector<int32_t> conflict_grouped_order(const std::vector<uint16_t> &lists, 
   while (!rem.empty()) {
     uint8_t load[32][16] = {};
     auto add = [&](int32_t c) {
-      for (int sl = 0; sl < 32; ++sl) ++load[sl][lists[(size_t)c * 32 + sl] & 15u];
+      for (int sl = 0; sl < 32; ++sl) ++load[sl][lists[(size_t)c * 32 + sl] % (unsigned)G];
       order.push_back(c);
     };
     add(take((size_t)(next() % rem.size())));
-    for (int g = 1; g < 16 && !rem.empty(); ++g) {
+    for (int g = 1; g < G && !rem.empty(); ++g) {
       size_t best = 0;
       int bcost = 1 << 30;
       for (int t = 0; t < 128; ++t) {
         const size_t idx = (size_t)(next() % rem.size());
         const uint16_t *l = lists.data() + (size_t)rem[idx] * 32;
         int cost = 0;
-        for (int sl = 0; sl < 32; ++sl) cost += load[sl][l[sl] & 15u];
+        for (int sl = 0; sl < 32; ++sl) cost += load[sl][l[sl] % (unsigned)G];
         if (cost < bcost) { bcost = cost; best = idx; }
       }
       add(take(best));
@@ -2523,7 +2528,8 @@ hipError_t launch_layers_lds_b(sdnn_net *net, const float *yin, float *yout, int
   while ((1 << shift) < net->B * (int)sizeof(float)) ++shift;
   const size_t lds = (size_t)2 * net->N * B * sizeof(float);
   const int grid = (int)std::max<int64_t>(1, (rows + B - 1) / B);
-  hipLaunchKernelGGL(k_layers_lds<B>, dim3(grid), dim3(1024), lds, net->stream, yin, yout, net->N, net->lp_dev, l0,
+  const LayerPtr *lp = net->lp_dev[B >= 16 ? 2 : (B == 8 ? 1 : 0)];  // the table grouped for this height
+  hipLaunchKernelGGL(k_layers_lds<B>, dim3(grid), dim3(1024), lds, net->stream, yin, yout, net->N, lp, l0,
                      net->L, net->ymax, ids, count, net->counts, net->masks, shift);
   return hipGetLastError();
 }
@@ -2898,14 +2904,19 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     // widths staged in LDS: positions in groups for the fused kernel, over all columns and over the
     // distinct columns
     if (net->path == 0) {
+      // one order per fused tile-height class the width allows (4 << c rows)
+      int nclass = 1;
+      while (nclass < 3 && (4 << nclass) <= fused_rows_max(net)) ++nclass;
       std::vector<int32_t> gsel;
       for (int32_t i = 0; i < nl; ++i)
         if (net->layers[(size_t)l0 + i].ell16) gsel.push_back(i);
-      const size_t ng = gsel.size();
-      std::vector<std::vector<int32_t>> gcol(2 * ng);   // [2q]: all columns, [2q + 1]: distinct ones
+      const size_t ng = gsel.size() * (size_t)nclass;
+      // u = (q * nclass + c) * 2 + v: layer gsel[q], class c, v = 0 all columns / 1 distinct ones
+      std::vector<std::vector<int32_t>> gcol(2 * ng);
       std::vector<std::vector<uint16_t>> gl(2 * ng);    // their [4][D][8] lists
       parallel_for((int32_t)(2 * ng), [&](int32_t u) {
-        const int32_t i = gsel[(size_t)u / 2];
+        const int32_t i = gsel[(size_t)u / 2 / (size_t)nclass];
+        const int cls = (u / 2) % nclass;
         const LayerDev &ld = net->layers[(size_t)l0 + i];
         std::vector<int32_t> pos;
         if (u % 2 == 0) {
@@ -2921,7 +2932,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         std::vector<uint16_t> lists((size_t)D * 32);
         for (int p = 0; p < D; ++p)
           for (int sl = 0; sl < 32; ++sl) lists[(size_t)p * 32 + sl] = (uint16_t)src_at(i, cp[pos[(size_t)p]] + sl);
-        const std::vector<int32_t> ord = conflict_grouped_order(lists, D);
+        const std::vector<int32_t> ord = conflict_grouped_order(lists, D, 16 >> cls);
         std::vector<int32_t> &gc = gcol[(size_t)u];
         std::vector<uint16_t> &g16 = gl[(size_t)u];
         gc.resize((size_t)D);
@@ -2952,11 +2963,12 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
           if (gcol[u].empty()) continue;
           HIP_OR_POISON(net, hipMemcpy(mg + co[u], gcol[u].data(), gcol[u].size() * sizeof(int32_t), hipMemcpyHostToDevice));
           HIP_OR_POISON(net, hipMemcpy(mg + lo[u], gl[u].data(), gl[u].size() * sizeof(uint16_t), hipMemcpyHostToDevice));
-          LayerDev &ld = net->layers[(size_t)l0 + gsel[u / 2]];
+          LayerDev &ld = net->layers[(size_t)l0 + gsel[u / 2 / (size_t)nclass]];
+          const int cls = (int)((u / 2) % (size_t)nclass);
           const int *gc = reinterpret_cast<const int *>(mg + co[u]);
           const uint4 *g16 = reinterpret_cast<const uint4 *>(mg + lo[u]);
-          if (u % 2 == 0) { ld.gcols = gc; ld.gell16 = g16; }
-          else { ld.gcolsc = gc; ld.gell16c = g16; }
+          if (u % 2 == 0) { ld.gcols[cls] = gc; ld.gell16[cls] = g16; }
+          else { ld.gcolsc[cls] = gc; ld.gell16c[cls] = g16; }
         }
       }
     }
@@ -2972,29 +2984,33 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     net->prev_rep = std::move(reps[(size_t)nl - 1]);
     net->prev_rep_layer = net->prev_rep.empty() ? -1 : l0 + nl - 1;
   }
-  // the device table of layers (for launches that run several layers)
-  if (!net->lp_dev) {
-    e = hipMalloc(reinterpret_cast<void **>(&net->lp_dev), (size_t)net->L * sizeof(LayerPtr));
+  // the device tables of layers (for launches that run several layers), one per tile-height class
+  if (!net->lp_dev[0]) {
+    LayerPtr *t = nullptr;
+    e = hipMalloc(reinterpret_cast<void **>(&t), (size_t)3 * net->L * sizeof(LayerPtr));
     if (e != hipSuccess) {
       (void)hipGetLastError();
-      net->lp_dev = nullptr;
       return fail(SDNN_ENOMEM, "hipMalloc of the layer table failed: %s", hipGetErrorString(e));
     }
-    net->allocations.push_back(net->lp_dev);
+    net->allocations.push_back(t);
+    for (int c = 0; c < 3; ++c) net->lp_dev[c] = t + (size_t)c * net->L;
   }
   {
     // from layer l0 - 1 when this load let it skip its duplicate columns
     const int32_t t0 = (l0 > 0 && net->layers[(size_t)l0 - 1].dedup_ok) ? l0 - 1 : l0;
     std::vector<LayerPtr> hp((size_t)(l0 + nl - t0));
-    for (int32_t l = t0; l < l0 + nl; ++l) {
-      const LayerDev &ld = net->layers[(size_t)l];
-      const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
-      // the fused kernel reads the positions in their grouped order where there is one
-      const uint4 *e16 = dd ? (ld.gell16c ? ld.gell16c : ld.ell16c) : (ld.gell16 ? ld.gell16 : ld.ell16);
-      const int *cl = dd ? (ld.gell16c ? ld.gcolsc : ld.cols) : (ld.gell16 ? ld.gcols : nullptr);
-      hp[(size_t)(l - t0)] = LayerPtr{ld.ell, e16, ld.bias, cl, ld.w, ld.K, dd ? ld.D : N};
+    for (int c = 0; c < 3; ++c) {
+      for (int32_t l = t0; l < l0 + nl; ++l) {
+        const LayerDev &ld = net->layers[(size_t)l];
+        const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
+        // the fused kernel reads the positions in their grouped order where there is one
+        const uint4 *g16 = dd ? ld.gell16c[c] : ld.gell16[c];
+        const uint4 *e16 = g16 ? g16 : (dd ? ld.ell16c : ld.ell16);
+        const int *cl = g16 ? (dd ? ld.gcolsc[c] : ld.gcols[c]) : (dd ? ld.cols : nullptr);
+        hp[(size_t)(l - t0)] = LayerPtr{ld.ell, e16, ld.bias, cl, ld.w, ld.K, dd ? ld.D : N};
+      }
+      HIP_OR_POISON(net, hipMemcpy(net->lp_dev[c] + t0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
     }
-    HIP_OR_POISON(net, hipMemcpy(net->lp_dev + t0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
   }
   net->n_loaded += nl;
   g_err.clear();
