@@ -398,6 +398,24 @@ def test_structured_duplicate_columns(order):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("n,m", [(4096, 900), (2048, 1800), (1024, 3000)])
+def test_fused_tile_heights(n, m):
+    """Rows that stay live (Bernoulli(0.6) inputs) reach the launch that runs every remaining layer
+    once two layers have kept 90% of them, with tiles of 4, 8 or 16 rows per workgroup for these
+    widths and row counts; each height reads its own grouped column order."""
+    nl = 8
+    rng = np.random.default_rng(n + m)
+    y0 = (rng.random((m, n)) < 0.6).astype(np.float32)
+    cp, ri, v = synth.layers_csc(14, 0, nl, n)
+    layers = [(cp[l], ri, v, np.full(n, -0.35, np.float32)) for l in range(nl)]
+    log(f"fused tile heights n={n} m={m} layers={nl}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
+    log(f"kinds {kinds}")
+    assert kinds[-1] == "k_layers_lds" and cats.size == m
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("case", ["tiles", "counted", "last-fused"])
 def test_structured_lds_columns(case):
     """Structured networks on widths staged in LDS: one column per group of equal columns in the
