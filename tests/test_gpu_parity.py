@@ -398,6 +398,26 @@ def test_structured_duplicate_columns(order):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("n", [4096, 5001])
+def test_maximum_column_degree(n):
+    """A column may hold up to 4096 sources, and the ELL width is a layer's largest degree: one
+    column of each layer takes 4096 sources, the others 0 to 8; signed weights, biases of both
+    signs, on both kernel paths (LDS tiles at 4096, global tiles at 5001)."""
+    rng = np.random.default_rng(n)
+    nl, m = 3, 40
+    layers = []
+    for _ in range(nl):
+        deg = rng.integers(0, 9, size=n)
+        deg[rng.integers(n)] = 4096
+        cp, ri, v = synth.random_csc(rng, n, deg, -1.0, 1.0)
+        layers.append((cp, ri, v, rng.uniform(-0.3, 0.3, size=n).astype(np.float32)))
+    y0 = (rng.random((m, n)) < 0.5).astype(np.float32) * rng.uniform(0, 2, (m, n)).astype(np.float32)
+    log(f"maximum column degree n={n} m={m}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert gpu.net.kernel_path == (0 if n <= 4096 else 1)
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("n,m", [(4096, 900), (2048, 1800), (1024, 3000)])
 def test_fused_tile_heights(n, m):
     """Rows that stay live (Bernoulli(0.6) inputs) reach the launch that runs every remaining layer
