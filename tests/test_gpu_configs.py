@@ -118,3 +118,27 @@ def test_all_live_sampled_rows(ci, nl):
                                  threads=THREADS)
     assert o.categories().size == sample.size
     np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
+
+
+def test_many_rows_sampled():
+    """Five times the configs' row count (300,000 inputs of the 1024-neuron, 120-layer network):
+    live lists longer than one compaction pass covers, a layer 0 by counts over 2^28 inputs; a
+    seeded sample of rows recomputed by the oracle, invariants on all rows."""
+    cfg = synth.CONFIGS[1]
+    m = 300_000
+    y0 = synth.config_inputs(cfg, 0, m)
+    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax)
+    gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
+    log(f"{m} rows of {cfg.name}: running the GPU")
+    cats = gpu.run(y0)
+    counts = gpu.net.live_counts()
+    log(f"{cats.size} categories; live counts {counts[:8].tolist()}")
+    assert (np.diff(counts) <= 0).all() and counts[0] == int((y0 != 0).any(axis=1).sum()) and cats.size == counts[-1]
+    rng = np.random.default_rng(7)
+    sample = np.sort(rng.choice(m, size=1000, replace=False))
+    o = oracle.run_config_layers(y0[sample], cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
+                                 cfg.ymax, threads=THREADS)
+    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
+    assert (oracle.padded_live_counts(o, cfg.n_layers) <= counts).all()
+    if o.categories().size:
+        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
