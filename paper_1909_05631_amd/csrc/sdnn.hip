@@ -7,25 +7,28 @@
 // categories: rows with any entry > 0 (Sec. V).
 //
 // Data layout in HBM
-//   Activations: row-major [M][N] fp32, indexed by input row id. Layer 0 reads the caller's y0;
-//   layers then ping-pong between two workspace buffers. A list of live row ids (ascending) selects
-//   which rows a layer reads; rows off the list are never touched again.
-//   Weights: per layer a slot-major ELL table [K][N] of (byte offset of the source row in the
-//   kernel's tile, fp32 weight) pairs: entry [s][j] is the s-th smallest source of output j, padded
-//   with (0, 0.0f) past the column's degree. Padding adds fma(y, 0, acc) = acc exactly because
-//   activations are finite. Slot-major order makes the entries a wave needs for one slot contiguous.
+//   Activations: path 0 (widths whose tiles fit LDS, N <= 4096) keeps row-major [M][N] fp32 rows
+//   and a list of live row ids; path 1 keeps feature-major tiles of 32 list positions ([N][32] fp32
+//   per tile, 128 bytes per source), or after layer 0 one-byte dictionary codes in tiles of 64 or
+//   128 positions, or bit tiles of 16 or 32 positions for binary inputs.
+//   Weights: per layer a slot-major ELL table [K][N] of (source offset, fp32 weight), entry [s][j]
+//   the s-th smallest source of output j, padded with (0, 0.0f); padding adds fma(y, 0, acc) = acc
+//   exactly. One-weight layers with 32 sources per column also get 16-bit source lists, [32][N]
+//   (path 1) and [4][N][8] (eight per 16-byte load), and, where columns share their list, the
+//   representative columns' lists alone.
 //
-// Kernels
-//   k_layer_lds<B>: one workgroup takes a tile of B live rows, stages it in LDS transposed to
-//     [k][B] (feature-major, so the B values of one source are contiguous), then every output j is
-//     computed by B/4 lanes, each holding 4 rows: one 16-byte LDS read per term serves 4 rows, and
-//     the term order is the ELL order (ascending source). Bias, ReLU and the YMAX clamp are applied
-//     before the store; a row's liveness is OR-reduced in LDS and written once per tile.
-//   k_to_fm + k_layer_gfm (widths whose tile does not fit LDS): the live rows are first copied into
-//     feature-major tiles of 32 rows in global memory ([N][32] per tile, 128 bytes per source), then
-//     workgroups gather 128-byte segments from a tile that stays resident in the L2 of the XCD that
-//     works on it (workgroup ids are mapped so that one XCD's workgroups share a tile).
-//   k_compact: stable compaction of the live-row list (wave ballot + prefix count).
+// Kernels (every output is the ascending-source fma chain above, so every path gives the same bits)
+//   path 0: k_layer_lds (one layer; B rows staged in LDS as [k][B]), k_layers_lds (every remaining
+//     layer in one launch, each workgroup's rows resident in LDS), layer 0 by counts of bit tiles.
+//   path 1, layer 0: k_pack_bits, then k_count_dict + k_layer_count (one-weight layers: adder-tree
+//     counts of set source bits, decoded by a dictionary) or k_layer_bits; non-binary inputs take
+//     k_to_fm + k_layer_gfm.
+//   path 1, later layers: k_layer_gfm_u8 (code tiles in), k_layer_gfm (fp32 tiles in),
+//     k_layer_gfm_small (at most 8 tiles, whole chains in flight). Workgroups are mapped so that
+//     each XCD gathers from its own tile, resident in its L2.
+//   Between layers: liveness words per tile (spread over cache lines, or per-workgroup partial
+//   words), k_compact (stable compaction of the live list), k_repack / k_repack_u8 (regroup live
+//   positions into fewer tiles), k_final_ids.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
