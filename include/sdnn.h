@@ -4,7 +4,7 @@
  * Computes the Sparse DNN Challenge inference of Kepner et al. (2019):
  *   Sec. II, batched inference equation:  Y_{l+1} = h(Y_l W_l + B_l), with h(y) = min(YMAX, max(y, 0))
  *   (ReLU with the challenge's upper limit, Sec. II; YMAX = 32 in the Sec. V listing), the bias added
- *   where Y_l W_l is nonzero (Sec. V listing: Y = Z + logical(Z).*b), for every layer l = 0..L-1;
+ *   only where Y_l W_l is nonzero (the Sec. V serial loop), for every layer l = 0..L-1;
  *   then the categories: the rows of the final Y with any entry > 0 (Sec. V, second timed step).
  *
  * Numerics: fp32. Every output is z = fma(y_{k_m}, w_m, ... fma(y_{k_0}, w_0, +0)) over the sources of

@@ -55,6 +55,8 @@ def lib():
         L.oracle_rows.restype = None
         L.oracle_margin.argtypes = [vp, vp]
         L.oracle_margin.restype = ctypes.c_double
+        L.oracle_min_final_rowmax.argtypes = [vp]
+        L.oracle_min_final_rowmax.restype = ctypes.c_double
         _lib = L
     return _lib
 
@@ -126,9 +128,15 @@ class Oracle:
         return out
 
     def margin(self) -> tuple[float, np.ndarray]:
+        """(min |z + b| over every layer applied so far and every entry with z != 0, the same per
+        row); +inf where no such entry was seen."""
         per = np.empty(max(self.m, 1), dtype=np.float64)
         m = lib().oracle_margin(self._h, _p(per))
         return float(m), per[: self.m]
+
+    def min_final_rowmax(self) -> float:
+        """Smallest row maximum of the current Y over the rows that are categories (+inf if none)."""
+        return float(lib().oracle_min_final_rowmax(self._h))
 
 
 def run(y0: np.ndarray, layers, ymax: float = 32.0, threads: int = 1) -> Oracle:

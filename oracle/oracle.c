@@ -7,10 +7,17 @@
  *
  * What it computes
  *   Sec. II, batched inference equation:  Y_{l+1} = h(Y_l W_l + B_l), h = ReLU capped at YMAX = 32.
- *   Sec. V, serial reference loop: for each layer, Z = Y*W; Y = Z + logical(Z).*b; Y(Y<0) = 0;
- *   Y(Y>YMAX) = YMAX. The bias is added only where Z is nonzero. (Sec. II writes B_l as the bias
- *   replicated over the nonzero rows of Y_l; for the nonpositive biases of Table 1 the two agree.)
+ *   Sec. V, serial reference loop: each layer forms the product Z of the activations and the
+ *   weights, adds the bias only to the entries of Z that are nonzero, and clamps the result to
+ *   [0, YMAX]. (Sec. II writes B_l as the bias replicated over the nonzero rows of Y_l; for the
+ *   nonpositive biases of Table 1 the two readings agree.)
  *   Sec. V, second timed step: the categories are the rows of the final Y with any entry > 0.
+ *
+ * Two diagnostics beside the result (test infrastructure for judging fp32 against other orders or
+ * precisions): the margin, min |z + b| over every layer and every entry whose product z is nonzero,
+ * per row and overall (an entry this close to the clamp at 0 may flip under a different rounding);
+ * and the smallest row maximum of the final Y over the rows that are categories (how far the
+ * weakest category is from being dropped).
  *
  * Precision and order. The paper does not fix a precision (its Matlab listing runs in Matlab's
  * double sparse type); this oracle computes in fp32 with one fixed order so that a correct GPU
@@ -115,7 +122,7 @@ static void *layer_rows(void *arg) {
         acc[j] = fmaf(yk, J->tw[e], acc[j]);
       }
     }
-    /* Y = Z + logical(Z).*b, then the clamps to [0, YMAX] */
+    /* bias on the nonzero entries of Z only, then the clamps to [0, YMAX] (Sec. V loop) */
     uint8_t any = 0;
     double m = o->margin[i];
     for (int32_t j = 0; j < N; ++j) {
@@ -234,6 +241,20 @@ double oracle_margin(void *h, double *per_row) {
   for (int64_t i = 0; i < o->M; ++i) {
     if (per_row) per_row[i] = o->margin[i];
     if (o->margin[i] < m) m = o->margin[i];
+  }
+  return m;
+}
+
+/* Smallest row maximum of the current Y over the rows with any entry > 0 (the categories);
+   +infinity when there is none. */
+double oracle_min_final_rowmax(void *h) {
+  oracle_t *o = (oracle_t *)h;
+  double m = INFINITY;
+  for (int64_t i = 0; i < o->M; ++i) {
+    const float *r = o->y + (size_t)i * o->N;
+    float mx = 0.0f;
+    for (int32_t j = 0; j < o->N; ++j) mx = r[j] > mx ? r[j] : mx;
+    if (mx > 0.0f && (double)mx < m) m = (double)mx;
   }
   return m;
 }

@@ -92,7 +92,8 @@ void parallel_for(int32_t n, F f) {
 // Device code
 
 __device__ __forceinline__ float activate(float z, float b, float ymax) {
-  // Sec. V: Y = Z + logical(Z).*b; Y(Y<0) = 0; Y(Y>YMAX) = YMAX. Zeros come out as +0.
+  // Sec. V loop: the bias goes only to nonzero products, then the result is clamped to [0, ymax].
+  // Zeros come out as +0.
   if (z == 0.0f) return 0.0f;
   const float t = z + b;
   return t > ymax ? ymax : (t > 0.0f ? t : 0.0f);

@@ -27,7 +27,7 @@ def dense_w(n, col_ptr, row_idx, val, dtype=np.float64):
 
 
 def matlab_layer(Y, W, b, ymax):
-    """Sec. V serial loop, one layer: Z = Y*W; Y = Z + logical(Z).*b; clamp to [0, YMAX]."""
+    """Sec. V serial loop, one layer: the product, the bias on its nonzero entries, the clamp to [0, YMAX]."""
     Z = Y @ W
     Yn = Z + (Z != 0) * b[None, :]
     Yn[Yn < 0] = 0
@@ -313,3 +313,125 @@ def test_threads_do_not_change_results():
         o4.layer(cp[l], ri, v, b, threads=4)
     np.testing.assert_array_equal(o1.rows(np.arange(m)), o4.rows(np.arange(m)))
     np.testing.assert_array_equal(o1.live_counts(), o4.live_counts())
+
+
+# ---- the margin and the smallest final row maximum (diagnostics of the oracle)
+
+def exact_margins(y0, layers, ymax):
+    """Integer networks, evaluated exactly in float64: per row, min |z + b| over every layer and
+    every entry with z != 0 (inf if none), the same with |z| in place of |z + b|, and the last
+    layer's minimum alone; plus the final Y."""
+    Y = y0.astype(np.float64)
+    n = y0.shape[1]
+    best = np.full(y0.shape[0], np.inf)
+    best_z = np.full(y0.shape[0], np.inf)
+    last = np.full(y0.shape[0], np.inf)
+    for (cp, ri, v, b) in layers:
+        Z = Y @ dense_w(n, cp, ri, v)
+        nz = Z != 0
+        T = Z + b.astype(np.float64)[None, :]
+        last = np.where(nz, np.abs(T), np.inf).min(axis=1) if n else last
+        best = np.minimum(best, last)
+        best_z = np.minimum(best_z, np.where(nz, np.abs(Z), np.inf).min(axis=1))
+        Y = np.clip(np.where(nz, T, 0.0), 0.0, ymax)
+    return best, best_z, last, Y
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_margin_on_integer_networks_is_exact(seed):
+    """Every value is a small integer, so |z + b| is exact: the oracle's per-row margins must equal
+    the float64 evaluation exactly. Across the seeds the margin differs from the minimum of |z| and
+    from the last layer's minimum on many rows, so tracking |z|, or restarting at every layer, fails."""
+    rng = np.random.default_rng(3000 + seed)
+    n, m, nl, ymax = int(rng.integers(4, 30)), int(rng.integers(8, 30)), int(rng.integers(2, 6)), 40.0
+    layers = random_int_net(rng, n, nl, max_deg=min(n, 8))
+    y0 = rng.integers(0, 3, size=(m, n)).astype(np.float32)
+    o = oracle.Oracle(y0, ymax)
+    for layer in layers:
+        o.layer(*layer)
+    best, best_z, last, Y = exact_margins(y0, layers, ymax)
+    m_all, per_row = o.margin()
+    np.testing.assert_array_equal(per_row, best)
+    assert m_all == best.min()
+    differs_z = int((best_z != best).sum())
+    differs_last = int((last != best).sum())
+    assert differs_z > 0 or differs_last > 0 or not np.isfinite(best).any()
+    cats = (Y > 0).any(axis=1)
+    expect = Y[cats].max(axis=1).min() if cats.any() else np.inf
+    assert o.min_final_rowmax() == expect
+
+
+def test_margin_planted_mistakes_are_caught():
+    """The integer-network check above, summed over its seeds, sees rows where |z| and |z + b| have
+    different minima and rows whose minimum is reached before the last layer: a margin computed
+    from |z| or restarted per layer cannot pass it."""
+    diff_z = diff_last = 0
+    for seed in range(8):
+        rng = np.random.default_rng(3000 + seed)
+        n, m, nl = int(rng.integers(4, 30)), int(rng.integers(8, 30)), int(rng.integers(2, 6))
+        layers = random_int_net(rng, n, nl, max_deg=min(n, 8))
+        y0 = rng.integers(0, 3, size=(m, n)).astype(np.float32)
+        best, best_z, last, _ = exact_margins(y0, layers, 40.0)
+        diff_z += int((best_z != best).sum())
+        diff_last += int((last != best).sum())
+    assert diff_z > 10 and diff_last > 10
+
+
+def test_margin_single_column_by_hand():
+    """Column 0 sums 1 * 0.5 + 1 * 0.25 = 0.75 and adds b = -0.5: |z + b| = 0.25 (|z| would be 0.75).
+    Column 1 has no source, so z = 0 and its bias -0.1 is not applied: it must not count (it would
+    give 0.1). Column 2 sums 1 * 2 = 2, b = -4: clamped to 0, |z + b| = 2."""
+    n = 3
+    cp = np.array([0, 2, 2, 3], dtype=np.int64)
+    ri = np.array([0, 1, 0], dtype=np.int32)
+    v = np.array([0.5, 0.25, 2.0], dtype=np.float32)
+    b = np.array([-0.5, -0.1, -4.0], dtype=np.float32)
+    o = oracle.Oracle(np.array([[1.0, 1.0, 0.0], [0.0, 0.0, 5.0]], dtype=np.float32), 32.0)
+    o.layer(cp, ri, v, b)
+    m, per_row = o.margin()
+    assert m == 0.25
+    np.testing.assert_array_equal(per_row, [0.25, np.inf])  # row 1 feeds no column: no term at all
+    np.testing.assert_array_equal(o.rows([0, 1]), [[0.25, 0.0, 0.0], [0.0, 0.0, 0.0]])
+    assert o.min_final_rowmax() == 0.25
+
+
+def test_margin_tie_probe_by_hand():
+    """The tie probe at b = -0.30: a constant row c = fp32(0.3)/2 = 5033165 * 2^-25 on the
+    configs' network (32 weights of 1/16 per column). Each product c/16 = 5033165 * 2^-29 is exact;
+    the exact sum of 32 of them is 2c = fp32(0.3), so z + b would be 0, but the sequential fp32
+    sum (recomputed here with numpy float32 scalars, round to nearest even) ends 3 * 2^-25 above
+    it: every entry of layer 1 has |z + b| = 3 * 2^-25 = 8.94e-8. Layer 2 then sums 32 terms of
+    (3 * 2^-25)/16 = 6 * 2^-25 exactly and adds b: |z + b| is about 0.3, so the margin stays at
+    layer 1's value (a per-layer restart would report 0.3), and the row dies."""
+    n = 1024
+    c = np.float32(0.3) / np.float32(2.0)
+    assert Fraction(float(c)) == Fraction(5033165, 2 ** 25)
+    acc = np.float32(0.0)
+    for _ in range(32):
+        acc = np.float32(acc + np.float32(c * np.float32(1.0 / 16.0)))
+    t1 = np.float32(acc + np.float32(-0.30))
+    assert Fraction(float(t1)) == Fraction(3, 2 ** 25)
+    cp, ri, v = synth.layers_csc(1, 0, 2, n)
+    b = np.full(n, -0.30, dtype=np.float32)
+    o = oracle.Oracle(np.full((1, n), c, dtype=np.float32), 32.0)
+    o.layer(cp[0], ri, v, b)
+    assert o.margin()[0] == float(t1)
+    assert o.min_final_rowmax() == float(t1)
+    o.layer(cp[1], ri, v, b)
+    assert o.margin()[0] == float(t1)
+    assert o.live == 0 and o.min_final_rowmax() == np.inf
+
+
+@pytest.mark.parametrize("bias", [-0.30, -0.45])
+def test_min_final_rowmax_closed_form(bias):
+    """An all-ones row saturates at YMAX = 32 from layer 6 on (closed form y_l = min(32, 2^l (1 + b) - b)),
+    so after 8 layers its row maximum is exactly 32, while an all-zero row is never a category."""
+    n = 1024
+    cp, ri, v = synth.layers_csc(1, 0, 8, n)
+    y0 = np.zeros((2, n), dtype=np.float32)
+    y0[1] = 1.0
+    o = oracle.Oracle(y0, 32.0)
+    for l in range(8):
+        o.layer(cp[l], ri, v, np.full(n, bias, dtype=np.float32))
+    np.testing.assert_array_equal(o.categories(), [1])
+    assert o.min_final_rowmax() == 32.0
