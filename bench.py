@@ -8,7 +8,10 @@ already resident in HBM. The metric is the paper's rate (Sec. V, Sec. VI-B):
 
 Workloads are the seeded synthetic stand-ins for the paper's networks and MNIST-derived inputs
 (synth.CONFIGS; Table 1 widths and biases, Table 2 depths). The default is the 65536-neuron,
-1920-layer network on 60,000 inputs.
+1920-layer network on 60,000 inputs, on the library's default kernels, which read every edge's
+weight and every neuron's bias from memory. --equal-value-kernels measures the opt-in kernels that
+exploit the workloads' equal weights and biases instead (a supplementary line: the paper's Sec. V
+lists exploiting repeated weight and bias values among what a submission should avoid).
 
 Prints ONE JSON line on stdout; progress goes to stderr.
 """
@@ -65,8 +68,39 @@ def layer_source(cfg, network: str):
     return lambda l0, nl: synth.layers_csc(cfg.net_id, l0, nl, cfg.n_neurons, cfg.k, cfg.weight)
 
 
-def workload_name(cfg, network: str) -> str:
-    return cfg.name if network == "union" else f"{network}-{cfg.name}"
+def workload_name(cfg, network: str, equal_values: bool = False) -> str:
+    name = cfg.name if network == "union" else f"{network}-{cfg.name}"
+    return name + ("-eqv" if equal_values else "")
+
+
+def host_cpus() -> dict:
+    """The host's CPUs as this process sees them: os.cpu_count() (nproc of the machine), the CPUs in
+    this process's affinity mask, the cgroup CPU quota (cpu.max, if any), the usable count (the
+    smallest of those), and the CPU model string."""
+    nproc = os.cpu_count() or 1
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        affinity = nproc
+    quota = None
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            q, period = f.read().split()[:2]
+        if q != "max":
+            quota = max(1, int(int(q) // int(period)))
+    except (OSError, ValueError):
+        quota = None
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    usable = min(x for x in (nproc, affinity, quota) if x)
+    return {"nproc": nproc, "affinity": affinity, "cgroup_quota": quota, "usable": usable, "model": model}
 
 
 # The supplementary all-live input set: Bernoulli(0.6) rows. Each column sums 32 weights of 1/16,
@@ -125,10 +159,15 @@ def cpu_baseline(cfg, target_s: float, threads: int, network: str = "union", inp
         rows = int(min(cfg.n_rows, max(rows * 2, rows * target_s / max(t, 1e-3))))
         t = run(rows)
     rate = rows * cfg.total_nnz / t
+    cpus = host_cpus()
     return {"value": rate, "unit": "inputs*edges/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpus["model"], "nproc": cpus["nproc"], "affinity_cpus": cpus["affinity"],
+            "cgroup_cpu_quota": cpus["cgroup_quota"],
             "sample": f"first {rows} of {cfg.n_rows} input rows of {workload_name(cfg, network)}, all {cfg.n_layers} layers "
                       f"(rows stop when dead, as on the GPU); {t:.2f} s of oracle layer evaluation on "
-                      f"{threads} host threads"}
+                      f"{threads} host threads (every CPU this process may use: the smallest of nproc "
+                      f"{cpus['nproc']}, its affinity mask {cpus['affinity']} and the cgroup quota "
+                      f"{cpus['cgroup_quota']}); {cpus['model']}"}
 
 
 def calibrate_copy(nbytes: int) -> int:
@@ -214,6 +253,11 @@ def main() -> int:
                     help="the config's stroke images (~19%% ones), or the supplementary all-live set "
                          "(Bernoulli(0.6) rows: every row stays live, so every layer runs at full shape)")
     ap.add_argument("--layers", type=int, default=0, help="run only the first LAYERS layers (0: all)")
+    ap.add_argument("--equal-value-kernels", action="store_true",
+                    help="supplementary: opt in to the kernels that exploit layers whose weights and biases "
+                         "are all equal (sdnn_enable_equal_value_kernels); the workload name gets '-eqv'")
+    ap.add_argument("--profile-steps", type=int, default=2,
+                    help="untimed steps run after the timed ones with per-layer events, for the roofline")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU-baseline time")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true", help="skip the per-layer events (no roofline)")
@@ -241,7 +285,7 @@ def main() -> int:
     torch.cuda.set_device(0)
     cfg = workload(synth.CONFIGS[args.config], args.inputs, args.layers)
     n, L, m = cfg.n_neurons, cfg.n_layers, cfg.n_rows
-    wname = workload_name(cfg, args.network)
+    wname = workload_name(cfg, args.network, args.equal_value_kernels)
     layers = layer_source(cfg, args.network)
     stream = torch.cuda.current_stream()
 
@@ -255,7 +299,7 @@ def main() -> int:
     density = float(y0.mean().item())
     log(f"{wname}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
     t0 = time.time()
-    net = sdnn.Net(n, L, cfg.ymax)
+    net = sdnn.Net(n, L, cfg.ymax, equal_value_kernels=args.equal_value_kernels)
     lchunk = max(1, min(64, (1 << 27) // (n * cfg.k)))
     for l0 in range(0, L, lchunk):
         nl = min(lchunk, L - l0)
@@ -276,10 +320,8 @@ def main() -> int:
     for i in range(args.warmup):
         cats = step()
         log(f"warmup {i}: {cats.size} categories")
-    if not args.no_profile:
-        # events around the large layers only: recording them around every layer of the long tail
-        # would slow the step it measures
-        net.set_profiling(True, large_only=True)
+    # the timed steps run with per-layer events off; the events are taken in a separate pass below
+    net.set_profiling(False)
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
@@ -298,6 +340,12 @@ def main() -> int:
 
     roofline = None
     if not args.no_profile:
+        # untimed pass with HIP events on the library's stream around the large layers only
+        # (recording them around every layer of the long tail would slow what they measure)
+        net.set_profiling(True, large_only=True)
+        for _ in range(max(1, args.profile_steps)):
+            step()
+        net.set_profiling(False)
         # the dominant kernel: the large layer with the most event time; its launches are the rounds
         # (or the pack + layer pair) that the event pair of that layer spans
         ms, runs = net.layer_times()
@@ -346,8 +394,7 @@ def main() -> int:
 
     cpu = None
     if not args.no_cpu_baseline:
-        threads = max(1, min(16, os.cpu_count() or 1))
-        cpu = cpu_baseline(cfg, args.cpu_seconds, threads, args.network, args.inputs)
+        cpu = cpu_baseline(cfg, args.cpu_seconds, host_cpus()["usable"], args.network, args.inputs)
 
     out = {
         "metric": "inference edges/sec (Ninputs*sum nnz(W)/t) + % HBM roofline, 1 MI355X",
@@ -363,6 +410,9 @@ def main() -> int:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wname, "network": "permutation-union" if args.network == "union" else "radix-kronecker",
+                   "kernels": ("supplementary: opt-in kernels exploiting equal weights and biases"
+                               if args.equal_value_kernels else
+                               "default: every edge's weight and every neuron's bias read from memory"),
                    "n_neurons": n, "n_layers": L, "n_rows": m, "bias": cfg.bias,
                    "ymax": cfg.ymax, "connections": cfg.total_nnz, "input_density": round(density, 4),
                    "inputs": "binary stroke images" if args.inputs == "strokes" else

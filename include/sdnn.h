@@ -55,6 +55,16 @@ typedef enum {
  * 1 <= n_neurons <= 65536, 1 <= n_layers <= 1000000. Host-only: touches no device. */
 sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, float ymax);
 
+/* Opt in (enable = 1) to kernels that exploit layers whose weights are all equal and whose biases
+ * are all equal: such a layer is read as one weight, one bias and 16-bit source lists; layer 0 on
+ * binary inputs is computed from counts of active sources; columns that share their source list are
+ * computed once. Results are bit-identical to the default. Off by default, because the paper's
+ * Sec. V lists exploiting the repetitive structure of weight and bias values among the things a
+ * challenge submission should avoid: by default every layer reads each edge's weight and each
+ * neuron's bias from memory. Host-only. Must precede the first sdnn_load_layers (SDNN_ESTATE
+ * afterwards); enable other than 0 or 1 is SDNN_EINVAL. */
+sdnn_status sdnn_enable_equal_value_kernels(sdnn_net *net, int32_t enable);
+
 /* Load layers [l0, l0 + nl) (Sec. V: load the DNN; create the bias vectors b_l).
  * Weights in CSC, one column per output neuron j (Sec. II: W(i, j) != 0 connects neuron i to
  * neuron j, and rows y multiply W from the left, so column j lists the inputs of neuron j):
@@ -68,10 +78,12 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
  * A column may hold at most 4096 sources. Each layer may be loaded once. The call copies the data
  * into device memory it owns (allocated here, on the current device) and packs it into the layout
  * the kernels read; it synchronizes `hip_stream` (a hipStream_t, or NULL for the default stream)
- * before returning. Columns of a one-weight layer with 32 sources that share their source list (and
- * so their output) are computed once when the next layer is loaded right after it, in the same call
- * or the next one; loading layers in ascending order therefore never costs speed, and any order
- * gives the same results. */
+ * before returning. With sdnn_enable_equal_value_kernels on, columns of a one-weight layer with 32
+ * sources that share their source list (and so their output) are computed once when the next layer
+ * is loaded right after it, in the same call or the next one; loading layers in ascending order
+ * therefore never costs speed, and any order gives the same results. The first call on a handle
+ * also creates the host-side objects the timed calls use (read-back events, pinned host words), so
+ * that sdnn_infer and sdnn_categories allocate nothing. */
 sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_t *col_ptr,
                              const int32_t *row_idx, const float *val, const float *bias,
                              void *hip_stream);
@@ -134,7 +146,8 @@ typedef enum {
   SDNN_KERNEL_BITS = 5,                 /* layer 0 from bit-packed binary inputs (k_pack_bits, k_layer_bits) */
   SDNN_KERNEL_BITS_TO_CODES = 6,        /* the same, writing one-byte dictionary codes */
   SDNN_KERNEL_BITS_COUNT = 7,           /* layer 0 of a uniform layer on binary inputs, by bit-sliced counts
-                                           (k_pack_bits, k_count_dict, k_layer_count) */
+                                           (k_pack_bits, k_count_dict, k_layer_count); only with
+                                           sdnn_enable_equal_value_kernels */
   SDNN_KERNEL_LDS_FUSED = 8             /* every layer from this one on, in one launch that keeps each
                                            workgroup's rows in LDS (k_layers_lds); the launch is counted
                                            at its first layer, later layers report 0 launches */

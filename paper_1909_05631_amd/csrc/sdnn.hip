@@ -2055,6 +2055,9 @@ struct sdnn_net {
   int device = -1;
   int cus = 0;
   bool poisoned = false;
+  // kernels that exploit layers whose weights and biases are all equal (opt-in, before any load;
+  // see sdnn_enable_equal_value_kernels)
+  bool equal_value_kernels = false;
   std::vector<LayerDev> layers;
   std::vector<void *> allocations;
   // duplicate columns: representatives of the last layer loaded (rep[j] = smallest column with j's
@@ -2598,6 +2601,16 @@ sdnn_status sdnn_create(sdnn_net **out, int32_t n_neurons, int32_t n_layers, flo
 
 int32_t sdnn_kernel_path(const sdnn_net *net) { return net ? net->path : -1; }
 
+sdnn_status sdnn_enable_equal_value_kernels(sdnn_net *net, int32_t enable) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (enable != 0 && enable != 1) return fail(SDNN_EINVAL, "enable must be 0 or 1");
+  if (net->n_loaded > 0) return fail(SDNN_ESTATE, "layers are already loaded");
+  net->equal_value_kernels = enable != 0;
+  g_err.clear();
+  return SDNN_OK;
+}
+
 sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_t *col_ptr, const int32_t *row_idx,
                              const float *val, const float *bias, void *hip_stream) {
   sdnn_status st = check_usable(net);
@@ -2641,7 +2654,9 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       same_b = same_b && std::memcmp(&bias[(size_t)i * N + j], &bias[(size_t)i * N], sizeof(float)) == 0;
     }
     K[(size_t)i] = std::max(kmax, 1);
-    uniform[(size_t)i] = kmax > 0 && kmin == kmax && same_w && same_b;
+    // the specialisations that read one weight and one bias per layer are opt-in: by default every
+    // layer reads each edge's weight and each neuron's bias from memory, whatever their values
+    uniform[(size_t)i] = net->equal_value_kernels && kmax > 0 && kmin == kmax && same_w && same_b;
   });
   for (int32_t i = 0; i < nl; ++i)
     if (!err[(size_t)i].empty()) return fail(SDNN_EINVAL, "%s", err[(size_t)i].c_str());
@@ -2733,6 +2748,15 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   if (net->device < 0) {
     HIP_OR_POISON(net, hipGetDevice(&net->device));
     HIP_OR_POISON(net, hipDeviceGetAttribute(&net->cus, hipDeviceAttributeMultiprocessorCount, net->device));
+    // the host-side objects sdnn_infer uses (read-back events, pinned read-back slots, the progress
+    // word in coherent host memory), created once here so that the timed calls allocate nothing
+    net->events.resize(4);
+    for (auto &ev : net->events) HIP_OR_POISON(net, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 8 * sizeof(int32_t), hipHostMallocDefault));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->progress), sizeof(unsigned long long),
+                                     hipHostMallocCoherent));
+    *net->progress = 0ull;
+    HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->progress_dev), net->progress, 0));
   } else {
     int dev = -1;
     HIP_OR_POISON(net, hipGetDevice(&dev));
@@ -3331,6 +3355,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       if (fout_codes && net->pinned[5] != 0) {
         // more than 256 distinct values: redo layer 0 with fp32 outputs (same liveness)
         fout_codes = false;
+        net->layer_kernel[0] = SDNN_KERNEL_BITS;
+        net->layer_launches[0] = 3;  // pack + the layer with codes + the layer again with fp32 outputs
         HIP_OR_POISON(net, net->bitsT == 32
                                ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur, false)
                                : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, false));
@@ -3398,9 +3424,20 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   return SDNN_OK;
 }
 
+sdnn_status infer_impl(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
+                       void *hip_stream);
+
 }  // namespace
 
 sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
+                       void *hip_stream) {
+  return infer_impl(net, y0, n_rows, workspace, workspace_bytes, hip_stream);
+}
+
+
+namespace {
+
+sdnn_status infer_impl(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
                        void *hip_stream) {
   sdnn_status st = check_usable(net);
   if (st != SDNN_OK) return st;
@@ -3416,15 +3453,6 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   int dev = -1;
   HIP_OR_POISON(net, hipGetDevice(&dev));
   if (dev != net->device) return fail(SDNN_EINVAL, "current device %d differs from the handle's device %d", dev, net->device);
-  if (net->events.empty()) {
-    net->events.resize(4);
-    for (auto &ev : net->events) HIP_OR_POISON(net, hipEventCreateWithFlags(&ev, hipEventDisableTiming));
-    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->pinned), 8 * sizeof(int32_t), hipHostMallocDefault));
-    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->progress), sizeof(unsigned long long),
-                                     hipHostMallocCoherent));
-    *net->progress = 0ull;
-    HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->progress_dev), net->progress, 0));
-  }
   char *ws = static_cast<char *>(workspace);
   net->M = n_rows;
   ++net->run_gen;
@@ -3468,6 +3496,8 @@ sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   g_err.clear();
   return SDNN_OK;
 }
+
+}  // namespace
 
 sdnn_status sdnn_categories(sdnn_net *net, int64_t *ids, int64_t capacity, int64_t *count) {
   sdnn_status st = check_usable(net);
@@ -3557,7 +3587,7 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
     pos.push_back(srcpos[(size_t)(it - live.begin())]);
     which.push_back(q);
   }
-  float *scratch = (net->final_fm == net->fm[0]) ? net->fm[1] : net->fm[0];
+  float *stage = (net->final_fm == net->fm[0]) ? net->fm[1] : net->fm[0];
   int *dpos = net->ids[net->final_list ^ 1];
   const int64_t batch = std::max<int64_t>(1, net->M);
   for (size_t b0 = 0; b0 < pos.size(); b0 += (size_t)batch) {
@@ -3565,11 +3595,11 @@ sdnn_status sdnn_final_rows(sdnn_net *net, const int64_t *ids, int64_t n, float 
     HIP_OR_POISON(net, hipMemcpy(dpos, pos.data() + b0, (size_t)nb * sizeof(int32_t), hipMemcpyHostToDevice));
     const int64_t items = (int64_t)nb * net->N;
     const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
-    hipLaunchKernelGGL(k_gather_rows, dim3(grid), dim3(256), 0, net->stream, net->final_fm, net->N, dpos, nb, scratch);
+    hipLaunchKernelGGL(k_gather_rows, dim3(grid), dim3(256), 0, net->stream, net->final_fm, net->N, dpos, nb, stage);
     HIP_OR_POISON(net, hipGetLastError());
     HIP_OR_POISON(net, hipStreamSynchronize(net->stream));
     std::vector<float> rows((size_t)nb * net->N);
-    HIP_OR_POISON(net, hipMemcpy(rows.data(), scratch, (size_t)nb * rowb, hipMemcpyDeviceToHost));
+    HIP_OR_POISON(net, hipMemcpy(rows.data(), stage, (size_t)nb * rowb, hipMemcpyDeviceToHost));
     for (int i = 0; i < nb; ++i) {
       float *dst = out_host + (size_t)which[b0 + (size_t)i] * net->N;
       std::memcpy(dst, rows.data() + (size_t)i * net->N, rowb);

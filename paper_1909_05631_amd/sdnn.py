@@ -15,7 +15,7 @@ STATUS = {0: "SDNN_OK", 1: "SDNN_EINVAL", 2: "SDNN_ENOMEM", 3: "SDNN_EDEVICE", 4
 EXPORTED_SYMBOLS = [
     "sdnn_create", "sdnn_load_layers", "sdnn_workspace_bytes", "sdnn_infer", "sdnn_categories",
     "sdnn_live_counts", "sdnn_final_rows", "sdnn_destroy", "sdnn_last_error", "sdnn_kernel_path",
-    "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info",
+    "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info", "sdnn_enable_equal_value_kernels",
 ]
 KERNEL_KINDS = {0: "none", 1: "k_layer_lds", 2: "k_layer_gfm", 3: "k_layer_gfm_u8", 4: "k_layer_gfm_small",
                 5: "k_pack_bits+k_layer_bits", 6: "k_pack_bits+k_layer_bits(codes)", 7: "k_pack_bits+k_layer_count",
@@ -58,8 +58,10 @@ def load_library():
         L.sdnn_set_profiling.argtypes = [vp, i32]
         L.sdnn_layer_times.argtypes = [vp, vp, vp]
         L.sdnn_layer_info.argtypes = [vp, vp, vp]
+        L.sdnn_enable_equal_value_kernels.argtypes = [vp, i32]
         for name in ("sdnn_create", "sdnn_load_layers", "sdnn_infer", "sdnn_categories", "sdnn_live_counts",
-                     "sdnn_final_rows", "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info"):
+                     "sdnn_final_rows", "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info",
+                     "sdnn_enable_equal_value_kernels"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -88,14 +90,19 @@ def _stream_handle(stream) -> int | None:
 
 
 class Net:
-    """A network of `n_layers` layers of `n_neurons` neurons (one libsdnn handle)."""
+    """A network of `n_layers` layers of `n_neurons` neurons (one libsdnn handle).
 
-    def __init__(self, n_neurons: int, n_layers: int, ymax: float = 32.0):
+    equal_value_kernels: opt in to the kernels that exploit layers whose weights and biases are all
+    equal (sdnn_enable_equal_value_kernels); off by default."""
+
+    def __init__(self, n_neurons: int, n_layers: int, ymax: float = 32.0, equal_value_kernels: bool = False):
         L = load_library()
         h = ctypes.c_void_p()
         _check(L.sdnn_create(ctypes.byref(h), n_neurons, n_layers, ymax))
         self._lib = L  # held so that close() still works while the interpreter shuts down
         self._h = h
+        if equal_value_kernels:
+            _check(L.sdnn_enable_equal_value_kernels(h, 1))
         self.n = n_neurons
         self.n_layers = n_layers
         self.ymax = ymax

@@ -1,8 +1,7 @@
 """GPU parity at the full sizes of the five workloads (Table 1 widths and biases, Table 2 depths,
 60,000 inputs as in Sec. IV; 2,000 for the small case), in the launch configuration the benchmark
-times. The two smaller widths are checked against the oracle on every row; the two largest on a
-seeded sample of rows the oracle recomputes on its own (rows are independent, Sec. V), plus the
-invariants that hold for every row."""
+times: every row against the oracle, with exact live counts, categories and surviving rows. The
+all-live set is checked on a seeded sample of rows (its live counts are all M, checked exactly)."""
 import os
 
 import numpy as np
@@ -17,10 +16,10 @@ pytestmark = pytest.mark.gpu
 THREADS = max(1, min(16, os.cpu_count() or 1))
 
 
-def gpu_config_run(cfg):
+def gpu_config_run(cfg, equal_values=False):
     log(f"{cfg.name}: generating inputs")
     y0 = synth.config_inputs(cfg)
-    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax)
+    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax, equal_values)
     log(f"{cfg.name}: loading {cfg.n_layers} layers")
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     log(f"{cfg.name}: running the GPU")
@@ -29,58 +28,47 @@ def gpu_config_run(cfg):
     return y0, gpu, cats
 
 
-@pytest.mark.parametrize("ci", [0, 1, 2])
+@pytest.mark.parametrize("ci", [0, 1, 2, 3, 4])
 def test_full_config_every_row(ci):
+    """Every row of the workload against the oracle (Sec. V: compare the computed categories): the
+    categories, every per-layer live count and every surviving row bit for bit."""
     cfg = synth.CONFIGS[ci]
     y0, gpu, cats = gpu_config_run(cfg)
     log(f"{cfg.name}: oracle on all {cfg.n_rows} rows")
     o = oracle.run_config_layers(y0, cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
                                  cfg.ymax, threads=THREADS)
+    log(f"{cfg.name}: oracle live counts {o.live_counts()[:8].tolist()}, {o.categories().size} categories")
     assert_parity(gpu, o, cats)
 
 
-@pytest.mark.parametrize("ci", [3, 4])
-def test_full_config_sampled_rows(ci):
+@pytest.mark.parametrize("ci", [2, 4])
+def test_full_config_every_row_equal_value_kernels(ci):
+    """The same with the opt-in kernels that exploit the configs' equal weights and biases (layer 0
+    by counts, one weight per layer): the supplementary measurement's path, on every row."""
     cfg = synth.CONFIGS[ci]
-    y0, gpu, cats = gpu_config_run(cfg)
-    counts = gpu.net.live_counts()
-    assert (np.diff(counts) <= 0).all() and counts[0] == int((y0 != 0).any(axis=1).sum())
-    assert cats.size == counts[-1]
-    rng = np.random.default_rng(ci)
-    sample = np.sort(rng.choice(cfg.n_rows, size=1500, replace=False))
-    log(f"{cfg.name}: oracle on {sample.size} sampled rows")
-    o = oracle.run_config_layers(y0[sample], cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
+    y0, gpu, cats = gpu_config_run(cfg, equal_values=True)
+    o = oracle.run_config_layers(y0, cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
                                  cfg.ymax, threads=THREADS)
-    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
-    oc = o.live_counts()
-    # every sampled row's survival layer agrees: counts over the sample can be recomputed from the
-    # oracle alone, and must not exceed the GPU's counts over all rows
-    assert (oracle.padded_live_counts(o, cfg.n_layers) <= counts).all()
-    if o.categories().size:
-        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
-    log(f"{cfg.name}: sample live counts {oc[:6].tolist()}")
+    assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("ci", [2, 3])
-def test_structured_full_config_sampled_rows(ci):
+def test_structured_full_config_every_row(ci, equal_values):
     """The second workload: structured (RadiX-Net style) layers of the config's width and depth on the
-    config's inputs, full size on the GPU; a seeded sample of rows recomputed by the oracle."""
+    config's inputs, full size on the GPU, every row against the oracle."""
     cfg = synth.CONFIGS[ci]
     n, L = cfg.n_neurons, cfg.n_layers
     y0 = synth.config_inputs(cfg)
-    gpu = GpuRun(n, L, cfg.ymax)
-    log(f"radix-{cfg.name}: loading {L} structured layers")
+    gpu = GpuRun(n, L, cfg.ymax, equal_values)
+    log(f"radix-{cfg.name}: loading {L} structured layers (equal_values={equal_values})")
     for l0 in range(0, L, 64):
         nl = min(64, L - l0)
         cp, ri, v = synth.radix_layers_csc(cfg.net_id, l0, nl, n, cfg.weight)
         gpu.load(l0, cp, ri, v, np.full((nl, n), cfg.bias, np.float32))
     cats = gpu.run(y0)
-    counts = gpu.net.live_counts()
-    log(f"radix-{cfg.name}: {cats.size} categories; live counts {counts[:8].tolist()}")
-    assert (np.diff(counts) <= 0).all() and cats.size == counts[-1]
-    rng = np.random.default_rng(100 + ci)
-    sample = np.sort(rng.choice(cfg.n_rows, size=600, replace=False))
-    o = oracle.Oracle(y0[sample], cfg.ymax)
+    log(f"radix-{cfg.name}: {cats.size} categories; live counts {gpu.net.live_counts()[:8].tolist()}")
+    o = oracle.Oracle(y0, cfg.ymax)
     bias = np.full(n, cfg.bias, np.float32)
     l = 0
     while l < L and o.live > 0:
@@ -89,18 +77,15 @@ def test_structured_full_config_sampled_rows(ci):
         for i in range(nl):
             o.layer(cp[i], ri, v, bias, THREADS)
         l += nl
-    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
-    assert (oracle.padded_live_counts(o, L) <= counts).all()
-    if o.categories().size:
-        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
+    assert_parity(gpu, o, cats)
     o.close()
 
 
-@pytest.mark.parametrize("ci,nl", [(2, 12), (4, 6)])
-def test_all_live_sampled_rows(ci, nl):
+@pytest.mark.parametrize("ci,nl,rows", [(2, 12, 4096), (4, 6, 512)])
+def test_all_live_sampled_rows(ci, nl, rows):
     """The supplementary all-live set: Bernoulli(0.6) rows on the config's network, which keep every
     row live at every layer, so each layer runs at its full shape (60,000 rows); the first nl layers.
-    A seeded sample of 64 rows is recomputed by the oracle."""
+    A seeded sample of `rows` rows is recomputed by the oracle."""
     import bench
     cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
     n, m = cfg.n_neurons, cfg.n_rows
@@ -113,17 +98,16 @@ def test_all_live_sampled_rows(ci, nl):
     log(f"{cfg.name}: {cats.size} categories; live counts {counts.tolist()}")
     assert (counts == m).all() and cats.size == m
     rng = np.random.default_rng(200 + ci)
-    sample = np.sort(rng.choice(m, size=64, replace=False))
+    sample = np.sort(rng.choice(m, size=rows, replace=False))
     o = oracle.run_config_layers(y0[sample], cfg.net_id, nl, n, cfg.k, cfg.weight, cfg.bias, cfg.ymax,
                                  threads=THREADS)
     assert o.categories().size == sample.size
     np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
 
 
-def test_many_rows_sampled():
+def test_many_rows_every_row():
     """Five times the configs' row count (300,000 inputs of the 1024-neuron, 120-layer network):
-    live lists longer than one compaction pass covers, a layer 0 by counts over 2^28 inputs; a
-    seeded sample of rows recomputed by the oracle, invariants on all rows."""
+    live lists longer than one compaction pass covers; every row against the oracle."""
     cfg = synth.CONFIGS[1]
     m = 300_000
     y0 = synth.config_inputs(cfg, 0, m)
@@ -131,14 +115,7 @@ def test_many_rows_sampled():
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     log(f"{m} rows of {cfg.name}: running the GPU")
     cats = gpu.run(y0)
-    counts = gpu.net.live_counts()
-    log(f"{cats.size} categories; live counts {counts[:8].tolist()}")
-    assert (np.diff(counts) <= 0).all() and counts[0] == int((y0 != 0).any(axis=1).sum()) and cats.size == counts[-1]
-    rng = np.random.default_rng(7)
-    sample = np.sort(rng.choice(m, size=1000, replace=False))
-    o = oracle.run_config_layers(y0[sample], cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
+    log(f"{cats.size} categories; live counts {gpu.net.live_counts()[:8].tolist()}")
+    o = oracle.run_config_layers(y0, cfg.net_id, cfg.n_layers, cfg.n_neurons, cfg.k, cfg.weight, cfg.bias,
                                  cfg.ymax, threads=THREADS)
-    np.testing.assert_array_equal(np.isin(sample, cats), np.isin(np.arange(sample.size), o.categories()))
-    assert (oracle.padded_live_counts(o, cfg.n_layers) <= counts).all()
-    if o.categories().size:
-        np.testing.assert_array_equal(gpu.net.final_rows(sample[o.categories()]), o.rows(o.categories()))
+    assert_parity(gpu, o, cats)

@@ -1,7 +1,11 @@
 """GPU parity: the HIP library (through its C ABI) against the CPU oracle on the same seeded inputs.
 
 Bar: categories and per-layer live counts bit-exact; surviving final activations within 1e-5
-relative (fp32), and in fact bit-identical because both sides sum in the same canonical order."""
+relative (fp32), and in fact bit-identical because both sides sum in the same canonical order.
+
+Tests run the library's default kernels, which read every edge's weight and every neuron's bias
+from memory; tests parametrized with `equal_values` also run the opt-in kernels that exploit layers
+whose weights and biases are all equal (sdnn_enable_equal_value_kernels)."""
 import numpy as np
 import pytest
 
@@ -28,8 +32,8 @@ def random_layers(rng, n, nl, max_deg, signed=True):
     return layers
 
 
-def run_both(n, layers, y0, ymax=32.0):
-    gpu = GpuRun(n, len(layers), ymax)
+def run_both(n, layers, y0, ymax=32.0, equal_values=False):
+    gpu = GpuRun(n, len(layers), ymax, equal_values)
     for l, (cp, ri, v, b) in enumerate(layers):
         gpu.load(l, cp, ri, v, b)
     cats = gpu.run(y0)
@@ -57,8 +61,9 @@ def test_tiny_random_networks(seed):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("n", [1024, 2048, 4096, 16384, 65536])
-def test_config_networks_mixed_inputs(n):
+def test_config_networks_mixed_inputs(n, equal_values):
     """The configs' permutation-union networks (32 weights of 1/16 per column) with inputs whose
     densities straddle the survival threshold, so categories are neither empty nor full; covers both
     kernel paths and the tile sizes of every width."""
@@ -72,8 +77,8 @@ def test_config_networks_mixed_inputs(n):
         y0 = (np.random.default_rng(4).random((m, n)) < np.random.default_rng(5).uniform(0.2, 0.7, (m, 1))).astype(np.float32)
     cp, ri, v = synth.layers_csc(9, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
-    log(f"config-net n={n} m={m} layers={nl}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"config-net n={n} m={m} layers={nl} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     assert 0 < cats.size < m
     assert_parity(gpu, o, cats)
 
@@ -195,9 +200,11 @@ def test_global_tile_large_lists(n, m, bias, lo, hi, kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("case", ["last", "fill", "adopt-odd"])
-def test_code_layer_outputs(case):
-    """The layer after a uniform layer 0 gathers one-byte codes and skips storing 32-row output segments
+def test_code_layer_outputs(case, equal_values):
+    """The layer after a large binary layer 0 (written as dictionary codes, or by counts with
+    equal_values) gathers one-byte codes and skips storing 32-row output segments
     that are zero in every row. Its tiles are then either repacked (reading only the stored segments)
     or, when the next layer or the final read-out takes them as they are, completed with zeros.
     "last": it is the last layer; "fill": it keeps nearly every row, so no repack follows; "adopt-odd":
@@ -214,8 +221,8 @@ def test_code_layer_outputs(case):
     if case == "fill":
         bias[1][:] = 0.10
     layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
-    log(f"code layer outputs case={case}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"code layer outputs case={case} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     kind, _ = gpu.net.layer_info()
     assert gpu.net.kernel_path == 1 and sdnn_kind(kind[1]) == "k_layer_gfm_u8"
     counts = oracle.padded_live_counts(o, nl)
@@ -226,13 +233,14 @@ def test_code_layer_outputs(case):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("n,m,kind", [(1024, 3000, "uniform"), (2048, 1500, "uniform"), (4096, 700, "uniform"),
                                       (1500, 900, "random"), (1024, 600, "dying")])
-def test_fused_layers(n, m, kind):
+def test_fused_layers(n, m, kind, equal_values):
     """Widths up to 4096: once few enough rows are live, one launch runs every remaining layer with each
-    workgroup's rows kept in LDS (16, 8 or 4 rows per workgroup by width and count). "uniform": one-weight
-    layers read through 16-bit source lists; "random": signed weights of random degree through the ELL;
-    "dying": every row dies inside the fused launch."""
+    workgroup's rows kept in LDS (16, 8 or 4 rows per workgroup by width and count). "uniform": layers
+    of one weight (read through 16-bit source lists with equal_values); "random": signed weights of
+    random degree; "dying": every row dies inside the fused launch."""
     nl = 10
     rng = np.random.default_rng(n + m)
     if kind == "random":
@@ -244,8 +252,8 @@ def test_fused_layers(n, m, kind):
         layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
         lo, hi = (0.45, 0.7) if kind != "dying" else (0.25, 0.35)
         y0 = (rng.random((m, n)) < rng.uniform(lo, hi, size=(m, 1))).astype(np.float32)
-    log(f"fused layers n={n} m={m} kind={kind}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"fused layers n={n} m={m} kind={kind} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     kinds, launches = gpu.net.layer_info()
     assert gpu.net.kernel_path == 0
     fused = [l for l in range(nl) if sdnn_kind(kinds[l]) == "k_layers_lds"]
@@ -256,11 +264,13 @@ def test_fused_layers(n, m, kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("n,kind", [(6000, "binary"), (5003, "binary"), (6000, "one-value")])
-def test_counting_layer0(n, kind):
-    """Layer 0 of a uniform network on more than 256 rows goes by counts of the bit-packed inputs, at
-    widths that are and are not multiples of 4. "one-value": a single input of 0.5 rules the bit route
-    out, and layer 0 runs on fp32 tiles."""
+def test_counting_layer0(n, kind, equal_values):
+    """Layer 0 of a uniform network on more than 256 binary rows: with equal_values by counts of the
+    bit-packed inputs, by default from the bit tiles with each edge's weight, written as dictionary
+    codes; at widths that are and are not multiples of 4. "one-value": a single input of 0.5 rules
+    the bit route out, and layer 0 runs on fp32 tiles."""
     m, nl = 700, 4
     rng = np.random.default_rng(n)
     y0 = (rng.random((m, n)) < rng.uniform(0.2, 0.6, size=(m, 1))).astype(np.float32)
@@ -269,16 +279,18 @@ def test_counting_layer0(n, kind):
         y0[300, 17] = 0.5
     cp, ri, v = synth.layers_csc(15, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, -0.35, np.float32)) for l in range(nl)]
-    log(f"counting layer 0 n={n} kind={kind}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"counting layer 0 n={n} kind={kind} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     kinds, _ = gpu.net.layer_info()
-    expect = "k_pack_bits+k_layer_count" if kind == "binary" else "k_layer_gfm"
+    bits = "k_pack_bits+k_layer_count" if equal_values else "k_pack_bits+k_layer_bits(codes)"
+    expect = bits if kind == "binary" else "k_layer_gfm"
     assert sdnn_kind(kinds[0]) == expect
     assert_parity(gpu, o, cats)
 
 
 @pytest.mark.parametrize("kind", ["binary", "one-value"])
 def test_counting_layer0_lds_widths(kind):
+    # the counting route exists only with the equal-value kernels
     """Widths staged in LDS, from 2^24 inputs: layer 0 of a uniform network goes by counts of the
     bit-packed rows and is written back as fp32 rows (one mask bit per list position), then the
     row tiles take over. "one-value": an input of 0.5 keeps layer 0 on the fp32 kernel."""
@@ -291,7 +303,7 @@ def test_counting_layer0_lds_widths(kind):
     cp, ri, v = synth.layers_csc(16, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, -0.30, np.float32)) for l in range(nl)]
     log(f"counting layer 0 on LDS widths kind={kind}")
-    gpu, o, cats = run_both(n, layers, y0)
+    gpu, o, cats = run_both(n, layers, y0, equal_values=True)
     kinds, _ = gpu.net.layer_info()
     assert gpu.net.kernel_path == 0
     assert sdnn_kind(kinds[0]) == ("k_pack_bits+k_layer_count" if kind == "binary" else "k_layer_lds")
@@ -343,7 +355,7 @@ def test_few_tile_rows_die_one_by_one(kind):
             v[cp[l][0]] = np.float32(0.125)
     layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
     log(f"few-tile rows die one by one kind={kind}")
-    gpu, o, cats = run_both(n, layers, y0)
+    gpu, o, cats = run_both(n, layers, y0, equal_values=kind == "one-weight")
     counts = oracle.padded_live_counts(o, nl)
     assert counts[-1] >= 6 and any(8 < c <= 16 for c in counts) and any(c <= 8 for c in counts)
     kinds, _ = gpu.net.layer_info()
@@ -351,8 +363,9 @@ def test_few_tile_rows_die_one_by_one(kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("n,m", [(1024, 400), (4096, 200), (16384, 80), (65536, 30)])
-def test_structured_networks(n, m):
+def test_structured_networks(n, m, equal_values):
     """Structured (RadiX-Net style) layers: a radix-2 base DNN Kronecker-expanded by 16 x 16 blocks,
     randomly relabelled per copy of the D base layers (Fig. 1, Table 1). Inputs of mixed density so
     that some rows survive; two copies and a layer of the third, on both kernel paths."""
@@ -363,8 +376,8 @@ def test_structured_networks(n, m):
     y0 = synth.inputs(40 + d, side, 0, m, "mixed", 0.3, 0.8)
     cp, ri, v = synth.radix_layers_csc(21, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
-    log(f"structured n={n} m={m} layers={nl}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"structured n={n} m={m} layers={nl} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     assert 0 < cats.size < m
     assert_parity(gpu, o, cats)
 
@@ -387,7 +400,7 @@ def test_structured_duplicate_columns(order):
     if order == "mixed-bias":
         bias[d][123] = np.float32(-0.41)
     layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
-    gpu = GpuRun(n, nl)
+    gpu = GpuRun(n, nl, equal_values=True)  # one column per group needs the equal-value kernels
     seq = range(nl - 1, -1, -1) if order == "reversed" else range(nl)
     for l in seq:
         gpu.load(l, cp[l], ri, v, bias[l])
@@ -418,18 +431,19 @@ def test_maximum_column_degree(n):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("n,m", [(4096, 900), (2048, 1800), (1024, 3000)])
-def test_fused_tile_heights(n, m):
+def test_fused_tile_heights(n, m, equal_values):
     """Rows that stay live (Bernoulli(0.6) inputs) reach the launch that runs every remaining layer
     once two layers have kept 90% of them, with tiles of 4, 8 or 16 rows per workgroup for these
-    widths and row counts; each height reads its own grouped column order."""
+    widths and row counts; with equal_values each height reads its own grouped column order."""
     nl = 8
     rng = np.random.default_rng(n + m)
     y0 = (rng.random((m, n)) < 0.6).astype(np.float32)
     cp, ri, v = synth.layers_csc(14, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, -0.35, np.float32)) for l in range(nl)]
-    log(f"fused tile heights n={n} m={m} layers={nl}")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"fused tile heights n={n} m={m} layers={nl} equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     kinds = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
     log(f"kinds {kinds}")
     assert kinds[-1] == "k_layers_lds" and cats.size == m
@@ -451,7 +465,7 @@ def test_structured_lds_columns(case):
     cp, ri, v = synth.radix_layers_csc(24, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, bias, np.float32)) for l in range(nl)]
     log(f"structured LDS columns case={case} n={n} m={m} layers={nl}")
-    gpu, o, cats = run_both(n, layers, y0)
+    gpu, o, cats = run_both(n, layers, y0, equal_values=True)
     kinds = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
     log(f"kinds {kinds}")
     if case == "tiles":
@@ -464,20 +478,21 @@ def test_structured_lds_columns(case):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("nl", [2, 5])
-def test_structured_code_layer_columns(nl):
-    """A structured network on more than 256 rows: layer 0 by counts, layer 1 gathers one-byte codes
-    and, its successor's sources mapped to the representatives, computes one column per group of
-    equal columns and stores all of their segments. nl=2: layer 1 is the last layer, whose final rows
-    are expanded through its groups."""
+def test_structured_code_layer_columns(nl, equal_values):
+    """A structured network on more than 256 rows: layer 0 writes one-byte codes (by counts with
+    equal_values), layer 1 gathers them and, with equal_values and its successor's sources mapped to
+    the representatives, computes one column per group of equal columns and stores all of their
+    segments. nl=2: layer 1 is the last layer, whose final rows are expanded through its groups."""
     n, m = 8192, 700
     d = synth.radix_depth(n)
     rng = np.random.default_rng(nl)
     y0 = (rng.random((m, n)) < rng.uniform(0.1, 0.5, size=(m, 1))).astype(np.float32)
     cp, ri, v = synth.radix_layers_csc(23, 0, nl, n)
     layers = [(cp[l], ri, v, np.full(n, -0.40, np.float32)) for l in range(nl)]
-    log(f"structured code layer columns n={n} nl={nl} (D={d})")
-    gpu, o, cats = run_both(n, layers, y0)
+    log(f"structured code layer columns n={n} nl={nl} (D={d}) equal_values={equal_values}")
+    gpu, o, cats = run_both(n, layers, y0, equal_values=equal_values)
     kinds, _ = gpu.net.layer_info()
     assert sdnn_kind(kinds[1]) == "k_layer_gfm_u8"
     assert 0 < cats.size < m
@@ -506,3 +521,39 @@ def test_profiling_modes():
     assert runs[large].tolist() == [2] * len(large) and (ms[large] > 0).all()
     assert (runs[[l for l in range(nl) if l not in large]] == 0).all()
     gpu.net.set_profiling(False)
+
+
+@pytest.mark.parametrize("n,m", [(16384, 700), (65536, 400)])
+@pytest.mark.parametrize("wkind", ["three-values", "random"])
+def test_value_agnostic_large_binary_batch(n, m, wkind):
+    """More than 256 binary rows through layers whose weights vary per edge and whose biases vary per
+    neuron, at both bit-tile heights (32 rows up to 16384 neurons, 16 beyond). "three-values":
+    weights drawn from {1/16, 3/32, 1/8} and biases from {-0.40, -0.45}, so layer 0's outputs take
+    154 distinct values: layer 0 writes one-byte codes through the value dictionary (claiming slots
+    with compare-and-swap across workgroups) and layer 1 gathers them with each edge's weight.
+    "random": uniform random weights, so the dictionary overflows and layer 0 is computed again with
+    fp32 outputs, which layer 1 gathers."""
+    nl = 3
+    rng = np.random.default_rng(n + (0 if wkind == "random" else 1))
+    cp, ri, v = synth.layers_csc(31, 0, nl, n)
+    layers = []
+    for l in range(nl):
+        if wkind == "random":
+            w = rng.uniform(0.02, 0.2, size=v.size).astype(np.float32)
+        else:
+            w = rng.choice(np.array([1 / 16, 3 / 32, 1 / 8], np.float32), size=v.size).astype(np.float32)
+        b = rng.choice(np.array([-0.40, -0.45], np.float32), size=n).astype(np.float32)
+        layers.append((cp[l], ri, w, b))
+    y0 = (rng.random((m, n)) < rng.uniform(0.15, 0.5, size=(m, 1))).astype(np.float32)
+    y0[3] = 0.0
+    log(f"value-agnostic large binary batch n={n} m={m} weights={wkind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, launches = gpu.net.layer_info()
+    if wkind == "random":
+        assert sdnn_kind(kinds[0]) == "k_pack_bits+k_layer_bits" and launches[0] == 3
+        assert sdnn_kind(kinds[1]) == "k_layer_gfm"
+    else:
+        assert sdnn_kind(kinds[0]) == "k_pack_bits+k_layer_bits(codes)"
+        assert sdnn_kind(kinds[1]) == "k_layer_gfm_u8"
+    assert oracle.padded_live_counts(o, nl)[1] > 256
+    assert_parity(gpu, o, cats)
