@@ -107,6 +107,17 @@ size_t sdnn_workspace_bytes(const sdnn_net *net, int64_t n_rows);
 sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace,
                        size_t workspace_bytes, void *hip_stream);
 
+/* TIMED. sdnn_infer for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same computation and results,
+ * with the workspace taken from a 64 MiB array in the library's device memory instead of a caller
+ * buffer. Allocates nothing (no hipMalloc, hipFree or allocating library call). The array is one per
+ * device, shared by every handle and call on that device, and keeps the last call's contents: calls
+ * that overlap on one device race, so serialize them (one stream, or wait for sdnn_categories) and
+ * read a run's diagnostics (sdnn_live_counts, sdnn_final_rows) before the next static run on that
+ * device. n_rows must satisfy sdnn_workspace_bytes(net, n_rows) <= 64 MiB; larger batches return
+ * SDNN_ERANGE (nothing is enqueued). Other arguments and errors as for sdnn_infer. */
+sdnn_status sdnn_infer_static(sdnn_net *net, const float *y0, int64_t n_rows, void *hip_stream);
+
 /* TIMED. Wait for the last sdnn_infer and report its categories (Sec. V: the rows of the final
  * matrix with entries > 0): 0-based row indexes into y0, ascending, written to ids (host,
  * capacity entries). *count receives the number of categories. ids == NULL or capacity < count

@@ -39,6 +39,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <type_traits>
@@ -2009,6 +2010,38 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   }
 }
 
+// The workspace of sdnn_infer_static: a file-scope array in device memory, 64 MiB, of which each
+// device that loads the library holds its own copy until the process ends. Host code never passes
+// the array's name to a kernel or a copy (on the host it is a stand-in, not a device address): it
+// uses the address hipGetSymbolAddress returns for the current device, looked up once per device.
+constexpr size_t kStaticWorkspaceBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticWorkspaceBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `device`, which must be the current device.
+sdnn_status scratch_address(int device, void **out) {
+  if (device < 0 || device >= kMaxDevices) return fail(SDNN_EINVAL, "device %d out of range", device);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(SDNN_EDEVICE, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    }
+    g_scratch_ptr[device] = p;
+  }
+  *out = g_scratch_ptr[device];
+  return SDNN_OK;
+}
+
+}  // namespace
+
 // ------------------------------------------------------------------------------------------------
 // Host side
 
@@ -2757,6 +2790,10 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
                                      hipHostMallocCoherent));
     *net->progress = 0ull;
     HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->progress_dev), net->progress, 0));
+    // the device address of the static workspace on this device (sdnn_infer_static)
+    void *sw = nullptr;
+    st = scratch_address(net->device, &sw);
+    if (st != SDNN_OK) return st;
   } else {
     int dev = -1;
     HIP_OR_POISON(net, hipGetDevice(&dev));
@@ -3432,6 +3469,22 @@ sdnn_status infer_impl(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
 sdnn_status sdnn_infer(sdnn_net *net, const float *y0, int64_t n_rows, void *workspace, size_t workspace_bytes,
                        void *hip_stream) {
   return infer_impl(net, y0, n_rows, workspace, workspace_bytes, hip_stream);
+}
+
+sdnn_status sdnn_infer_static(sdnn_net *net, const float *y0, int64_t n_rows, void *hip_stream) {
+  sdnn_status st = check_usable(net);
+  if (st != SDNN_OK) return st;
+  if (n_rows < 0) return fail(SDNN_EINVAL, "n_rows %lld out of range", (long long)n_rows);
+  const size_t need = sdnn_workspace_bytes(net, n_rows);
+  if (need > kStaticWorkspaceBytes)
+    return fail(SDNN_ERANGE, "%lld rows need %zu bytes of workspace; the static workspace holds %zu",
+                (long long)n_rows, need, kStaticWorkspaceBytes);
+  int dev = -1;
+  HIP_OR_POISON(net, hipGetDevice(&dev));
+  void *ws = nullptr;
+  st = scratch_address(dev, &ws);
+  if (st != SDNN_OK) return st;
+  return infer_impl(net, y0, n_rows, ws, kStaticWorkspaceBytes, hip_stream);
 }
 
 

@@ -16,6 +16,7 @@ EXPORTED_SYMBOLS = [
     "sdnn_create", "sdnn_load_layers", "sdnn_workspace_bytes", "sdnn_infer", "sdnn_categories",
     "sdnn_live_counts", "sdnn_final_rows", "sdnn_destroy", "sdnn_last_error", "sdnn_kernel_path",
     "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info", "sdnn_enable_equal_value_kernels",
+    "sdnn_infer_static",
 ]
 KERNEL_KINDS = {0: "none", 1: "k_layer_lds", 2: "k_layer_gfm", 3: "k_layer_gfm_u8", 4: "k_layer_gfm_small",
                 5: "k_pack_bits+k_layer_bits", 6: "k_pack_bits+k_layer_bits(codes)", 7: "k_pack_bits+k_layer_count",
@@ -59,9 +60,10 @@ def load_library():
         L.sdnn_layer_times.argtypes = [vp, vp, vp]
         L.sdnn_layer_info.argtypes = [vp, vp, vp]
         L.sdnn_enable_equal_value_kernels.argtypes = [vp, i32]
+        L.sdnn_infer_static.argtypes = [vp, vp, i64, vp]
         for name in ("sdnn_create", "sdnn_load_layers", "sdnn_infer", "sdnn_categories", "sdnn_live_counts",
                      "sdnn_final_rows", "sdnn_set_profiling", "sdnn_layer_times", "sdnn_layer_info",
-                     "sdnn_enable_equal_value_kernels"):
+                     "sdnn_enable_equal_value_kernels", "sdnn_infer_static"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -143,6 +145,12 @@ class Net:
         self.rows = n_rows
         _check(load_library().sdnn_infer(self._h, _dev_ptr(y0) if n_rows else None, n_rows, _dev_ptr(workspace),
                                          workspace_bytes, _stream_handle(stream)))
+
+    def infer_static(self, y0, n_rows: int, stream=None) -> None:
+        """sdnn_infer with the library's static device workspace (no allocation; see sdnn.h)."""
+        self.rows = n_rows
+        _check(load_library().sdnn_infer_static(self._h, _dev_ptr(y0) if n_rows else None, n_rows,
+                                                _stream_handle(stream)))
 
     def categories(self) -> np.ndarray:
         L = load_library()
