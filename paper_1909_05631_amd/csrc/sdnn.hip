@@ -162,9 +162,11 @@ __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsi
                        int *__restrict__ misc, unsigned *__restrict__ dict, int M, int L,
                        unsigned *__restrict__ spread, size_t spread_words) {
   const int st = gridDim.x * blockDim.x;
-  // value dictionary: slot 0 holds +0.0 (bit pattern 0), every other slot is free
+  // value dictionary (see dict_code): code 0 is +0.0, whose key 0 sits in its hash slot 0; every
+  // other slot is free and the next code is 1
   if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < 256; i += blockDim.x) dict[i] = i == 0 ? 0u : 0x7fc00000u;
+    for (int i = threadIdx.x; i < 769; i += blockDim.x)
+      dict[i] = i < 256 ? 0u : i < 512 ? (i == 256 ? 0u : 0x7fc00000u) : i < 768 ? (i == 512 ? 0u : 0xffffffffu) : 1u;
   if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = (threadIdx.x == kNposSlot) ? M : 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
@@ -210,10 +212,15 @@ __global__ __launch_bounds__(256) void k_spread_to_masks(unsigned *__restrict__ 
   }
 }
 
+// With notify set, thread 0 finally stores (tag << 40) | (flags << 32) | count into that word of
+// coherent host memory, flags = bit 0: misc[0] (a layer-0 input is not 0 or 1), bit 1:
+// misc[kOverflowSlot] (the value dictionary is full); the host waits on it instead of a copy and a
+// stream synchronization.
 __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, int B, const int *__restrict__ ids_in,
                                                   int *__restrict__ ids_out, int *__restrict__ src_out,
                                                   const int *__restrict__ count_in, int *__restrict__ count_out,
-                                                  int *__restrict__ count_out2) {
+                                                  int *__restrict__ count_out2, const int *__restrict__ misc,
+                                                  unsigned long long *__restrict__ notify, unsigned long long tag) {
   __shared__ int toff[kCompactTiles];
   __shared__ unsigned tmask[kCompactTiles];
   __shared__ int wsum[16];
@@ -269,6 +276,11 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
   if (tid == 0) {
     *count_out = base;
     if (count_out2) *count_out2 = base;
+    if (notify) {
+      const unsigned long long flags = (misc[0] != 0 ? 1ull : 0ull) | (misc[kOverflowSlot] != 0 ? 2ull : 0ull);
+      __hip_atomic_store(notify, (tag << 40) | (flags << 32) | (unsigned long long)(unsigned)base, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_SYSTEM);
+    }
   }
 }
 
@@ -427,7 +439,8 @@ __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chu
 template <int B, int KC>
 __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                     const int2 *__restrict__ ell, int K,
-                                                    const uint4 *__restrict__ ell16, float wc,
+                                                    const uint4 *__restrict__ ell16, const float *__restrict__ w8,
+                                                    float wc,
                                                     const float *__restrict__ bias, float ymax,
                                                     const int *__restrict__ ids, const int *__restrict__ count,
                                                     unsigned *__restrict__ masks, int *__restrict__ rownz,
@@ -510,14 +523,29 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
       // current group's LDS reads and fma chain run.
       const int2 *ej = ell + j;
       if (ell16) {
-        // one weight wc and 32 sources per column, eight per 16-byte load ([4][N][8] u16); all
-        // four loads are in flight before the first group's LDS reads
+        // 32 sources per column, eight per 16-byte load ([4][N][8] u16), with their weights in the
+        // same grouping (w8, two 16-byte loads per eight) or the layer's one weight wc; all loads
+        // are in flight before the first group's LDS reads
         uint4 ix[4];
+        float4 wq[8];
 #pragma unroll
         for (int g = 0; g < 4; ++g) ix[g] = ell16[(size_t)g * ncols + j];
+        if (w8) {
+          const float4 *w4 = reinterpret_cast<const float4 *>(w8);
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            wq[2 * g] = w4[((size_t)g * ncols + j) * 2];
+            wq[2 * g + 1] = w4[((size_t)g * ncols + j) * 2 + 1];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) wq[i] = make_float4(wc, wc, wc, wc);
+        }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
+          const float wg[8] = {wq[2 * g].x, wq[2 * g].y, wq[2 * g].z, wq[2 * g].w,
+                               wq[2 * g + 1].x, wq[2 * g + 1].y, wq[2 * g + 1].z, wq[2 * g + 1].w};
           float4 v[8];
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
@@ -526,10 +554,10 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
           }
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
-            a0 = fmaf(v[q].x, wc, a0);
-            a1 = fmaf(v[q].y, wc, a1);
-            a2 = fmaf(v[q].z, wc, a2);
-            a3 = fmaf(v[q].w, wc, a3);
+            a0 = fmaf(v[q].x, wg[q], a0);
+            a1 = fmaf(v[q].y, wg[q], a1);
+            a2 = fmaf(v[q].z, wg[q], a2);
+            a3 = fmaf(v[q].w, wg[q], a3);
           }
         }
       } else if constexpr (KC > 0) {
@@ -609,7 +637,9 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
 // Device view of one layer for kernels that run several layers in one launch.
 struct LayerPtr {
   const int2 *ell;     // slot-major ELL, offsets in units of 1 << ell_shift bytes per source
-  const uint4 *ell16;  // one-weight layer with 32 sources per column: [4][D][8] u16 sources, else null
+  const uint4 *ell16;  // layer with 32 sources per column: [4][D][8] u16 sources, else null
+  const float *w8;     // with ell16: the weights in the same grouping, [4][D][8] fp32; null for a
+                       // uniform layer (weight w)
   const float *bias;
   const int *cols;     // with ell16: the D columns computed (null: all N, D = N)
   float w;             // the weight of a one-weight layer
@@ -694,13 +724,28 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
 #pragma unroll
       for (int c = 0; c < RPL; ++c) a[c] = 0.0f;
       if (P.ell16) {
-        // 32 sources, eight per 16-byte load ([4][D][8] u16); all four loads in flight first
+        // 32 sources, eight per 16-byte load ([4][D][8] u16), and their weights (eight per two
+        // 16-byte loads from w8, or the layer's one weight); every load in flight first
         uint4 ix[4];
+        float4 wq[8];
 #pragma unroll
         for (int g = 0; g < 4; ++g) ix[g] = P.ell16[(size_t)g * ncols + jp];
+        if (P.w8) {
+          const float4 *w4 = reinterpret_cast<const float4 *>(P.w8);
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            wq[2 * g] = w4[((size_t)g * ncols + jp) * 2];
+            wq[2 * g + 1] = w4[((size_t)g * ncols + jp) * 2 + 1];
+          }
+        } else {
+#pragma unroll
+          for (int i = 0; i < 8; ++i) wq[i] = make_float4(P.w, P.w, P.w, P.w);
+        }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
+          const float wg[8] = {wq[2 * g].x, wq[2 * g].y, wq[2 * g].z, wq[2 * g].w,
+                               wq[2 * g + 1].x, wq[2 * g + 1].y, wq[2 * g + 1].z, wq[2 * g + 1].w};
           float v[8][RPL];
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
@@ -710,7 +755,7 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
 #pragma unroll
           for (int q = 0; q < 8; ++q)
 #pragma unroll
-            for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[q][c], P.w, a[c]);
+            for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[q][c], wg[q], a[c]);
         }
       } else {
         for (int sl = 0; sl < P.K; ++sl) {
@@ -799,32 +844,49 @@ __global__ __launch_bounds__(256) void k_to_fm(const float *__restrict__ yin, fl
   }
 }
 
-// Stages the sources of a chunk of outputs [c0, c0 + nout) of a layer with one weight (16-bit
-// source lists src16[slot][N]) into LDS as dst[slot][CH] = source * scale, eight per 16-byte load;
-// outputs past nout get 0.
-template <int KC, int CH>
-__device__ __forceinline__ void stage_src16(unsigned *dst, const unsigned short *__restrict__ src16, int N, int c0,
-                                            int nout, unsigned scale) {
-  static_assert(CH % 8 == 0, "eight sources per load");
-  for (int i = threadIdx.x; i < KC * CH / 8; i += blockDim.x) {
+// Weight layouts read by the global-tile kernels:
+//   kWEll:  a layer of any width K: the slot-major ELL of (source offset, weight bits), K from the
+//           launch (the general fallback);
+//   kWOne:  32 sources per column as 16-bit lists src16[slot][column], one weight wc for the whole
+//           layer (only with the equal-value kernels);
+//   kWEdge: 32 sources per column as 16-bit lists src16[slot][column] and each edge's weight in
+//           w32[slot][column] (6 bytes per edge).
+constexpr int kWEll = 0, kWOne = 1, kWEdge = 2;
+
+// Stage the 16-bit sources (and, for kWEdge, the weights) of outputs [c0, c0 + nout) of a layer
+// into LDS as srcs[slot][CH] and wts[slot][CH], with 16-byte loads where the rows are aligned;
+// outputs past nout get source 0 and weight 0 (they are computed but never stored).
+template <int WM, int CH>
+__device__ __forceinline__ void stage_lists(unsigned short *srcs, float *wts, const unsigned short *__restrict__ src16,
+                                            const float *__restrict__ w32, int ncols, int c0, int nout) {
+  static_assert(CH % 8 == 0, "whole 16-byte groups");
+  for (int i = threadIdx.x; i < 32 * CH / 8; i += blockDim.x) {
     const int sl = i / (CH / 8), pr = (i % (CH / 8)) * 8;
-    const unsigned short *sp = src16 + (size_t)sl * N + c0 + pr;
-    unsigned o[8];
+    const unsigned short *sp = src16 + (size_t)sl * ncols + c0 + pr;
+    uint4 v;
     if (pr + 7 < nout && (reinterpret_cast<uintptr_t>(sp) & 15) == 0) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(sp);
-      const unsigned w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        o[2 * c] = w[c] & 0xffffu;
-        o[2 * c + 1] = w[c] >> 16;
-      }
+      v = *reinterpret_cast<const uint4 *>(sp);
     } else {
+      unsigned o[4] = {0u, 0u, 0u, 0u};
 #pragma unroll
-      for (int c = 0; c < 8; ++c) o[c] = pr + c < nout ? (unsigned)sp[c] : 0u;
+      for (int c = 0; c < 8; ++c) o[c >> 1] |= (pr + c < nout ? (unsigned)sp[c] : 0u) << (16 * (c & 1));
+      v = make_uint4(o[0], o[1], o[2], o[3]);
     }
-    uint4 *d = reinterpret_cast<uint4 *>(dst + sl * CH + pr);
-    d[0] = make_uint4(o[0] * scale, o[1] * scale, o[2] * scale, o[3] * scale);
-    d[1] = make_uint4(o[4] * scale, o[5] * scale, o[6] * scale, o[7] * scale);
+    *reinterpret_cast<uint4 *>(srcs + sl * CH + pr) = v;
+  }
+  if constexpr (WM == kWEdge) {
+    for (int i = threadIdx.x; i < 32 * CH / 4; i += blockDim.x) {
+      const int sl = i / (CH / 4), pr = (i % (CH / 4)) * 4;
+      const float *wp = w32 + (size_t)sl * ncols + c0 + pr;
+      float4 v;
+      if (pr + 3 < nout && (reinterpret_cast<uintptr_t>(wp) & 15) == 0) {
+        v = *reinterpret_cast<const float4 *>(wp);
+      } else {
+        v = make_float4(pr < nout ? wp[0] : 0.0f, pr + 1 < nout ? wp[1] : 0.0f, pr + 2 < nout ? wp[2] : 0.0f,
+                        pr + 3 < nout ? wp[3] : 0.0f);
+      }
+      *reinterpret_cast<float4 *>(wts + sl * CH + pr) = v;
+    }
   }
 }
 
@@ -868,14 +930,13 @@ __device__ __forceinline__ RoundSplit round_split(int ntl, int tpx, int nchunks)
 // kGfmOutputs = 64 outputs. Lane = (row b = lane % 32, h = lane / 32): a source segment of 128
 // bytes is read by 32 lanes with 4-byte loads (on gfx950 4-byte lane loads gather a segment three
 // times faster than 16-byte ones), so a wave instruction serves 2 outputs; each lane runs the
-// chains of 8 outputs (16 per wave), one slot ahead, and the results go out as 128-byte row
-// segments. gridDim must be a multiple of 8: workgroup x runs on XCD x % 8, and the workgroups of
-// XCD x share the output chunks of one tile, which therefore stays in that XCD's L2 (or, for the
-// widest layers, in the Infinity Cache) for the whole launch. With fewer than 8 tiles left, each
-// tile's chunks are split over 8 / ntiles XCDs. For KC > 0 the chunk's ELL rows are staged in LDS
-// with 16-byte loads, so the gathers are the only per-output memory reads; with CW (a layer whose
-// weights are all wc) the staged entries are 16-bit source lists, a quarter of the ELL's bytes.
-// Slots past the list's end hold zeros in fin and get zeros in fout.
+// chains of the 8 consecutive outputs 16 wave + 8 h .. + 7, one slot ahead, and the results go out
+// as 128-byte row segments. gridDim must be a multiple of 8: workgroup x runs on XCD x % 8, and the
+// workgroups of XCD x share the output chunks of one tile, which therefore stays in that XCD's L2
+// (or, for the widest layers, in the Infinity Cache) for the whole launch. With fewer than 8 tiles
+// left, each tile's chunks are split over 8 / ntiles XCDs. With 16-bit lists (WM != kWEll) the
+// chunk's sources (and kWEdge weights) are staged in LDS, so the gathers are the only per-output
+// memory reads. Slots past the list's end hold zeros in fin and get zeros in fout.
 //
 // Workgroup 0 of the first round also does the list bookkeeping of the layer sequence: with
 // count_out set (a layer that follows one without compaction) it counts the previous layer's live
@@ -883,25 +944,24 @@ __device__ __forceinline__ RoundSplit round_split(int ntl, int tpx, int nchunks)
 // clears that buffer, the one the next layer will use (three buffers rotate by layer). With
 // count_out set and no live row left (rows that die stay dead), the layer writes nothing.
 // Live rows go to masks, or with spread set to the spread words of each tile (see or_mask). With
-// cols set (CW only), the launch computes the ncols columns cols[p] alone, their source lists in
+// cols set (kWOne only), the launch computes the ncols columns cols[p] alone, their source lists in
 // src16 as [K][ncols]; the other columns equal one of these and are neither computed nor stored.
-template <int FMR, int KC, bool CW>
+template <int WM>
 __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin, float *__restrict__ fout, int N,
                                                    const int2 *__restrict__ ell, int K,
-                                                   const unsigned short *__restrict__ src16, float wc,
+                                                   const unsigned short *__restrict__ src16,
+                                                   const float *__restrict__ w32, float wc,
                                                    const float *__restrict__ bias, float ymax,
                                                    const int *__restrict__ npos, unsigned *__restrict__ masks,
                                                    int tile0, const unsigned *__restrict__ masks_prev,
                                                    unsigned *__restrict__ masks_clear, int *__restrict__ count_out,
                                                    unsigned *__restrict__ spread, const int *__restrict__ cols,
                                                    int ncols, int tpx) {
-  static_assert(FMR == 32, "the lane layout covers 32 rows with one lane per row");
-  constexpr int CH = kGfmOutputs, OPL = 8;
+  constexpr int FMR = 32, CH = kGfmOutputs, OPL = 8;
   static_assert(CH == 4 * 2 * OPL, "4 waves x 2 halves x OPL outputs");
-  static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
-  constexpr int KS = KC > 0 ? KC : 1;
-  __shared__ int2 ells[CW ? 1 : KS * CH];
-  __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * FMR
+  constexpr bool LISTS = WM != kWEll;
+  __shared__ __align__(16) unsigned short srcs[LISTS ? 32 * CH : 8];
+  __shared__ __align__(16) float wts[WM == kWEdge ? 32 * CH : 4];
   __shared__ float bstage[CH];
   __shared__ int cstage[CH];  // output column of each chunk position
   __shared__ unsigned rowmask;
@@ -934,66 +994,53 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
   const int nvalid = active ? min(FMR, R - t * FMR) : 0;
   const float *tb = fin + (size_t)t * N * FMR + b;
   float *ob = fout + (size_t)t * N * FMR + b;
-  const int jw = wave * 2 * OPL + h;  // this lane's outputs in the chunk: jw + 2i, i < OPL
+  const int jl0 = wave * 2 * OPL + h * OPL;  // this lane's outputs in the chunk: jl0 .. jl0 + OPL - 1
   bool live = false;
   for (int chunk = rs.first; chunk < cend; chunk += rs.step) {
     const int c0 = chunk * CH;
     const int nout = min(CH, ncols - c0);
-    __syncthreads();  // the previous chunk is done with ells / bstage / cstage
+    __syncthreads();  // the previous chunk is done with srcs / wts / bstage / cstage
     for (int i = tid; i < CH; i += blockDim.x) {
       const int col = i < nout ? (cols ? cols[c0 + i] : c0 + i) : 0;
       cstage[i] = col;
       bstage[i] = i < nout ? bias[col] : 0.0f;
     }
-    if constexpr (CW) {
-      stage_src16<KC, CH>(offs, src16, ncols, c0, nout, FMR);
-    } else if constexpr (KC > 0) {
-      // stage [slot][64 outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
-      for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
-        const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
-        const int2 *src = ell + (size_t)sl * N + c0 + pr;
-        int4 v = make_int4(0, 0, 0, 0);
-        if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
-          v = *reinterpret_cast<const int4 *>(src);
-        } else {
-          if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
-          if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
-        }
-        *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
-      }
-    }
+    if constexpr (LISTS) stage_lists<WM, CH>(srcs, wts, src16, w32, ncols, c0, nout);
     __syncthreads();
     float acc[OPL];
 #pragma unroll
     for (int i = 0; i < OPL; ++i) acc[i] = 0.0f;
-    if constexpr (KC > 0) {
+    if constexpr (LISTS) {
       // software pipeline kDepth slots deep: a slot's gathers are issued kDepth - 1 slots before
       // its fmas (each gather is one row of one output, so the depth is what keeps enough
       // segments in flight to cover the L2 latency)
       constexpr int kDepth = 4;
-      float g[kDepth][OPL], wv[kDepth][OPL];
+      float g[kDepth][OPL];
       auto fetch = [&](int sl, int bf) {
+        const unsigned short *sp = srcs + sl * CH + jl0;
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) {
-          if constexpr (CW) {
-            g[bf][i] = tb[offs[sl * CH + jw + 2 * i]];
-            wv[bf][i] = wc;
-          } else {
-            const int2 e = ells[sl * CH + jw + 2 * i];
-            g[bf][i] = tb[(unsigned)e.x >> 2];
-            wv[bf][i] = __int_as_float(e.y);
-          }
-        }
+        for (int i = 0; i < OPL; ++i) g[bf][i] = tb[(unsigned)sp[i] * (unsigned)FMR];
       };
 #pragma unroll
       for (int sl = 0; sl < kDepth - 1; ++sl) fetch(sl, sl);
 #pragma unroll
-      for (int sl = 0; sl < KC; ++sl) {
-        if (sl + kDepth - 1 < KC) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
+      for (int sl = 0; sl < 32; ++sl) {
+        if (sl + kDepth - 1 < 32) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
+        // the slot's weights from LDS (two 16-byte reads), while its gathers are in flight
+        float wv[OPL];
+        if constexpr (WM == kWEdge) {
+          const float4 x = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0);
+          const float4 y = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0 + 4);
+          wv[0] = x.x; wv[1] = x.y; wv[2] = x.z; wv[3] = x.w;
+          wv[4] = y.x; wv[5] = y.y; wv[6] = y.z; wv[7] = y.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < OPL; ++i) wv[i] = wc;
+        }
         mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) acc[i] = fmaf(g[sl % kDepth][i], wv[sl % kDepth][i], acc[i]);
+        for (int i = 0; i < OPL; ++i) acc[i] = fmaf(g[sl % kDepth][i], wv[i], acc[i]);
 #pragma unroll
         for (int i = 0; i < OPL; i += 4) pin4(acc[i], acc[i + 1], acc[i + 2], acc[i + 3]);
       }
@@ -1001,14 +1048,14 @@ __global__ __launch_bounds__(256) void k_layer_gfm(const float *__restrict__ fin
       for (int sl = 0; sl < K; ++sl) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const int2 e = ell[(size_t)sl * N + min(c0 + jw + 2 * i, N - 1)];
+          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + i, N - 1)];
           acc[i] = fmaf(tb[(unsigned)e.x >> 2], __int_as_float(e.y), acc[i]);
         }
       }
     }
 #pragma unroll
     for (int i = 0; i < OPL; ++i) {
-      const int jl = jw + 2 * i;
+      const int jl = jl0 + i;
       if (jl < nout) {
         const float y = activate(acc[i], bstage[jl], ymax);
         __builtin_nontemporal_store(y, ob + (size_t)cstage[jl] * FMR);
@@ -1228,14 +1275,37 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
 }
 
 constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 128 registers each
+// bits per entry of k_layer_bits' table that turns input bits into floats (4: 16 entries of 16
+// bytes; 8: 256 entries of 32 bytes)
+#ifndef SDNN_BITS_LUT
+#define SDNN_BITS_LUT 4
+#endif
+constexpr int kLutBits = SDNN_BITS_LUT;
+constexpr int kLutF4 = (1 << kLutBits) * kLutBits / 4;  // float4 entries of the table
+// bound on k_layer_bits' static LDS (table, mask word, dictionary cache), beside its dynamic tile
+constexpr int kBitsStaticLds = 8192 + 512 + kLutF4 * 16;
+static_assert(kLutF4 * 16 + 4 + 2 * 1024 * 4 <= kBitsStaticLds, "static LDS bound");
 
-// Value dictionary for one-byte activation codes: a 256-slot open-addressing table of fp32 bit
-// patterns in device memory; a value's code is its slot, so decoding is dict[code]. Slot 0 holds
-// +0.0 from the start (its hash is 0), so zero bytes decode to zero. kDictEmpty (a NaN pattern,
-// never an activation) marks free slots. Slots are claimed with compare-and-swap and never change
-// afterwards, so a workgroup may cache them in LDS.
+// Value dictionary for one-byte activation codes, in device memory (kDictWords words):
+//   val[256]   the value (fp32 bit pattern) of each code: decoding is val[code];
+//   key[256]   an open-addressing hash table of the values seen, by dict_hash;
+//   code[256]  the code of the value in each hash slot (kNoCode until it is published);
+//   next       the next free code.
+// Codes are handed out in order 0, 1, 2, ... (code 0 is +0.0, whose key sits in its hash slot 0
+// from the start), so a layer's first 32 values decode from distinct LDS banks. A value's slot is
+// claimed with compare-and-swap; the lane that claims it takes the next code and publishes it
+// (relaxed device-scope atomics: a reader needs the code word itself, and the values are read by
+// later kernels only); slots and codes never change afterwards, so a workgroup may cache them in
+// LDS. kDictEmpty (a
+// NaN pattern, never an activation) marks free slots.
 constexpr unsigned kDictEmpty = 0x7fc00000u;
+constexpr unsigned kNoCode = 0xffffffffu;
 constexpr int kDictSlots = 256;
+constexpr int kDictKey = 256, kDictCode = 512, kDictNext = 768, kDictWords = 1024;
+// a value whose slot was claimed by another lane waits this many reads at most for its code (the
+// claimer publishes it a few instructions after its compare-and-swap); past the bound the
+// dictionary counts as full, which sends the layer to its fp32 outputs
+constexpr int kDictWaitReads = 1 << 16;
 // Code tiles hold CR list positions (code_rows below): [tile][N][CR] bytes, list position p at tile
 // p / CR, byte p % CR.
 // The code-tile height goes with the bit tiles that write them: 128 rows after 32-row bit tiles,
@@ -1250,62 +1320,113 @@ __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
 }
 
-// Code of y: probe the workgroup's LDS copy, then the global table (claiming a free slot on the
-// way). A full table sets *overflow and returns 0; the caller's output is then not used.
-__device__ unsigned dict_code(float y, unsigned *dl, unsigned *gd, int *overflow) {
-  const unsigned key = __float_as_uint(y);
+// A workgroup's LDS cache of the dictionary: kCacheEntries (key, code) entries in two-way sets
+// (entries 2i and 2i + 1), set chosen by a multiplicative hash (a 24-bit multiply, full rate) that
+// spreads the values of a layer well (checked on the workloads' value sets). An entry is claimed
+// once, by compare-and-swap of its key from kDictEmpty to kCacheBusy; the claimer writes the code,
+// then the key (one wave's LDS operations take effect in order; a compiler barrier keeps the order);
+// entries are never replaced. A reader loads the keys before the codes, so a key it sees has its
+// code in place; kCacheBusy (a NaN pattern) never matches a value.
+constexpr int kCacheEntries = 1024;
+constexpr unsigned kCacheBusy = 0x7fc00001u;
+__device__ __forceinline__ unsigned cache_set(unsigned key) {  // first entry of the key's set (even)
+  return (__umul24(key ^ (key >> 16), 0x9E3779u) >> 12) & (unsigned)(kCacheEntries - 2);
+}
+
+// Code of the value with bits `key` from the global table, claiming a free slot and a code on the
+// way, then recorded in the LDS cache (dlk, dlc) if its set has a free entry. A full dictionary
+// sets *overflow and returns 0; the caller's output is then not used.
+__device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, unsigned *dlc, unsigned *gd,
+                                                   int *overflow) {
+  unsigned *gkey = gd + kDictKey, *gcode = gd + kDictCode;
   unsigned h = dict_hash(key);
   for (int i = 0; i < kDictSlots; ++i) {
-    const unsigned cur = dl[h];
-    if (cur == key) return h;
-    if (cur == kDictEmpty) break;
-    h = (h + 1) & (kDictSlots - 1);
-  }
-  h = dict_hash(key);
-  for (int i = 0; i < kDictSlots; ++i) {
-    unsigned cur = __hip_atomic_load(&gd[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    unsigned cur = __hip_atomic_load(&gkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    bool won = false;
     if (cur == kDictEmpty) {
-      const unsigned prev = atomicCAS(&gd[h], kDictEmpty, key);
-      cur = prev == kDictEmpty ? key : prev;
+      const unsigned prev = atomicCAS(&gkey[h], kDictEmpty, key);
+      won = prev == kDictEmpty;
+      cur = won ? key : prev;
     }
-    dl[h] = cur;
-    if (cur == key) return h;
+    if (won) {
+      // this lane claimed the slot: it takes the next code, records the value, publishes the code
+      const unsigned c = atomicAdd(gd + kDictNext, 1u);
+      if (c < (unsigned)kDictSlots) gd[c] = key;
+      __hip_atomic_store(&gcode[h], c < (unsigned)kDictSlots ? c : kNoCode - 1u, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (cur == key) {
+      unsigned c = kNoCode;
+      for (int it = 0; it < kDictWaitReads && c == kNoCode; ++it)
+        c = __hip_atomic_load(&gcode[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (c >= (unsigned)kDictSlots) break;  // no code left, or none published within the bound
+      const unsigned st = cache_set(key);
+      if (dlk[st] != key && dlk[st + 1] != key) {
+#pragma unroll
+        for (unsigned wy = 0; wy < 2; ++wy) {
+          if (atomicCAS(&dlk[st + wy], kDictEmpty, kCacheBusy) == kDictEmpty) {
+            dlc[st + wy] = c;
+            mem_fence_compiler();
+            __hip_atomic_store(&dlk[st + wy], key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            break;
+          }
+        }
+      }
+      return c;
+    }
     h = (h + 1) & (kDictSlots - 1);
   }
   *overflow = 1;
   return 0;
 }
+// The cache's answer for `key`: *code, and whether it was there.
+__device__ __forceinline__ bool cache_lookup(unsigned key, const unsigned *dlk, const unsigned *dlc, unsigned *code) {
+  const unsigned st = cache_set(key);
+  const uint2 k = *reinterpret_cast<const uint2 *>(dlk + st);
+  mem_fence_compiler();  // the keys are read before the codes
+  const uint2 c = *reinterpret_cast<const uint2 *>(dlc + st);
+  *code = k.x == key ? c.x : c.y;
+  return k.x == key || k.y == key;
+}
+__device__ __forceinline__ unsigned dict_code(float y, unsigned *dlk, unsigned *dlc, unsigned *gd, int *overflow) {
+  const unsigned key = __float_as_uint(y);
+  unsigned c;
+  if (cache_lookup(key, dlk, dlc, &c)) return c;
+  return dict_code_slow(key, dlk, dlc, gd, overflow);
+}
 
 // One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
-// (source k of list position CR t + b), decoded as dict[code]; the output is fp32
-// tiles of 32 rows as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST =
-// CR / 32). Code tiles [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR
-// bytes: RL = CR / 4 lanes read it with 4-byte loads (4 codes each), so a wave instruction serves
-// 64 / RL outputs (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane =
-// (r = lane % RL: rows 4r..4r+3, o = lane / RL); a lane runs OPL outputs, and a work item is a chunk
-// of 4 waves' outputs. The dictionary and the chunk's sources sit in LDS. A 32-row output segment
-// that is zero in every row is not stored; its bit in seglive (one bit per fp32 tile and source)
-// says so. Registers are held to 5 waves per SIMD (more waves keep more gathers in flight; 6 spill).
-// Live rows go to masks, or with spread set to the spread words of each fp32 tile (see or_mask).
-// With cols set (CW only), the launch computes the ncols columns cols[p] alone (see k_layer_gfm),
-// stores every segment of them and leaves seglive untouched.
-template <int KC, bool CW, int CR>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_layer_gfm_u8(const unsigned char *__restrict__ cin, float *__restrict__ fout,
-                                                      int N, const int2 *__restrict__ ell, int K,
-                                                      const unsigned short *__restrict__ src16, float wc,
-                                                      const float *__restrict__ bias, float ymax,
-                                                      const float *__restrict__ dict, const int *__restrict__ npos,
-                                                      unsigned *__restrict__ masks, unsigned *__restrict__ seglive,
-                                                      int tile0, unsigned *__restrict__ spread,
-                                                      const int *__restrict__ cols, int ncols, int tpx) {
+// (source k of list position CR t + b), decoded as dict[code]; the output is fp32 tiles of 32 rows
+// as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST = CR / 32). Code tiles
+// [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR bytes: RL = CR / 4
+// lanes read it with 4-byte loads (4 codes each), so a wave instruction serves OPI = 64 / RL outputs
+// (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane = (r = lane % RL: rows
+// 4r..4r+3, o = lane / RL); the lane runs the OPL = 8 consecutive outputs jw + 8 o .. jw + 8 o + 7 of
+// its wave's block of OPI * 8, so for every slot its sources come from LDS one 16-bit read each and
+// its weights in two 16-byte reads. A work item is a chunk of 4 waves' outputs. The dictionary and
+// the chunk's lists sit in LDS (kWEdge: 6 bytes per entry, 24 KiB, which leaves room for 5
+// workgroups per CU). A 32-row output segment that is zero in every row is not stored; its bit in
+// seglive (one bit per fp32 tile and source) says so. Registers are held to 5 waves per SIMD for
+// 64-row codes (more waves keep more gathers in flight; 6 spill) and 4 for 128-row codes, whose
+// lanes track twice the live rows (5 spill). Live rows go to masks, or with spread set to the
+// spread words of each fp32 tile (see or_mask). With cols set (kWOne only), the launch computes the
+// ncols columns cols[p] alone (see k_layer_gfm), stores every segment of them and leaves seglive
+// untouched.
+template <int WM, int CR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 5 : 4))) void k_layer_gfm_u8(
+    const unsigned char *__restrict__ cin, float *__restrict__ fout, int N, const int2 *__restrict__ ell, int K,
+    const unsigned short *__restrict__ src16, const float *__restrict__ w32, float wc, const float *__restrict__ bias,
+    float ymax, const float *__restrict__ dict, const int *__restrict__ npos, unsigned *__restrict__ masks,
+    unsigned *__restrict__ seglive, int tile0, unsigned *__restrict__ spread, const int *__restrict__ cols, int ncols,
+    int tpx) {
   constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
+  constexpr bool LISTS = WM != kWEll;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
-  static_assert(!CW || KC > 0, "one-weight layers take staged source lists");
-  constexpr int KS = KC > 0 ? KC : 1;
+  static_assert(32 % (OPI * OPL) == 0, "a wave's outputs lie within one bitmap word");
   __shared__ float dl[kDictSlots];
-  __shared__ int2 ells[CW ? 1 : KS * CH];
-  __shared__ unsigned offs[CW ? KS * CH : 1];  // CW: source * CR
+  __shared__ __align__(16) unsigned short srcs[LISTS ? 32 * CH : 8];
+  __shared__ __align__(16) float wts[WM == kWEdge ? 32 * CH : 4];
   __shared__ float bstage[CH];
   __shared__ int cstage[CH];  // output column of each chunk position
   __shared__ unsigned segw[ST][CH / 32];
@@ -1321,88 +1442,67 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
   const int cend = rs.cend;
   const int r = lane % RL, o = lane / RL;
   const int nvalid = active ? min(CR, R - t * CR) : 0;
-  const unsigned char *tb = cin + (size_t)t * N * CR + 4 * r;
   // output rows 4r..4r+3 of the code tile: fp32 tile ST t + r / 8, slots (4r) % 32; the list's
   // fp32 tiles end at (R + 31) / 32, so the last code tile may lack some of its fp32 tiles
   const int otile = ST * t + (r >> 3);
   float *obase = fout + ((size_t)otile * N) * 32 + (4 * r) % 32;
   const bool has_tile = otile * 32 < R;
   const int NW = (N + 31) / 32;
+  // the tile base is uniform, so a gather is one 32-bit offset from it
+  const unsigned char *tbs = cin + (size_t)t * N * CR;
+  const unsigned lofs = 4u * r;
   // live rows seen by this lane: bit 4 (r % 16) + c of word r / 16
   unsigned long long lm[CR / 64];
 #pragma unroll
   for (int h = 0; h < CR / 64; ++h) lm[h] = 0ull;
   const int jw = wave * OPI * OPL;  // first output of this wave in the chunk
+  const int jl0 = jw + o * OPL;     // this lane's outputs: jl0 .. jl0 + OPL - 1
   for (int chunk = rs.first; chunk < cend; chunk += rs.step) {
     const int c0 = chunk * CH;
     const int nout = min(CH, ncols - c0);
-    __syncthreads();  // the previous chunk is done with ells / bstage / cstage / segw
+    __syncthreads();  // the previous chunk is done with srcs / wts / bstage / cstage / segw
     for (int i = tid; i < CH; i += blockDim.x) {
       const int col = i < nout ? (cols ? cols[c0 + i] : c0 + i) : 0;
       cstage[i] = col;
       bstage[i] = i < nout ? bias[col] : 0.0f;
     }
     if (tid < ST * (CH / 32)) segw[tid / (CH / 32)][tid % (CH / 32)] = 0u;
-    if constexpr (CW) {
-      stage_src16<KC, CH>(offs, src16, ncols, c0, nout, CR);
-    } else if constexpr (KC > 0) {
-      // stage [slot][CH outputs]: two entries per 16-byte load; outputs past N get (0, 0.0f)
-      for (int i = tid; i < KC * CH / 2; i += blockDim.x) {
-        const int sl = i / (CH / 2), pr = (i % (CH / 2)) * 2;
-        const int2 *src = ell + (size_t)sl * N + c0 + pr;
-        int4 v = make_int4(0, 0, 0, 0);
-        if (pr + 1 < nout && (reinterpret_cast<uintptr_t>(src) & 15) == 0) {
-          v = *reinterpret_cast<const int4 *>(src);
-        } else {
-          if (pr < nout) { v.x = src[0].x; v.y = src[0].y; }
-          if (pr + 1 < nout) { v.z = src[1].x; v.w = src[1].y; }
-        }
-        // source offsets: fp32 32-row segments are 128 bytes, code segments CR
-        v.x = (int)(((unsigned)v.x >> 7) * CR);
-        v.z = (int)(((unsigned)v.z >> 7) * CR);
-        *reinterpret_cast<int4 *>(&ells[sl * CH + pr]) = v;
-      }
-    }
+    if constexpr (LISTS) stage_lists<WM, CH>(srcs, wts, src16, w32, ncols, c0, nout);
     __syncthreads();
-    const int jl0 = jw + o;  // this lane's outputs: jl0 + OPI i, i < OPL
     float acc[OPL][4];
 #pragma unroll
     for (int i = 0; i < OPL; ++i)
 #pragma unroll
       for (int c = 0; c < 4; ++c) acc[i][c] = 0.0f;
-    auto term = [&](int i, unsigned word, float w) {
-#pragma unroll
-      for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dl[(word >> (8 * c)) & 255u], w, acc[i][c]);
-    };
-    if constexpr (KC > 0) {
+    if constexpr (LISTS) {
       // software pipeline: a slot's gathers are issued one slot before its fmas (deeper pipelines
       // measure no faster: the gathers are limited by the vector-memory path, not by latency)
       constexpr int kDepth = 2;
       unsigned wd[kDepth][OPL];
-      float wv[kDepth][OPL];
-      // the tile base is uniform, so a gather is one 32-bit offset from it
-      const unsigned char *tbs = cin + (size_t)t * N * CR;
-      const unsigned lofs = 4u * r;
       auto fetch = [&](int sl, int bf) {
+        const unsigned short *sp = srcs + sl * CH + jl0;
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) {
-          if constexpr (CW) {
-            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + (offs[sl * CH + jl0 + OPI * i] + lofs));
-            wv[bf][i] = wc;
-          } else {
-            const int2 e = ells[sl * CH + jl0 + OPI * i];
-            wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)e.x + lofs));
-            wv[bf][i] = __int_as_float(e.y);
-          }
-        }
+        for (int i = 0; i < OPL; ++i)
+          wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)sp[i] * (unsigned)CR + lofs));
       };
 #pragma unroll
       for (int sl = 0; sl < kDepth - 1; ++sl) fetch(sl, sl);
 #pragma unroll
-      for (int sl = 0; sl < KC; ++sl) {
-        if (sl + kDepth - 1 < KC) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
+      for (int sl = 0; sl < 32; ++sl) {
+        if (sl + kDepth - 1 < 32) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
         mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
+        // the slot's weights from LDS (two 16-byte reads, ahead of the dictionary reads below)
+        float wv[OPL];
+        if constexpr (WM == kWEdge) {
+          const float4 a = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0);
+          const float4 b = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0 + 4);
+          wv[0] = a.x; wv[1] = a.y; wv[2] = a.z; wv[3] = a.w;
+          wv[4] = b.x; wv[5] = b.y; wv[6] = b.z; wv[7] = b.w;
+        } else {
+#pragma unroll
+          for (int i = 0; i < OPL; ++i) wv[i] = wc;
+        }
         // dictionary lookups run LA words ahead of the fmas that use them
         constexpr int LA = 2;
         float dv[LA + 1][4];
@@ -1417,7 +1517,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
           if (i + LA < OPL) lookup(i + LA);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dv[i % (LA + 1)][c], wv[sl % kDepth][i], acc[i][c]);
+          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dv[i % (LA + 1)][c], wv[i], acc[i][c]);
           __builtin_amdgcn_sched_barrier(0);
         }
         // this slot's fmas complete here, before the slot after next is fetched
@@ -1425,21 +1525,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
         for (int i = 0; i < OPL; ++i) pin4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
       }
     } else {
+      const unsigned char *tb = tbs + lofs;
       for (int sl = 0; sl < K; ++sl) {
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + OPI * i, N - 1)];
-          term(i, *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR), __int_as_float(e.y));
+          const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + i, N - 1)];
+          const unsigned word = *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dl[(word >> (8 * c)) & 255u], __int_as_float(e.y), acc[i][c]);
         }
       }
     }
-    // segment bits of this wave's outputs (jw .. jw + OPI OPL, within one bitmap word), per fp32 tile
+    // segment bits of this wave's outputs (jw .. jw + OPI OPL - 1, within one bitmap word), per fp32 tile
     unsigned seg[ST];
 #pragma unroll
     for (int q = 0; q < ST; ++q) seg[q] = 0u;
 #pragma unroll
     for (int i = 0; i < OPL; ++i) {
-      const int jl = jl0 + OPI * i;
+      const int jl = jl0 + i;
       const float b = bstage[jl];
       const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
                                    activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
@@ -1453,11 +1556,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
 #pragma unroll
       for (int h = 0; h < CR / 64; ++h)
         if ((r >> 4) == h) lm[h] |= (unsigned long long)bits << (4 * (r & 15));
+      // output jw + 8 oo + i of fp32 tile q is stored by lanes oo RL + 8 q .. + 7
 #pragma unroll
       for (int oo = 0; oo < OPI; ++oo)
 #pragma unroll
         for (int q = 0; q < ST; ++q)
-          seg[q] |= (((bal >> (oo * RL + 8 * q)) & 0xffull) != 0ull ? 1u : 0u) << ((jw % 32) + oo + OPI * i);
+          seg[q] |= (((bal >> (oo * RL + 8 * q)) & 0xffull) != 0ull ? 1u : 0u) << ((jw % 32) + oo * OPL + i);
     }
     if (lane == 0)
 #pragma unroll
@@ -1621,31 +1725,36 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
 }
 
 // Layer 0 from bit tiles of T rows (T = 16 or 32): every term is fma(bit, w, acc) with bit 0 or 1,
-// the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim kBitsThreads. LDS holds
-// the tile's N words and a 16-entry table that turns 4 bits into 4 floats. Lane = output j; each
-// lane carries the T rows of its output, so one ELL entry and one word serve T edge-rows. Results
+// the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim kBitsThreads. LDS
+// holds the tile's N words and a table that turns kLutBits input bits into as many floats (16
+// entries of 4 floats: few distinct entries, so a wave's reads of it are mostly broadcasts). Lane =
+// output j; each lane carries the T rows of its output, so one ELL entry and one word serve T
+// edge-rows; for 16-row tiles the table reads of a term are issued one term ahead. Results
 // go to feature-major tiles of 32 rows (list position p at tile p / 32, slot p % 32): a lane writes
 // its T rows of output j as T / 4 16-byte stores. Slots past the list's end get zeros.
 // word_shift turns an ELL source offset into the byte offset of the source's word in the tile.
 // KC = 32: the 32 ELL entries of a lane's output are all loaded before the first term is used.
 // CODES: instead of fp32 values, write each output's one-byte code in the value dictionary gd
-// (same tile layout, one byte per row); a full dictionary sets *overflow.
+// (same tile layout, one byte per row); a full dictionary sets *overflow. With *skip set (an input
+// that is not 0 or 1) the kernel does nothing.
 template <int T, int KC, bool CODES>
 __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
                                                      float *__restrict__ fout, int N, const int2 *__restrict__ ell,
                                                      int K, int word_shift, const float *__restrict__ bias,
                                                      float ymax, const int *__restrict__ count,
                                                      unsigned *__restrict__ masks, unsigned *__restrict__ gd,
-                                                     int *__restrict__ overflow) {
+                                                     int *__restrict__ overflow, const int *__restrict__ skip) {
+  if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
-  // dynamic LDS: 16-entry table (256 B), the tile's live-row mask (16 B slot), the dictionary copy
-  // (1 KiB), then the tile
+  // static LDS (addresses known at compile time, so they fold into the instructions' offsets): the
+  // table, the tile's live-row mask and the dictionary cache; dynamic LDS: the tile
+  __shared__ float4 lut[kLutF4];
+  __shared__ unsigned tilemask;
+  __shared__ __align__(8) unsigned dlk[kCacheEntries];
+  __shared__ __align__(8) unsigned dlc[kCacheEntries];
   extern __shared__ float4 smem[];
-  float4 *lut = smem;
-  unsigned &tilemask = *reinterpret_cast<unsigned *>(smem + 16);
-  unsigned *dl = reinterpret_cast<unsigned *>(smem + 17);
-  W *tile = reinterpret_cast<W *>(smem + 17 + kDictSlots / 4);
+  W *tile = reinterpret_cast<W *>(smem);
   const int R = *count;
   const int ntiles = (R + T - 1) / T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
@@ -1655,10 +1764,14 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   // codes with whole tiles as items: keep the tiles of one code group on one XCD
   const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (CR / T)) == 0;
   const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
-  if (tid < 16) lut[tid] = make_float4((float)(tid & 1), (float)((tid >> 1) & 1), (float)((tid >> 2) & 1), (float)((tid >> 3) & 1));
+  for (int i = tid; i < kLutF4; i += blockDim.x) {
+    constexpr int per = kLutBits / 4;  // float4 per entry
+    const unsigned q = (unsigned)(i / per) >> (4 * (i % per));  // entry i / per, bits 4 (i % per) ..
+    lut[i] = make_float4((float)(q & 1u), (float)((q >> 1) & 1u), (float)((q >> 2) & 1u), (float)((q >> 3) & 1u));
+  }
   if (tid == 0) tilemask = 0u;
   if (CODES)
-    for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = kDictEmpty;
+    for (int i = tid; i < kCacheEntries; i += blockDim.x) dlk[i] = kDictEmpty;
   for (int w = blockIdx.x; w < items; w += gridDim.x) {
     const int t = grouped ? code_group_tile(w, CR / T) : w / ch.nchunks;
     const int c = grouped ? 0 : w % ch.nchunks;
@@ -1688,11 +1801,30 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
       float acc[T];
 #pragma unroll
       for (int b = 0; b < T; ++b) acc[b] = 0.0f;
-      // one term: the source's word gives the T input bits; each nibble picks 4 floats (0 or 1)
-      auto term = [&](unsigned word, float wv) {
-        float4 v[T / 4];
+      // the source's word gives the T input bits; each group of kLutBits picks that many floats
+      // (0 or 1) from the table
+      auto expand = [&](unsigned word, float4 (&v)[T / 4]) {
+        if constexpr (kLutBits == 4) {
+          // byte offset of nibble 2k's entry: byte k of (word << 4) with its low 4 bits cleared; of
+          // nibble 2k + 1's: byte k of word, likewise (one byte-select and per nibble)
+          const unsigned x = word << 4;
+          const char *lb = reinterpret_cast<const char *>(lut);
 #pragma unroll
-        for (int n = 0; n < T / 4; ++n) v[n] = lut[(word >> (4 * n)) & 15u];
+          for (int k = 0; k < T / 8; ++k) {
+            v[2 * k] = *reinterpret_cast<const float4 *>(lb + ((x >> (8 * k)) & 0xF0u));
+            v[2 * k + 1] = *reinterpret_cast<const float4 *>(lb + ((word >> (8 * k)) & 0xF0u));
+          }
+        } else {
+          constexpr int per = kLutBits / 4;
+#pragma unroll
+          for (int n = 0; n < T / kLutBits; ++n) {
+            const unsigned e = (word >> (kLutBits * n)) & ((1u << kLutBits) - 1u);
+#pragma unroll
+            for (int q = 0; q < per; ++q) v[per * n + q] = lut[per * e + q];
+          }
+        }
+      };
+      auto apply = [&](const float4 (&v)[T / 4], float wv) {
 #pragma unroll
         for (int n = 0; n < T / 4; ++n) {
           acc[4 * n] = fmaf(v[n].x, wv, acc[4 * n]);
@@ -1704,53 +1836,60 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
       if constexpr (KC > 0) {
         // slots go in groups of 16 with the issue order pinned by scheduling barriers: a group's
         // tile words are read while the next group's ELL entries load, then its terms run
-        static_assert(KC % 16 == 0, "KC must be a multiple of 16");
-        int2 e[16];
+        // slots in groups of G (16 rows: 16 with the table reads one term ahead; 32 rows: 8, reads
+        // not ahead, which keeps the lane within 128 registers)
+        constexpr int G = T == 16 ? 16 : 8;
+        constexpr bool AHEAD = T == 16;
+        static_assert(KC % G == 0, "KC must be a multiple of the group");
+        int2 e[G];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) e[i] = ej[(size_t)i * N];
+        for (int i = 0; i < G; ++i) e[i] = ej[(size_t)i * N];
 #pragma unroll
-        for (int h = 0; h < KC; h += 16) {
+        for (int h = 0; h < KC; h += G) {
           mem_fence_compiler();
-          unsigned wd[16];
-          float wv[16];
+          unsigned wd[G];
+          float wv[G];
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
+          for (int i = 0; i < G; ++i) {
             wd[i] = *reinterpret_cast<const W *>(tb + (e[i].x >> word_shift));
             wv[i] = __int_as_float(e[i].y);
           }
-          if (h + 16 < KC) {
+          if (h + G < KC) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) e[i] = ej[(size_t)(h + 16 + i) * N];
+            for (int i = 0; i < G; ++i) e[i] = ej[(size_t)(h + G + i) * N];
           }
           mem_fence_compiler();
-          // table reads run one term ahead of the fmas
-          float4 vc[T / 4], vn[T / 4];
+          if constexpr (AHEAD) {
+            // table reads run one term ahead of the fmas (two buffers by parity: no copies)
+            float4 vb[2][T / 4];
+            expand(wd[0], vb[0]);
 #pragma unroll
-          for (int n = 0; n < T / 4; ++n) vc[n] = lut[(wd[0] >> (4 * n)) & 15u];
+            for (int i = 0; i < G; ++i) {
+              if (i + 1 < G) expand(wd[i + 1], vb[(i + 1) & 1]);
+              apply(vb[i & 1], wv[i]);
+              // this term's fmas complete here, and the next table reads are issued after them
 #pragma unroll
-          for (int i = 0; i < 16; ++i) {
-            if (i + 1 < 16) {
-#pragma unroll
-              for (int n = 0; n < T / 4; ++n) vn[n] = lut[(wd[i + 1] >> (4 * n)) & 15u];
+              for (int b = 0; b < T; b += 4) pin4(acc[b], acc[b + 1], acc[b + 2], acc[b + 3]);
+              mem_fence_compiler();
             }
+          } else {
 #pragma unroll
-            for (int n = 0; n < T / 4; ++n) {
-              acc[4 * n] = fmaf(vc[n].x, wv[i], acc[4 * n]);
-              acc[4 * n + 1] = fmaf(vc[n].y, wv[i], acc[4 * n + 1]);
-              acc[4 * n + 2] = fmaf(vc[n].z, wv[i], acc[4 * n + 2]);
-              acc[4 * n + 3] = fmaf(vc[n].w, wv[i], acc[4 * n + 3]);
-              vc[n] = vn[n];
+            for (int i = 0; i < G; ++i) {
+              float4 v[T / 4];
+              expand(wd[i], v);
+              apply(v, wv[i]);
+#pragma unroll
+              for (int b = 0; b < T; b += 4) pin4(acc[b], acc[b + 1], acc[b + 2], acc[b + 3]);
+              mem_fence_compiler();
             }
-            // this term's fmas complete here, and the next table reads are issued after them
-#pragma unroll
-            for (int b = 0; b < T; b += 4) pin4(acc[b], acc[b + 1], acc[b + 2], acc[b + 3]);
-            mem_fence_compiler();
           }
         }
       } else {
         for (int sl = 0; sl < K; ++sl) {
           const int2 e = ej[(size_t)sl * N];
-          term(*reinterpret_cast<const W *>(tb + (e.x >> word_shift)), __int_as_float(e.y));
+          float4 v[T / 4];
+          expand(*reinterpret_cast<const W *>(tb + (e.x >> word_shift)), v);
+          apply(v, __int_as_float(e.y));
         }
       }
       if (jin) {
@@ -1759,18 +1898,31 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         if constexpr (CODES) {
           uint4 *dst = reinterpret_cast<uint4 *>(reinterpret_cast<unsigned char *>(fout) +
                                                  ((size_t)(p0 / CR) * N + j) * CR + p0 % CR);
-          unsigned cw[T / 4];
+          // every row's value (in place of its accumulator), then per 16 rows the LDS cache's codes;
+          // the full lookup (global table included) only on a lane where one of them missed
 #pragma unroll
-          for (int n = 0; n < T / 4; ++n) {
-            unsigned word = 0u;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const float y = activate(acc[4 * n + u], bj, ymax);
-              live |= (y > 0.0f ? 1u : 0u) << (4 * n + u);
-              word |= dict_code(y, dl, gd, overflow) << (8 * u);
-            }
-            cw[n] = word;
+          for (int u = 0; u < T; ++u) {
+            acc[u] = activate(acc[u], bj, ymax);
+            live |= (acc[u] > 0.0f ? 1u : 0u) << u;
           }
+          unsigned cw[T / 4];
+          // rows [R0, R0 + 16), R0 a compile-time constant (so that every array index is one)
+          auto encode16 = [&](auto r0c) {
+            constexpr int R0 = decltype(r0c)::value;
+            unsigned code[16];
+            bool miss = false;
+#pragma unroll
+            for (int u = 0; u < 16; ++u) miss |= !cache_lookup(__float_as_uint(acc[R0 + u]), dlk, dlc, &code[u]);
+            if (miss) {
+#pragma unroll
+              for (int u = 0; u < 16; ++u) code[u] = dict_code(acc[R0 + u], dlk, dlc, gd, overflow);
+            }
+#pragma unroll
+            for (int n = 0; n < 4; ++n)
+              cw[R0 / 4 + n] = code[4 * n] | (code[4 * n + 1] << 8) | (code[4 * n + 2] << 16) | (code[4 * n + 3] << 24);
+          };
+          encode16(std::integral_constant<int, 0>{});
+          if constexpr (T == 32) encode16(std::integral_constant<int, 16>{});
 #pragma unroll
           for (int n = 0; n < T / 16; ++n) dst[n] = make_uint4(cw[4 * n], cw[4 * n + 1], cw[4 * n + 2], cw[4 * n + 3]);
           // the rest of the last code tile gets code 0 (+0.0)
@@ -1851,8 +2003,9 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
                                                       const int *__restrict__ count, unsigned *__restrict__ masks,
                                                       float *__restrict__ yout, const int *__restrict__ ids,
                                                       const unsigned *__restrict__ dict, const int *__restrict__ cols,
-                                                      int ncols) {
+                                                      int ncols, const int *__restrict__ skip) {
   static_assert(!ROWMAJOR || T == 32, "rows of fp32 outputs from 32-row bit tiles");
+  if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
   constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
@@ -2052,12 +2205,15 @@ struct LayerDev {
   // uniform layer: every column holds exactly K sources, all weights are w and all biases b
   bool uniform = false;
   float w = 0.0f, b = 0.0f;
-  // uniform layer with K == 32 on widths staged in LDS, and layer 0 of any width: [K/8][N][8] u16
-  // source indices, eight per 16-byte load
+  // layer with K == 32 on widths staged in LDS, and uniform layer 0 of any width: [K/8][N][8] u16
+  // source indices, eight per 16-byte load; unless the layer is uniform, its weights in the same
+  // grouping, [K/8][N][8] fp32 (w8)
   const uint4 *ell16 = nullptr;
-  // global-tile path, uniform layer with K == 32 and N <= 65536: [K][N] u16 source indices (the
-  // ELL's sources without the repeated weight)
+  const float *w8 = nullptr;
+  // global-tile path, layer with K == 32 and N <= 65536: [K][N] u16 source indices (the ELL's
+  // sources), and unless the layer is uniform its weights [K][N] fp32 beside them (w32)
   const unsigned short *src16 = nullptr;
+  const float *w32 = nullptr;
   // distinct columns (uniform layer with K == 32): columns with equal source lists have equal
   // outputs, so only the D representatives cols[0..D) need computing, with their source lists in
   // src16c ([K][D] u16, beside src16) and ell16c ([K/8][D][8], beside ell16). Usable (dedup_ok) once
@@ -2073,6 +2229,7 @@ struct LayerDev {
   // is the column at position p, gell16[c] its sources
   const int *gcols[3] = {}, *gcolsc[3] = {};
   const uint4 *gell16[3] = {}, *gell16c[3] = {};
+  const float *gw8[3] = {};  // the weights of gell16's positions (layers with w8)
   int D = 0;
   bool dedup_ok = false;
 };
@@ -2116,7 +2273,7 @@ struct sdnn_net {
   int *rownz = nullptr, *counts = nullptr;
   int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [2] dictionary full,
                         // [4 + i] positions in list i
-  unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (256 fp32 bit patterns)
+  unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (kDictWords words; decoding reads the first 256)
   unsigned *seglive = nullptr;  // path 1: per fp32 tile, one bit per source: the segment was stored
   unsigned *part[2] = {nullptr, nullptr};  // path 1: partial liveness words of few-tile layers, by layer parity
   unsigned *spread = nullptr;              // path 1: liveness words of large layers, one 128-byte line each
@@ -2130,6 +2287,10 @@ struct sdnn_net {
   // progress word of few-tile layers, in coherent host memory written by the device (see
   // progress_word); progress_dev is its device address
   unsigned long long *progress = nullptr, *progress_dev = nullptr;
+  // word in coherent host memory where a compaction reports its count and flags (see k_compact);
+  // notify_dev is its device address, notify_seq the tag of the last report asked for
+  unsigned long long *notify = nullptr, *notify_dev = nullptr;
+  uint32_t notify_seq = 0;
   uint32_t run_gen = 0;      // generation of the current infer, in the progress word's top bits
   std::vector<hipEvent_t> events;
   // profiling
@@ -2176,7 +2337,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
-  w.dict = off; off += 256 * sizeof(unsigned);
+  w.dict = off; off += 1024 * sizeof(unsigned);
   w.seglive = off;
   if (net->path == 1) off += align_up(rows / 32 * (size_t)((net->N + 31) / 32) * sizeof(unsigned), a);
   for (int i = 0; i < 2; ++i) {
@@ -2212,8 +2373,8 @@ hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerD
   // distinct columns only, when the layer's duplicates need not be computed
   const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
   hipLaunchKernelGGL((k_layer_lds<B, KC>), dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
-                     ld.ell, ld.K, dd ? ld.ell16c : ld.ell16, ld.w, ld.bias, net->ymax, ids, count, net->masks, rownz,
-                     dd ? ld.cols : nullptr, dd ? ld.D : net->N);
+                     ld.ell, ld.K, dd ? ld.ell16c : ld.ell16, dd ? nullptr : ld.w8, ld.w, ld.bias, net->ymax, ids,
+                     count, net->masks, rownz, dd ? ld.cols : nullptr, dd ? ld.D : net->N);
   return hipGetLastError();
 }
 
@@ -2240,7 +2401,7 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   const dim3 grid(8 * per_xcd);
   *S_out = per_xcd * parts;
   *nt_out = ntiles_h;
-  if (ld.src16)
+  if (ld.uniform && ld.src16)
     hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
                        ld.ell, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev,
                        prev_S, prev_nt, masks_prev, masks_clear, count_out, live_before, progress, progress_tag,
@@ -2291,18 +2452,18 @@ hipError_t launch_gfm(sdnn_net *net, const LayerDev &ld, const float *fin, float
   const dim3 grid(8 * per_xcd);
   for (int r = 0; r < rounds; ++r) {
     int *cnt = r == 0 ? count_out : nullptr;
-    if (ld.K == 32 && ld.src16)
-      hipLaunchKernelGGL((k_layer_gfm<32, 32, true>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         s16, ld.w, ld.bias, net->ymax, npos, masks, r * 8 * tpx, masks_prev, masks_clear, cnt, spread,
-                         cols, ncols, tpx);
-    else if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm<32, 32, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
-                         (const int *)nullptr, net->N, 1);
+    if (ld.K == 32 && ld.src16 && ld.uniform)
+      hipLaunchKernelGGL((k_layer_gfm<kWOne>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K, s16,
+                         (const float *)nullptr, ld.w, ld.bias, net->ymax, npos, masks, r * 8 * tpx, masks_prev,
+                         masks_clear, cnt, spread, cols, ncols, tpx);
+    else if (ld.K == 32 && ld.src16 && ld.w32)
+      hipLaunchKernelGGL((k_layer_gfm<kWEdge>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         ld.src16, ld.w32, 0.0f, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt,
+                         spread, (const int *)nullptr, net->N, 1);
     else
-      hipLaunchKernelGGL((k_layer_gfm<32, 0, false>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
-                         ld.src16, ld.w, ld.bias, net->ymax, npos, masks, r * 8, masks_prev, masks_clear, cnt, spread,
-                         (const int *)nullptr, net->N, 1);
+      hipLaunchKernelGGL((k_layer_gfm<kWEll>), grid, dim3(256), 0, net->stream, fin, fout, net->N, ld.ell, ld.K,
+                         (const unsigned short *)nullptr, (const float *)nullptr, 0.0f, ld.bias, net->ymax, npos,
+                         masks, r * 8, masks_prev, masks_clear, cnt, spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2317,7 +2478,8 @@ hipError_t launch_to_fm(sdnn_net *net, const float *y, float *fm, const int *ids
 template <int T>
 size_t bits_lds_bytes(const sdnn_net *net) {
   using W = typename BitWord<T>::type;
-  return 17 * 16 + kDictSlots * 4 + ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+  // dynamic part (the tile); the table and the dictionary cache are static
+  return ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
 }
 
 template <int T>
@@ -2334,7 +2496,7 @@ hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bi
   static bool configured = false;
   if (!configured) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T, KC, CODES>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - kBitsStaticLds);
     if (e != hipSuccess) return e;
     configured = true;
   }
@@ -2348,7 +2510,7 @@ hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bi
   while ((1 << wshift) < (int)sizeof(W)) ++wshift;
   hipLaunchKernelGGL((k_layer_bits<T, KC, CODES>), dim3(net->cus * per_cu), dim3(kBitsThreads), lds, net->stream,
                      reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, shift - wshift, ld.bias, net->ymax,
-                     count, net->masks, net->dict, net->misc + kOverflowSlot);
+                     count, net->masks, net->dict, net->misc + kOverflowSlot, net->misc);
   return hipGetLastError();
 }
 
@@ -2490,7 +2652,7 @@ hipError_t launch_layer_count_k(sdnn_net *net, const LayerDev &ld, const void *b
                      reinterpret_cast<const W *>(bits), cout, net->N,
                      dd ? (ld.ell16cs ? ld.ell16cs : ld.ell16c) : (ld.ell16s ? ld.ell16s : ld.ell16), net->misc, count, masks,
                      yout, ids, reinterpret_cast<const unsigned *>(net->dict), dd ? ld.cols : nullptr,
-                     dd ? ld.D : net->N);
+                     dd ? ld.D : net->N, net->misc);
   return hipGetLastError();
 }
 template <int T>
@@ -2518,18 +2680,18 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   const int rounds = (int)((max_tiles + 8 * tpx - 1) / (8 * tpx));
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
-    if (ld.K == 32 && ld.src16)
-      hipLaunchKernelGGL((k_layer_gfm_u8<32, true, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive,
-                         r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
-    else if (ld.K == 32)
-      hipLaunchKernelGGL((k_layer_gfm_u8<32, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
+    if (ld.K == 32 && ld.src16 && ld.uniform)
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+                         dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, dict, npos, masks,
+                         net->seglive, r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
+    else if (ld.K == 32 && ld.src16 && ld.w32)
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+                         ld.K, ld.src16, ld.w32, 0.0f, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
                          net->spread, (const int *)nullptr, net->N, 1);
     else
-      hipLaunchKernelGGL((k_layer_gfm_u8<0, false, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
-                         ld.K, ld.src16, ld.w, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
-                         net->spread, (const int *)nullptr, net->N, 1);
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+                         ld.K, (const unsigned short *)nullptr, (const float *)nullptr, 0.0f, ld.bias, net->ymax, dict,
+                         npos, masks, net->seglive, r * 8, net->spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -2790,6 +2952,10 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
                                      hipHostMallocCoherent));
     *net->progress = 0ull;
     HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->progress_dev), net->progress, 0));
+    HIP_OR_POISON(net, hipHostMalloc(reinterpret_cast<void **>(&net->notify), sizeof(unsigned long long),
+                                     hipHostMallocCoherent));
+    *net->notify = 0ull;
+    HIP_OR_POISON(net, hipHostGetDevicePointer(reinterpret_cast<void **>(&net->notify_dev), net->notify, 0));
     // the device address of the static workspace on this device (sdnn_infer_static)
     void *sw = nullptr;
     st = scratch_address(net->device, &sw);
@@ -2822,61 +2988,100 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
     }
   }
   if (net->path == 1 && N <= 65536) {
-    // uniform layers with 32 sources per column: 16-bit source lists, [K][N] like the ELL
+    // layers with 32 sources per column: 16-bit source lists, [K][N] like the ELL, and unless the
+    // layer is uniform its weights [K][N] fp32 (6 bytes per edge for the large-layer kernels)
     std::vector<int32_t> sel;
     for (int32_t i = 0; i < nl; ++i)
-      if (net->layers[(size_t)l0 + i].uniform && net->layers[(size_t)l0 + i].K == 32) sel.push_back(i);
+      if (net->layers[(size_t)l0 + i].K == 32) sel.push_back(i);
     if (!sel.empty()) {
       const size_t per = (size_t)32 * N;
+      std::vector<size_t> woff(sel.size() + 1, 0);  // weight arrays of the non-uniform layers
+      for (size_t q = 0; q < sel.size(); ++q)
+        woff[q + 1] = woff[q] + (net->layers[(size_t)l0 + sel[q]].uniform ? 0 : per);
       std::vector<uint16_t> hs(per * sel.size());
+      std::vector<float> hw(woff[sel.size()]);
       parallel_for((int32_t)sel.size(), [&](int32_t q) {
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         uint16_t *dst = hs.data() + per * (size_t)q;
-        for (int32_t j = 0; j < N; ++j)
-          for (int sl = 0; sl < 32; ++sl) dst[(size_t)sl * N + j] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
+        const bool weights = woff[(size_t)q + 1] > woff[(size_t)q];
+        float *wd = hw.data() + woff[(size_t)q];
+        for (int32_t j = 0; j < N; ++j) {
+          // a column with fewer than 32 sources is padded with (source 0, weight +0), which adds
+          // fma(y, +0, acc) = acc exactly, as in the ELL
+          const int deg = (int)(cp[j + 1] - cp[j]);
+          for (int sl = 0; sl < 32; ++sl) {
+            dst[(size_t)sl * N + j] = sl < deg ? (uint16_t)src_at(sel[(size_t)q], cp[j] + sl) : (uint16_t)0;
+            if (weights) wd[(size_t)sl * N + j] = sl < deg ? val[cp[j] + sl] : 0.0f;
+          }
+        }
       });
+      const size_t sbytes = align_up(hs.size() * sizeof(uint16_t), 256);
+      const size_t wbytes = hw.size() * sizeof(float);
       char *ms = nullptr;
-      e = hipMalloc(reinterpret_cast<void **>(&ms), hs.size() * sizeof(uint16_t));
+      e = hipMalloc(reinterpret_cast<void **>(&ms), sbytes + wbytes);
       if (e != hipSuccess) {
         (void)hipGetLastError();
-        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", hs.size() * sizeof(uint16_t), hipGetErrorString(e));
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", sbytes + wbytes, hipGetErrorString(e));
       }
       net->allocations.push_back(ms);
       HIP_OR_POISON(net, hipMemcpyAsync(ms, hs.data(), hs.size() * sizeof(uint16_t), hipMemcpyHostToDevice, s));
+      if (wbytes) HIP_OR_POISON(net, hipMemcpyAsync(ms + sbytes, hw.data(), wbytes, hipMemcpyHostToDevice, s));
       HIP_OR_POISON(net, hipStreamSynchronize(s));
-      for (size_t q = 0; q < sel.size(); ++q)
-        net->layers[(size_t)l0 + sel[q]].src16 = reinterpret_cast<const unsigned short *>(ms) + per * q;
+      for (size_t q = 0; q < sel.size(); ++q) {
+        LayerDev &ld = net->layers[(size_t)l0 + sel[q]];
+        ld.src16 = reinterpret_cast<const unsigned short *>(ms) + per * q;
+        if (!ld.uniform) ld.w32 = reinterpret_cast<const float *>(ms + sbytes) + woff[q];
+      }
     }
   }
   {
     // 16-bit source indices in groups of 8 per output ([4][N][8] u16, one 16-byte load per group):
-    // every uniform layer with 32 sources per column on widths staged in LDS, and layer 0 of a
-    // uniform network of any width (for the counting kernel)
+    // every layer with 32 sources per column on widths staged in LDS, with its weights grouped the
+    // same way ([4][N][8] fp32) unless it is uniform; and layer 0 of a uniform network of any width
+    // (for the counting kernel). Columns with fewer than 32 sources are padded with (source 0,
+    // weight +0), a no-op term as in the ELL.
     std::vector<int32_t> sel;
     for (int32_t i = 0; i < nl; ++i) {
       const LayerDev &ld = net->layers[(size_t)l0 + i];
-      if (ld.uniform && ld.K == 32 && N <= 65536 && (net->path == 0 || l0 + i == 0)) sel.push_back(i);
+      if (ld.K == 32 && N <= 65536 && (net->path == 0 || (ld.uniform && l0 + i == 0))) sel.push_back(i);
     }
     if (!sel.empty()) {
       const size_t per = (size_t)32 * N;
+      std::vector<size_t> woff(sel.size() + 1, 0);
+      for (size_t q = 0; q < sel.size(); ++q)
+        woff[q + 1] = woff[q] + (net->layers[(size_t)l0 + sel[q]].uniform ? 0 : per);
       std::vector<uint16_t> h16(per * sel.size());
+      std::vector<float> hw(woff[sel.size()]);
       parallel_for((int32_t)sel.size(), [&](int32_t q) {
         const int64_t *cp = col_ptr + (size_t)sel[(size_t)q] * (N + 1);
         uint16_t *dst = h16.data() + per * (size_t)q;
-        for (int32_t j = 0; j < N; ++j)
-          for (int sl = 0; sl < 32; ++sl)
-            dst[((size_t)(sl / 8) * N + j) * 8 + sl % 8] = (uint16_t)src_at(sel[(size_t)q], cp[j] + sl);
+        const bool weights = woff[(size_t)q + 1] > woff[(size_t)q];
+        float *wd = hw.data() + woff[(size_t)q];
+        for (int32_t j = 0; j < N; ++j) {
+          const int deg = (int)(cp[j + 1] - cp[j]);
+          for (int sl = 0; sl < 32; ++sl) {
+            const size_t at = ((size_t)(sl / 8) * N + j) * 8 + sl % 8;
+            dst[at] = sl < deg ? (uint16_t)src_at(sel[(size_t)q], cp[j] + sl) : (uint16_t)0;
+            if (weights) wd[at] = sl < deg ? val[cp[j] + sl] : 0.0f;
+          }
+        }
       });
+      const size_t sbytes = align_up(h16.size() * sizeof(uint16_t), 256);
+      const size_t wbytes = hw.size() * sizeof(float);
       char *m16 = nullptr;
-      e = hipMalloc(reinterpret_cast<void **>(&m16), h16.size() * sizeof(uint16_t));
+      e = hipMalloc(reinterpret_cast<void **>(&m16), sbytes + wbytes);
       if (e != hipSuccess) {
         (void)hipGetLastError();
-        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", h16.size() * sizeof(uint16_t), hipGetErrorString(e));
+        return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", sbytes + wbytes, hipGetErrorString(e));
       }
       net->allocations.push_back(m16);
       HIP_OR_POISON(net, hipMemcpy(m16, h16.data(), h16.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
-      for (size_t q = 0; q < sel.size(); ++q)
-        net->layers[(size_t)l0 + sel[q]].ell16 = reinterpret_cast<const uint4 *>(m16) + (per / 8) * q;
+      if (wbytes) HIP_OR_POISON(net, hipMemcpy(m16 + sbytes, hw.data(), wbytes, hipMemcpyHostToDevice));
+      for (size_t q = 0; q < sel.size(); ++q) {
+        LayerDev &ld = net->layers[(size_t)l0 + sel[q]];
+        ld.ell16 = reinterpret_cast<const uint4 *>(m16) + (per / 8) * q;
+        if (!ld.uniform) ld.w8 = reinterpret_cast<const float *>(m16 + sbytes) + woff[q];
+      }
     }
   }
   {
@@ -2979,6 +3184,7 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
       // u = (q * nclass + c) * 2 + v: layer gsel[q], class c, v = 0 all columns / 1 distinct ones
       std::vector<std::vector<int32_t>> gcol(2 * ng);
       std::vector<std::vector<uint16_t>> gl(2 * ng);    // their [4][D][8] lists
+      std::vector<std::vector<float>> gw(2 * ng);       // and weights (layers with w8)
       parallel_for((int32_t)(2 * ng), [&](int32_t u) {
         const int32_t i = gsel[(size_t)u / 2 / (size_t)nclass];
         const int cls = (u / 2) % nclass;
@@ -2994,27 +3200,44 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         if (pos.empty()) return;
         const int64_t *cp = col_ptr + (size_t)i * (N + 1);
         const int D = (int)pos.size();
+        const bool weights = ld.w8 != nullptr;
+        // sources (and weights) by position; short columns padded with (0, +0) as in ell16
         std::vector<uint16_t> lists((size_t)D * 32);
-        for (int p = 0; p < D; ++p)
-          for (int sl = 0; sl < 32; ++sl) lists[(size_t)p * 32 + sl] = (uint16_t)src_at(i, cp[pos[(size_t)p]] + sl);
+        std::vector<float> wl(weights ? (size_t)D * 32 : 0);
+        for (int p = 0; p < D; ++p) {
+          const int32_t j = pos[(size_t)p];
+          const int deg = (int)(cp[j + 1] - cp[j]);
+          for (int sl = 0; sl < 32; ++sl) {
+            lists[(size_t)p * 32 + sl] = sl < deg ? (uint16_t)src_at(i, cp[j] + sl) : (uint16_t)0;
+            if (weights) wl[(size_t)p * 32 + sl] = sl < deg ? val[cp[j] + sl] : 0.0f;
+          }
+        }
         const std::vector<int32_t> ord = conflict_grouped_order(lists, D, 16 >> cls);
         std::vector<int32_t> &gc = gcol[(size_t)u];
         std::vector<uint16_t> &g16 = gl[(size_t)u];
+        std::vector<float> &g32 = gw[(size_t)u];
         gc.resize((size_t)D);
         g16.resize((size_t)D * 32);
+        if (weights) g32.resize((size_t)D * 32);
         for (int p = 0; p < D; ++p) {
           const int32_t q = ord[(size_t)p];
           gc[(size_t)p] = pos[(size_t)q];
-          for (int sl = 0; sl < 32; ++sl) g16[((size_t)(sl / 8) * D + p) * 8 + sl % 8] = lists[(size_t)q * 32 + sl];
+          for (int sl = 0; sl < 32; ++sl) {
+            const size_t at = ((size_t)(sl / 8) * D + p) * 8 + sl % 8;
+            g16[at] = lists[(size_t)q * 32 + sl];
+            if (weights) g32[at] = wl[(size_t)q * 32 + sl];
+          }
         }
       });
       size_t bytes = 0;
-      std::vector<size_t> co(2 * ng), lo(2 * ng);
+      std::vector<size_t> co(2 * ng), lo(2 * ng), wo(2 * ng);
       for (size_t u = 0; u < 2 * ng; ++u) {
         co[u] = bytes;
         bytes += align_up(gcol[u].size() * sizeof(int32_t), 256);
         lo[u] = bytes;
         bytes += align_up(gl[u].size() * sizeof(uint16_t), 256);
+        wo[u] = bytes;
+        bytes += align_up(gw[u].size() * sizeof(float), 256);
       }
       if (bytes) {
         char *mg = nullptr;
@@ -3028,11 +3251,17 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
           if (gcol[u].empty()) continue;
           HIP_OR_POISON(net, hipMemcpy(mg + co[u], gcol[u].data(), gcol[u].size() * sizeof(int32_t), hipMemcpyHostToDevice));
           HIP_OR_POISON(net, hipMemcpy(mg + lo[u], gl[u].data(), gl[u].size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+          if (!gw[u].empty())
+            HIP_OR_POISON(net, hipMemcpy(mg + wo[u], gw[u].data(), gw[u].size() * sizeof(float), hipMemcpyHostToDevice));
           LayerDev &ld = net->layers[(size_t)l0 + gsel[u / 2 / (size_t)nclass]];
           const int cls = (int)((u / 2) % (size_t)nclass);
           const int *gc = reinterpret_cast<const int *>(mg + co[u]);
           const uint4 *g16 = reinterpret_cast<const uint4 *>(mg + lo[u]);
-          if (u % 2 == 0) { ld.gcols[cls] = gc; ld.gell16[cls] = g16; }
+          if (u % 2 == 0) {
+            ld.gcols[cls] = gc;
+            ld.gell16[cls] = g16;
+            if (!gw[u].empty()) ld.gw8[cls] = reinterpret_cast<const float *>(mg + wo[u]);
+          }
           else { ld.gcolsc[cls] = gc; ld.gell16c[cls] = g16; }
         }
       }
@@ -3072,7 +3301,9 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         const uint4 *g16 = dd ? ld.gell16c[c] : ld.gell16[c];
         const uint4 *e16 = g16 ? g16 : (dd ? ld.ell16c : ld.ell16);
         const int *cl = g16 ? (dd ? ld.gcolsc[c] : ld.gcols[c]) : (dd ? ld.cols : nullptr);
-        hp[(size_t)(l - t0)] = LayerPtr{ld.ell, e16, ld.bias, cl, ld.w, ld.K, dd ? ld.D : N};
+        // per-edge weights in the same grouping as the sources (null for a uniform layer)
+        const float *w8 = ld.w8 ? (g16 ? ld.gw8[c] : ld.w8) : nullptr;
+        hp[(size_t)(l - t0)] = LayerPtr{ld.ell, e16, w8, ld.bias, cl, ld.w, ld.K, dd ? ld.D : N};
       }
       HIP_OR_POISON(net, hipMemcpy(net->lp_dev[c] + t0, hp.data(), hp.size() * sizeof(LayerPtr), hipMemcpyHostToDevice));
     }
@@ -3122,6 +3353,47 @@ hipError_t poll_step(sdnn_net *net, PollRing &ring, int32_t l, int32_t idx, int6
   return hipSuccess;
 }
 
+// Report of a compaction enqueued with a tag (see k_compact): the live count and the flags.
+struct Report {
+  int64_t count = 0;
+  bool nonbinary = false, overflow = false;
+};
+
+// Tag for the next reporting compaction (24 bits, never 0: the word starts at 0).
+unsigned long long next_report_tag(sdnn_net *net) {
+  net->notify_seq = (net->notify_seq + 1) & 0xffffffu;
+  if (net->notify_seq == 0) net->notify_seq = 1;
+  return net->notify_seq;
+}
+
+// Wait for the report tagged `tag`: spin on the word in coherent host memory (no OS wake-up in the
+// way); if none arrives within 2 s, wait for the stream and read the count (at count_dev) and the
+// flags by copies.
+hipError_t wait_report(sdnn_net *net, unsigned long long tag, const int *count_dev, Report *r) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t it = 1;; ++it) {
+    const unsigned long long w = __atomic_load_n(net->notify, __ATOMIC_ACQUIRE);
+    if ((w >> 40) == tag) {
+      r->count = (int64_t)(w & 0xffffffffull);
+      r->nonbinary = ((w >> 32) & 1ull) != 0;
+      r->overflow = ((w >> 33) & 1ull) != 0;
+      return hipSuccess;
+    }
+    if ((it & 4095u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(2)) break;
+    __builtin_ia32_pause();
+  }
+  hipError_t e = hipStreamSynchronize(net->stream);
+  if (e != hipSuccess) return e;
+  int32_t v[3] = {0, 0, 0};
+  e = hipMemcpy(&v[0], count_dev, sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(&v[1], net->misc, sizeof(int32_t), hipMemcpyDeviceToHost);
+  if (e == hipSuccess) e = hipMemcpy(&v[2], net->misc + kOverflowSlot, sizeof(int32_t), hipMemcpyDeviceToHost);
+  r->count = v[0];
+  r->nonbinary = v[1] != 0;
+  r->overflow = v[2] != 0;
+  return e;
+}
+
 // LDS-tile path: row-major activations ping-pong between two buffers; the live list is compacted
 // after every layer.
 sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
@@ -3153,7 +3425,8 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
       }
       // the final list: positions still live after the last layer (bits per 32 positions)
       hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, 32, net->ids[cur], net->ids[cur ^ 1],
-                         (int *)nullptr, net->counts + l, net->counts + net->L, (int *)nullptr);
+                         (int *)nullptr, net->counts + l, net->counts + net->L, (int *)nullptr, (const int *)nullptr,
+                         (unsigned long long *)nullptr, 0ull);
       HIP_OR_POISON(net, hipGetLastError());
       cur ^= 1;
       net->layers_run = net->L;
@@ -3188,15 +3461,17 @@ sdnn_status infer_lds(sdnn_net *net, const float *y0, int M) {
     net->layer_kernel[(size_t)l] = counted ? SDNN_KERNEL_BITS_COUNT : SDNN_KERNEL_LDS_TILE;
     net->layer_launches[(size_t)l] = counted ? 3 : 1;
     if (net->profiling) net->prof_rec[(size_t)l] = rec;
+    const unsigned long long tag = next_report_tag(net);
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, net->masks, mask_rows, net->ids[cur], net->ids[cur ^ 1],
-                       (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr);
+                       (int *)nullptr, net->counts + l, net->counts + l + 1, (int *)nullptr, net->misc,
+                       net->notify_dev, tag);
     HIP_OR_POISON(net, hipGetLastError());
     cur ^= 1;
     yin = yout;
-    HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-    HIP_OR_POISON(net, hipStreamSynchronize(s));
+    Report rp;
+    HIP_OR_POISON(net, wait_report(net, tag, net->counts + l + 1, &rp));
     const int64_t before = live_bound;
-    live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
+    live_bound = std::min<int64_t>(live_bound, rp.count);
     kept = (l > 0 && live_bound * 10 >= before * 9) ? kept + 1 : 0;
   }
   net->layers_run = l;
@@ -3263,6 +3538,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       __builtin_ia32_pause();
     }
   };
+  bool bits_route = false;  // layer 0 went to the bit-tile kernels (unless the report says otherwise)
   int32_t l = 0;
   for (; l < net->L && live_bound > 0; ++l) {
     const bool small = l > 0 && P <= one_round;
@@ -3285,14 +3561,15 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       // the pack pass addresses rows with 32-bit offsets (in floats, or float4 when N % 4 == 0)
       const uint64_t units = (uint64_t)M * (uint64_t)net->N / ((net->N & 3) == 0 ? 4 : 1);
       const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 && units < (1ull << 32) &&
-                            (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <= 160 * 1024;
-      bool bits_route = false;
+                            (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <=
+                                160 * 1024 - kBitsStaticLds;
       if (try_bits) {
+        // the bit-tile kernels that follow exit at once if the pack finds an input other than 0 or 1
+        // (misc[0]); the host learns of it from the layer's compaction report and then computes
+        // layer 0 on fp32 tiles (no host round trip inside the layer)
         HIP_OR_POISON(net, net->bitsT == 32 ? launch_pack_bits<32>(net, y0, net->fm[0], net->ids[cur], npos + cur)
                                             : launch_pack_bits<16>(net, y0, net->fm[0], net->ids[cur], npos + cur));
-        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 6, net->misc, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-        HIP_OR_POISON(net, hipStreamSynchronize(s));
-        bits_route = net->pinned[6] == 0;
+        bits_route = true;
       }
       const LayerDev &ld0 = net->layers[0];
       if (bits_route && P > one_round && net->L > 1 && ld0.uniform && ld0.ell16 && ld0.w > 0.0f) {
@@ -3362,7 +3639,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       }
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
-    auto compact = [&]() -> hipError_t {
+    // compaction of this layer's live rows; with tag != 0 it reports its count and flags
+    auto compact = [&](unsigned long long tag = 0) -> hipError_t {
       hipError_t e = finalize_parts();
       if (e != hipSuccess) return e;
       if (spread_used) {
@@ -3373,23 +3651,34 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         spread_used = false;
       }
       hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, mk, 32, net->ids[cur], net->ids[cur ^ 1],
-                         net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1));
+                         net->src[cur ^ 1], npos + cur, net->counts + l + 1, npos + (cur ^ 1), net->misc,
+                         tag ? net->notify_dev : nullptr, tag);
       last_list = cur ^ 1;
       return hipGetLastError();
     };
     compacted = false;
     bool adopt;
     if (!small) {
-      // a large layer: compact, and read the exact count back (the next layer is large, so the
-      // wait is short relative to it)
-      HIP_OR_POISON(net, compact());
+      // a large layer: compact, and wait for its exact count (the next layer is large, so the wait
+      // is short relative to it)
+      unsigned long long tag = next_report_tag(net);
+      HIP_OR_POISON(net, compact(tag));
       compacted = true;
-      HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-      if (fout_codes)
-        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 5, net->misc + kOverflowSlot, sizeof(int32_t),
-                                          hipMemcpyDeviceToHost, s));
-      HIP_OR_POISON(net, hipStreamSynchronize(s));
-      if (fout_codes && net->pinned[5] != 0) {
+      Report rp;
+      HIP_OR_POISON(net, wait_report(net, tag, net->counts + l + 1, &rp));
+      if (l == 0 && bits_route && rp.nonbinary) {
+        // an input is not 0 or 1: the bit-tile kernel exited at once; layer 0 on fp32 tiles
+        fout_codes = false;
+        HIP_OR_POISON(net, launch_to_fm(net, y0, net->fm[0], net->ids[cur], npos + cur, nullptr));
+        HIP_OR_POISON(net, launch_gfm(net, net->layers[0], net->fm[0], fout, npos + cur, tiles(P), mk, nullptr,
+                                      nullptr, nullptr, net->spread));
+        spread_used = true;
+        net->layer_kernel[0] = SDNN_KERNEL_GLOBAL_TILE;
+        net->layer_launches[0] = 2 + gfm_launches(net, net->layers[0], tiles(P), 0);
+        tag = next_report_tag(net);
+        HIP_OR_POISON(net, compact(tag));
+        HIP_OR_POISON(net, wait_report(net, tag, net->counts + l + 1, &rp));
+      } else if (fout_codes && rp.overflow) {
         // more than 256 distinct values: redo layer 0 with fp32 outputs (same liveness)
         fout_codes = false;
         net->layer_kernel[0] = SDNN_KERNEL_BITS;
@@ -3397,11 +3686,11 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         HIP_OR_POISON(net, net->bitsT == 32
                                ? launch_layer_bits<32>(net, net->layers[0], net->fm[0], fout, npos + cur, false)
                                : launch_layer_bits<16>(net, net->layers[0], net->fm[0], fout, npos + cur, false));
-        HIP_OR_POISON(net, compact());
-        HIP_OR_POISON(net, hipMemcpyAsync(net->pinned + 7, net->counts + l + 1, sizeof(int32_t), hipMemcpyDeviceToHost, s));
-        HIP_OR_POISON(net, hipStreamSynchronize(s));
+        tag = next_report_tag(net);
+        HIP_OR_POISON(net, compact(tag));
+        HIP_OR_POISON(net, wait_report(net, tag, net->counts + l + 1, &rp));
       }
-      live_bound = std::min<int64_t>(live_bound, net->pinned[7]);
+      live_bound = std::min<int64_t>(live_bound, rp.count);
       adopt = live_bound == 0 || tiles(live_bound) * 20 <= tiles(P) * 19;
     } else {
       adopt = tiles(live_bound) < tiles(P);
@@ -3450,7 +3739,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     const int32_t last = l - 1;
     HIP_OR_POISON(net, finalize_parts());
     hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, s, masks_for(last), 32, net->ids[cur], net->ids[cur ^ 1],
-                       net->src[cur ^ 1], npos + cur, net->counts + last + 1, npos + (cur ^ 1));
+                       net->src[cur ^ 1], npos + cur, net->counts + last + 1, npos + (cur ^ 1), (const int *)nullptr,
+                       (unsigned long long *)nullptr, 0ull);
     HIP_OR_POISON(net, hipGetLastError());
     last_list = cur ^ 1;
   }
@@ -3724,6 +4014,7 @@ void sdnn_destroy(sdnn_net *net) {
   for (auto &ev : net->events) (void)hipEventDestroy(ev);
   if (net->pinned) (void)hipHostFree(net->pinned);
   if (net->progress) (void)hipHostFree(net->progress);
+  if (net->notify) (void)hipHostFree(net->notify);
   delete net;
 }
 

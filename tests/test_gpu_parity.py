@@ -557,3 +557,28 @@ def test_value_agnostic_large_binary_batch(n, m, wkind):
         assert sdnn_kind(kinds[1]) == "k_layer_gfm_u8"
     assert oracle.padded_live_counts(o, nl)[1] > 256
     assert_parity(gpu, o, cats)
+
+
+@pytest.mark.parametrize("n,kind", [(6000, "binary"), (6000, "scaled"), (12001, "binary"), (2048, "binary"),
+                                    (2048, "scaled")])
+def test_mixed_degrees_up_to_32(n, kind):
+    """Layers whose largest column degree is 32 but whose columns hold 8 to 32 sources, with signed
+    per-edge weights: the kernels that read 32 sources per column from 16-bit lists must pad the
+    shorter columns with no-op terms. More than 256 rows, so the large-layer kernels run on the
+    global-tile path (one-byte codes after a binary layer 0, fp32 tiles after a scaled one), and
+    the per-layer and fused LDS kernels on widths staged in LDS."""
+    rng = np.random.default_rng(n + len(kind))
+    m, nl = 900, 5
+    layers = []
+    for _ in range(nl):
+        deg = rng.integers(8, 33, size=n)
+        deg[rng.integers(n)] = 32
+        cp, ri, v = synth.random_csc(rng, n, deg, -0.05, 0.25)
+        layers.append((cp, ri, v, rng.uniform(-0.35, -0.25, size=n).astype(np.float32)))
+    y0 = (rng.random((m, n)) < rng.uniform(0.3, 0.7, size=(m, 1))).astype(np.float32)
+    if kind == "scaled":
+        y0 *= np.float32(1.25)
+    log(f"mixed degrees up to 32 n={n} kind={kind}")
+    gpu, o, cats = run_both(n, layers, y0)
+    assert 0 < cats.size
+    assert_parity(gpu, o, cats)
