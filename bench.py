@@ -36,27 +36,13 @@ def log(msg: str) -> None:
     print(f"[bench {time.strftime('%H:%M:%S')}] {msg}", file=sys.stderr, flush=True)
 
 
-def algorithmic_layer_bytes(n: int, nnz: int, r_in: int, r_out: int, d_in: int | None = None,
-                            d_out: int | None = None) -> int:
+def algorithmic_layer_bytes(n: int, nnz: int, r_in: int, r_out: int) -> int:
     """Bytes one layer must move with dense fp32 live rows: read the live input rows, write the rows
-    that stay live, read the weights (index + value) and the bias once. With equal columns (same
-    sources, weights and bias, hence equal outputs), only the d_out distinct output columns need
-    computing and storing, and a layer reads only the d_in distinct columns of its input (all n for
-    layer 0, whose input is the caller's rows)."""
+    that stay live, read the weights (index + value) and the bias once. Every column counts, also
+    where columns are equal (the method computes each of them)."""
     if r_in == 0:
         return 0
-    d_in = n if d_in is None else d_in
-    d_out = n if d_out is None else d_out
-    return 4 * (d_in * r_in + d_out * r_out) + 8 * nnz * d_out // n + 4 * d_out
-
-
-def distinct_columns(layers, l: int, n: int) -> int:
-    """Number of distinct columns of layer l (columns with equal source lists; weights and bias are
-    uniform in these workloads)."""
-    cp, ri, _ = layers(l, 1)
-    k = int(cp[0][1] - cp[0][0])
-    cols = ri[int(cp[0][0]):int(cp[0][-1])].reshape(n, k)
-    return int(np.unique(cols, axis=0).shape[0])
+    return 4 * n * (r_in + r_out) + 8 * nnz + 4 * n
 
 
 def layer_source(cfg, network: str):
@@ -356,18 +342,8 @@ def main() -> int:
         # a launch that runs every remaining layer (kind 8) is timed at its first layer and covers
         # the algorithmic bytes of all of them
         covered = range(lay, L) if sdnn.KERNEL_KINDS.get(int(kind[lay])) == "k_layers_lds" else [lay]
-        dcache = {}
-
-        def dcols(l):
-            # distinct columns, counted for the structured layers (the union layers have none equal)
-            if args.network == "union" or l < 0:
-                return n
-            if l not in dcache:
-                dcache[l] = distinct_columns(layers, l, n)
-            return dcache[l]
-
         def layer_bytes(l):
-            return algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1]), dcols(l - 1), dcols(l))
+            return algorithmic_layer_bytes(n, nnz, int(counts[l]), int(counts[l + 1]))
 
         algo = sum(layer_bytes(l) for l in covered)
         nl = max(int(launches[lay]), 1)

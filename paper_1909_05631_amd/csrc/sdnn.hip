@@ -1315,6 +1315,12 @@ __host__ __device__ constexpr int code_rows(int T) { return T == 32 ? 128 : 64; 
 // outputs per work item of k_layer_gfm_u8: 4 waves x (64 / (CR / 4)) outputs per wave instruction
 // x 8 outputs per lane
 __host__ __device__ constexpr int u8_outputs(int CR) { return 4 * (64 / (CR / 4)) * 8; }
+// rows per lane of k_layer_gfm_u8 (8: 8-byte gathers, for 64-row codes; 4 for 128-row codes, whose
+// lanes would otherwise hold too many accumulators)
+#ifndef SDNN_U8_RPL
+#define SDNN_U8_RPL 8
+#endif
+__host__ __device__ constexpr int u8_rows_per_lane(int CR) { return CR == 64 ? SDNN_U8_RPL : 4; }
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
@@ -1398,32 +1404,36 @@ __device__ __forceinline__ unsigned dict_code(float y, unsigned *dlk, unsigned *
 // One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
 // (source k of list position CR t + b), decoded as dict[code]; the output is fp32 tiles of 32 rows
 // as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST = CR / 32). Code tiles
-// [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR bytes: RL = CR / 4
-// lanes read it with 4-byte loads (4 codes each), so a wave instruction serves OPI = 64 / RL outputs
-// (4-byte lane loads gather far faster than 16-byte ones, per segment). Lane = (r = lane % RL: rows
-// 4r..4r+3, o = lane / RL); the lane runs the OPL = 8 consecutive outputs jw + 8 o .. jw + 8 o + 7 of
-// its wave's block of OPI * 8, so for every slot its sources come from LDS one 16-bit read each and
-// its weights in two 16-byte reads. A work item is a chunk of 4 waves' outputs. The dictionary and
-// the chunk's lists sit in LDS (kWEdge: 6 bytes per entry, 24 KiB, which leaves room for 5
-// workgroups per CU). A 32-row output segment that is zero in every row is not stored; its bit in
-// seglive (one bit per fp32 tile and source) says so. Registers are held to 5 waves per SIMD for
-// 64-row codes (more waves keep more gathers in flight; 6 spill) and 4 for 128-row codes, whose
-// lanes track twice the live rows (5 spill). Live rows go to masks, or with spread set to the
-// spread words of each fp32 tile (see or_mask). With cols set (kWOne only), the launch computes the
-// ncols columns cols[p] alone (see k_layer_gfm), stores every segment of them and leaves seglive
-// untouched.
-template <int WM, int CR>
+// [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR bytes: RL = CR / RPL
+// lanes read it, RPL codes each (RPL = 4: 4-byte loads; 8: 8-byte loads, which halves the gather
+// instructions and their address arithmetic), so a wave instruction serves OPI = 64 / RL outputs.
+// Lane = (r = lane % RL: rows RPL r .. RPL r + RPL - 1, o = lane / RL); the lane runs the OPL
+// consecutive outputs jw + OPL o .. + OPL - 1 of its wave's block of OPI * OPL (4 OPL RPL = 128
+// accumulator rows per lane would not fit: OPL RPL = 32), so for every slot its sources come from
+// LDS one 16-bit read each and its weights in 16-byte reads. A work item is a chunk of 4 waves'
+// outputs. The dictionary and the chunk's lists sit in LDS (kWEdge: 6 bytes per entry, 24 KiB,
+// which leaves room for 5 workgroups per CU). A 32-row output segment that is zero in every row is
+// not stored; its bit in seglive (one bit per fp32 tile and source) says so. Registers are held to
+// 5 waves per SIMD for 64-row codes (more waves keep more gathers in flight; 6 spill) and 4 for
+// 128-row codes. Live rows go to masks, or with spread set to the spread words of each fp32 tile
+// (see or_mask). With cols set (kWOne only), the launch computes the ncols columns cols[p] alone
+// (see k_layer_gfm), stores every segment of them and leaves seglive untouched.
+template <int WM, int CR, int RPL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 5 : 4))) void k_layer_gfm_u8(
     const unsigned char *__restrict__ cin, float *__restrict__ fout, int N, const int2 *__restrict__ ell, int K,
     const unsigned short *__restrict__ src16, const float *__restrict__ w32, float wc, const float *__restrict__ bias,
     float ymax, const float *__restrict__ dict, const int *__restrict__ npos, unsigned *__restrict__ masks,
     unsigned *__restrict__ seglive, int tile0, unsigned *__restrict__ spread, const int *__restrict__ cols, int ncols,
     int tpx) {
-  constexpr int RL = CR / 4, OPI = 64 / RL, OPL = 8, CH = 4 * OPI * OPL, ST = CR / 32;
+  static_assert(RPL == 4 || RPL == 8, "4 or 8 rows per lane");
+  constexpr int RL = CR / RPL, OPI = 64 / RL, OPL = 32 / RPL, CH = 4 * OPI * OPL, ST = CR / 32;
+  constexpr int DW = RPL / 4;    // code dwords per gather
+  constexpr int LPS = 32 / RPL;  // lanes per 32-row output segment
   constexpr bool LISTS = WM != kWEll;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
-  static_assert(32 % (OPI * OPL) == 0, "a wave's outputs lie within one bitmap word");
+  static_assert(32 % (OPI * OPL) == 0 || (OPI * OPL) % 32 == 0, "bitmap words");
+  static_assert(OPI * OPL <= 32, "a wave's outputs lie within one bitmap word");
   __shared__ float dl[kDictSlots];
   __shared__ __align__(16) unsigned short srcs[LISTS ? 32 * CH : 8];
   __shared__ __align__(16) float wts[WM == kWEdge ? 32 * CH : 4];
@@ -1442,16 +1452,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
   const int cend = rs.cend;
   const int r = lane % RL, o = lane / RL;
   const int nvalid = active ? min(CR, R - t * CR) : 0;
-  // output rows 4r..4r+3 of the code tile: fp32 tile ST t + r / 8, slots (4r) % 32; the list's
-  // fp32 tiles end at (R + 31) / 32, so the last code tile may lack some of its fp32 tiles
-  const int otile = ST * t + (r >> 3);
-  float *obase = fout + ((size_t)otile * N) * 32 + (4 * r) % 32;
+  // output rows RPL r .. of the code tile: fp32 tile ST t + RPL r / 32, slots (RPL r) % 32; the
+  // list's fp32 tiles end at (R + 31) / 32, so the last code tile may lack some of its fp32 tiles
+  const int otile = ST * t + (RPL * r) / 32;
+  float *obase = fout + ((size_t)otile * N) * 32 + (RPL * r) % 32;
   const bool has_tile = otile * 32 < R;
   const int NW = (N + 31) / 32;
   // the tile base is uniform, so a gather is one 32-bit offset from it
   const unsigned char *tbs = cin + (size_t)t * N * CR;
-  const unsigned lofs = 4u * r;
-  // live rows seen by this lane: bit 4 (r % 16) + c of word r / 16
+  const unsigned lofs = (unsigned)(RPL * r);
+  // live rows seen by this lane: bit (RPL r + c) % 64 of word (RPL r) / 64
   unsigned long long lm[CR / 64];
 #pragma unroll
   for (int h = 0; h < CR / 64; ++h) lm[h] = 0ull;
@@ -1469,21 +1479,29 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
     if (tid < ST * (CH / 32)) segw[tid / (CH / 32)][tid % (CH / 32)] = 0u;
     if constexpr (LISTS) stage_lists<WM, CH>(srcs, wts, src16, w32, ncols, c0, nout);
     __syncthreads();
-    float acc[OPL][4];
+    float acc[OPL][RPL];
 #pragma unroll
     for (int i = 0; i < OPL; ++i)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) acc[i][c] = 0.0f;
+      for (int c = 0; c < RPL; ++c) acc[i][c] = 0.0f;
     if constexpr (LISTS) {
       // software pipeline: a slot's gathers are issued one slot before its fmas (deeper pipelines
       // measure no faster: the gathers are limited by the vector-memory path, not by latency)
       constexpr int kDepth = 2;
-      unsigned wd[kDepth][OPL];
+      unsigned wd[kDepth][OPL][DW];
       auto fetch = [&](int sl, int bf) {
         const unsigned short *sp = srcs + sl * CH + jl0;
 #pragma unroll
-        for (int i = 0; i < OPL; ++i)
-          wd[bf][i] = *reinterpret_cast<const unsigned *>(tbs + ((unsigned)sp[i] * (unsigned)CR + lofs));
+        for (int i = 0; i < OPL; ++i) {
+          const unsigned char *gp = tbs + ((unsigned)sp[i] * (unsigned)CR + lofs);
+          if constexpr (DW == 2) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(gp);
+            wd[bf][i][0] = v.x;
+            wd[bf][i][1] = v.y;
+          } else {
+            wd[bf][i][0] = *reinterpret_cast<const unsigned *>(gp);
+          }
+        }
       };
 #pragma unroll
       for (int sl = 0; sl < kDepth - 1; ++sl) fetch(sl, sl);
@@ -1492,37 +1510,42 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
         if (sl + kDepth - 1 < 32) fetch(sl + kDepth - 1, (sl + kDepth - 1) % kDepth);
         mem_fence_compiler();
         __builtin_amdgcn_sched_barrier(0);
-        // the slot's weights from LDS (two 16-byte reads, ahead of the dictionary reads below)
+        // the slot's weights from LDS (16-byte reads, ahead of the dictionary reads below)
         float wv[OPL];
         if constexpr (WM == kWEdge) {
-          const float4 a = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0);
-          const float4 b = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0 + 4);
-          wv[0] = a.x; wv[1] = a.y; wv[2] = a.z; wv[3] = a.w;
-          wv[4] = b.x; wv[5] = b.y; wv[6] = b.z; wv[7] = b.w;
+#pragma unroll
+          for (int i = 0; i < OPL; i += 4) {
+            const float4 a = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0 + i);
+            wv[i] = a.x; wv[i + 1] = a.y; wv[i + 2] = a.z; wv[i + 3] = a.w;
+          }
         } else {
 #pragma unroll
           for (int i = 0; i < OPL; ++i) wv[i] = wc;
         }
-        // dictionary lookups run LA words ahead of the fmas that use them
+        // dictionary lookups run LA code dwords ahead of the fmas that use them
+        constexpr int NQ = OPL * DW;  // code dwords of the slot
         constexpr int LA = 2;
         float dv[LA + 1][4];
-        auto lookup = [&](int i) {
+        auto lookup = [&](int q) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) dv[i % (LA + 1)][c] = dl[(wd[sl % kDepth][i] >> (8 * c)) & 255u];
+          for (int c = 0; c < 4; ++c) dv[q % (LA + 1)][c] = dl[(wd[sl % kDepth][q / DW][q % DW] >> (8 * c)) & 255u];
         };
 #pragma unroll
-        for (int i = 0; i < LA; ++i) lookup(i);
+        for (int q = 0; q < LA; ++q) lookup(q);
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) {
-          if (i + LA < OPL) lookup(i + LA);
+        for (int q = 0; q < NQ; ++q) {
+          if (q + LA < NQ) lookup(q + LA);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dv[i % (LA + 1)][c], wv[i], acc[i][c]);
+          for (int c = 0; c < 4; ++c)
+            acc[q / DW][4 * (q % DW) + c] = fmaf(dv[q % (LA + 1)][c], wv[q / DW], acc[q / DW][4 * (q % DW) + c]);
           __builtin_amdgcn_sched_barrier(0);
         }
         // this slot's fmas complete here, before the slot after next is fetched
 #pragma unroll
-        for (int i = 0; i < OPL; ++i) pin4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+        for (int i = 0; i < OPL; ++i)
+#pragma unroll
+          for (int c = 0; c < RPL; c += 4) pin4(acc[i][c], acc[i][c + 1], acc[i][c + 2], acc[i][c + 3]);
       }
     } else {
       const unsigned char *tb = tbs + lofs;
@@ -1530,9 +1553,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
           const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + i, N - 1)];
-          const unsigned word = *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR);
 #pragma unroll
-          for (int c = 0; c < 4; ++c) acc[i][c] = fmaf(dl[(word >> (8 * c)) & 255u], __int_as_float(e.y), acc[i][c]);
+          for (int d = 0; d < DW; ++d) {
+            const unsigned word = *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR + 4 * d);
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              acc[i][4 * d + c] = fmaf(dl[(word >> (8 * c)) & 255u], __int_as_float(e.y), acc[i][4 * d + c]);
+          }
         }
       }
     }
@@ -1544,24 +1571,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
     for (int i = 0; i < OPL; ++i) {
       const int jl = jl0 + i;
       const float b = bstage[jl];
-      const float4 y = make_float4(activate(acc[i][0], b, ymax), activate(acc[i][1], b, ymax),
-                                   activate(acc[i][2], b, ymax), activate(acc[i][3], b, ymax));
-      const unsigned bits = jl < nout ? (y.x > 0.0f ? 1u : 0u) | (y.y > 0.0f ? 2u : 0u) | (y.z > 0.0f ? 4u : 0u) |
-                                            (y.w > 0.0f ? 8u : 0u)
-                                      : 0u;
+      float y[RPL];
+      unsigned bits = 0u;
+#pragma unroll
+      for (int c = 0; c < RPL; ++c) {
+        y[c] = activate(acc[i][c], b, ymax);
+        bits |= (jl < nout && y[c] > 0.0f ? 1u : 0u) << c;
+      }
       const unsigned long long bal = __ballot(bits != 0u);
-      // the 8 lanes of this lane's output segment: lanes (lane & ~7) .. + 7
-      if (jl < nout && has_tile && (cols || ((bal >> (lane & ~7)) & 0xffull) != 0ull))
-        store_stream(reinterpret_cast<float4 *>(obase + (size_t)cstage[jl] * 32), y);
+      // the LPS lanes of this lane's output segment: lanes (lane & ~(LPS - 1)) .. + LPS - 1
+      constexpr unsigned long long kSegLanes = (1ull << LPS) - 1ull;
+      if (jl < nout && has_tile && (cols || ((bal >> (lane & ~(LPS - 1))) & kSegLanes) != 0ull)) {
+#pragma unroll
+        for (int c = 0; c < RPL; c += 4)
+          store_stream(reinterpret_cast<float4 *>(obase + (size_t)cstage[jl] * 32 + c),
+                       make_float4(y[c], y[c + 1], y[c + 2], y[c + 3]));
+      }
 #pragma unroll
       for (int h = 0; h < CR / 64; ++h)
-        if ((r >> 4) == h) lm[h] |= (unsigned long long)bits << (4 * (r & 15));
-      // output jw + 8 oo + i of fp32 tile q is stored by lanes oo RL + 8 q .. + 7
+        if ((RPL * r) / 64 == h) lm[h] |= (unsigned long long)bits << ((RPL * r) % 64);
+      // output jw + OPL oo + i of fp32 tile q is stored by lanes oo RL + LPS q .. + LPS - 1
 #pragma unroll
       for (int oo = 0; oo < OPI; ++oo)
 #pragma unroll
         for (int q = 0; q < ST; ++q)
-          seg[q] |= (((bal >> (oo * RL + 8 * q)) & 0xffull) != 0ull ? 1u : 0u) << ((jw % 32) + oo * OPL + i);
+          seg[q] |= (((bal >> (oo * RL + LPS * q)) & kSegLanes) != 0ull ? 1u : 0u) << ((jw % 32) + oo * OPL + i);
     }
     if (lane == 0)
 #pragma unroll
@@ -2681,15 +2715,15 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16 && ld.uniform)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
                          dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, dict, npos, masks,
                          net->seglive, r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
     else if (ld.K == 32 && ld.src16 && ld.w32)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w32, 0.0f, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
                          net->spread, (const int *)nullptr, net->N, 1);
     else
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, (const unsigned short *)nullptr, (const float *)nullptr, 0.0f, ld.bias, net->ymax, dict,
                          npos, masks, net->seglive, r * 8, net->spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();

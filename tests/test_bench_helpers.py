@@ -13,19 +13,9 @@ def test_algorithmic_layer_bytes_counts_rows_weights_and_bias():
     assert bench.algorithmic_layer_bytes(4, 8, 2, 1) == 48 + 64 + 16
     # nothing enters: nothing moves
     assert bench.algorithmic_layer_bytes(4, 8, 0, 0) == 0
-    # equal columns: 16 columns in groups of 4 read 4 distinct input columns and write 4 outputs;
-    # the weights of 4 of the 16 columns are read
-    assert bench.algorithmic_layer_bytes(16, 16 * 32, 10, 5, 4, 4) == 4 * (4 * 10 + 4 * 5) + 8 * 4 * 32 + 4 * 4
-    # every column distinct: the same as the plain count
-    assert bench.algorithmic_layer_bytes(16, 512, 10, 5, 16, 16) == bench.algorithmic_layer_bytes(16, 512, 10, 5)
-
-
-def test_distinct_columns():
-    n, k = 8, 2
-    # columns 0..3 read (0, 1); columns 4..7 read (2, 3): two distinct lists
-    ri = np.array([0, 1] * 4 + [2, 3] * 4, np.int32)
-    cp = [np.arange(0, n * k + 1, k, dtype=np.int64)]
-    assert bench.distinct_columns(lambda l0, nl: (cp, ri, None), 0, n) == 2
+    # the n65536 network's layer 1 on the stroke inputs: 60,000 rows in, 8,103 out
+    n, nnz = 65536, 32 * 65536
+    assert bench.algorithmic_layer_bytes(n, nnz, 60000, 8103) == 4 * n * 68103 + 8 * nnz + 4 * n
 
 
 def test_committed_records_follow_the_kernel_source(tmp_path, monkeypatch):
