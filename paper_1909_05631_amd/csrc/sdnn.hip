@@ -13,16 +13,19 @@
 //   128 positions, or bit tiles of 16 or 32 positions for binary inputs.
 //   Weights: per layer a slot-major ELL table [K][N] of (source offset, fp32 weight), entry [s][j]
 //   the s-th smallest source of output j, padded with (0, 0.0f); padding adds fma(y, 0, acc) = acc
-//   exactly. One-weight layers with 32 sources per column also get 16-bit source lists, [32][N]
-//   (path 1) and [4][N][8] (eight per 16-byte load), and, where columns share their list, the
-//   representative columns' lists alone.
+//   exactly. Layers with 32 sources per column also get 16-bit source lists with their fp32
+//   weights beside them: [32][N] u16 + [32][N] fp32 (path 1, six bytes per edge) and [4][N][8]
+//   u16 + fp32 (path 0, eight per 16-byte load). With the opt-in equal-value kernels, a layer whose
+//   weights and biases are all equal keeps one weight instead, and where columns share their list
+//   only the representative columns' lists.
 //
 // Kernels (every output is the ascending-source fma chain above, so every path gives the same bits)
 //   path 0: k_layer_lds (one layer; B rows staged in LDS as [k][B]), k_layers_lds (every remaining
-//     layer in one launch, each workgroup's rows resident in LDS), layer 0 by counts of bit tiles.
-//   path 1, layer 0: k_pack_bits, then k_count_dict + k_layer_count (one-weight layers: adder-tree
-//     counts of set source bits, decoded by a dictionary) or k_layer_bits; non-binary inputs take
-//     k_to_fm + k_layer_gfm.
+//     layer in one launch, each workgroup's rows resident in LDS), and, opt-in, layer 0 by counts
+//     of bit tiles.
+//   path 1, layer 0: k_pack_bits, then k_layer_bits (or, opt-in for one-weight layers,
+//     k_count_dict + k_layer_count: adder-tree counts of set source bits, decoded by a
+//     dictionary); non-binary inputs take k_to_fm + k_layer_gfm.
 //   path 1, later layers: k_layer_gfm_u8 (code tiles in), k_layer_gfm (fp32 tiles in),
 //     k_layer_gfm_small (at most 8 tiles, whole chains in flight). Workgroups are mapped so that
 //     each XCD gathers from its own tile, resident in its L2.
