@@ -1143,11 +1143,13 @@ __global__ __launch_bounds__(kPartThreads) void k_finalize_masks(const unsigned 
 // per tile). Workgroup 0 turns the previous layer's partial words part_prev (prev_S slots, prev_nt
 // tiles) into its mask words masks_prev, or, with part_prev null, reads those words; then it writes
 // their live count to count_out (if set) and to the progress word (if set), and clears masks_clear.
-// With cols set (CW only), only the ncols columns cols[p] are computed (see k_layer_gfm).
-template <int KC, bool CW>
+// WM picks the weight layout (kWEll, kWOne, kWEdge; see k_layer_gfm). With cols set (kWOne only),
+// only the ncols columns cols[p] are computed (see k_layer_gfm).
+template <int KC, int WM>
 __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const float *__restrict__ fin, float *__restrict__ fout, int N, const int2 *__restrict__ ell,
-    const unsigned short *__restrict__ src16, float wc, const float *__restrict__ bias, float ymax,
+    const unsigned short *__restrict__ src16, const float *__restrict__ w32, float wc,
+    const float *__restrict__ bias, float ymax,
     const int *__restrict__ npos, int ntiles_h, unsigned *__restrict__ part_out,
     const unsigned *__restrict__ part_prev, int prev_S, int prev_nt, unsigned *__restrict__ masks_prev,
     unsigned *__restrict__ masks_clear, int *__restrict__ count_out, const int *__restrict__ live_before,
@@ -1188,14 +1190,15 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
     const int j = chunk * CH + wave * 8 + h;
     const int jj = min(j, ncols - 1);
     const int col = cols ? cols[jj] : jj;  // output column
-    // byte offsets of the sources' segments and the weights (CW: 16-bit source lists, weight wc)
+    // byte offsets of the sources' segments and the weights (16-bit source lists with one weight wc
+    // or each edge's weight beside them, or ELL entries)
     unsigned eo[KC];
     float ew[KC];
 #pragma unroll
     for (int i = 0; i < KC; ++i) {
-      if constexpr (CW) {
+      if constexpr (WM != kWEll) {
         eo[i] = (unsigned)src16[(size_t)i * ncols + jj] * (FMR * 4);
-        ew[i] = wc;
+        ew[i] = WM == kWEdge ? w32[(size_t)i * ncols + jj] : wc;
       } else {
         const int2 e = ell[(size_t)i * N + jj];
         eo[i] = (unsigned)e.x;
@@ -2439,15 +2442,20 @@ hipError_t launch_gfm_small(sdnn_net *net, const LayerDev &ld, const float *fin,
   *S_out = per_xcd * parts;
   *nt_out = ntiles_h;
   if (ld.uniform && ld.src16)
-    hipLaunchKernelGGL((k_layer_gfm_small<32, true>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
-                       ld.ell, dd ? ld.src16c : ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev,
-                       prev_S, prev_nt, masks_prev, masks_clear, count_out, live_before, progress, progress_tag,
-                       dd ? ld.cols : nullptr, ncols);
+    hipLaunchKernelGGL((k_layer_gfm_small<32, kWOne>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
+                       ld.ell, dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, npos,
+                       ntiles_h, part_out, part_prev, prev_S, prev_nt, masks_prev, masks_clear, count_out, live_before,
+                       progress, progress_tag, dd ? ld.cols : nullptr, ncols);
+  else if (ld.src16 && ld.w32)
+    hipLaunchKernelGGL((k_layer_gfm_small<32, kWEdge>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
+                       ld.ell, ld.src16, ld.w32, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S,
+                       prev_nt, masks_prev, masks_clear, count_out, live_before, progress, progress_tag,
+                       (const int *)nullptr, net->N);
   else
-    hipLaunchKernelGGL((k_layer_gfm_small<32, false>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
-                       ld.ell, ld.src16, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out, part_prev, prev_S, prev_nt,
-                       masks_prev, masks_clear, count_out, live_before, progress, progress_tag, (const int *)nullptr,
-                       net->N);
+    hipLaunchKernelGGL((k_layer_gfm_small<32, kWEll>), grid, dim3(kPartThreads), 0, net->stream, fin, fout, net->N,
+                       ld.ell, ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, npos, ntiles_h, part_out,
+                       part_prev, prev_S, prev_nt, masks_prev, masks_clear, count_out, live_before, progress,
+                       progress_tag, (const int *)nullptr, net->N);
   return hipGetLastError();
 }
 
