@@ -97,10 +97,10 @@ void parallel_for(int32_t n, F f) {
 
 __device__ __forceinline__ float activate(float z, float b, float ymax) {
   // Sec. V loop: the bias goes only to nonzero products, then the result is clamped to [0, ymax].
-  // Zeros come out as +0.
-  if (z == 0.0f) return 0.0f;
-  const float t = z + b;
-  return t > ymax ? ymax : (t > 0.0f ? t : 0.0f);
+  // Zeros come out as +0: for z != 0 the sum t is never -0 (x + y = -0 needs x = y = -0, and a sum
+  // of nonzero values that is zero is +0), so the median of (t, +0, ymax), ymax > 0, is +0 for t <= 0.
+  const float t = __builtin_amdgcn_fmed3f(z + b, 0.0f, ymax);
+  return z == 0.0f ? 0.0f : t;
 }
 
 // Keeps the compiler from moving memory accesses across this point (no instruction is emitted):
@@ -1288,9 +1288,12 @@ constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 1
 #endif
 constexpr int kLutBits = SDNN_BITS_LUT;
 constexpr int kLutF4 = (1 << kLutBits) * kLutBits / 4;  // float4 entries of the table
-// bound on k_layer_bits' static LDS (table, mask word, dictionary cache), beside its dynamic tile
-constexpr int kBitsStaticLds = 8192 + 512 + kLutF4 * 16;
-static_assert(kLutF4 * 16 + 4 + 2 * 1024 * 4 <= kBitsStaticLds, "static LDS bound");
+// k_layer_bits' LDS tile: one bit word per neuron, sized for the widest network of its height
+// (T = 32 for up to 16384 neurons, 16 for up to 65536); static, so that its address is a constant
+// that folds into the LDS instructions' offsets. Beside it: the table, the mask word and the
+// dictionary cache (under 9 KiB).
+__host__ __device__ constexpr int bits_tile_bytes(int T) { return T == 32 ? 16384 * 4 : 65536 * 2; }
+static_assert(bits_tile_bytes(16) + 9 * 1024 <= 160 * 1024, "LDS of k_layer_bits");
 
 // Value dictionary for one-byte activation codes, in device memory (kDictWords words):
 //   val[256]   the value (fp32 bit pattern) of each code: decoding is val[code];
@@ -1318,15 +1321,34 @@ constexpr int kDictWaitReads = 1 << 16;
 // whose counting workgroups then fill each 128-byte segment in 4 parts; 64 rows after 16-row bit
 // tiles (4 parts each as well). Taller segments serve more rows per gather request.
 __host__ __device__ constexpr int code_rows(int T) { return T == 32 ? 128 : 64; }
-// outputs per work item of k_layer_gfm_u8: 4 waves x (64 / (CR / 4)) outputs per wave instruction
-// x 8 outputs per lane
-__host__ __device__ constexpr int u8_outputs(int CR) { return 4 * (64 / (CR / 4)) * 8; }
 // rows per lane of k_layer_gfm_u8 (8: 8-byte gathers, for 64-row codes; 4 for 128-row codes, whose
 // lanes would otherwise hold too many accumulators)
 #ifndef SDNN_U8_RPL
 #define SDNN_U8_RPL 8
 #endif
 __host__ __device__ constexpr int u8_rows_per_lane(int CR) { return CR == 64 ? SDNN_U8_RPL : 4; }
+// outputs per lane of k_layer_gfm_u8 (at most 32 / rows per lane accumulators' worth)
+#ifndef SDNN_U8_OPL
+#define SDNN_U8_OPL (32 / SDNN_U8_RPL)
+#endif
+__host__ __device__ constexpr int u8_outs_per_lane(int CR) { return CR == 64 ? SDNN_U8_OPL : 8; }
+// outputs per work item: 4 waves x outputs per wave instruction (64 / lanes per code segment) x
+// outputs per lane
+__host__ __device__ constexpr int u8_outputs(int CR) {
+  return 4 * (64 / (CR / u8_rows_per_lane(CR))) * u8_outs_per_lane(CR);
+}
+// k_layer_gfm_u8's software pipeline: slots whose gathers are in flight (SDNN_U8_DEPTH - 1 ahead),
+// code dwords whose dictionary reads run ahead of the fmas (SDNN_U8_LA), waves per SIMD the
+// registers are held to at 64-row codes (SDNN_U8_WAVES)
+#ifndef SDNN_U8_DEPTH
+#define SDNN_U8_DEPTH 2
+#endif
+#ifndef SDNN_U8_LA
+#define SDNN_U8_LA 2
+#endif
+#ifndef SDNN_U8_WAVES
+#define SDNN_U8_WAVES 5
+#endif
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
   return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
@@ -1342,7 +1364,11 @@ __device__ __forceinline__ unsigned dict_hash(unsigned key) {
 constexpr int kCacheEntries = 1024;
 constexpr unsigned kCacheBusy = 0x7fc00001u;
 __device__ __forceinline__ unsigned cache_set(unsigned key) {  // first entry of the key's set (even)
-  return (__umul24(key ^ (key >> 16), 0x9E3779u) >> 12) & (unsigned)(kCacheEntries - 2);
+  // the low 32 bits of (low 24 bits of key ^ (key >> 16)) times 0x9E3779, by the full-rate 24-bit
+  // multiply (the compiler would pick the quarter-rate 32-bit one)
+  unsigned h;
+  asm("v_mul_u32_u24 %0, 0x9e3779, %1" : "=v"(h) : "v"(key ^ (key >> 16)));
+  return (h >> 12) & (unsigned)(kCacheEntries - 2);
 }
 
 // Code of the value with bits `key` from the global table, claiming a free slot and a code on the
@@ -1424,15 +1450,17 @@ __device__ __forceinline__ unsigned dict_code(float y, unsigned *dlk, unsigned *
 // 128-row codes. Live rows go to masks, or with spread set to the spread words of each fp32 tile
 // (see or_mask). With cols set (kWOne only), the launch computes the ncols columns cols[p] alone
 // (see k_layer_gfm), stores every segment of them and leaves seglive untouched.
-template <int WM, int CR, int RPL>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 5 : 4))) void k_layer_gfm_u8(
+template <int WM, int CR, int RPL, int OPL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? SDNN_U8_WAVES : 4))) void k_layer_gfm_u8(
     const unsigned char *__restrict__ cin, float *__restrict__ fout, int N, const int2 *__restrict__ ell, int K,
     const unsigned short *__restrict__ src16, const float *__restrict__ w32, float wc, const float *__restrict__ bias,
     float ymax, const float *__restrict__ dict, const int *__restrict__ npos, unsigned *__restrict__ masks,
     unsigned *__restrict__ seglive, int tile0, unsigned *__restrict__ spread, const int *__restrict__ cols, int ncols,
     int tpx) {
   static_assert(RPL == 4 || RPL == 8, "4 or 8 rows per lane");
-  constexpr int RL = CR / RPL, OPI = 64 / RL, OPL = 32 / RPL, CH = 4 * OPI * OPL, ST = CR / 32;
+  static_assert(OPL == 2 || OPL % 4 == 0, "weights are read in pairs or quads");
+  static_assert(OPL * RPL <= 32, "accumulators per lane");
+  constexpr int RL = CR / RPL, OPI = 64 / RL, CH = 4 * OPI * OPL, ST = CR / 32;
   constexpr int DW = RPL / 4;    // code dwords per gather
   constexpr int LPS = 32 / RPL;  // lanes per 32-row output segment
   constexpr bool LISTS = WM != kWEll;
@@ -1493,7 +1521,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
     if constexpr (LISTS) {
       // software pipeline: a slot's gathers are issued one slot before its fmas (deeper pipelines
       // measure no faster: the gathers are limited by the vector-memory path, not by latency)
-      constexpr int kDepth = 2;
+      constexpr int kDepth = SDNN_U8_DEPTH;
       unsigned wd[kDepth][OPL][DW];
       auto fetch = [&](int sl, int bf) {
         const unsigned short *sp = srcs + sl * CH + jl0;
@@ -1518,7 +1546,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
         __builtin_amdgcn_sched_barrier(0);
         // the slot's weights from LDS (16-byte reads, ahead of the dictionary reads below)
         float wv[OPL];
-        if constexpr (WM == kWEdge) {
+        if constexpr (WM == kWEdge && OPL == 2) {
+          const float2 a = *reinterpret_cast<const float2 *>(wts + sl * CH + jl0);
+          wv[0] = a.x; wv[1] = a.y;
+        } else if constexpr (WM == kWEdge) {
 #pragma unroll
           for (int i = 0; i < OPL; i += 4) {
             const float4 a = *reinterpret_cast<const float4 *>(wts + sl * CH + jl0 + i);
@@ -1530,7 +1561,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
         }
         // dictionary lookups run LA code dwords ahead of the fmas that use them
         constexpr int NQ = OPL * DW;  // code dwords of the slot
-        constexpr int LA = 2;
+        constexpr int LA = SDNN_U8_LA;
         float dv[LA + 1][4];
         auto lookup = [&](int q) {
 #pragma unroll
@@ -1764,6 +1795,27 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
   if (__ballot(bad) && lane == 0) *nonbinary = 1;
 }
 
+// (byte k of u) & 0xF0 in one instruction: a bitwise and whose first operand is byte k of u (a
+// byte-select on the operand); f0 holds 0xF0.
+__device__ __forceinline__ unsigned byte_and_f0(unsigned u, int k, unsigned f0) {
+  unsigned r;
+  switch (k) {
+    case 0: return u & 0xF0u;
+    case 1:
+      asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1 src1_sel:DWORD"
+          : "=v"(r) : "v"(u), "v"(f0));
+      return r;
+    case 2:
+      asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2 src1_sel:DWORD"
+          : "=v"(r) : "v"(u), "v"(f0));
+      return r;
+    default:
+      asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3 src1_sel:DWORD"
+          : "=v"(r) : "v"(u), "v"(f0));
+      return r;
+  }
+}
+
 // Layer 0 from bit tiles of T rows (T = 16 or 32): every term is fma(bit, w, acc) with bit 0 or 1,
 // the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim kBitsThreads. LDS
 // holds the tile's N words and a table that turns kLutBits input bits into as many floats (16
@@ -1772,7 +1824,8 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
 // edge-rows; for 16-row tiles the table reads of a term are issued one term ahead. Results
 // go to feature-major tiles of 32 rows (list position p at tile p / 32, slot p % 32): a lane writes
 // its T rows of output j as T / 4 16-byte stores. Slots past the list's end get zeros.
-// word_shift turns an ELL source offset into the byte offset of the source's word in the tile.
+// An ELL source offset (k * 128: the source's segment in a 32-row fp32 tile) shifted right by
+// kWordShift is the byte offset of the source's word in the bit tile.
 // KC = 32: the 32 ELL entries of a lane's output are all loaded before the first term is used.
 // CODES: instead of fp32 values, write each output's one-byte code in the value dictionary gd
 // (same tile layout, one byte per row); a full dictionary sets *overflow. With *skip set (an input
@@ -1780,21 +1833,33 @@ __global__ __launch_bounds__(256) void k_pack_bits(const float *__restrict__ yin
 template <int T, int KC, bool CODES>
 __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitWord<T>::type *__restrict__ bits,
                                                      float *__restrict__ fout, int N, const int2 *__restrict__ ell,
-                                                     int K, int word_shift, const float *__restrict__ bias,
+                                                     int K, const float *__restrict__ bias,
                                                      float ymax, const int *__restrict__ count,
                                                      unsigned *__restrict__ masks, unsigned *__restrict__ gd,
                                                      int *__restrict__ overflow, const int *__restrict__ skip) {
   if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
+  constexpr int kWordShift = sizeof(W) == 2 ? 6 : 5;  // 128 bytes per source -> sizeof(W)
+  const unsigned f0 = 0xF0u;                            // the byte-select ands' mask, in a register
   // static LDS (addresses known at compile time, so they fold into the instructions' offsets): the
   // table, the tile's live-row mask and the dictionary cache; dynamic LDS: the tile
-  __shared__ float4 lut[kLutF4];
-  __shared__ unsigned tilemask;
-  __shared__ __align__(8) unsigned dlk[kCacheEntries];
-  __shared__ __align__(8) unsigned dlc[kCacheEntries];
-  extern __shared__ float4 smem[];
-  W *tile = reinterpret_cast<W *>(smem);
+  // one struct fixes the layout: the table at LDS address 0 and the tile after the small arrays,
+  // so that every LDS address here is a register plus a constant that fits the instruction offset
+  struct BitsLds {
+    float4 lut[kLutF4];
+    unsigned dlk[kCacheEntries];
+    unsigned dlc[kCacheEntries];
+    unsigned tilemask;
+    unsigned pad[3];
+    W tile[bits_tile_bytes(T) / sizeof(W)];
+  };
+  __shared__ __align__(16) BitsLds sm;
+  float4 *const lut = sm.lut;
+  unsigned *const dlk = sm.dlk;
+  unsigned *const dlc = sm.dlc;
+  unsigned &tilemask = sm.tilemask;
+  W *const tile = sm.tile;
   const int R = *count;
   const int ntiles = (R + T - 1) / T;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
@@ -1837,7 +1902,13 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
       if (blk >= blocks) break;
       const int j = blk * 64 + lane;
       const bool jin = j < N;
-      const int2 *ej = ell + (jin ? j : 0);
+      // ELL entries by a 32-bit offset from the (uniform) layer base: the slot's base advances in
+      // scalar registers, the lane's offset stays put
+      const unsigned jo8 = (jin ? (unsigned)j : 0u) * (unsigned)sizeof(int2);
+      auto ej = [&](int sl) {
+        const char *eb = reinterpret_cast<const char *>(ell + (size_t)sl * N);
+        return *reinterpret_cast<const int2 *>(eb + jo8);
+      };
       float acc[T];
 #pragma unroll
       for (int b = 0; b < T; ++b) acc[b] = 0.0f;
@@ -1851,8 +1922,8 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
           const char *lb = reinterpret_cast<const char *>(lut);
 #pragma unroll
           for (int k = 0; k < T / 8; ++k) {
-            v[2 * k] = *reinterpret_cast<const float4 *>(lb + ((x >> (8 * k)) & 0xF0u));
-            v[2 * k + 1] = *reinterpret_cast<const float4 *>(lb + ((word >> (8 * k)) & 0xF0u));
+            v[2 * k] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(x, k, f0));
+            v[2 * k + 1] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(word, k, f0));
           }
         } else {
           constexpr int per = kLutBits / 4;
@@ -1883,7 +1954,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         static_assert(KC % G == 0, "KC must be a multiple of the group");
         int2 e[G];
 #pragma unroll
-        for (int i = 0; i < G; ++i) e[i] = ej[(size_t)i * N];
+        for (int i = 0; i < G; ++i) e[i] = ej(i);
 #pragma unroll
         for (int h = 0; h < KC; h += G) {
           mem_fence_compiler();
@@ -1891,12 +1962,12 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
           float wv[G];
 #pragma unroll
           for (int i = 0; i < G; ++i) {
-            wd[i] = *reinterpret_cast<const W *>(tb + (e[i].x >> word_shift));
+            wd[i] = *reinterpret_cast<const W *>(tb + ((unsigned)e[i].x >> kWordShift));
             wv[i] = __int_as_float(e[i].y);
           }
           if (h + G < KC) {
 #pragma unroll
-            for (int i = 0; i < G; ++i) e[i] = ej[(size_t)(h + G + i) * N];
+            for (int i = 0; i < G; ++i) e[i] = ej(h + G + i);
           }
           mem_fence_compiler();
           if constexpr (AHEAD) {
@@ -1926,9 +1997,9 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         }
       } else {
         for (int sl = 0; sl < K; ++sl) {
-          const int2 e = ej[(size_t)sl * N];
+          const int2 e = ej(sl);
           float4 v[T / 4];
-          expand(*reinterpret_cast<const W *>(tb + (e.x >> word_shift)), v);
+          expand(*reinterpret_cast<const W *>(tb + ((unsigned)e.x >> kWordShift)), v);
           apply(v, __int_as_float(e.y));
         }
       }
@@ -2048,6 +2119,8 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
+  constexpr int kWordShift = sizeof(W) == 2 ? 6 : 5;  // 128 bytes per source -> sizeof(W)
+  const unsigned f0 = 0xF0u;                            // the byte-select ands' mask, in a register
   constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
   extern __shared__ float4 smem[];
   unsigned &tilemask = *reinterpret_cast<unsigned *>(smem);
@@ -2521,10 +2594,9 @@ hipError_t launch_to_fm(sdnn_net *net, const float *y, float *fm, const int *ids
 }
 
 template <int T>
-size_t bits_lds_bytes(const sdnn_net *net) {
+size_t bits_tile_bytes_needed(const sdnn_net *net) {
   using W = typename BitWord<T>::type;
-  // dynamic part (the tile); the table and the dictionary cache are static
-  return ((size_t)net->N * sizeof(W) + 15) / 16 * 16;
+  return (size_t)net->N * sizeof(W);
 }
 
 template <int T>
@@ -2538,23 +2610,10 @@ hipError_t launch_pack_bits(sdnn_net *net, const float *yin, void *bits, const i
 template <int T, int KC, bool CODES>
 hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bits, float *fout, const int *count) {
   using W = typename BitWord<T>::type;
-  static bool configured = false;
-  if (!configured) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&k_layer_bits<T, KC, CODES>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - kBitsStaticLds);
-    if (e != hipSuccess) return e;
-    configured = true;
-  }
-  // one workgroup per CU: 16 waves at up to 128 registers fill the register file
-  const size_t lds = bits_lds_bytes<T>(net);
+  // one workgroup per CU: 16 waves at up to 128 registers fill the register file; LDS is static
   const int per_cu = 1;
-  // ELL source offsets are k * 32 * 4 bytes (32-row fp32 tiles); a word sits at k * sizeof(W)
-  int shift = 0;
-  while ((1 << shift) < 32 * (int)sizeof(float)) ++shift;
-  int wshift = 0;
-  while ((1 << wshift) < (int)sizeof(W)) ++wshift;
-  hipLaunchKernelGGL((k_layer_bits<T, KC, CODES>), dim3(net->cus * per_cu), dim3(kBitsThreads), lds, net->stream,
-                     reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, shift - wshift, ld.bias, net->ymax,
+  hipLaunchKernelGGL((k_layer_bits<T, KC, CODES>), dim3(net->cus * per_cu), dim3(kBitsThreads), 0, net->stream,
+                     reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, ld.bias, net->ymax,
                      count, net->masks, net->dict, net->misc + kOverflowSlot, net->misc);
   return hipGetLastError();
 }
@@ -2726,15 +2785,15 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   const float *dict = reinterpret_cast<const float *>(net->dict);
   for (int r = 0; r < rounds; ++r) {
     if (ld.K == 32 && ld.src16 && ld.uniform)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
                          dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, dict, npos, masks,
                          net->seglive, r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
     else if (ld.K == 32 && ld.src16 && ld.w32)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w32, 0.0f, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
                          net->spread, (const int *)nullptr, net->N, 1);
     else
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR, u8_rows_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, (const unsigned short *)nullptr, (const float *)nullptr, 0.0f, ld.bias, net->ymax, dict,
                          npos, masks, net->seglive, r * 8, net->spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
@@ -3606,8 +3665,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       // the pack pass addresses rows with 32-bit offsets (in floats, or float4 when N % 4 == 0)
       const uint64_t units = (uint64_t)M * (uint64_t)net->N / ((net->N & 3) == 0 ? 4 : 1);
       const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 && units < (1ull << 32) &&
-                            (net->bitsT == 32 ? bits_lds_bytes<32>(net) : bits_lds_bytes<16>(net)) <=
-                                160 * 1024 - kBitsStaticLds;
+                            (net->bitsT == 32 ? bits_tile_bytes_needed<32>(net) <= bits_tile_bytes(32)
+                                              : bits_tile_bytes_needed<16>(net) <= bits_tile_bytes(16));
       if (try_bits) {
         // the bit-tile kernels that follow exit at once if the pack finds an input other than 0 or 1
         // (misc[0]); the host learns of it from the layer's compaction report and then computes
