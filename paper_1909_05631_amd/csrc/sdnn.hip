@@ -439,6 +439,8 @@ __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chu
 // blockDim 1024. KC is the compile-time ELL width (0: use the runtime K). With cols set (one-weight
 // layers through ell16 only), the ncols columns cols[p] alone are computed and written, their
 // source lists in ell16 as [4][ncols][8]; the other columns equal one of them (see k_layer_gfm).
+// With place set, neuron k is staged at tile row place[k] and ell16 holds tile rows (placed
+// sources; see bank_placement), which only changes which LDS banks the reads fall in.
 template <int B, int KC>
 __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yin, float *__restrict__ yout, int N,
                                                     const int2 *__restrict__ ell, int K,
@@ -447,7 +449,8 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
                                                     const float *__restrict__ bias, float ymax,
                                                     const int *__restrict__ ids, const int *__restrict__ count,
                                                     unsigned *__restrict__ masks, int *__restrict__ rownz,
-                                                    const int *__restrict__ cols, int ncols) {
+                                                    const int *__restrict__ cols, int ncols,
+                                                    const unsigned short *__restrict__ place) {
   extern __shared__ float4 smem[];
   const char *tile = reinterpret_cast<const char *>(smem);
   float *tilef = reinterpret_cast<float *>(smem);
@@ -485,11 +488,15 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
           v[c4] = (b < nvalid) ? reinterpret_cast<const float4 *>(yin + (size_t)ids[p0 + b] * N)[q]
                                : make_float4(0.f, 0.f, 0.f, 0.f);
         }
-        float4 *dst = reinterpret_cast<float4 *>(tilef + (size_t)(4 * q) * B + bq * 4);
-        dst[0] = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
-        dst[B / 4] = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
-        dst[2 * (B / 4)] = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
-        dst[3 * (B / 4)] = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
+        // neuron k goes to tile row place[k] (k itself without a placement)
+        int rk[4];
+#pragma unroll
+        for (int c4 = 0; c4 < 4; ++c4) rk[c4] = place ? (int)place[4 * q + c4] : 4 * q + c4;
+        float *dst = tilef + bq * 4;
+        *reinterpret_cast<float4 *>(dst + (size_t)rk[0] * B) = make_float4(v[0].x, v[1].x, v[2].x, v[3].x);
+        *reinterpret_cast<float4 *>(dst + (size_t)rk[1] * B) = make_float4(v[0].y, v[1].y, v[2].y, v[3].y);
+        *reinterpret_cast<float4 *>(dst + (size_t)rk[2] * B) = make_float4(v[0].z, v[1].z, v[2].z, v[3].z);
+        *reinterpret_cast<float4 *>(dst + (size_t)rk[3] * B) = make_float4(v[0].w, v[1].w, v[2].w, v[3].w);
         if (count_nz) {
 #pragma unroll
           for (int c4 = 0; c4 < 4; ++c4)
@@ -500,7 +507,7 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
       for (int it = tid; it < N * B; it += blockDim.x) {
         const int b = it % B, k = it / B;
         const float v = (b < nvalid) ? yin[(size_t)ids[p0 + b] * N + k] : 0.0f;
-        tilef[(size_t)k * B + b] = v;
+        tilef[(size_t)(place ? (int)place[k] : k) * B + b] = v;
         if (count_nz && v != 0.0f) rowany[b] = 1;
       }
     }
@@ -2323,6 +2330,11 @@ struct LayerDev {
   // grouping, [K/8][N][8] fp32 (w8)
   const uint4 *ell16 = nullptr;
   const float *w8 = nullptr;
+  // LDS row placement for k_layer_lds (path 0, the first kPlacedLayers layers with ell16): neuron k
+  // of the layer's input is staged at tile row place[k], and pell16 is ell16 with every source k
+  // replaced by place[k] (see bank_placement)
+  const unsigned short *place = nullptr;
+  const uint4 *pell16 = nullptr;
   // global-tile path, layer with K == 32 and N <= 65536: [K][N] u16 source indices (the ELL's
   // sources), and unless the layer is uniform its weights [K][N] fp32 beside them (w32)
   const unsigned short *src16 = nullptr;
@@ -2346,6 +2358,73 @@ struct LayerDev {
   int D = 0;
   bool dedup_ok = false;
 };
+
+// Layers (from layer 0) that get an LDS row placement: the per-layer kernel runs the first layers
+// of a batch, before the fused launch takes over.
+constexpr int kPlacedLayers = 64;
+
+// LDS row placement for k_layer_lds. The kernel reads a source's B rows (B * 4 bytes) with 16-byte
+// lane reads; an LDS cycle serves 16 lanes (256 bytes, 64 banks), which are the G = 64 / B
+// consecutive output columns of a group at one slot. Row r of the tile starts at bank (r B) mod 64,
+// so the group's reads of distinct sources collide when their rows agree mod G; the cycles a read
+// takes are the largest number of distinct sources on one residue. The sources of a column are
+// fixed (and their order, which is the summation order), but the row of each neuron in the tile is
+// free: this local search swaps the rows of two neurons whenever the summed cycles of the (group,
+// slot) reads that involve them do not grow. h16: the layer's [4][N][8] source groups (ell16).
+std::vector<uint16_t> bank_placement(const uint16_t *h16, int N, int B, uint64_t seed, int iters) {
+  const int G = std::max(1, 64 / B);
+  std::vector<uint16_t> place((size_t)N);
+  for (int k = 0; k < N; ++k) place[(size_t)k] = (uint16_t)k;
+  if (G < 2 || N < 2 * G) return place;
+  auto srcof = [&](int j, int sl) { return (int)h16[((size_t)(sl / 8) * N + j) * 8 + sl % 8]; };
+  const int ngroups = (N + G - 1) / G;
+  // (group, slot) reads of each neuron, as a CSR over neurons
+  std::vector<int> deg((size_t)N + 1, 0);
+  for (int j = 0; j < N; ++j)
+    for (int sl = 0; sl < 32; ++sl) ++deg[(size_t)srcof(j, sl) + 1];
+  for (int k = 0; k < N; ++k) deg[(size_t)k + 1] += deg[(size_t)k];
+  std::vector<int> occ((size_t)deg[(size_t)N]), fill(deg.begin(), deg.end() - 1);
+  for (int j = 0; j < N; ++j)
+    for (int sl = 0; sl < 32; ++sl) occ[(size_t)fill[(size_t)srcof(j, sl)]++] = (j / G) * 32 + sl;
+  auto cycles = [&](int gs) {
+    const int g = gs / 32, sl = gs % 32;
+    int rows[64], n = 0, load[64] = {0}, m = 0;
+    for (int j = g * G; j < std::min(N, g * G + G); ++j) {
+      const int k = srcof(j, sl);
+      bool dup = false;
+      for (int t = 0; t < n; ++t) dup |= rows[t] == k;
+      if (dup) continue;
+      rows[n++] = k;
+      m = std::max(m, ++load[place[(size_t)k] % G]);
+    }
+    return m;
+  };
+  (void)ngroups;
+  uint64_t x = seed;
+  auto next = [&]() {  // SplitMix64
+    x += 0x9E3779B97F4A7C15ull;
+    uint64_t z = x;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+  };
+  std::vector<int> touched;
+  for (int it = 0; it < iters; ++it) {
+    const int a = (int)(next() % (uint64_t)N), c = (int)(next() % (uint64_t)N);
+    if (place[(size_t)a] % G == place[(size_t)c] % G) continue;
+    touched.clear();
+    for (int t = deg[(size_t)a]; t < deg[(size_t)a + 1]; ++t) touched.push_back(occ[(size_t)t]);
+    for (int t = deg[(size_t)c]; t < deg[(size_t)c + 1]; ++t) touched.push_back(occ[(size_t)t]);
+    std::sort(touched.begin(), touched.end());
+    touched.erase(std::unique(touched.begin(), touched.end()), touched.end());
+    int before = 0, after = 0;
+    for (int gs : touched) before += cycles(gs);
+    std::swap(place[(size_t)a], place[(size_t)c]);
+    for (int gs : touched) after += cycles(gs);
+    if (after > before) std::swap(place[(size_t)a], place[(size_t)c]);
+  }
+  return place;
+}
 
 }  // namespace
 
@@ -2485,9 +2564,11 @@ hipError_t launch_lds(sdnn_net *net, const float *yin, float *yout, const LayerD
   const int per_cu = lds <= 64 * 1024 ? 2 : 1;
   // distinct columns only, when the layer's duplicates need not be computed
   const bool dd = ld.ell16 && ld.ell16c && ld.cols && ld.dedup_ok;
+  const bool placed = !dd && ld.place && ld.pell16;
   hipLaunchKernelGGL((k_layer_lds<B, KC>), dim3(net->cus * per_cu), dim3(1024), lds, net->stream, yin, yout, net->N,
-                     ld.ell, ld.K, dd ? ld.ell16c : ld.ell16, dd ? nullptr : ld.w8, ld.w, ld.bias, net->ymax, ids,
-                     count, net->masks, rownz, dd ? ld.cols : nullptr, dd ? ld.D : net->N);
+                     ld.ell, ld.K, dd ? ld.ell16c : (placed ? ld.pell16 : ld.ell16), dd ? nullptr : ld.w8, ld.w,
+                     ld.bias, net->ymax, ids, count, net->masks, rownz, dd ? ld.cols : nullptr, dd ? ld.D : net->N,
+                     placed ? ld.place : nullptr);
   return hipGetLastError();
 }
 
@@ -3185,6 +3266,40 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
         LayerDev &ld = net->layers[(size_t)l0 + sel[q]];
         ld.ell16 = reinterpret_cast<const uint4 *>(m16) + (per / 8) * q;
         if (!ld.uniform) ld.w8 = reinterpret_cast<const float *>(m16 + sbytes) + woff[q];
+      }
+      // LDS row placements of the first layers on widths staged in LDS (bank_placement): per layer
+      // place [N] u16 and the placed sources [4][N][8] u16
+      std::vector<int32_t> psel;
+      for (size_t q = 0; q < sel.size(); ++q)
+        if (net->path == 0 && l0 + sel[q] < kPlacedLayers) psel.push_back((int32_t)q);
+      if (!psel.empty()) {
+        const size_t pbytes = align_up((size_t)N * sizeof(uint16_t), 256);
+        const size_t per_layer = pbytes + per * sizeof(uint16_t);
+        std::vector<uint16_t> hp(per_layer / sizeof(uint16_t) * psel.size());
+        parallel_for((int32_t)psel.size(), [&](int32_t i) {
+          const size_t q = (size_t)psel[(size_t)i];
+          const uint16_t *src = h16.data() + per * q;
+          const std::vector<uint16_t> place =
+              bank_placement(src, N, net->B, 0x5DB1ull * (uint64_t)(l0 + sel[q] + 1), 25 * N);
+          uint16_t *out = hp.data() + per_layer / sizeof(uint16_t) * (size_t)i;
+          std::copy(place.begin(), place.end(), out);
+          uint16_t *po = out + pbytes / sizeof(uint16_t);
+          for (size_t t = 0; t < per; ++t) po[t] = place[src[t]];
+        });
+        char *mp = nullptr;
+        e = hipMalloc(reinterpret_cast<void **>(&mp), hp.size() * sizeof(uint16_t));
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", hp.size() * sizeof(uint16_t),
+                      hipGetErrorString(e));
+        }
+        net->allocations.push_back(mp);
+        HIP_OR_POISON(net, hipMemcpy(mp, hp.data(), hp.size() * sizeof(uint16_t), hipMemcpyHostToDevice));
+        for (size_t i = 0; i < psel.size(); ++i) {
+          LayerDev &ld = net->layers[(size_t)l0 + sel[(size_t)psel[i]]];
+          ld.place = reinterpret_cast<const unsigned short *>(mp + per_layer * i);
+          ld.pell16 = reinterpret_cast<const uint4 *>(mp + per_layer * i + pbytes);
+        }
       }
     }
   }
