@@ -1872,7 +1872,12 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
   const int blocks = (N + 63) / 64;                 // output blocks of 64
   const int rounds = (blocks + nw - 1) / nw;        // rounds of one block per wave
-  const Chunking ch = chunking(ntiles, rounds);
+  // Every tile's outputs in 8 chunks, item w taking chunk w % 8: with the grid a multiple of 8, that
+  // is the XCD the workgroup runs on, so each XCD reads one eighth of the layer's ELL (2.1 MB at
+  // 65536 neurons), which stays in its L2 while every tile passes; with whole tiles per workgroup
+  // each tile re-read the whole ELL (16.8 MB) through the L2s, tens of GB per layer. A tile is then
+  // staged 8 times (its bits are 1/16 of the ELL's bytes at 16 rows).
+  const Chunking ch = chunking(ntiles, rounds, gridDim.x % 8 == 0 ? 8 : 1);
   // codes with whole tiles as items: keep the tiles of one code group on one XCD
   const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (CR / T)) == 0;
   const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
