@@ -72,6 +72,7 @@ constexpr int kMaxDegree = 4096;
 constexpr int kLdsTileBytes = 128 * 1024;  // activation tile budget per workgroup
 constexpr int kGfmOutputs = 64;            // outputs per work item of k_layer_gfm
 constexpr int kPollEvery = 16;             // layers between live-count read-backs
+constexpr int64_t kEncodeMinRows = 2048;   // live rows from which a fp32-input layer tries codes
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -158,6 +159,20 @@ __device__ __forceinline__ bool any_nonzero(float4 v) {
 
 // misc[0]: a layer-0 input is not 0 or 1; misc[kOverflowSlot]: the value dictionary is full;
 // misc[3]: first live count of a uniform layer 0; misc[kNposSlot + i]: positions in live list i.
+// The value dictionary's initial state (its layout is described with dict_code below): code 0 is
+// +0.0, whose key 0 sits in its hash slot 0; every other slot is free and the next code is 1.
+constexpr unsigned kDictEmpty = 0x7fc00000u;
+constexpr unsigned kNoCode = 0xffffffffu;
+constexpr int kDictSlots = 256;       // codes
+constexpr int kDictHashSlots = 1024;  // hash table slots
+constexpr int kDictKey = kDictSlots, kDictCode = kDictKey + kDictHashSlots, kDictNext = kDictCode + kDictHashSlots,
+              kDictWords = kDictNext + 256;
+__device__ __forceinline__ void dict_init(unsigned *dict, int t, int nt) {
+  for (int i = t; i <= kDictNext; i += nt)
+    dict[i] = i < kDictKey ? 0u : i < kDictCode ? (i == kDictKey ? 0u : kDictEmpty)
+                                : i < kDictNext ? (i == kDictCode ? 0u : kNoCode) : 1u;
+}
+
 constexpr int kOverflowSlot = 2;
 constexpr int kNposSlot = 4;
 __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsigned *__restrict__ masks2,
@@ -167,9 +182,7 @@ __global__ void k_init(int *__restrict__ ids, unsigned *__restrict__ masks, unsi
   const int st = gridDim.x * blockDim.x;
   // value dictionary (see dict_code): code 0 is +0.0, whose key 0 sits in its hash slot 0; every
   // other slot is free and the next code is 1
-  if (blockIdx.x == 0)
-    for (int i = threadIdx.x; i < 769; i += blockDim.x)
-      dict[i] = i < 256 ? 0u : i < 512 ? (i == 256 ? 0u : 0x7fc00000u) : i < 768 ? (i == 512 ? 0u : 0xffffffffu) : 1u;
+  if (blockIdx.x == 0) dict_init(dict, threadIdx.x, blockDim.x);
   if (blockIdx.x == 0 && threadIdx.x < 8) misc[threadIdx.x] = (threadIdx.x == kNposSlot) ? M : 0;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < M; i += st) {
     ids[i] = i;
@@ -1304,8 +1317,9 @@ static_assert(bits_tile_bytes(16) + 9 * 1024 <= 160 * 1024, "LDS of k_layer_bits
 
 // Value dictionary for one-byte activation codes, in device memory (kDictWords words):
 //   val[256]   the value (fp32 bit pattern) of each code: decoding is val[code];
-//   key[256]   an open-addressing hash table of the values seen, by dict_hash;
-//   code[256]  the code of the value in each hash slot (kNoCode until it is published);
+//   key[1024]  an open-addressing hash table of the values seen, by dict_hash (four slots per code,
+//              so that probes stay short also when the 256 codes run out);
+//   code[1024] the code of the value in each hash slot (kNoCode until it is published);
 //   next       the next free code.
 // Codes are handed out in order 0, 1, 2, ... (code 0 is +0.0, whose key sits in its hash slot 0
 // from the start), so a layer's first 32 values decode from distinct LDS banks. A value's slot is
@@ -1314,10 +1328,6 @@ static_assert(bits_tile_bytes(16) + 9 * 1024 <= 160 * 1024, "LDS of k_layer_bits
 // later kernels only); slots and codes never change afterwards, so a workgroup may cache them in
 // LDS. kDictEmpty (a
 // NaN pattern, never an activation) marks free slots.
-constexpr unsigned kDictEmpty = 0x7fc00000u;
-constexpr unsigned kNoCode = 0xffffffffu;
-constexpr int kDictSlots = 256;
-constexpr int kDictKey = 256, kDictCode = 512, kDictNext = 768, kDictWords = 1024;
 // a value whose slot was claimed by another lane waits this many reads at most for its code (the
 // claimer publishes it a few instructions after its compare-and-swap); past the bound the
 // dictionary counts as full, which sends the layer to its fp32 outputs
@@ -1358,7 +1368,11 @@ __host__ __device__ constexpr int u8_outputs(int CR) {
 #endif
 
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
-  return (key ^ (key >> 8) ^ (key >> 16) ^ (key >> 24)) & (kDictSlots - 1);
+  // (low 24 bits of key ^ (key >> 16)) * 0x9E3779, bits 14..23 (full-rate 24-bit multiply); key 0
+  // hashes to slot 0
+  unsigned h;
+  asm("v_mul_u32_u24 %0, 0x9e3779, %1" : "=v"(h) : "v"(key ^ (key >> 16)));
+  return (h >> 14) & (unsigned)(kDictHashSlots - 1);
 }
 
 // A workgroup's LDS cache of the dictionary: kCacheEntries (key, code) entries in two-way sets
@@ -1380,12 +1394,14 @@ __device__ __forceinline__ unsigned cache_set(unsigned key) {  // first entry of
 
 // Code of the value with bits `key` from the global table, claiming a free slot and a code on the
 // way, then recorded in the LDS cache (dlk, dlc) if its set has a free entry. A full dictionary
-// sets *overflow and returns 0; the caller's output is then not used.
+// sets *overflow and returns 0; the caller's output is then not used. Once *overflow is set (by any
+// lane) every call returns at its next probe.
 __device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, unsigned *dlc, unsigned *gd,
                                                    int *overflow) {
   unsigned *gkey = gd + kDictKey, *gcode = gd + kDictCode;
   unsigned h = dict_hash(key);
-  for (int i = 0; i < kDictSlots; ++i) {
+  for (int i = 0; i < kDictHashSlots; ++i) {
+    if (__hip_atomic_load(overflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return 0;
     unsigned cur = __hip_atomic_load(&gkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     bool won = false;
     if (cur == kDictEmpty) {
@@ -1419,7 +1435,7 @@ __device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, 
       }
       return c;
     }
-    h = (h + 1) & (kDictSlots - 1);
+    h = (h + 1) & (kDictHashSlots - 1);
   }
   *overflow = 1;
   return 0;
@@ -1711,6 +1727,78 @@ template <>
 struct BitWord<32> {
   using type = unsigned int;
 };
+
+// The value dictionary back to its initial state (code 0 = +0.0, every other slot free, next code
+// 1) and its overflow flag cleared, before a later layer's outputs are encoded into it.
+__global__ void k_dict_reset(unsigned *__restrict__ dict, int *__restrict__ overflow) {
+  dict_init(dict, threadIdx.x, blockDim.x);
+  if (threadIdx.x == 0) *overflow = 0;
+}
+
+// Encode the fp32 tiles of a layer's input (32 list positions each) as one-byte dictionary codes in
+// tiles of CR positions, cout[t][k][b] = code of the value at list position CR t + b of source k,
+// so that the layer can gather them with k_layer_gfm_u8 (exact: a code decodes to the stored bits).
+// A thread encodes 16 positions of one source (one 16-byte store). Positions at or past *npos get
+// code 0 and are not read. Codes come from gd through a per-workgroup LDS cache, as in
+// k_layer_bits; more than 256 distinct values set *overflow, and every thread stops at its next
+// item (the caller then keeps the fp32 tiles).
+template <int CR>
+__global__ __launch_bounds__(256) void k_encode(const float *__restrict__ fin, unsigned char *__restrict__ cout, int N,
+                                                const int *__restrict__ npos, unsigned *__restrict__ gd,
+                                                int *__restrict__ overflow) {
+  __shared__ __align__(8) unsigned dlk[kCacheEntries];
+  __shared__ __align__(8) unsigned dlc[kCacheEntries];
+  for (int i = threadIdx.x; i < kCacheEntries; i += blockDim.x) dlk[i] = kDictEmpty;
+  __syncthreads();
+  const int R = *npos;
+  constexpr int QPS = CR / 16;  // 16-position groups per source segment
+  const size_t items = (size_t)((R + CR - 1) / CR) * N * QPS;
+  const size_t step = (size_t)gridDim.x * blockDim.x;
+  for (size_t it = (size_t)blockIdx.x * blockDim.x + threadIdx.x; it < items; it += step) {
+    if (__hip_atomic_load(overflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return;
+    const int q = (int)(it % QPS);
+    const size_t rest = it / QPS;
+    const int k = (int)(rest % N);
+    const size_t t = rest / N;
+    const int p0 = (int)t * CR + q * 16;  // first list position of the group
+    unsigned code[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) code[u] = 0u;
+    if (p0 < R) {
+      // the group lies in one 32-position fp32 tile (p0 % 16 == 0)
+      const float4 *src = reinterpret_cast<const float4 *>(fin + ((size_t)(p0 >> 5) * N + k) * 32 + (p0 & 31));
+      float v[16];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 x = src[g];
+        v[4 * g] = x.x; v[4 * g + 1] = x.y; v[4 * g + 2] = x.z; v[4 * g + 3] = x.w;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = p0 + u < R ? v[u] : 0.0f;
+      bool miss = false;
+#pragma unroll
+      for (int u = 0; u < 16; ++u) miss |= !cache_lookup(__float_as_uint(v[u]), dlk, dlc, &code[u]);
+      if (miss) {
+#pragma unroll
+        for (int u = 0; u < 16; ++u) code[u] = dict_code(v[u], dlk, dlc, gd, overflow);
+      }
+    }
+    uint4 w;
+    w.x = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+    w.y = code[4] | (code[5] << 8) | (code[6] << 16) | (code[7] << 24);
+    w.z = code[8] | (code[9] << 8) | (code[10] << 16) | (code[11] << 24);
+    w.w = code[12] | (code[13] << 8) | (code[14] << 16) | (code[15] << 24);
+    store_stream(reinterpret_cast<uint4 *>(cout + (t * N + k) * CR + q * 16), w);
+  }
+}
+
+// Reports the overflow flag to the host through the coherent report word (as k_compact does,
+// with a count of 0).
+__global__ void k_report_overflow(const int *__restrict__ overflow, unsigned long long *__restrict__ notify,
+                                  unsigned long long tag) {
+  const unsigned long long flags = *overflow != 0 ? 2ull : 0ull;
+  __hip_atomic_store(notify, (tag << 40) | (flags << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
 
 // Layer-0 inputs as bits (the challenge inputs are binary images, Sec. IV): pack the live rows into
 // feature-major bit tiles, bits[t][k] bit b = (Y[ids[t*T + b]][k] != 0). Any entry other than 0
@@ -2534,7 +2622,7 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.rownz = off; off += ib;
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
-  w.dict = off; off += 1024 * sizeof(unsigned);
+  w.dict = off; off += align_up(kDictWords * sizeof(unsigned), a);
   w.seglive = off;
   if (net->path == 1) off += align_up(rows / 32 * (size_t)((net->N + 31) / 32) * sizeof(unsigned), a);
   for (int i = 0; i < 2; ++i) {
@@ -3775,10 +3863,39 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     bool spread_used = false;  // this layer's liveness is in the spread words
     bool seglive_out = false;  // fout's all-zero segments were skipped (net->seglive says which)
     unsigned *mk = masks_for(l);
-    fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
     const bool rec = net->profiling && (net->prof_mode == 1 || !small);
     if (net->profiling) net->prof_rec[(size_t)l] = rec;
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
+    bool encoded = false;  // this layer reads codes that k_encode wrote from fp32 tiles
+    if (l > 0 && !fin_codes && compacted && live_bound >= kEncodeMinRows && !net->equal_value_kernels) {
+      // a large layer on fp32 tiles: if its inputs take at most 256 distinct values (saturated rows
+      // do), encode them as one-byte codes into the free buffer and gather those instead; a fuller
+      // dictionary stops the encoding early and the layer reads the fp32 tiles
+      unsigned char *cbuf = reinterpret_cast<unsigned char *>((fin == net->fm[1]) ? net->fm[0] : net->fm[1]);
+      hipLaunchKernelGGL(k_dict_reset, dim3(1), dim3(256), 0, s, net->dict, net->misc + kOverflowSlot);
+      HIP_OR_POISON(net, hipGetLastError());
+      const int cr = code_rows(net->bitsT);
+      const int64_t items = (live_bound + cr - 1) / cr * (int64_t)net->N * (cr / 16);
+      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+      if (cr == 128)
+        hipLaunchKernelGGL(k_encode<128>, dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, net->dict,
+                           net->misc + kOverflowSlot);
+      else
+        hipLaunchKernelGGL(k_encode<64>, dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, net->dict,
+                           net->misc + kOverflowSlot);
+      HIP_OR_POISON(net, hipGetLastError());
+      const unsigned long long tag = next_report_tag(net);
+      hipLaunchKernelGGL(k_report_overflow, dim3(1), dim3(1), 0, s, net->misc + kOverflowSlot, net->notify_dev, tag);
+      HIP_OR_POISON(net, hipGetLastError());
+      Report rp;
+      HIP_OR_POISON(net, wait_report(net, tag, npos + cur, &rp));
+      if (!rp.overflow) {
+        fin = reinterpret_cast<const float *>(cbuf);
+        fin_codes = true;
+        encoded = true;
+      }
+    }
+    fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
     if (l == 0) {
       // layer 0 reads the caller's rows; binary inputs go through bit tiles (built in fm[0]),
       // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
@@ -3824,14 +3941,15 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         net->layer_launches[0] = 1 + gfm_launches(net, net->layers[0], tiles(P), 0) + (try_bits ? 1 : 0);
       }
     } else if (fin_codes) {
-      // follows layer 0, which is always compacted: no count to take over
+      // follows layer 0 or a layer whose outputs were encoded, both compacted: no count to take over
       HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
                                        npos + cur, tiles(P), mk, &seglive_out));
       spread_used = true;
       fout_cols = ocols_on ? lcur.cols : nullptr;
       net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
       const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
-      net->layer_launches[(size_t)l] = gfm_launches(net, net->layers[(size_t)l], tiles(P), st * 32);
+      // (with the dictionary reset, the encoding and its report when this layer encoded its inputs)
+      net->layer_launches[(size_t)l] = gfm_launches(net, net->layers[(size_t)l], tiles(P), st * 32) + (encoded ? 3 : 0);
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];

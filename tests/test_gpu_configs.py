@@ -105,6 +105,38 @@ def test_all_live_sampled_rows(ci, nl, rows):
     np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
 
 
+@pytest.mark.parametrize("ci,nl,rows", [(3, 11, 64), (4, 11, 32)])
+def test_encoded_layer_inputs(ci, nl, rows):
+    """All-live rows on the two widest networks (60,000 rows, 32-row fp32 tiles, code tiles of 128
+    and 64 rows): the inputs of layers 2-7 take far more than 256 distinct values, so their encoding
+    into one-byte codes overflows the dictionary and stops, and those layers gather fp32; from layer
+    8 on every entry is 32 (saturated), the encoding succeeds and the layers gather codes. A seeded
+    sample of rows is recomputed by the oracle; every count must be the row count."""
+    import bench
+    from paper_1909_05631_amd import sdnn
+    cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
+    n, m = cfg.n_neurons, cfg.n_rows
+    y0 = bench.input_rows(cfg, "alllive", 0, m)
+    gpu = GpuRun(n, nl, cfg.ymax)
+    log(f"{cfg.name}: loading {nl} layers")
+    gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
+    cats = gpu.run(y0)
+    counts = gpu.net.live_counts()
+    kinds, launches = gpu.net.layer_info()
+    names = [sdnn.KERNEL_KINDS.get(int(k)) for k in kinds]
+    log(f"{cfg.name}: live counts {counts.tolist()}; kernels {names}")
+    assert (counts == m).all() and cats.size == m
+    assert names[0] == "k_pack_bits+k_layer_bits(codes)" and names[1] == "k_layer_gfm_u8"
+    assert any(k == "k_layer_gfm" for k in names[2:8])           # encodings that overflowed
+    assert all(k == "k_layer_gfm_u8" for k in names[8:nl])       # encoded inputs
+    rng = np.random.default_rng(300 + ci)
+    sample = np.sort(rng.choice(m, size=rows, replace=False))
+    o = oracle.run_config_layers(y0[sample], cfg.net_id, nl, n, cfg.k, cfg.weight, cfg.bias, cfg.ymax,
+                                 threads=THREADS)
+    assert o.categories().size == sample.size
+    np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
+
+
 def test_many_rows_every_row():
     """Five times the configs' row count (300,000 inputs of the 1024-neuron, 120-layer network):
     live lists longer than one compaction pass covers; every row against the oracle."""
