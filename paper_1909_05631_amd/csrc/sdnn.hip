@@ -448,6 +448,12 @@ __device__ __forceinline__ Chunking chunking(int ntiles, int rounds, int min_chu
   return {(rounds + rpc - 1) / rpc, rpc};
 }
 
+// LDS reads in flight ahead of the fmas in the LDS-tile kernels' 32-term chains
+#ifndef SDNN_LDS_AHEAD
+#define SDNN_LDS_AHEAD 6
+#endif
+constexpr int kLdsAhead = SDNN_LDS_AHEAD;
+
 // One layer with the activation tile staged in LDS. B rows per tile (4 <= B <= 32, a multiple of 4);
 // blockDim 1024. KC is the compile-time ELL width (0: use the runtime K). With cols set (one-weight
 // layers through ell16 only), the ncols columns cols[p] alone are computed and written, their
@@ -564,24 +570,30 @@ __global__ __launch_bounds__(1024) void k_layer_lds(const float *__restrict__ yi
 #pragma unroll
           for (int i = 0; i < 8; ++i) wq[i] = make_float4(wc, wc, wc, wc);
         }
+        // the 32 terms in order, each slot's LDS read issued kLdsAhead slots before its fmas (a
+        // rotating buffer, so reads stay in flight across the groups of eight)
+        auto src_of = [&](int sl) {
+          const uint4 &g = ix[sl / 8];
+          const unsigned pr = (sl % 8) < 2 ? g.x : (sl % 8) < 4 ? g.y : (sl % 8) < 6 ? g.z : g.w;
+          return (sl & 1) ? (pr >> 16) : (pr & 0xffffu);
+        };
+        auto w_of = [&](int sl) {
+          const float4 &q = wq[sl / 4];
+          return (sl % 4) == 0 ? q.x : (sl % 4) == 1 ? q.y : (sl % 4) == 2 ? q.z : q.w;
+        };
+        auto rd = [&](int sl) { return *reinterpret_cast<const float4 *>(tile + src_of(sl) * (unsigned)(B * 4) + qoff); };
+        float4 buf[kLdsAhead];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
-          const float wg[8] = {wq[2 * g].x, wq[2 * g].y, wq[2 * g].z, wq[2 * g].w,
-                               wq[2 * g + 1].x, wq[2 * g + 1].y, wq[2 * g + 1].z, wq[2 * g + 1].w};
-          float4 v[8];
+        for (int q = 0; q < kLdsAhead; ++q) buf[q] = rd(q);
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const unsigned k = (q & 1) ? (pr[q >> 1] >> 16) : (pr[q >> 1] & 0xffffu);
-            v[q] = *reinterpret_cast<const float4 *>(tile + k * (unsigned)(B * 4) + qoff);
-          }
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            a0 = fmaf(v[q].x, wg[q], a0);
-            a1 = fmaf(v[q].y, wg[q], a1);
-            a2 = fmaf(v[q].z, wg[q], a2);
-            a3 = fmaf(v[q].w, wg[q], a3);
-          }
+        for (int sl = 0; sl < 32; ++sl) {
+          const float4 v = buf[sl % kLdsAhead];
+          if (sl + kLdsAhead < 32) buf[sl % kLdsAhead] = rd(sl + kLdsAhead);
+          const float w = w_of(sl);
+          a0 = fmaf(v.x, w, a0);
+          a1 = fmaf(v.y, w, a1);
+          a2 = fmaf(v.z, w, a2);
+          a3 = fmaf(v.w, w, a3);
         }
       } else if constexpr (KC > 0) {
         static_assert(KC % 8 == 0, "KC must be a multiple of 8");
@@ -764,21 +776,28 @@ __global__ __launch_bounds__(1024) void k_layers_lds(const float *__restrict__ y
 #pragma unroll
           for (int i = 0; i < 8; ++i) wq[i] = make_float4(P.w, P.w, P.w, P.w);
         }
+        // the 32 terms in order, each slot's LDS read issued kLdsAhead slots before its fmas
+        auto src_of = [&](int sl) {
+          const uint4 &g = ix[sl / 8];
+          const unsigned pr = (sl % 8) < 2 ? g.x : (sl % 8) < 4 ? g.y : (sl % 8) < 6 ? g.z : g.w;
+          return (sl & 1) ? (pr >> 16) : (pr & 0xffffu);
+        };
+        auto w_of = [&](int sl) {
+          const float4 &q = wq[sl / 4];
+          return (sl % 4) == 0 ? q.x : (sl % 4) == 1 ? q.y : (sl % 4) == 2 ? q.z : q.w;
+        };
+        float buf[kLdsAhead][RPL];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const unsigned pr[4] = {ix[g].x, ix[g].y, ix[g].z, ix[g].w};
-          const float wg[8] = {wq[2 * g].x, wq[2 * g].y, wq[2 * g].z, wq[2 * g].w,
-                               wq[2 * g + 1].x, wq[2 * g + 1].y, wq[2 * g + 1].z, wq[2 * g + 1].w};
-          float v[8][RPL];
+        for (int q = 0; q < kLdsAhead; ++q) lds_rows_load<RPL>(tq + src_of(q) * (unsigned)(B * 4), buf[q]);
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const unsigned k = (q & 1) ? (pr[q >> 1] >> 16) : (pr[q >> 1] & 0xffffu);
-            lds_rows_load<RPL>(tq + k * (unsigned)(B * 4), v[q]);
-          }
+        for (int sl = 0; sl < 32; ++sl) {
+          float v[RPL];
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
+          for (int c = 0; c < RPL; ++c) v[c] = buf[sl % kLdsAhead][c];
+          if (sl + kLdsAhead < 32) lds_rows_load<RPL>(tq + src_of(sl + kLdsAhead) * (unsigned)(B * 4), buf[sl % kLdsAhead]);
+          const float w = w_of(sl);
 #pragma unroll
-            for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[q][c], wg[q], a[c]);
+          for (int c = 0; c < RPL; ++c) a[c] = fmaf(v[c], w, a[c]);
         }
       } else {
         for (int sl = 0; sl < P.K; ++sl) {
