@@ -189,10 +189,19 @@ def copy_bandwidth(nbytes: int = 1 << 30, reps: int = 5) -> float:
     return 2 * nbytes / best / 1e9
 
 
-def kernel_source_sha() -> str:
+def source_code_sha(text: str) -> str:
+    """SHA-256 of C/HIP source text with comments removed and whitespace collapsed: it changes with
+    the code and not with its comments."""
     import hashlib
-    with open(os.path.join(ROOT, "paper_1909_05631_amd", "csrc", "sdnn.hip"), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    import re
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return hashlib.sha256(" ".join(text.split()).encode()).hexdigest()
+
+
+def kernel_source_sha() -> str:
+    with open(os.path.join(ROOT, "paper_1909_05631_amd", "csrc", "sdnn.hip")) as f:
+        return source_code_sha(f.read())
 
 
 def committed_traffic(workload: str, kernel: str):

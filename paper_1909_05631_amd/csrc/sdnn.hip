@@ -2434,7 +2434,8 @@ struct LayerDev {
   const int2 *ell = nullptr;
   const float *bias = nullptr;
   int K = 0;
-  // uniform layer: every column holds exactly K sources, all weights are w and all biases b
+  // uniform layer (set only with the opt-in equal-value kernels): every column holds exactly K
+  // sources, all weights are w and all biases b
   bool uniform = false;
   float w = 0.0f, b = 0.0f;
   // layer with K == 32 on widths staged in LDS, and uniform layer 0 of any width: [K/8][N][8] u16

@@ -55,3 +55,13 @@ def test_workload_names():
     assert bench.workload(c4, "alllive", 16).name == "alllive-n65536-l16-m60000"
     assert bench.workload(c4, "alllive", 16).total_nnz == 16 * c4.nnz_per_layer
     assert bench.workload_name(bench.workload(synth.CONFIGS[2], "strokes", 40), "radix") == "radix-n4096-l40-m60000"
+
+
+def test_source_code_sha_ignores_comments_only():
+    """The counter records stay valid across comment edits of the kernel source, not across code
+    edits."""
+    a = "int f(int x) { return x + 1; }  // one\n/* block */\n"
+    b = "// header\nint f(int x) {\n  return x + 1;  /* two */\n}\n"
+    c = "int f(int x) { return x + 2; }\n"
+    assert bench.source_code_sha(a) == bench.source_code_sha(b)
+    assert bench.source_code_sha(a) != bench.source_code_sha(c)
