@@ -1320,13 +1320,9 @@ __global__ __launch_bounds__(kPartThreads) void k_layer_gfm_small(
 }
 
 constexpr int kBitsThreads = 1024;  // k_layer_bits workgroup: 16 waves, up to 128 registers each
-// bits per entry of k_layer_bits' table that turns input bits into floats (4: 16 entries of 16
-// bytes; 8: 256 entries of 32 bytes)
-#ifndef SDNN_BITS_LUT
-#define SDNN_BITS_LUT 4
-#endif
-constexpr int kLutBits = SDNN_BITS_LUT;
-constexpr int kLutF4 = (1 << kLutBits) * kLutBits / 4;  // float4 entries of the table
+// k_layer_bits' table that turns 4 input bits into 4 floats: 16 entries of 16 bytes (a 256-entry
+// table of 8 bits measured twice as slow: its reads spread over more banks)
+constexpr int kLutF4 = 16;
 // k_layer_bits' LDS tile: one bit word per neuron, sized for the widest network of its height
 // (T = 32 for up to 16384 neurons, 16 for up to 65536); static, so that its address is a constant
 // that folds into the LDS instructions' offsets. Beside it: the table, the mask word and the
@@ -1932,7 +1928,7 @@ __device__ __forceinline__ unsigned byte_and_f0(unsigned u, int k, unsigned f0) 
 
 // Layer 0 from bit tiles of T rows (T = 16 or 32): every term is fma(bit, w, acc) with bit 0 or 1,
 // the same fp32 chain as the general kernels since 1*w and 0*w are exact. blockDim kBitsThreads. LDS
-// holds the tile's N words and a table that turns kLutBits input bits into as many floats (16
+// holds the tile's N words and a table that turns 4 input bits into as many floats (16
 // entries of 4 floats: few distinct entries, so a wave's reads of it are mostly broadcasts). Lane =
 // output j; each lane carries the T rows of its output, so one ELL entry and one word serve T
 // edge-rows; for 16-row tiles the table reads of a term are issued one term ahead. Results
@@ -1988,11 +1984,8 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   // codes with whole tiles as items: keep the tiles of one code group on one XCD
   const bool grouped = CODES && ch.nchunks == 1 && gridDim.x % (8 * (CR / T)) == 0;
   const int items = grouped ? (ntiles + gridDim.x - 1) / gridDim.x * gridDim.x : ntiles * ch.nchunks;
-  for (int i = tid; i < kLutF4; i += blockDim.x) {
-    constexpr int per = kLutBits / 4;  // float4 per entry
-    const unsigned q = (unsigned)(i / per) >> (4 * (i % per));  // entry i / per, bits 4 (i % per) ..
-    lut[i] = make_float4((float)(q & 1u), (float)((q >> 1) & 1u), (float)((q >> 2) & 1u), (float)((q >> 3) & 1u));
-  }
+  for (int i = tid; i < kLutF4; i += blockDim.x)
+    lut[i] = make_float4((float)(i & 1), (float)((i >> 1) & 1), (float)((i >> 2) & 1), (float)((i >> 3) & 1));
   if (tid == 0) tilemask = 0u;
   if (CODES)
     for (int i = tid; i < kCacheEntries; i += blockDim.x) dlk[i] = kDictEmpty;
@@ -2031,27 +2024,17 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
       float acc[T];
 #pragma unroll
       for (int b = 0; b < T; ++b) acc[b] = 0.0f;
-      // the source's word gives the T input bits; each group of kLutBits picks that many floats
-      // (0 or 1) from the table
+      // the source's word gives the T input bits; each nibble picks four floats (0 or 1) from the
+      // table
       auto expand = [&](unsigned word, float4 (&v)[T / 4]) {
-        if constexpr (kLutBits == 4) {
-          // byte offset of nibble 2k's entry: byte k of (word << 4) with its low 4 bits cleared; of
-          // nibble 2k + 1's: byte k of word, likewise (one byte-select and per nibble)
-          const unsigned x = word << 4;
-          const char *lb = reinterpret_cast<const char *>(lut);
+        // byte offset of nibble 2k's entry: byte k of (word << 4) with its low 4 bits cleared; of
+        // nibble 2k + 1's: byte k of word, likewise (one byte-select and per nibble)
+        const unsigned x = word << 4;
+        const char *lb = reinterpret_cast<const char *>(lut);
 #pragma unroll
-          for (int k = 0; k < T / 8; ++k) {
-            v[2 * k] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(x, k, f0));
-            v[2 * k + 1] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(word, k, f0));
-          }
-        } else {
-          constexpr int per = kLutBits / 4;
-#pragma unroll
-          for (int n = 0; n < T / kLutBits; ++n) {
-            const unsigned e = (word >> (kLutBits * n)) & ((1u << kLutBits) - 1u);
-#pragma unroll
-            for (int q = 0; q < per; ++q) v[per * n + q] = lut[per * e + q];
-          }
+        for (int k = 0; k < T / 8; ++k) {
+          v[2 * k] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(x, k, f0));
+          v[2 * k + 1] = *reinterpret_cast<const float4 *>(lb + byte_and_f0(word, k, f0));
         }
       };
       auto apply = [&](const float4 (&v)[T / 4], float wv) {
