@@ -73,7 +73,7 @@ def test_integer_networks_match_float64_dense(seed):
 
 
 def test_bias_only_where_z_nonzero():
-    """Sec. V adds b only where Z != 0 (logical(Z)); with b > 0 a column whose products cancel to
+    """Sec. V adds b only where Z != 0 (a numeric nonzero mask); with b > 0 a column whose products cancel to
     exactly 0 must stay 0, while the Sec. II row-replication reading would give b."""
     n = 3
     # column 0: sources 0, 1 with weights 1, -1 -> z = y0 - y1 = 0 for y0 == y1
