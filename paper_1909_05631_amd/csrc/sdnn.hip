@@ -153,6 +153,12 @@ __device__ __forceinline__ float4 load_stream_f4(const float4 *p) {
 }
 
 
+// Raw buffer resource over `bytes` bytes at p (stride 0, offsets in bytes): an access past the end
+// reads zeros. The third dword is the gfx9 default format word.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *p, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes, 0x00020000);
+}
+
 __device__ __forceinline__ bool any_nonzero(float4 v) {
   return v.x != 0.0f || v.y != 0.0f || v.z != 0.0f || v.w != 0.0f;
 }
@@ -1934,8 +1940,8 @@ __device__ __forceinline__ unsigned byte_and_f0(unsigned u, int k, unsigned f0) 
 // edge-rows; for 16-row tiles the table reads of a term are issued one term ahead. Results
 // go to feature-major tiles of 32 rows (list position p at tile p / 32, slot p % 32): a lane writes
 // its T rows of output j as T / 4 16-byte stores. Slots past the list's end get zeros.
-// An ELL source offset (k * 128: the source's segment in a 32-row fp32 tile) shifted right by
-// kWordShift is the byte offset of the source's word in the bit tile.
+// ell is the layer's ELL with source k given as k * sizeof(word), the byte offset of its word in
+// the bit tile (LayerDev::ellw).
 // KC = 32: the 32 ELL entries of a lane's output are all loaded before the first term is used.
 // CODES: instead of fp32 values, write each output's one-byte code in the value dictionary gd
 // (same tile layout, one byte per row); a full dictionary sets *overflow. With *skip set (an input
@@ -1950,7 +1956,6 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
   if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
-  constexpr int kWordShift = sizeof(W) == 2 ? 6 : 5;  // 128 bytes per source -> sizeof(W)
   const unsigned f0 = 0xF0u;                            // the byte-select ands' mask, in a register
   // static LDS (addresses known at compile time, so they fold into the instructions' offsets): the
   // table, the tile's live-row mask and the dictionary cache; dynamic LDS: the tile
@@ -2009,17 +2014,18 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
     const char *tb = reinterpret_cast<const char *>(tile);
     unsigned live = 0u;
     const int r_end = min(rounds, (c + 1) * ch.rounds_per_chunk);
+    const unsigned ell_row = (unsigned)N * (unsigned)sizeof(int2);  // bytes per ELL slot
+    const __amdgpu_buffer_rsrc_t ersrc = buffer_rsrc(ell, (unsigned)K * ell_row);
     for (int r = c * ch.rounds_per_chunk; r < r_end; ++r) {
       const int blk = r * nw + wave;
       if (blk >= blocks) break;
       const int j = blk * 64 + lane;
       const bool jin = j < N;
-      // ELL entries by a 32-bit offset from the (uniform) layer base: the slot's base advances in
-      // scalar registers, the lane's offset stays put
+      // ELL entries by buffer loads: the lane's offset in a vector register, the slot's offset
+      // (sl * N * 8) in a scalar one, so that no vector instruction forms an address
       const unsigned jo8 = (jin ? (unsigned)j : 0u) * (unsigned)sizeof(int2);
       auto ej = [&](int sl) {
-        const char *eb = reinterpret_cast<const char *>(ell + (size_t)sl * N);
-        return *reinterpret_cast<const int2 *>(eb + jo8);
+        return __builtin_bit_cast(int2, __builtin_amdgcn_raw_buffer_load_b64(ersrc, jo8, (unsigned)sl * ell_row, 0));
       };
       float acc[T];
 #pragma unroll
@@ -2064,7 +2070,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
           float wv[G];
 #pragma unroll
           for (int i = 0; i < G; ++i) {
-            wd[i] = *reinterpret_cast<const W *>(tb + ((unsigned)e[i].x >> kWordShift));
+            wd[i] = *reinterpret_cast<const W *>(tb + (unsigned)e[i].x);
             wv[i] = __int_as_float(e[i].y);
           }
           if (h + G < KC) {
@@ -2101,7 +2107,7 @@ __global__ __launch_bounds__(kBitsThreads) void k_layer_bits(const typename BitW
         for (int sl = 0; sl < K; ++sl) {
           const int2 e = ej(sl);
           float4 v[T / 4];
-          expand(*reinterpret_cast<const W *>(tb + ((unsigned)e.x >> kWordShift)), v);
+          expand(*reinterpret_cast<const W *>(tb + (unsigned)e.x), v);
           apply(v, __int_as_float(e.y));
         }
       }
@@ -2415,6 +2421,9 @@ sdnn_status scratch_address(int device, void **out) {
 
 struct LayerDev {
   const int2 *ell = nullptr;
+  // layer 0 of the global-tile path (bit route): the ELL with each source given as the byte offset
+  // of its word in a bit tile (source k * sizeof(word)) instead of its offset in a 32-row fp32 tile
+  const int2 *ellw = nullptr;
   const float *bias = nullptr;
   int K = 0;
   // uniform layer (set only with the opt-in equal-value kernels): every column holds exactly K
@@ -2790,7 +2799,7 @@ hipError_t launch_layer_bits_k(sdnn_net *net, const LayerDev &ld, const void *bi
   // one workgroup per CU: 16 waves at up to 128 registers fill the register file; LDS is static
   const int per_cu = 1;
   hipLaunchKernelGGL((k_layer_bits<T, KC, CODES>), dim3(net->cus * per_cu), dim3(kBitsThreads), 0, net->stream,
-                     reinterpret_cast<const W *>(bits), fout, net->N, ld.ell, ld.K, ld.bias, net->ymax,
+                     reinterpret_cast<const W *>(bits), fout, net->N, ld.ellw, ld.K, ld.bias, net->ymax,
                      count, net->masks, net->dict, net->misc + kOverflowSlot, net->misc);
   return hipGetLastError();
 }
@@ -3254,6 +3263,23 @@ sdnn_status sdnn_load_layers(sdnn_net *net, int32_t l0, int32_t nl, const int64_
   }
   net->allocations.push_back(mem);
   hipStream_t s = reinterpret_cast<hipStream_t>(hip_stream);
+  if (l0 == 0 && net->bitsT > 0 && K[0] <= 32) {
+    // layer 0 on the bit route: its ELL again, with source offsets in bit-tile words (k * 128 bytes
+    // in a 32-row fp32 tile becomes k * sizeof(word))
+    const size_t n0 = (size_t)N * K[0];
+    const int wsz = net->bitsT == 32 ? 4 : 2;
+    std::vector<int2> hw0(n0);
+    for (size_t q = 0; q < n0; ++q) hw0[q] = make_int2(host_ell[q].x / stride * wsz, host_ell[q].y);
+    char *m0 = nullptr;
+    e = hipMalloc(reinterpret_cast<void **>(&m0), std::max<size_t>(n0, 1) * sizeof(int2));
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(SDNN_ENOMEM, "hipMalloc of %zu bytes failed: %s", n0 * sizeof(int2), hipGetErrorString(e));
+    }
+    net->allocations.push_back(m0);
+    HIP_OR_POISON(net, hipMemcpy(m0, hw0.data(), n0 * sizeof(int2), hipMemcpyHostToDevice));
+    net->layers[0].ellw = reinterpret_cast<const int2 *>(m0);
+  }
   HIP_OR_POISON(net, hipMemcpyAsync(mem, host_ell.data(), ell_words * sizeof(int2), hipMemcpyHostToDevice, s));
   HIP_OR_POISON(net, hipMemcpyAsync(mem + ell_bytes, bias, bias_bytes, hipMemcpyHostToDevice, s));
   HIP_OR_POISON(net, hipStreamSynchronize(s));
@@ -3904,7 +3930,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       // others through feature-major tiles in fm[0]; both passes also find the nonzero input rows
       // the pack pass addresses rows with 32-bit offsets (in floats, or float4 when N % 4 == 0)
       const uint64_t units = (uint64_t)M * (uint64_t)net->N / ((net->N & 3) == 0 ? 4 : 1);
-      const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 && units < (1ull << 32) &&
+      const bool try_bits = net->bitsT > 0 && net->layers[0].K <= 32 && net->layers[0].ellw && units < (1ull << 32) &&
                             (net->bitsT == 32 ? bits_tile_bytes_needed<32>(net) <= bits_tile_bytes(32)
                                               : bits_tile_bytes_needed<16>(net) <= bits_tile_bytes(16));
       if (try_bits) {
