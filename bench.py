@@ -248,6 +248,9 @@ def main() -> int:
                     help="the config's stroke images (~19%% ones), or the supplementary all-live set "
                          "(Bernoulli(0.6) rows: every row stays live, so every layer runs at full shape)")
     ap.add_argument("--layers", type=int, default=0, help="run only the first LAYERS layers (0: all)")
+    ap.add_argument("--shard", type=int, default=1, metavar="G",
+                    help="time one GPU's share of a G-GPU data-parallel split (rows are interleaved: this is "
+                         "the share of GPU 0, input rows i with i %% G == 0); no CPU baseline")
     ap.add_argument("--equal-value-kernels", action="store_true",
                     help="supplementary: opt in to the kernels that exploit layers whose weights and biases "
                          "are all equal (sdnn_enable_equal_value_kernels); the workload name gets '-eqv'")
@@ -279,18 +282,24 @@ def main() -> int:
         return 2
     torch.cuda.set_device(0)
     cfg = workload(synth.CONFIGS[args.config], args.inputs, args.layers)
-    n, L, m = cfg.n_neurons, cfg.n_layers, cfg.n_rows
-    wname = workload_name(cfg, args.network, args.equal_value_kernels)
+    if args.shard < 1:
+        print("--shard needs G >= 1", file=sys.stderr)
+        return 2
+    G = args.shard
+    n, L = cfg.n_neurons, cfg.n_layers
+    m = (cfg.n_rows + G - 1) // G  # rows 0, G, 2G, ... of the workload
+    wname = workload_name(cfg, args.network, args.equal_value_kernels) + (f"-shard0of{G}" if G > 1 else "")
     layers = layer_source(cfg, args.network)
     stream = torch.cuda.current_stream()
 
     # ---------------- untimed: load the network and inputs into HBM (Sec. V, load steps)
     t0 = time.time()
     y0 = torch.empty((m, n), dtype=torch.float32, device="cuda")
-    chunk = max(1, (1 << 28) // (4 * n))
-    for r0 in range(0, m, chunk):
-        nr = min(chunk, m - r0)
-        y0[r0:r0 + nr].copy_(torch.from_numpy(input_rows(cfg, args.inputs, r0, nr)))
+    chunk = max(G, (1 << 28) // (4 * n) // G * G)
+    for r0 in range(0, cfg.n_rows, chunk):
+        nr = min(chunk, cfg.n_rows - r0)
+        rows = input_rows(cfg, args.inputs, r0, nr)[::G]  # r0 is a multiple of G
+        y0[r0 // G:r0 // G + rows.shape[0]].copy_(torch.from_numpy(np.ascontiguousarray(rows)))
     density = float(y0.mean().item())
     log(f"{wname}: inputs on device ({m} x {n}, density {density:.3f}) in {time.time() - t0:.1f} s")
     t0 = time.time()
@@ -378,7 +387,7 @@ def main() -> int:
                                      "achieved": round(tot_bytes / (tot_ms * 1e-3) / 1e9, 2) if tot_ms > 0 else None}}
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and G == 1:
         cpu = cpu_baseline(cfg, args.cpu_seconds, host_cpus()["usable"], args.network, args.inputs)
 
     out = {
@@ -402,7 +411,8 @@ def main() -> int:
                    "ymax": cfg.ymax, "connections": cfg.total_nnz, "input_density": round(density, 4),
                    "inputs": "binary stroke images" if args.inputs == "strokes" else
                              f"binary Bernoulli({ALL_LIVE_DENSITY}) rows, all live (supplementary set)",
-                   "parallelism": "none (1 GPU)"},
+                   "parallelism": "none (1 GPU)" if G == 1 else
+                                  f"GPU 0's share of a {G}-GPU row split (rows i % {G} == 0), timed on 1 GPU"},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "live_edges_per_s": live_edges / t_step,
