@@ -2227,8 +2227,6 @@ __global__ __launch_bounds__(1024) void k_layer_count(const typename BitWord<T>:
   if (*skip) return;  // an input is not 0 or 1 (found by k_pack_bits): the layer goes another way
   constexpr int CR = code_rows(T);
   using W = typename BitWord<T>::type;
-  constexpr int kWordShift = sizeof(W) == 2 ? 6 : 5;  // 128 bytes per source -> sizeof(W)
-  const unsigned f0 = 0xF0u;                            // the byte-select ands' mask, in a register
   constexpr int OPL = T == 16 ? 2 : 1;  // outputs per lane
   extern __shared__ float4 smem[];
   unsigned &tilemask = *reinterpret_cast<unsigned *>(smem);
