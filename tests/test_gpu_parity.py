@@ -176,6 +176,30 @@ def test_layer0_bit_route(n, kind):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("n,m,maxdeg", [(6000, 300, 20), (6000, 60, 20), (20000, 300, 12), (6000, 100, 0)])
+def test_layer0_bit_route_short_columns(n, m, maxdeg):
+    """Layer 0 on the bit route when its columns hold fewer than 32 sources (the kernel's runtime
+    slot loop over a narrower ELL, read as word offsets), with more than 256 rows (one-byte codes out)
+    and fewer (fp32 out), at both bit-tile heights; maxdeg 0 is a layer without edges, whose outputs
+    are all zero, so every row dies at once."""
+    rng = np.random.default_rng(n + m + maxdeg)
+    nl = 4
+    layers = []
+    for l in range(nl):
+        hi = maxdeg if l == 0 else 32
+        deg = rng.integers(0, hi + 1, size=n) if hi > 0 else np.zeros(n, dtype=np.int64)
+        cp, ri, v = synth.random_csc(rng, n, deg, -0.05, 0.3)
+        layers.append((cp, ri, v, rng.uniform(-0.3, -0.1, size=n).astype(np.float32)))
+    y0 = (rng.random((m, n)) < rng.uniform(0.3, 0.7, size=(m, 1))).astype(np.float32)
+    log(f"bit route, short columns n={n} m={m} maxdeg={maxdeg}")
+    gpu, o, cats = run_both(n, layers, y0)
+    kinds, _ = gpu.net.layer_info()
+    assert sdnn_kind(kinds[0]).startswith("k_pack_bits+k_layer_bits")
+    if maxdeg == 0:
+        assert cats.size == 0 and gpu.net.live_counts()[1] == 0
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("n,m,bias,lo,hi,kind", [
     (6000, 1100, -0.40, 0.10, 0.40, "binary"),     # 1100 -> 561 -> 213 -> ... -> 7: large, then small layers
     (6000, 1100, -0.35, 0.10, 0.30, "binary"),     # every row dies by layer 4
