@@ -23,7 +23,7 @@ def torch_cuda():
     return torch
 
 
-class GpuRun:
+class GpuNet:
     """One libsdnn network with its device buffers (torch memory) for a given input batch."""
 
     def __init__(self, n: int, n_layers: int, ymax: float = 32.0, equal_values: bool = False):
@@ -60,7 +60,7 @@ def oracle_run(y0, layers, ymax=32.0, threads=8):
     return oracle.run(y0, layers, ymax, threads)
 
 
-def assert_parity(gpu: GpuRun, o: oracle.Oracle, cats: np.ndarray, check_rows=True, rel_tol=1e-5):
+def assert_parity(gpu: GpuNet, o: oracle.Oracle, cats: np.ndarray, check_rows=True, rel_tol=1e-5):
     """Categories and live counts exactly; surviving rows within rel_tol (fp32 values; the canonical
     order makes them bit-identical, which is asserted too)."""
     ocats = o.categories()

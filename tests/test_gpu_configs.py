@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 import synth
-from tests.gpu_util import GpuRun, assert_parity, log
+from tests.gpu_util import GpuNet, assert_parity, log
 
 pytestmark = pytest.mark.gpu
 
@@ -19,7 +19,7 @@ THREADS = max(1, min(16, os.cpu_count() or 1))
 def gpu_config_run(cfg, equal_values=False):
     log(f"{cfg.name}: generating inputs")
     y0 = synth.config_inputs(cfg)
-    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax, equal_values)
+    gpu = GpuNet(cfg.n_neurons, cfg.n_layers, cfg.ymax, equal_values)
     log(f"{cfg.name}: loading {cfg.n_layers} layers")
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     log(f"{cfg.name}: running the GPU")
@@ -60,7 +60,7 @@ def test_structured_full_config_every_row(ci, equal_values):
     cfg = synth.CONFIGS[ci]
     n, L = cfg.n_neurons, cfg.n_layers
     y0 = synth.config_inputs(cfg)
-    gpu = GpuRun(n, L, cfg.ymax, equal_values)
+    gpu = GpuNet(n, L, cfg.ymax, equal_values)
     log(f"radix-{cfg.name}: loading {L} structured layers (equal_values={equal_values})")
     for l0 in range(0, L, 64):
         nl = min(64, L - l0)
@@ -90,7 +90,7 @@ def test_all_live_sampled_rows(ci, nl, rows):
     cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
     n, m = cfg.n_neurons, cfg.n_rows
     y0 = bench.input_rows(cfg, "alllive", 0, m)
-    gpu = GpuRun(n, nl, cfg.ymax)
+    gpu = GpuNet(n, nl, cfg.ymax)
     log(f"{cfg.name}: loading {nl} layers")
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     cats = gpu.run(y0)
@@ -117,7 +117,7 @@ def test_encoded_layer_inputs(ci, nl, rows):
     cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
     n, m = cfg.n_neurons, cfg.n_rows
     y0 = bench.input_rows(cfg, "alllive", 0, m)
-    gpu = GpuRun(n, nl, cfg.ymax)
+    gpu = GpuNet(n, nl, cfg.ymax)
     log(f"{cfg.name}: loading {nl} layers")
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     cats = gpu.run(y0)
@@ -143,7 +143,7 @@ def test_many_rows_every_row():
     cfg = synth.CONFIGS[1]
     m = 300_000
     y0 = synth.config_inputs(cfg, 0, m)
-    gpu = GpuRun(cfg.n_neurons, cfg.n_layers, cfg.ymax)
+    gpu = GpuNet(cfg.n_neurons, cfg.n_layers, cfg.ymax)
     gpu.load_config_layers(cfg.net_id, cfg.k, cfg.weight, cfg.bias)
     log(f"{m} rows of {cfg.name}: running the GPU")
     cats = gpu.run(y0)

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import synth
-from tests.gpu_util import GpuRun, assert_parity, log
+from tests.gpu_util import GpuNet, assert_parity, log
 
 
 def sdnn_kind(k):
@@ -33,7 +33,7 @@ def random_layers(rng, n, nl, max_deg, signed=True):
 
 
 def run_both(n, layers, y0, ymax=32.0, equal_values=False):
-    gpu = GpuRun(n, len(layers), ymax, equal_values)
+    gpu = GpuNet(n, len(layers), ymax, equal_values)
     for l, (cp, ri, v, b) in enumerate(layers):
         gpu.load(l, cp, ri, v, b)
     cats = gpu.run(y0)
@@ -125,7 +125,7 @@ def test_rerun_is_deterministic_and_batches_independent():
     n, nl, m = 4096, 12, 130
     y0 = synth.inputs(31, 64, 0, m, "mixed", 0.3, 0.6)
     cp, ri, v = synth.layers_csc(2, 0, nl, n)
-    gpu = GpuRun(n, nl)
+    gpu = GpuNet(n, nl)
     gpu.load(0, cp, ri, v, np.full((nl, n), -0.35, np.float32))
     a = gpu.run(y0)
     ra = gpu.net.final_rows(a)
@@ -424,7 +424,7 @@ def test_structured_duplicate_columns(order):
     if order == "mixed-bias":
         bias[d][123] = np.float32(-0.41)
     layers = [(cp[l], ri, v, bias[l]) for l in range(nl)]
-    gpu = GpuRun(n, nl, equal_values=True)  # one column per group needs the equal-value kernels
+    gpu = GpuNet(n, nl, equal_values=True)  # one column per group needs the equal-value kernels
     seq = range(nl - 1, -1, -1) if order == "reversed" else range(nl)
     for l in seq:
         gpu.load(l, cp[l], ri, v, bias[l])
@@ -530,7 +530,7 @@ def test_profiling_modes():
     rng = np.random.default_rng(7)
     y0 = (rng.random((m, n)) < rng.uniform(0.10, 0.40, size=(m, 1))).astype(np.float32)
     cp, ri, v = synth.layers_csc(12, 0, nl, n)
-    gpu = GpuRun(n, nl)
+    gpu = GpuNet(n, nl)
     gpu.load(0, cp, ri, v, np.full((nl, n), bias, np.float32))
     gpu.net.set_profiling(True)
     gpu.run(y0)
