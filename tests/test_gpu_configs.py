@@ -105,7 +105,7 @@ def test_all_live_sampled_rows(ci, nl, rows):
     np.testing.assert_array_equal(gpu.net.final_rows(sample), o.rows(o.categories()))
 
 
-@pytest.mark.parametrize("ci,nl,rows", [(3, 11, 64), (4, 11, 32)])
+@pytest.mark.parametrize("ci,nl,rows", [(3, 11, 512), (4, 11, 256)])
 def test_encoded_layer_inputs(ci, nl, rows):
     """All-live rows on the two widest networks (60,000 rows, 32-row fp32 tiles, code tiles of 128
     and 64 rows): the inputs of layers 2-7 take far more than 256 distinct values, so their encoding
