@@ -159,14 +159,17 @@ typedef enum {
   SDNN_KERNEL_BITS_COUNT = 7,           /* layer 0 of a uniform layer on binary inputs, by bit-sliced counts
                                            (k_pack_bits, k_count_dict, k_layer_count); only with
                                            sdnn_enable_equal_value_kernels */
-  SDNN_KERNEL_LDS_FUSED = 8             /* every layer from this one on, in one launch that keeps each
+  SDNN_KERNEL_LDS_FUSED = 8,            /* every layer from this one on, in one launch that keeps each
                                            workgroup's rows in LDS (k_layers_lds); the launch is counted
                                            at its first layer, later layers report 0 launches */
+  SDNN_KERNEL_GLOBAL_TILE_CODES16 = 9   /* two-byte dictionary codes of the inputs, for inputs of 257 to
+                                           4096 distinct values (k_layer_gfm_u8 on 16-bit codes) */
 } sdnn_kernel_kind;
 
 /* Diagnostics (untimed). For each layer of the last sdnn_infer: the kernel family that ran it
- * (sdnn_kernel_kind) and its number of kernel launches (for layers timed with events, the event
- * pair spans these launches). kernel, launches: host arrays of n_layers entries. */
+ * (sdnn_kernel_kind) and its number of kernel launches, those that encoded its inputs included (for
+ * layers timed with events, the event pair spans these launches). kernel, launches: host arrays of
+ * n_layers entries. */
 sdnn_status sdnn_layer_info(sdnn_net *net, int32_t *kernel, int32_t *launches);
 
 /* Free the handle and its device memory. NULL is a no-op. */

@@ -173,10 +173,26 @@ constexpr int kDictSlots = 256;       // codes
 constexpr int kDictHashSlots = 1024;  // hash table slots
 constexpr int kDictKey = kDictSlots, kDictCode = kDictKey + kDictHashSlots, kDictNext = kDictCode + kDictHashSlots,
               kDictWords = kDictNext + 256;
+// The two dictionaries: one-byte codes (above) and two-byte codes (4096 values, for layer inputs
+// that take more than 256). Words: val[kSlots] | key[kHash] | code[kHash] | next; the hash slot of
+// a key is bits kHashShift.. of its 24-bit multiplicative hash, the LDS cache set bits kCacheShift..
+template <int CB> struct DictShape;
+template <> struct DictShape<1> {
+  static constexpr int kSlots = kDictSlots, kHash = kDictHashSlots, kHashShift = 14, kCache = 1024, kCacheShift = 12;
+};
+template <> struct DictShape<2> {
+  static constexpr int kSlots = 4096, kHash = 16384, kHashShift = 10, kCache = 2048, kCacheShift = 11;
+};
+template <int CB> __host__ __device__ constexpr int dict_key_off() { return DictShape<CB>::kSlots; }
+template <int CB> __host__ __device__ constexpr int dict_code_off() { return dict_key_off<CB>() + DictShape<CB>::kHash; }
+template <int CB> __host__ __device__ constexpr int dict_next_off() { return dict_code_off<CB>() + DictShape<CB>::kHash; }
+template <int CB> __host__ __device__ constexpr int dict_words() { return dict_next_off<CB>() + 256; }
+static_assert(dict_words<1>() == kDictWords, "one-byte dictionary layout");
+template <int CB = 1>
 __device__ __forceinline__ void dict_init(unsigned *dict, int t, int nt) {
-  for (int i = t; i <= kDictNext; i += nt)
-    dict[i] = i < kDictKey ? 0u : i < kDictCode ? (i == kDictKey ? 0u : kDictEmpty)
-                                : i < kDictNext ? (i == kDictCode ? 0u : kNoCode) : 1u;
+  constexpr int KEY = dict_key_off<CB>(), CODE = dict_code_off<CB>(), NEXT = dict_next_off<CB>();
+  for (int i = t; i <= NEXT; i += nt)
+    dict[i] = i < KEY ? 0u : i < CODE ? (i == KEY ? 0u : kDictEmpty) : i < NEXT ? (i == CODE ? 0u : kNoCode) : 1u;
 }
 
 constexpr int kOverflowSlot = 2;
@@ -1387,13 +1403,19 @@ __host__ __device__ constexpr int u8_outputs(int CR) {
 #ifndef SDNN_U8_WAVES
 #define SDNN_U8_WAVES 5
 #endif
+// One XCD's L2. Two-byte codes are tried only for layers whose fp32 input tile (32 rows of every
+// source) is larger: at 65536 sources they gather faster than the fp32 tiles, which live in the
+// Infinity Cache, while at 16384 the fp32 tiles stay in L2 and the codes (whose 4096-entry
+// dictionary also halves the workgroups per CU) measure slower, encoding included.
+constexpr size_t kXcdL2Bytes = (size_t)4 << 20;
 
+template <int CB = 1>
 __device__ __forceinline__ unsigned dict_hash(unsigned key) {
-  // (low 24 bits of key ^ (key >> 16)) * 0x9E3779, bits 14..23 (full-rate 24-bit multiply); key 0
-  // hashes to slot 0
+  // (low 24 bits of key ^ (key >> 16)) * 0x9E3779, bits kHashShift.. (full-rate 24-bit multiply);
+  // key 0 hashes to slot 0
   unsigned h;
   asm("v_mul_u32_u24 %0, 0x9e3779, %1" : "=v"(h) : "v"(key ^ (key >> 16)));
-  return (h >> 14) & (unsigned)(kDictHashSlots - 1);
+  return (h >> DictShape<CB>::kHashShift) & (unsigned)(DictShape<CB>::kHash - 1);
 }
 
 // A workgroup's LDS cache of the dictionary: kCacheEntries (key, code) entries in two-way sets
@@ -1403,25 +1425,28 @@ __device__ __forceinline__ unsigned dict_hash(unsigned key) {
 // then the key (one wave's LDS operations take effect in order; a compiler barrier keeps the order);
 // entries are never replaced. A reader loads the keys before the codes, so a key it sees has its
 // code in place; kCacheBusy (a NaN pattern) never matches a value.
-constexpr int kCacheEntries = 1024;
+constexpr int kCacheEntries = DictShape<1>::kCache;
 constexpr unsigned kCacheBusy = 0x7fc00001u;
+template <int CB = 1>
 __device__ __forceinline__ unsigned cache_set(unsigned key) {  // first entry of the key's set (even)
   // the low 32 bits of (low 24 bits of key ^ (key >> 16)) times 0x9E3779, by the full-rate 24-bit
   // multiply (the compiler would pick the quarter-rate 32-bit one)
   unsigned h;
   asm("v_mul_u32_u24 %0, 0x9e3779, %1" : "=v"(h) : "v"(key ^ (key >> 16)));
-  return (h >> 12) & (unsigned)(kCacheEntries - 2);
+  return (h >> DictShape<CB>::kCacheShift) & (unsigned)(DictShape<CB>::kCache - 2);
 }
 
 // Code of the value with bits `key` from the global table, claiming a free slot and a code on the
 // way, then recorded in the LDS cache (dlk, dlc) if its set has a free entry. A full dictionary
 // sets *overflow and returns 0; the caller's output is then not used. Once *overflow is set (by any
 // lane) every call returns at its next probe.
+template <int CB = 1>
 __device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, unsigned *dlc, unsigned *gd,
                                                    int *overflow) {
-  unsigned *gkey = gd + kDictKey, *gcode = gd + kDictCode;
-  unsigned h = dict_hash(key);
-  for (int i = 0; i < kDictHashSlots; ++i) {
+  constexpr int SLOTS = DictShape<CB>::kSlots, HASH = DictShape<CB>::kHash;
+  unsigned *gkey = gd + dict_key_off<CB>(), *gcode = gd + dict_code_off<CB>();
+  unsigned h = dict_hash<CB>(key);
+  for (int i = 0; i < HASH; ++i) {
     if (__hip_atomic_load(overflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return 0;
     unsigned cur = __hip_atomic_load(&gkey[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     bool won = false;
@@ -1432,17 +1457,17 @@ __device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, 
     }
     if (won) {
       // this lane claimed the slot: it takes the next code, records the value, publishes the code
-      const unsigned c = atomicAdd(gd + kDictNext, 1u);
-      if (c < (unsigned)kDictSlots) gd[c] = key;
-      __hip_atomic_store(&gcode[h], c < (unsigned)kDictSlots ? c : kNoCode - 1u, __ATOMIC_RELAXED,
+      const unsigned c = atomicAdd(gd + dict_next_off<CB>(), 1u);
+      if (c < (unsigned)SLOTS) gd[c] = key;
+      __hip_atomic_store(&gcode[h], c < (unsigned)SLOTS ? c : kNoCode - 1u, __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     }
     if (cur == key) {
       unsigned c = kNoCode;
       for (int it = 0; it < kDictWaitReads && c == kNoCode; ++it)
         c = __hip_atomic_load(&gcode[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (c >= (unsigned)kDictSlots) break;  // no code left, or none published within the bound
-      const unsigned st = cache_set(key);
+      if (c >= (unsigned)SLOTS) break;  // no code left, or none published within the bound
+      const unsigned st = cache_set<CB>(key);
       if (dlk[st] != key && dlk[st + 1] != key) {
 #pragma unroll
         for (unsigned wy = 0; wy < 2; ++wy) {
@@ -1456,46 +1481,57 @@ __device__ __forceinline__ unsigned dict_code_slow(unsigned key, unsigned *dlk, 
       }
       return c;
     }
-    h = (h + 1) & (kDictHashSlots - 1);
+    h = (h + 1) & (HASH - 1);
   }
   *overflow = 1;
   return 0;
 }
 // The cache's answer for `key`: *code, and whether it was there.
+template <int CB = 1>
 __device__ __forceinline__ bool cache_lookup(unsigned key, const unsigned *dlk, const unsigned *dlc, unsigned *code) {
-  const unsigned st = cache_set(key);
+  const unsigned st = cache_set<CB>(key);
   const uint2 k = *reinterpret_cast<const uint2 *>(dlk + st);
   mem_fence_compiler();  // the keys are read before the codes
   const uint2 c = *reinterpret_cast<const uint2 *>(dlc + st);
   *code = k.x == key ? c.x : c.y;
   return k.x == key || k.y == key;
 }
+template <int CB = 1>
 __device__ __forceinline__ unsigned dict_code(float y, unsigned *dlk, unsigned *dlc, unsigned *gd, int *overflow) {
   const unsigned key = __float_as_uint(y);
   unsigned c;
-  if (cache_lookup(key, dlk, dlc, &c)) return c;
-  return dict_code_slow(key, dlk, dlc, gd, overflow);
+  if (cache_lookup<CB>(key, dlk, dlc, &c)) return c;
+  return dict_code_slow<CB>(key, dlk, dlc, gd, overflow);
 }
 
-// One round of a layer whose input tiles hold one-byte codes of the activations, cin[t][k][b]
+// waves per SIMD the registers of k_layer_gfm_u8 are held to (with two-byte codes and staged weights,
+// 40 KiB of LDS per workgroup leave room for 3)
+constexpr int u8_waves(int WM, int CR, int CB) {
+  return CB == 2 && WM == kWEdge ? 3 : CR == 64 && CB == 1 ? SDNN_U8_WAVES : 4;
+}
+
+// One round of a layer whose input tiles hold CB-byte codes of the activations, cin[t][k][b]
 // (source k of list position CR t + b), decoded as dict[code]; the output is fp32 tiles of 32 rows
 // as in k_layer_gfm (code tile t covers output tiles ST t .. ST t + ST - 1, ST = CR / 32). Code tiles
-// [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. A code segment is CR bytes: RL = CR / RPL
-// lanes read it, RPL codes each (RPL = 4: 4-byte loads; 8: 8-byte loads, which halves the gather
-// instructions and their address arithmetic), so a wave instruction serves OPI = 64 / RL outputs.
+// [tile0, tile0 + 8) go one per XCD, as in k_layer_gfm. Two-byte codes (CB = 2, 4096-entry
+// dictionary, CR = 64) double the bytes of every gather and leave the rest as it is. A code segment
+// is CR codes: RL = CR / RPL lanes read it, RPL codes each (RPL = 4: 4-byte loads; 8: 8-byte loads,
+// which halves the gather instructions and their address arithmetic; 16-byte loads for two-byte
+// codes), so a wave instruction serves OPI = 64 / RL outputs.
 // Lane = (r = lane % RL: rows RPL r .. RPL r + RPL - 1, o = lane / RL); the lane runs the OPL
 // consecutive outputs jw + OPL o .. + OPL - 1 of its wave's block of OPI * OPL (4 OPL RPL = 128
 // accumulator rows per lane would not fit: OPL RPL = 32), so for every slot its sources come from
 // LDS one 16-bit read each and its weights in 16-byte reads. A work item is a chunk of 4 waves'
 // outputs. The dictionary and the chunk's lists sit in LDS (kWEdge: 6 bytes per entry, 24 KiB,
-// which leaves room for 5 workgroups per CU). A 32-row output segment that is zero in every row is
-// not stored; its bit in seglive (one bit per fp32 tile and source) says so. Registers are held to
-// 5 waves per SIMD for 64-row codes (more waves keep more gathers in flight; 6 spill) and 4 for
-// 128-row codes. Live rows go to masks, or with spread set to the spread words of each fp32 tile
-// (see or_mask). With cols set (kWOne only), the launch computes the ncols columns cols[p] alone
+// which leaves room for 5 workgroups per CU; 40 KiB with the two-byte codes' dictionary). A 32-row
+// output segment that is zero in every row is not stored; its bit in seglive (one bit per fp32
+// tile and source) says so. Registers are held to 5 waves per SIMD for one-byte 64-row codes (more
+// waves keep more gathers in flight; 6 spill), 4 for 128-row codes and 3 for two-byte codes with
+// staged weights (u8_waves). Live rows go to masks, or with spread set to the spread words of each
+// fp32 tile (see or_mask). With cols set (kWOne only), the launch computes the ncols columns cols[p] alone
 // (see k_layer_gfm), stores every segment of them and leaves seglive untouched.
-template <int WM, int CR, int RPL, int OPL>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? SDNN_U8_WAVES : 4))) void k_layer_gfm_u8(
+template <int WM, int CR, int RPL, int OPL, int CB = 1>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(u8_waves(WM, CR, CB)))) void k_layer_gfm_u8(
     const unsigned char *__restrict__ cin, float *__restrict__ fout, int N, const int2 *__restrict__ ell, int K,
     const unsigned short *__restrict__ src16, const float *__restrict__ w32, float wc, const float *__restrict__ bias,
     float ymax, const float *__restrict__ dict, const int *__restrict__ npos, unsigned *__restrict__ masks,
@@ -1505,14 +1541,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
   static_assert(OPL == 2 || OPL % 4 == 0, "weights are read in pairs or quads");
   static_assert(OPL * RPL <= 32, "accumulators per lane");
   constexpr int RL = CR / RPL, OPI = 64 / RL, CH = 4 * OPI * OPL, ST = CR / 32;
-  constexpr int DW = RPL / 4;    // code dwords per gather
-  constexpr int LPS = 32 / RPL;  // lanes per 32-row output segment
+  constexpr int DW = RPL * CB / 4;  // code dwords per gather
+  constexpr int CPD = 4 / CB;       // codes per dword
+  constexpr unsigned CMASK = (unsigned)DictShape<CB>::kSlots - 1u;  // (codes below kSlots)
+  constexpr int LPS = 32 / RPL;     // lanes per 32-row output segment
+  static_assert(CB == 1 || CB == 2, "one- or two-byte codes");
   constexpr bool LISTS = WM != kWEll;
   static_assert(CR == 64 || CR == 128, "code segments of 64 or 128 rows");
   static_assert(CH % 32 == 0 && CH == u8_outputs(CR), "a chunk covers whole bitmap words");
   static_assert(32 % (OPI * OPL) == 0 || (OPI * OPL) % 32 == 0, "bitmap words");
   static_assert(OPI * OPL <= 32, "a wave's outputs lie within one bitmap word");
-  __shared__ float dl[kDictSlots];
+  __shared__ float dl[DictShape<CB>::kSlots];
   __shared__ __align__(16) unsigned short srcs[LISTS ? 32 * CH : 8];
   __shared__ __align__(16) float wts[WM == kWEdge ? 32 * CH : 4];
   __shared__ float bstage[CH];
@@ -1520,7 +1559,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
   __shared__ unsigned segw[ST][CH / 32];
   __shared__ unsigned long long rowmask[CR / 64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < kDictSlots; i += blockDim.x) dl[i] = dict[i];
+  for (int i = tid; i < DictShape<CB>::kSlots; i += blockDim.x) dl[i] = dict[i];
   if (tid < CR / 64) rowmask[tid] = 0ull;
   const int R = *npos;
   const int nchunks = (ncols + CH - 1) / CH;
@@ -1537,8 +1576,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
   const bool has_tile = otile * 32 < R;
   const int NW = (N + 31) / 32;
   // the tile base is uniform, so a gather is one 32-bit offset from it
-  const unsigned char *tbs = cin + (size_t)t * N * CR;
-  const unsigned lofs = (unsigned)(RPL * r);
+  const unsigned char *tbs = cin + (size_t)t * N * CR * CB;
+  const unsigned lofs = (unsigned)(RPL * r * CB);  // byte offset of the lane's rows in a segment
   // live rows seen by this lane: bit (RPL r + c) % 64 of word (RPL r) / 64
   unsigned long long lm[CR / 64];
 #pragma unroll
@@ -1571,8 +1610,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
         const unsigned short *sp = srcs + sl * CH + jl0;
 #pragma unroll
         for (int i = 0; i < OPL; ++i) {
-          const unsigned char *gp = tbs + ((unsigned)sp[i] * (unsigned)CR + lofs);
-          if constexpr (DW == 2) {
+          const unsigned char *gp = tbs + ((unsigned)sp[i] * (unsigned)(CR * CB) + lofs);
+          if constexpr (DW == 4) {
+            const uint4 v = *reinterpret_cast<const uint4 *>(gp);
+            wd[bf][i][0] = v.x;
+            wd[bf][i][1] = v.y;
+            wd[bf][i][2] = v.z;
+            wd[bf][i][3] = v.w;
+          } else if constexpr (DW == 2) {
             const uint2 v = *reinterpret_cast<const uint2 *>(gp);
             wd[bf][i][0] = v.x;
             wd[bf][i][1] = v.y;
@@ -1606,10 +1651,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
         // dictionary lookups run LA code dwords ahead of the fmas that use them
         constexpr int NQ = OPL * DW;  // code dwords of the slot
         constexpr int LA = SDNN_U8_LA;
-        float dv[LA + 1][4];
+        float dv[LA + 1][CPD];
         auto lookup = [&](int q) {
 #pragma unroll
-          for (int c = 0; c < 4; ++c) dv[q % (LA + 1)][c] = dl[(wd[sl % kDepth][q / DW][q % DW] >> (8 * c)) & 255u];
+          for (int c = 0; c < CPD; ++c)
+            dv[q % (LA + 1)][c] = dl[(wd[sl % kDepth][q / DW][q % DW] >> (8 * CB * c)) & CMASK];
         };
 #pragma unroll
         for (int q = 0; q < LA; ++q) lookup(q);
@@ -1618,8 +1664,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
           if (q + LA < NQ) lookup(q + LA);
           __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int c = 0; c < 4; ++c)
-            acc[q / DW][4 * (q % DW) + c] = fmaf(dv[q % (LA + 1)][c], wv[q / DW], acc[q / DW][4 * (q % DW) + c]);
+          for (int c = 0; c < CPD; ++c)
+            acc[q / DW][CPD * (q % DW) + c] = fmaf(dv[q % (LA + 1)][c], wv[q / DW], acc[q / DW][CPD * (q % DW) + c]);
           __builtin_amdgcn_sched_barrier(0);
         }
         // this slot's fmas complete here, before the slot after next is fetched
@@ -1636,10 +1682,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(CR == 64 ? 
           const int2 e = ell[(size_t)sl * N + min(c0 + jl0 + i, N - 1)];
 #pragma unroll
           for (int d = 0; d < DW; ++d) {
-            const unsigned word = *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * CR + 4 * d);
+            const unsigned word = *reinterpret_cast<const unsigned *>(tb + ((unsigned)e.x >> 7) * (CR * CB) + 4 * d);
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-              acc[i][4 * d + c] = fmaf(dl[(word >> (8 * c)) & 255u], __int_as_float(e.y), acc[i][4 * d + c]);
+            for (int c = 0; c < CPD; ++c)
+              acc[i][CPD * d + c] = fmaf(dl[(word >> (8 * CB * c)) & CMASK], __int_as_float(e.y), acc[i][CPD * d + c]);
           }
         }
       }
@@ -1751,25 +1797,28 @@ struct BitWord<32> {
 
 // The value dictionary back to its initial state (code 0 = +0.0, every other slot free, next code
 // 1) and its overflow flag cleared, before a later layer's outputs are encoded into it.
+template <int CB>
 __global__ void k_dict_reset(unsigned *__restrict__ dict, int *__restrict__ overflow) {
-  dict_init(dict, threadIdx.x, blockDim.x);
-  if (threadIdx.x == 0) *overflow = 0;
+  dict_init<CB>(dict, blockIdx.x * blockDim.x + threadIdx.x, gridDim.x * blockDim.x);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *overflow = 0;
 }
 
-// Encode the fp32 tiles of a layer's input (32 list positions each) as one-byte dictionary codes in
+// Encode the fp32 tiles of a layer's input (32 list positions each) as CB-byte dictionary codes in
 // tiles of CR positions, cout[t][k][b] = code of the value at list position CR t + b of source k,
 // so that the layer can gather them with k_layer_gfm_u8 (exact: a code decodes to the stored bits).
-// A thread encodes 16 positions of one source (one 16-byte store). Positions at or past *npos get
-// code 0 and are not read. Codes come from gd through a per-workgroup LDS cache, as in
-// k_layer_bits; more than 256 distinct values set *overflow, and every thread stops at its next
-// item (the caller then keeps the fp32 tiles).
-template <int CR>
+// A thread encodes 16 positions of one source (16 CB bytes, one or two 16-byte stores). Positions
+// at or past *npos get code 0 and are not read. Codes come from gd (the dictionary of CB-byte
+// codes) through a per-workgroup LDS cache, as in k_layer_bits; more distinct values than the
+// dictionary holds set *overflow, and every thread stops at its next item (the caller then keeps
+// the fp32 tiles).
+template <int CR, int CB>
 __global__ __launch_bounds__(256) void k_encode(const float *__restrict__ fin, unsigned char *__restrict__ cout, int N,
                                                 const int *__restrict__ npos, unsigned *__restrict__ gd,
                                                 int *__restrict__ overflow) {
-  __shared__ __align__(8) unsigned dlk[kCacheEntries];
-  __shared__ __align__(8) unsigned dlc[kCacheEntries];
-  for (int i = threadIdx.x; i < kCacheEntries; i += blockDim.x) dlk[i] = kDictEmpty;
+  constexpr int CE = DictShape<CB>::kCache;
+  __shared__ __align__(8) unsigned dlk[CE];
+  __shared__ __align__(8) unsigned dlc[CE];
+  for (int i = threadIdx.x; i < CE; i += blockDim.x) dlk[i] = kDictEmpty;
   __syncthreads();
   const int R = *npos;
   constexpr int QPS = CR / 16;  // 16-position groups per source segment
@@ -1798,18 +1847,26 @@ __global__ __launch_bounds__(256) void k_encode(const float *__restrict__ fin, u
       for (int u = 0; u < 16; ++u) v[u] = p0 + u < R ? v[u] : 0.0f;
       bool miss = false;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) miss |= !cache_lookup(__float_as_uint(v[u]), dlk, dlc, &code[u]);
+      for (int u = 0; u < 16; ++u) miss |= !cache_lookup<CB>(__float_as_uint(v[u]), dlk, dlc, &code[u]);
       if (miss) {
 #pragma unroll
-        for (int u = 0; u < 16; ++u) code[u] = dict_code(v[u], dlk, dlc, gd, overflow);
+        for (int u = 0; u < 16; ++u) code[u] = dict_code<CB>(v[u], dlk, dlc, gd, overflow);
       }
     }
-    uint4 w;
-    w.x = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
-    w.y = code[4] | (code[5] << 8) | (code[6] << 16) | (code[7] << 24);
-    w.z = code[8] | (code[9] << 8) | (code[10] << 16) | (code[11] << 24);
-    w.w = code[12] | (code[13] << 8) | (code[14] << 16) | (code[15] << 24);
-    store_stream(reinterpret_cast<uint4 *>(cout + (t * N + k) * CR + q * 16), w);
+    uint4 *dst = reinterpret_cast<uint4 *>(cout + ((t * N + k) * CR + q * 16) * CB);
+    if constexpr (CB == 1) {
+      uint4 w;
+      w.x = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+      w.y = code[4] | (code[5] << 8) | (code[6] << 16) | (code[7] << 24);
+      w.z = code[8] | (code[9] << 8) | (code[10] << 16) | (code[11] << 24);
+      w.w = code[12] | (code[13] << 8) | (code[14] << 16) | (code[15] << 24);
+      store_stream(dst, w);
+    } else {
+      store_stream(dst, make_uint4(code[0] | (code[1] << 16), code[2] | (code[3] << 16), code[4] | (code[5] << 16),
+                                   code[6] | (code[7] << 16)));
+      store_stream(dst + 1, make_uint4(code[8] | (code[9] << 16), code[10] | (code[11] << 16),
+                                       code[12] | (code[13] << 16), code[14] | (code[15] << 16)));
+    }
   }
 }
 
@@ -2569,6 +2626,7 @@ struct sdnn_net {
   int *misc = nullptr;  // device flags and counters: [0] a layer-0 input is not 0 or 1, [2] dictionary full,
                         // [4 + i] positions in list i
   unsigned *dict = nullptr;  // value dictionary of one-byte activation codes (kDictWords words; decoding reads the first 256)
+  unsigned *dict16 = nullptr;  // path 1: the dictionary of two-byte codes (dict_words<2>() words)
   unsigned *seglive = nullptr;  // path 1: per fp32 tile, one bit per source: the segment was stored
   unsigned *part[2] = {nullptr, nullptr};  // path 1: partial liveness words of few-tile layers, by layer parity
   unsigned *spread = nullptr;              // path 1: liveness words of large layers, one 128-byte line each
@@ -2610,8 +2668,8 @@ namespace {
   } while (0)
 
 struct WsLayout {
-  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, seglive, part[2], spread, spread_words, final_ids,
-      total;
+  size_t act[2], ids[2], src[2], masks[3], rownz, counts, misc, dict, dict16, seglive, part[2], spread, spread_words,
+      final_ids, total;
 };
 
 // Two activation buffers: row-major [M][N] (path 0) or feature-major tiles of 32 rows (path 1).
@@ -2633,6 +2691,8 @@ WsLayout layout_for(const sdnn_net *net, int64_t M) {
   w.counts = off; off += align_up((size_t)(net->L + 1) * sizeof(int), a);
   w.misc = off; off += a;
   w.dict = off; off += align_up(kDictWords * sizeof(unsigned), a);
+  w.dict16 = off;
+  if (net->path == 1) off += align_up((size_t)dict_words<2>() * sizeof(unsigned), a);
   w.seglive = off;
   if (net->path == 1) off += align_up(rows / 32 * (size_t)((net->N + 31) / 32) * sizeof(unsigned), a);
   for (int i = 0; i < 2; ++i) {
@@ -2951,7 +3011,7 @@ hipError_t launch_layer_count(sdnn_net *net, const LayerDev &ld, const void *bit
 
 // A layer whose input tiles hold dictionary codes of CR rows (see k_layer_gfm_u8); rounds of 8 code
 // tiles. max_tiles: host bound on the 32-row tiles of the list.
-template <int CR>
+template <int CR, int CB = 1>
 hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
                             int64_t max_tiles, unsigned *masks, bool *seglive_used) {
   max_tiles = (max_tiles + CR / 32 - 1) / (CR / 32);  // code tiles
@@ -2960,24 +3020,33 @@ hipError_t launch_gfm_u8_cr(sdnn_net *net, const LayerDev &ld, const unsigned ch
   const bool dd = ld.K == 32 && ld.src16 && ld.cols && ld.dedup_ok;
   const int ncols = dd ? ld.D : net->N;
   *seglive_used = !dd;
-  const int tpx = dd ? tiles_per_xcd((size_t)ncols * CR) : 1;  // see launch_gfm
+  const int tpx = dd ? tiles_per_xcd((size_t)ncols * CR * CB) : 1;  // see launch_gfm
   const int nchunks = (ncols + u8_outputs(CR) - 1) / u8_outputs(CR);
   const int64_t parts = 8 / std::max<int64_t>(1, std::min<int64_t>(8, max_tiles));
   const int per_xcd = tpx * std::max(1, (int)std::min<int64_t>(net->cus, (nchunks + parts - 1) / parts));
   const dim3 grid(8 * per_xcd);
   const int rounds = (int)((max_tiles + 8 * tpx - 1) / (8 * tpx));
-  const float *dict = reinterpret_cast<const float *>(net->dict);
+  const float *dict = reinterpret_cast<const float *>(CB == 1 ? net->dict : net->dict16);
   for (int r = 0; r < rounds; ++r) {
-    if (ld.K == 32 && ld.src16 && ld.uniform)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
-                         dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, dict, npos, masks,
-                         net->seglive, r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
-    else if (ld.K == 32 && ld.src16 && ld.w32)
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+    // (two-byte codes come only from encodings, which the opt-in uniform-layer kernels never use)
+    if constexpr (CB == 1) {
+      if (ld.K == 32 && ld.src16 && ld.uniform) {
+        hipLaunchKernelGGL((k_layer_gfm_u8<kWOne, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR), CB>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell, ld.K,
+                           dd ? ld.src16c : ld.src16, (const float *)nullptr, ld.w, ld.bias, net->ymax, dict, npos, masks,
+                           net->seglive, r * 8 * tpx, net->spread, dd ? ld.cols : nullptr, ncols, tpx);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        continue;
+      }
+    } else if (ld.uniform) {
+      return hipErrorInvalidValue;
+    }
+    if (ld.K == 32 && ld.src16 && ld.w32)
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEdge, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR), CB>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, ld.src16, ld.w32, 0.0f, ld.bias, net->ymax, dict, npos, masks, net->seglive, r * 8,
                          net->spread, (const int *)nullptr, net->N, 1);
     else
-      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR)>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
+      hipLaunchKernelGGL((k_layer_gfm_u8<kWEll, CR, u8_rows_per_lane(CR), u8_outs_per_lane(CR), CB>), grid, dim3(256), 0, net->stream, cin, fout, net->N, ld.ell,
                          ld.K, (const unsigned short *)nullptr, (const float *)nullptr, 0.0f, ld.bias, net->ymax, dict,
                          npos, masks, net->seglive, r * 8, net->spread, (const int *)nullptr, net->N, 1);
     hipError_t e = hipGetLastError();
@@ -2989,6 +3058,13 @@ hipError_t launch_gfm_u8(sdnn_net *net, const LayerDev &ld, const unsigned char 
                          int64_t max_tiles, unsigned *masks, bool *seglive_used) {
   return code_rows(net->bitsT) == 128 ? launch_gfm_u8_cr<128>(net, ld, cin, fout, npos, max_tiles, masks, seglive_used)
                                       : launch_gfm_u8_cr<64>(net, ld, cin, fout, npos, max_tiles, masks, seglive_used);
+}
+// A layer whose inputs are two-byte codes (64-row code tiles, dictionary dict16; only layers wider
+// than 32768 neurons use them, and those have 64-row code tiles)
+hipError_t launch_gfm_u16(sdnn_net *net, const LayerDev &ld, const unsigned char *cin, float *fout, const int *npos,
+                          int64_t max_tiles, unsigned *masks, bool *seglive_used) {
+  if (code_rows(net->bitsT) != 64) return hipErrorInvalidValue;
+  return launch_gfm_u8_cr<64, 2>(net, ld, cin, fout, npos, max_tiles, masks, seglive_used);
 }
 
 // Rows per workgroup of k_layers_lds: at most the largest of 16, 8, 4 whose two tiles fit 128 KiB
@@ -3838,7 +3914,9 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   int64_t live_bound = M;  // host bound on the live rows
   const float *fin = nullptr;
   float *fout = nullptr;
-  bool fin_codes = false, fout_codes = false;  // the tiles hold one-byte dictionary codes
+  bool fin_codes = false, fout_codes = false;  // the tiles hold dictionary codes
+  bool fin_wide = false;  // fin's codes are two bytes (k_encode<64, 2>), else one
+  bool wide_ok = true;    // a two-byte encoding is worth trying
   int last_list = 0;
   bool compacted = true;   // the last layer run has been followed by a compaction
   PollRing ring;
@@ -3894,32 +3972,59 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     if (net->profiling) net->prof_rec[(size_t)l] = rec;
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     bool encoded = false;  // this layer reads codes that k_encode wrote from fp32 tiles
+    int encode_tries = 0;  // launches spent on encodings of this layer's inputs
     if (l > 0 && !fin_codes && compacted && live_bound >= kEncodeMinRows && !net->equal_value_kernels) {
       // a large layer on fp32 tiles: if its inputs take at most 256 distinct values (saturated rows
-      // do), encode them as one-byte codes into the free buffer and gather those instead; a fuller
-      // dictionary stops the encoding early and the layer reads the fp32 tiles
+      // do), encode them as one-byte codes into the free buffer and gather those instead; else, if
+      // they take at most 4096 and the fp32 tiles outgrow the L2 (kXcdL2Bytes), as two-byte codes;
+      // a full dictionary stops an encoding early, and when both stop the layer reads the fp32 tiles
       unsigned char *cbuf = reinterpret_cast<unsigned char *>((fin == net->fm[1]) ? net->fm[0] : net->fm[1]);
-      hipLaunchKernelGGL(k_dict_reset, dim3(1), dim3(256), 0, s, net->dict, net->misc + kOverflowSlot);
-      HIP_OR_POISON(net, hipGetLastError());
-      const int cr = code_rows(net->bitsT);
-      const int64_t items = (live_bound + cr - 1) / cr * (int64_t)net->N * (cr / 16);
-      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
-      if (cr == 128)
-        hipLaunchKernelGGL(k_encode<128>, dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, net->dict,
-                           net->misc + kOverflowSlot);
-      else
-        hipLaunchKernelGGL(k_encode<64>, dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, net->dict,
-                           net->misc + kOverflowSlot);
-      HIP_OR_POISON(net, hipGetLastError());
-      const unsigned long long tag = next_report_tag(net);
-      hipLaunchKernelGGL(k_report_overflow, dim3(1), dim3(1), 0, s, net->misc + kOverflowSlot, net->notify_dev, tag);
-      HIP_OR_POISON(net, hipGetLastError());
-      Report rp;
-      HIP_OR_POISON(net, wait_report(net, tag, npos + cur, &rp));
-      if (!rp.overflow) {
-        fin = reinterpret_cast<const float *>(cbuf);
-        fin_codes = true;
-        encoded = true;
+      auto try_encode = [&](int cb) -> hipError_t {
+        unsigned *gd = cb == 1 ? net->dict : net->dict16;
+        if (cb == 1)
+          hipLaunchKernelGGL(k_dict_reset<1>, dim3(1), dim3(256), 0, s, gd, net->misc + kOverflowSlot);
+        else
+          hipLaunchKernelGGL(k_dict_reset<2>, dim3(16), dim3(256), 0, s, gd, net->misc + kOverflowSlot);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int cr = code_rows(net->bitsT);
+        const int64_t items = (live_bound + cr - 1) / cr * (int64_t)net->N * (cr / 16);
+        const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, (items + 255) / 256));
+        if (cb == 2 && cr != 64) return hipErrorInvalidValue;
+        if (cb == 2)
+          hipLaunchKernelGGL((k_encode<64, 2>), dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, gd,
+                             net->misc + kOverflowSlot);
+        else if (cr == 128)
+          hipLaunchKernelGGL((k_encode<128, 1>), dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, gd,
+                             net->misc + kOverflowSlot);
+        else
+          hipLaunchKernelGGL((k_encode<64, 1>), dim3(grid), dim3(256), 0, s, fin, cbuf, net->N, npos + cur, gd,
+                             net->misc + kOverflowSlot);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const unsigned long long tag = next_report_tag(net);
+        hipLaunchKernelGGL(k_report_overflow, dim3(1), dim3(1), 0, s, net->misc + kOverflowSlot, net->notify_dev, tag);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        Report rp;
+        e = wait_report(net, tag, npos + cur, &rp);
+        if (e != hipSuccess) return e;
+        encode_tries += 3;
+        if (!rp.overflow) {
+          fin = reinterpret_cast<const float *>(cbuf);
+          fin_codes = true;
+          fin_wide = cb == 2;
+          encoded = true;
+          if (cb == 1) wide_ok = true;
+        }
+        return hipSuccess;
+      };
+      HIP_OR_POISON(net, try_encode(1));
+      if (!encoded && net->dict16 && wide_ok && (size_t)net->N * 32 * sizeof(float) > kXcdL2Bytes) {
+        HIP_OR_POISON(net, try_encode(2));
+        // inputs with more than 4096 values: the layers after it are not tried again until the
+        // inputs of one of them fit 256 values (values that grow more varied stay so for a while)
+        if (!encoded) wide_ok = false;
       }
     }
     fout = (fin == net->fm[1]) ? net->fm[0] : net->fm[1];
@@ -3969,14 +4074,17 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       }
     } else if (fin_codes) {
       // follows layer 0 or a layer whose outputs were encoded, both compacted: no count to take over
-      HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], reinterpret_cast<const unsigned char *>(fin), fout,
-                                       npos + cur, tiles(P), mk, &seglive_out));
+      const unsigned char *cin = reinterpret_cast<const unsigned char *>(fin);
+      if (fin_wide)
+        HIP_OR_POISON(net, launch_gfm_u16(net, net->layers[(size_t)l], cin, fout, npos + cur, tiles(P), mk, &seglive_out));
+      else
+        HIP_OR_POISON(net, launch_gfm_u8(net, net->layers[(size_t)l], cin, fout, npos + cur, tiles(P), mk, &seglive_out));
       spread_used = true;
       fout_cols = ocols_on ? lcur.cols : nullptr;
-      net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE_CODES;
+      net->layer_kernel[(size_t)l] = fin_wide ? SDNN_KERNEL_GLOBAL_TILE_CODES16 : SDNN_KERNEL_GLOBAL_TILE_CODES;
       const int st = code_rows(net->bitsT) / 32;  // fp32 tiles per code tile
-      // (with the dictionary reset, the encoding and its report when this layer encoded its inputs)
-      net->layer_launches[(size_t)l] = gfm_launches(net, net->layers[(size_t)l], tiles(P), st * 32) + (encoded ? 3 : 0);
+      // (with the dictionary resets, encodings and their reports when this layer encoded its inputs)
+      net->layer_launches[(size_t)l] = gfm_launches(net, net->layers[(size_t)l], tiles(P), st * 32) + encode_tries;
     } else {
       // after a layer without compaction, this launch counts that layer's live rows
       const LayerDev &ld = net->layers[(size_t)l];
@@ -4004,7 +4112,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         spread_used = !small;
         fout_cols = ocols_on ? lcur.cols : nullptr;
         net->layer_kernel[(size_t)l] = SDNN_KERNEL_GLOBAL_TILE;
-        net->layer_launches[(size_t)l] = gfm_launches(net, ld, tiles(P), 0);
+        net->layer_launches[(size_t)l] = gfm_launches(net, ld, tiles(P), 0) + encode_tries;
       }
     }
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_end[(size_t)l], s));
@@ -4096,7 +4204,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       }
       fin = fout;
     }
-    fin_codes = fout_codes;
+    fin_codes = fout_codes;  // (one-byte codes: a layer writes no others)
+    fin_wide = false;
     // counts[l] is final once layer l has run (written by a compaction or by layer l's launch)
     if (reported)
       HIP_OR_POISON(net, follow_progress(l));
@@ -4183,6 +4292,7 @@ sdnn_status infer_impl(sdnn_net *net, const float *y0, int64_t n_rows, void *wor
   net->counts = reinterpret_cast<int *>(ws + w.counts);
   net->misc = reinterpret_cast<int *>(ws + w.misc);
   net->dict = reinterpret_cast<unsigned *>(ws + w.dict);
+  net->dict16 = net->path == 1 ? reinterpret_cast<unsigned *>(ws + w.dict16) : nullptr;
   net->seglive = reinterpret_cast<unsigned *>(ws + w.seglive);
   for (int i = 0; i < 2; ++i) net->part[i] = reinterpret_cast<unsigned *>(ws + w.part[i]);
   net->spread = reinterpret_cast<unsigned *>(ws + w.spread);

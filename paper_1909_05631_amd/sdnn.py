@@ -20,7 +20,7 @@ EXPORTED_SYMBOLS = [
 ]
 KERNEL_KINDS = {0: "none", 1: "k_layer_lds", 2: "k_layer_gfm", 3: "k_layer_gfm_u8", 4: "k_layer_gfm_small",
                 5: "k_pack_bits+k_layer_bits", 6: "k_pack_bits+k_layer_bits(codes)", 7: "k_pack_bits+k_layer_count",
-                8: "k_layers_lds"}
+                8: "k_layers_lds", 9: "k_layer_gfm_u16"}
 
 
 class SdnnError(RuntimeError):

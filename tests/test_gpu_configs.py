@@ -108,10 +108,11 @@ def test_all_live_sampled_rows(ci, nl, rows):
 @pytest.mark.parametrize("ci,nl,rows", [(3, 11, 512), (4, 11, 256)])
 def test_encoded_layer_inputs(ci, nl, rows):
     """All-live rows on the two widest networks (60,000 rows, 32-row fp32 tiles, code tiles of 128
-    and 64 rows): the inputs of layers 2-7 take far more than 256 distinct values, so their encoding
-    into one-byte codes overflows the dictionary and stops, and those layers gather fp32; from layer
-    8 on every entry is 32 (saturated), the encoding succeeds and the layers gather codes. A seeded
-    sample of rows is recomputed by the oracle; every count must be the row count."""
+    and 64 rows): the inputs of layers 2-7 take more than 256 distinct values, so their encoding
+    into one-byte codes overflows the dictionary and stops, and those layers gather two-byte codes
+    (up to 4096 values) or fp32; from layer 8 on every entry is 32 (saturated), the one-byte
+    encoding succeeds and the layers gather one-byte codes. A seeded sample of rows is recomputed by
+    the oracle; every count must be the row count."""
     import bench
     from paper_1909_05631_amd import sdnn
     cfg = bench.workload(synth.CONFIGS[ci], "alllive", nl)
@@ -127,8 +128,9 @@ def test_encoded_layer_inputs(ci, nl, rows):
     log(f"{cfg.name}: live counts {counts.tolist()}; kernels {names}")
     assert (counts == m).all() and cats.size == m
     assert names[0] == "k_pack_bits+k_layer_bits(codes)" and names[1] == "k_layer_gfm_u8"
-    assert any(k == "k_layer_gfm" for k in names[2:8])           # encodings that overflowed
-    assert all(k == "k_layer_gfm_u8" for k in names[8:nl])       # encoded inputs
+    assert all(k in ("k_layer_gfm", "k_layer_gfm_u16") for k in names[2:8])  # one-byte encodings overflowed
+    assert "k_layer_gfm" in names[2:8]                                       # and two-byte ones too
+    assert all(k == "k_layer_gfm_u8" for k in names[8:nl])                   # encoded inputs
     rng = np.random.default_rng(300 + ci)
     sample = np.sort(rng.choice(m, size=rows, replace=False))
     o = oracle.run_config_layers(y0[sample], cfg.net_id, nl, n, cfg.k, cfg.weight, cfg.bias, cfg.ymax,
