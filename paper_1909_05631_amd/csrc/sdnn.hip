@@ -322,94 +322,6 @@ __global__ __launch_bounds__(1024) void k_compact(unsigned *__restrict__ masks, 
   }
 }
 
-// After a compaction of the global-tile path: move the live positions of a layer's output tiles
-// into fresh tiles, dst[t][k][b] = the value at list position src[32t + b] of the source tiles
-// (tile src / 32, slot src % 32), for positions below *npos; zero past it. A work item is one new
-// tile and kRepackSources sources. The new tile's rows come from at most 32 old tiles (src is
-// ascending); for each of them, 8 lanes read a source's whole 128-byte segment (one 16-byte load
-// each), keep the rows the new tile takes, and place them in an LDS stage from which the new
-// segments are written whole. So each needed old segment is read once, coalesced. With seglive
-// set, an old segment whose bit there is clear was never stored (all its rows are zero) and is not
-// read. With cols set (tiles of a layer that computed only the columns cols[0..ncols); seglive is
-// then null), only those sources are moved.
-constexpr int kRepackSources = 256;
-__global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
-                                                const int *__restrict__ src, const int *__restrict__ npos,
-                                                const unsigned *__restrict__ seglive, const int *__restrict__ cols,
-                                                int ncols) {
-  __shared__ int otile[32];            // distinct old tiles of this new tile
-  __shared__ unsigned omask[32];       // their slots that this new tile takes
-  __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
-  __shared__ int nold;
-  __shared__ unsigned segw[32];        // seglive words of the old tiles for the current 32 sources
-  __shared__ float stage[32][33];
-  const int R = *npos;
-  const int ntiles = (R + 31) / 32;
-  const int nkc = (ncols + kRepackSources - 1) / kRepackSources;
-  const int tid = threadIdx.x, kk = tid >> 3, q = tid & 7;
-  const int NW = (N + 31) / 32;
-  for (int item = blockIdx.x; item < ntiles * nkc; item += gridDim.x) {
-    const int t = item / nkc, k0 = (item % nkc) * kRepackSources;
-    const int nb = min(32, R - t * 32);
-    if (tid == 0) {
-      int n = 0, last = -1;
-      for (int b = 0; b < nb; ++b) {
-        const int sp = src[t * 32 + b];
-        const int ot = sp >> 5;
-        if (ot != last) {
-          otile[n] = ot;
-          omask[n] = 0u;
-          ++n;
-          last = ot;
-        }
-        omask[n - 1] |= 1u << (sp & 31);
-        bslot[n - 1][sp & 31] = (unsigned char)b;
-      }
-      nold = n;
-    }
-    __syncthreads();
-    const int n = nold;
-    for (int kb = 0; kb < kRepackSources; kb += 32) {
-      const int kp = k0 + kb + kk;  // source position; the source is cols[kp] with a column list
-      const int k = kp < ncols ? (cols ? cols[kp] : kp) : N;
-      // rows not taken from any old tile (past nb) stay zero
-      for (int i = tid; i < 32 * 32; i += blockDim.x) stage[i >> 5][i & 31] = 0.0f;
-      // k0 + kb is a multiple of 32: one bitmap word per old tile covers these sources, bit kk
-      if (tid < n) segw[tid] = seglive ? seglive[(size_t)otile[tid] * NW + ((k0 + kb) >> 5)] : ~0u;
-      __syncthreads();
-      if (k < N) {
-        // old tiles in batches of 8: the batch's loads are all issued before the first is used
-        for (int i0 = 0; i0 < n; i0 += 8) {
-          float4 v[8];
-          unsigned mm[8];
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            const int i = min(i0 + u, n - 1);
-            mm[u] = i0 + u < n && ((segw[i] >> kk) & 1u) ? (omask[i] >> (4 * q)) & 15u : 0u;
-            // without a branch: a quad that is not needed reads the first one of the old tiles
-            // instead (a cache hit), so the eight loads issue back to back
-            const size_t at = mm[u] ? ((size_t)otile[i] * N + k) * 32 : 0;
-            v[u] = *(reinterpret_cast<const float4 *>(sfm + at) + q);
-          }
-#pragma unroll
-          for (int u = 0; u < 8; ++u) {
-            if (!mm[u]) continue;
-            const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-              if ((mm[u] >> c) & 1u) stage[kk][bslot[i0 + u][4 * q + c]] = e[c];
-          }
-        }
-      }
-      __syncthreads();
-      if (k < N)
-        *reinterpret_cast<float4 *>(dfm + ((size_t)t * N + k) * 32 + 4 * q) =
-            make_float4(stage[kk][4 * q], stage[kk][4 * q + 1], stage[kk][4 * q + 2], stage[kk][4 * q + 3]);
-      __syncthreads();
-    }
-  }
-}
-
 // Zeros into the 128-byte segments of fp32 tiles [0, (*npos + 31) / 32) whose seglive bit is clear
 // (segments that a producer skipped because all their rows are zero), for readers that take the
 // tiles as they are. 8 lanes write one segment.
@@ -1876,6 +1788,130 @@ __global__ void k_report_overflow(const int *__restrict__ overflow, unsigned lon
                                   unsigned long long tag) {
   const unsigned long long flags = *overflow != 0 ? 2ull : 0ull;
   __hip_atomic_store(notify, (tag << 40) | (flags << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// After a compaction of the global-tile path: move the live positions of a layer's output tiles
+// into fresh tiles, dst[t][k][b] = the value at list position src[32t + b] of the source tiles
+// (tile src / 32, slot src % 32), for positions below *npos; zero past it. A work item is one new
+// tile and kRepackSources sources. The new tile's rows come from at most 32 old tiles (src is
+// ascending); for each of them, 8 lanes read a source's whole 128-byte segment (one 16-byte load
+// each), keep the rows the new tile takes, and place them in an LDS stage from which the new
+// segments are written whole. So each needed old segment is read once, coalesced. With seglive
+// set, an old segment whose bit there is clear was never stored (all its rows are zero) and is not
+// read. With cols set (tiles of a layer that computed only the columns cols[0..ncols); seglive is
+// then null), only those sources are moved.
+// With CB = 1 the new tiles are written as one-byte dictionary codes instead, in code tiles of CR
+// positions as k_encode writes them (dcodes; cols must be null): the repack and the encoding of the
+// next layer's inputs in one pass. Every position of the last code tile is written (code 0 past
+// *npos). A full dictionary sets *overflow, and the workgroups stop at their next work item (the
+// caller then repacks the fp32 tiles).
+constexpr int kRepackSources = 256;
+template <int CB = 0, int CR = 32>
+__global__ __launch_bounds__(256) void k_repack(const float *__restrict__ sfm, float *__restrict__ dfm, int N,
+                                                const int *__restrict__ src, const int *__restrict__ npos,
+                                                const unsigned *__restrict__ seglive, const int *__restrict__ cols,
+                                                int ncols, unsigned char *__restrict__ dcodes, unsigned *__restrict__ gd,
+                                                int *__restrict__ overflow) {
+  __shared__ int otile[32];            // distinct old tiles of this new tile
+  __shared__ unsigned omask[32];       // their slots that this new tile takes
+  __shared__ unsigned char bslot[32][32];  // old tile i, old slot s -> new slot
+  __shared__ int nold;
+  __shared__ unsigned segw[32];        // seglive words of the old tiles for the current 32 sources
+  __shared__ float stage[32][33];
+  static_assert(CB == 0 || CB == 1, "fp32 tiles or one-byte codes");
+  constexpr int CE = CB > 0 ? kCacheEntries : 2;
+  __shared__ __align__(8) unsigned dlk[CE];  // the dictionary's LDS cache (CB > 0)
+  __shared__ __align__(8) unsigned dlc[CE];
+  __shared__ int stop;
+  if constexpr (CB > 0) {
+    for (int i = threadIdx.x; i < CE; i += blockDim.x) dlk[i] = kDictEmpty;
+  }
+  const int R = *npos;
+  // (codes: every 32-position tile of the last code tile, those past the list all zero)
+  const int ntiles = CB > 0 ? (R + CR - 1) / CR * (CR / 32) : (R + 31) / 32;
+  const int nkc = (ncols + kRepackSources - 1) / kRepackSources;
+  const int tid = threadIdx.x, kk = tid >> 3, q = tid & 7;
+  const int NW = (N + 31) / 32;
+  for (int item = blockIdx.x; item < ntiles * nkc; item += gridDim.x) {
+    const int t = item / nkc, k0 = (item % nkc) * kRepackSources;
+    const int nb = max(0, min(32, R - t * 32));
+    if constexpr (CB > 0) {
+      if (tid == 0) stop = __hip_atomic_load(overflow, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __syncthreads();
+      if (stop) return;  // uniform: every thread read the one word
+    }
+    if (tid == 0) {
+      int n = 0, last = -1;
+      for (int b = 0; b < nb; ++b) {
+        const int sp = src[t * 32 + b];
+        const int ot = sp >> 5;
+        if (ot != last) {
+          otile[n] = ot;
+          omask[n] = 0u;
+          ++n;
+          last = ot;
+        }
+        omask[n - 1] |= 1u << (sp & 31);
+        bslot[n - 1][sp & 31] = (unsigned char)b;
+      }
+      nold = n;
+    }
+    __syncthreads();
+    const int n = nold;
+    for (int kb = 0; kb < kRepackSources; kb += 32) {
+      const int kp = k0 + kb + kk;  // source position; the source is cols[kp] with a column list
+      const int k = kp < ncols ? (cols ? cols[kp] : kp) : N;
+      // rows not taken from any old tile (past nb) stay zero
+      for (int i = tid; i < 32 * 32; i += blockDim.x) stage[i >> 5][i & 31] = 0.0f;
+      // k0 + kb is a multiple of 32: one bitmap word per old tile covers these sources, bit kk
+      if (tid < n) segw[tid] = seglive ? seglive[(size_t)otile[tid] * NW + ((k0 + kb) >> 5)] : ~0u;
+      __syncthreads();
+      if (k < N) {
+        // old tiles in batches of 8: the batch's loads are all issued before the first is used
+        for (int i0 = 0; i0 < n; i0 += 8) {
+          float4 v[8];
+          unsigned mm[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int i = min(i0 + u, n - 1);
+            mm[u] = i0 + u < n && ((segw[i] >> kk) & 1u) ? (omask[i] >> (4 * q)) & 15u : 0u;
+            // without a branch: a quad that is not needed reads the first one of the old tiles
+            // instead (a cache hit), so the eight loads issue back to back
+            const size_t at = mm[u] ? ((size_t)otile[i] * N + k) * 32 : 0;
+            v[u] = *(reinterpret_cast<const float4 *>(sfm + at) + q);
+          }
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (!mm[u]) continue;
+            const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+              if ((mm[u] >> c) & 1u) stage[kk][bslot[i0 + u][4 * q + c]] = e[c];
+          }
+        }
+      }
+      __syncthreads();
+      if constexpr (CB > 0) {
+        if (k < N) {
+          // codes of rows 4q .. 4q + 3 of this 32-position tile, at its place in its code tile
+          unsigned c[4];
+          bool miss = false;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) miss |= !cache_lookup(__float_as_uint(stage[kk][4 * q + u]), dlk, dlc, &c[u]);
+          if (miss) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) c[u] = dict_code(stage[kk][4 * q + u], dlk, dlc, gd, overflow);
+          }
+          unsigned char *d = dcodes + ((size_t)(t / (CR / 32)) * N + k) * CR + (t % (CR / 32)) * 32 + 4 * q;
+          *reinterpret_cast<unsigned *>(d) = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
+        }
+      } else if (k < N) {
+        *reinterpret_cast<float4 *>(dfm + ((size_t)t * N + k) * 32 + 4 * q) =
+            make_float4(stage[kk][4 * q], stage[kk][4 * q + 1], stage[kk][4 * q + 2], stage[kk][4 * q + 3]);
+      }
+      __syncthreads();
+    }
+  }
 }
 
 // Layer-0 inputs as bits (the challenge inputs are binary images, Sec. IV): pack the live rows into
@@ -3917,6 +3953,8 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
   bool fin_codes = false, fout_codes = false;  // the tiles hold dictionary codes
   bool fin_wide = false;  // fin's codes are two bytes (k_encode<64, 2>), else one
   bool wide_ok = true;    // a two-byte encoding is worth trying
+  bool next_tried = false;     // the repack after this layer tried one-byte codes for the next layer
+  bool repacked_codes = false;  // ... and wrote them (else fp32 tiles)
   int last_list = 0;
   bool compacted = true;   // the last layer run has been followed by a compaction
   PollRing ring;
@@ -3973,9 +4011,13 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
     if (rec) HIP_OR_POISON(net, hipEventRecord(net->prof_start[(size_t)l], s));
     bool encoded = false;  // this layer reads codes that k_encode wrote from fp32 tiles
     int encode_tries = 0;  // launches spent on encodings of this layer's inputs
+    const bool tried = next_tried;  // the repack before this layer tried one-byte codes (they overflowed)
+    next_tried = false;
+    repacked_codes = false;
     if (l > 0 && !fin_codes && compacted && live_bound >= kEncodeMinRows && !net->equal_value_kernels) {
       // a large layer on fp32 tiles: if its inputs take at most 256 distinct values (saturated rows
-      // do), encode them as one-byte codes into the free buffer and gather those instead; else, if
+      // do), encode them as one-byte codes into the free buffer and gather those instead (unless the
+      // repack before this layer found that they do not fit: tried); else, if
       // they take at most 4096 and the fp32 tiles outgrow the L2 (kXcdL2Bytes), as two-byte codes;
       // a full dictionary stops an encoding early, and when both stop the layer reads the fp32 tiles
       unsigned char *cbuf = reinterpret_cast<unsigned char *>((fin == net->fm[1]) ? net->fm[0] : net->fm[1]);
@@ -4019,7 +4061,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
         }
         return hipSuccess;
       };
-      HIP_OR_POISON(net, try_encode(1));
+      if (!tried) HIP_OR_POISON(net, try_encode(1));
       if (!encoded && net->dict16 && wide_ok && (size_t)net->N * 32 * sizeof(float) > kXcdL2Bytes) {
         HIP_OR_POISON(net, try_encode(2));
         // inputs with more than 4096 values: the layers after it are not tried again until the
@@ -4133,6 +4175,37 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       last_list = cur ^ 1;
       return hipGetLastError();
     };
+    // the repack of this layer's outputs as the next layer's one-byte codes (k_repack<1, CR>), into
+    // dst; sets repacked_codes when the dictionary held every value
+    auto repack_codes = [&](float *dst) -> hipError_t {
+      unsigned *gd = net->dict;
+      hipLaunchKernelGGL(k_dict_reset<1>, dim3(1), dim3(256), 0, s, gd, net->misc + kOverflowSlot);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      const int cr = code_rows(net->bitsT);
+      const int64_t items = (live_bound + cr - 1) / cr * (cr / 32) * ((net->N + kRepackSources - 1) / kRepackSources);
+      const int grid = (int)std::max<int64_t>(1, std::min<int64_t>(net->cus * 8, items));
+      unsigned char *dc = reinterpret_cast<unsigned char *>(dst);
+      const unsigned *sl = seglive_out ? net->seglive : nullptr;
+      int *of = net->misc + kOverflowSlot;
+      const int *sp = net->src[cur ^ 1], *np = npos + (cur ^ 1);
+      if (cr == 128)
+        hipLaunchKernelGGL((k_repack<1, 128>), dim3(grid), dim3(256), 0, s, fout, (float *)nullptr, net->N, sp, np, sl,
+                           (const int *)nullptr, net->N, dc, gd, of);
+      else
+        hipLaunchKernelGGL((k_repack<1, 64>), dim3(grid), dim3(256), 0, s, fout, (float *)nullptr, net->N, sp, np, sl,
+                           (const int *)nullptr, net->N, dc, gd, of);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      const unsigned long long tag = next_report_tag(net);
+      hipLaunchKernelGGL(k_report_overflow, dim3(1), dim3(1), 0, s, of, net->notify_dev, tag);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      Report rp;
+      e = wait_report(net, tag, np, &rp);
+      if (e == hipSuccess && !rp.overflow) repacked_codes = true;
+      return e;
+    };
     compacted = false;
     bool adopt;
     if (!small) {
@@ -4187,9 +4260,21 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       else if (fout_codes)
         hipLaunchKernelGGL(k_repack_u8<64>, dim3(grid), dim3(256), 0, s, reinterpret_cast<const unsigned char *>(fout),
                            reinterpret_cast<unsigned char *>(dst), net->N, net->src[cur ^ 1], npos + (cur ^ 1));
-      else
-        hipLaunchKernelGGL(k_repack, dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1], npos + (cur ^ 1),
-                           seglive_out ? net->seglive : nullptr, fout_cols, fout_cols ? lcur.D : net->N);
+      else {
+        // the next layer encodes its inputs if they fit a dictionary (see the start of the loop):
+        // the repack writes one-byte codes itself, and falls back to fp32 tiles when they overflow
+        // (two-byte codes are then tried by k_encode from the fp32 tiles: written by the repack
+        // they measured slower, 30.9 ms per step against 30.4 at 65536 neurons and 60,000 inputs)
+        if (live_bound >= kEncodeMinRows && !net->equal_value_kernels && !fout_cols) {
+          next_tried = true;
+          HIP_OR_POISON(net, repack_codes(dst));
+          if (repacked_codes) wide_ok = true;
+        }
+        if (!repacked_codes)
+          hipLaunchKernelGGL((k_repack<0, 32>), dim3(grid), dim3(256), 0, s, fout, dst, net->N, net->src[cur ^ 1],
+                             npos + (cur ^ 1), seglive_out ? net->seglive : nullptr, fout_cols,
+                             fout_cols ? lcur.D : net->N, (unsigned char *)nullptr, (unsigned *)nullptr, (int *)nullptr);
+      }
       HIP_OR_POISON(net, hipGetLastError());
       fin = dst;
       cur ^= 1;
@@ -4204,7 +4289,7 @@ sdnn_status infer_gfm(sdnn_net *net, const float *y0, int M) {
       }
       fin = fout;
     }
-    fin_codes = fout_codes;  // (one-byte codes: a layer writes no others)
+    fin_codes = fout_codes || repacked_codes;  // (one-byte codes: a layer or a repack writes no others)
     fin_wide = false;
     // counts[l] is final once layer l has run (written by a compaction or by layer l's launch)
     if (reported)

@@ -52,11 +52,11 @@ def test_full_config_every_row_equal_value_kernels(ci):
     assert_parity(gpu, o, cats)
 
 
-@pytest.mark.parametrize("equal_values", [False, True])
-@pytest.mark.parametrize("ci", [2, 3])
+@pytest.mark.parametrize("ci,equal_values", [(2, False), (2, True), (3, False), (3, True), (4, False)])
 def test_structured_full_config_every_row(ci, equal_values):
     """The second workload: structured (RadiX-Net style) layers of the config's width and depth on the
-    config's inputs, full size on the GPU, every row against the oracle."""
+    config's inputs, full size on the GPU, every row against the oracle. At 16384 and 65536 neurons
+    the repacks after layers 1-3 write the next layer's inputs as one- or two-byte codes."""
     cfg = synth.CONFIGS[ci]
     n, L = cfg.n_neurons, cfg.n_layers
     y0 = synth.config_inputs(cfg)

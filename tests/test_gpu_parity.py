@@ -507,8 +507,8 @@ def test_two_byte_codes(n, ell):
     """Layer inputs of 257 to 4096 distinct values are gathered as two-byte codes where the fp32
     tiles are larger than an XCD's L2 (40,000 neurons: 5 MB; at 6000 the same layers gather fp32).
     Weights that are multiples of 1/64 on binary inputs give layer 0 a few hundred output values:
-    its one-byte codes overflow (it writes fp32), the one-byte encoding of layer 1's inputs
-    overflows and the two-byte one holds.
+    its one-byte codes overflow (it writes fp32), and the rows with two nonzero inputs (15%) die, so
+    the repack after it encodes layer 1's inputs: one-byte codes overflow, two-byte ones hold.
     Layer 1's random weights give millions of values: both encodings of layer 2's inputs overflow
     (fp32 gather). Layer 2 saturates every entry (one value: one-byte codes for layer 3); layer 3's
     weights, multiples of 1/2048 on inputs of 32, give a few hundred values again, so layer 4
@@ -527,15 +527,19 @@ def test_two_byte_codes(n, ell):
         return cp[0], ri, v, np.full(n, bias, np.float32)
 
     wide = 40 if ell else 32
-    layers = [layer(0, 1 / 64, 32, -0.3), layer(1, 0, wide, -0.2), layer(2, 1 / 64, 32, 40.0),
+    layers = [layer(0, 1 / 64, 32, -1.2), layer(1, 0, wide, -0.2), layer(2, 1 / 64, 32, 40.0),
               layer(3, 1 / 2048, 32, -0.3), layer(4, 0, wide, -0.2, 0.05), layer(5, 1 / 64, 32, -0.3)]
     y0 = (rng.random((m, n)) < 0.5).astype(np.float32)
+    for i in np.nonzero(rng.random(m) < 0.15)[0]:
+        y0[i] = 0.0
+        y0[i, rng.choice(n, 2, replace=False)] = 1.0
     log(f"two-byte codes n={n} ell={ell}")
     gpu, o, cats = run_both(n, layers, y0)
     kind, launches = gpu.net.layer_info()
     names = [sdnn_kind(k) for k in kind]
     log(f"kernels {names}, launches {launches.tolist()}")
-    assert (gpu.net.live_counts() == m).all()
+    counts = gpu.net.live_counts()
+    assert counts[0] == m and 2048 <= counts[1] < 0.9 * m  # rows die in layer 0: its outputs are repacked
     coded = "k_layer_gfm_u16" if n * 32 * 4 > 4 << 20 else "k_layer_gfm"
     assert names == ["k_pack_bits+k_layer_bits", coded, "k_layer_gfm", "k_layer_gfm_u8", coded, "k_layer_gfm"]
     assert_parity(gpu, o, cats)
