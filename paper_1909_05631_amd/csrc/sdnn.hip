@@ -181,7 +181,7 @@ template <> struct DictShape<1> {
   static constexpr int kSlots = kDictSlots, kHash = kDictHashSlots, kHashShift = 14, kCache = 1024, kCacheShift = 12;
 };
 template <> struct DictShape<2> {
-  static constexpr int kSlots = 4096, kHash = 16384, kHashShift = 10, kCache = 2048, kCacheShift = 11;
+  static constexpr int kSlots = 4096, kHash = 16384, kHashShift = 10, kCache = 4096, kCacheShift = 10;
 };
 template <int CB> __host__ __device__ constexpr int dict_key_off() { return DictShape<CB>::kSlots; }
 template <int CB> __host__ __device__ constexpr int dict_code_off() { return dict_key_off<CB>() + DictShape<CB>::kHash; }
