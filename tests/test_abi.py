@@ -33,6 +33,16 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, name), name
 
 
+def test_kernel_kinds_match_the_header():
+    """The binding's names of the layer kernel families cover exactly the values of the header's
+    sdnn_kernel_kind enum (what sdnn_layer_info reports)."""
+    text = open(os.path.join(ROOT, "include", "sdnn.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    body = re.search(r"typedef enum \{(.*?)\} sdnn_kernel_kind;", text, flags=re.S).group(1)
+    values = {int(v) for v in re.findall(r"SDNN_KERNEL_[A-Z0-9_]+\s*=\s*(\d+)", body)}
+    assert values == set(sdnn.KERNEL_KINDS)
+
+
 def _status(fn, *args):
     return fn(*args)
 
