@@ -1440,8 +1440,8 @@ constexpr int u8_waves(int WM, int CR, int CB) {
 // tile and source) says so. Registers are held to 5 waves per SIMD for one-byte 64-row codes (more
 // waves keep more gathers in flight; 6 spill), 4 for 128-row codes and 3 for two-byte codes with
 // staged weights (u8_waves). Live rows go to masks, or with spread set to the spread words of each
-// fp32 tile (see or_mask). With cols set (kWOne only), the launch computes the ncols columns cols[p] alone
-// (see k_layer_gfm), stores every segment of them and leaves seglive untouched.
+// fp32 tile (see or_mask). With cols set (kWOne only), the launch computes the ncols columns
+// cols[p] alone (see k_layer_gfm), stores every segment of them and leaves seglive untouched.
 template <int WM, int CR, int RPL, int OPL, int CB = 1>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(u8_waves(WM, CR, CB)))) void k_layer_gfm_u8(
     const unsigned char *__restrict__ cin, float *__restrict__ fout, int N, const int2 *__restrict__ ell, int K,
