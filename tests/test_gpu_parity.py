@@ -545,6 +545,34 @@ def test_two_byte_codes(n, ell):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("nvals", [4096, 4097])
+def test_two_byte_dictionary_capacity(nvals):
+    """The two-byte dictionary's capacity, exactly: layer 0 gives column j the single source j with
+    weight 1 + (j mod (nvals - 1)) / 8192 (exact in fp32) and bias -0.5, so on binary rows its outputs
+    take exactly nvals distinct values (+0 and nvals - 1 others). 4096 values fit the 4096 codes and
+    layer 1 gathers two-byte codes; 4097 overflow the dictionary and layer 1 gathers fp32 tiles.
+    40,000 neurons (two-byte codes are tried where the fp32 tiles outgrow the L2), 2100 rows."""
+    n, m = 40000, 2100
+    rng = np.random.default_rng(71)
+    cp0 = np.arange(n + 1, dtype=np.int64)
+    ri0 = np.arange(n, dtype=np.int32)
+    v0 = (1.0 + (np.arange(n) % (nvals - 1)) / 8192.0).astype(np.float32)
+    layers = [(cp0, ri0, v0, np.full(n, -0.5, np.float32))]
+    for l in (1, 2):
+        cp, ri, _ = synth.layers_csc(70, l, 1, n)
+        layers.append((cp[0], ri, rng.uniform(0.0, 0.125, size=ri.size).astype(np.float32),
+                       np.full(n, -0.2, np.float32)))
+    y0 = (rng.random((m, n)) < 0.5).astype(np.float32)
+    log(f"two-byte dictionary capacity: {nvals} values")
+    gpu, o, cats = run_both(n, layers, y0)
+    names = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
+    log(f"kernels {names}")
+    assert (gpu.net.live_counts() == m).all()
+    layer1 = "k_layer_gfm_u16" if nvals <= 4096 else "k_layer_gfm"
+    assert names == ["k_pack_bits+k_layer_bits", layer1, "k_layer_gfm"]
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("nl", [2, 5])
 def test_structured_code_layer_columns(nl, equal_values):
