@@ -545,14 +545,15 @@ def test_two_byte_codes(n, ell):
     assert_parity(gpu, o, cats)
 
 
-@pytest.mark.parametrize("nvals", [4096, 4097])
-def test_two_byte_dictionary_capacity(nvals):
-    """The two-byte dictionary's capacity, exactly: layer 0 gives column j the single source j with
-    weight 1 + (j mod (nvals - 1)) / 8192 (exact in fp32) and bias -0.5, so on binary rows its outputs
-    take exactly nvals distinct values (+0 and nvals - 1 others). 4096 values fit the 4096 codes and
-    layer 1 gathers two-byte codes; 4097 overflow the dictionary and layer 1 gathers fp32 tiles.
-    40,000 neurons (two-byte codes are tried where the fp32 tiles outgrow the L2), 2100 rows."""
-    n, m = 40000, 2100
+@pytest.mark.parametrize("n,nvals", [(6000, 256), (6000, 257), (40000, 4096), (40000, 4097)])
+def test_dictionary_capacity(n, nvals):
+    """The dictionaries' capacities, exactly: layer 0 gives column j the single source j with weight
+    1 + (j mod (nvals - 1)) / 8192 (exact in fp32) and bias -0.5, so on binary rows its outputs take
+    exactly nvals distinct values (+0 and nvals - 1 others). 256 values fit the one-byte codes that
+    layer 0 writes and layer 1 gathers; at 257 layer 0 rewrites fp32 tiles. At 40,000 neurons (where
+    two-byte codes are tried: the fp32 tiles outgrow the L2) 4096 values fit the two-byte codes of
+    layer 1's inputs; 4097 overflow them and layer 1 gathers fp32 tiles. 2100 rows."""
+    m = 2100
     rng = np.random.default_rng(71)
     cp0 = np.arange(n + 1, dtype=np.int64)
     ri0 = np.arange(n, dtype=np.int32)
@@ -563,13 +564,16 @@ def test_two_byte_dictionary_capacity(nvals):
         layers.append((cp[0], ri, rng.uniform(0.0, 0.125, size=ri.size).astype(np.float32),
                        np.full(n, -0.2, np.float32)))
     y0 = (rng.random((m, n)) < 0.5).astype(np.float32)
-    log(f"two-byte dictionary capacity: {nvals} values")
+    log(f"dictionary capacity: n={n}, {nvals} values")
     gpu, o, cats = run_both(n, layers, y0)
     names = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
     log(f"kernels {names}")
     assert (gpu.net.live_counts() == m).all()
-    layer1 = "k_layer_gfm_u16" if nvals <= 4096 else "k_layer_gfm"
-    assert names == ["k_pack_bits+k_layer_bits", layer1, "k_layer_gfm"]
+    expect = {256: ["k_pack_bits+k_layer_bits(codes)", "k_layer_gfm_u8"],
+              257: ["k_pack_bits+k_layer_bits", "k_layer_gfm"],
+              4096: ["k_pack_bits+k_layer_bits", "k_layer_gfm_u16"],
+              4097: ["k_pack_bits+k_layer_bits", "k_layer_gfm"]}[nvals]
+    assert names == expect + ["k_layer_gfm"]
     assert_parity(gpu, o, cats)
 
 
