@@ -577,6 +577,38 @@ def test_dictionary_capacity(n, nvals):
     assert_parity(gpu, o, cats)
 
 
+@pytest.mark.parametrize("nvals", [256, 257])
+def test_repack_dictionary_capacity(nvals):
+    """The repack that writes the next layer's one-byte codes, at the dictionary's exact bound.
+    Layer 0 passes the binary inputs through (identity, weight 1, bias 0: two values, one-byte
+    codes). Layer 1 gives column j < 3000 the single source j with weight 1 + (j mod (nvals - 1)) /
+    8192 and bias -0.5, and kills the other columns (bias -5), so its outputs take exactly nvals
+    values, and the 15% of rows whose ones all lie in the killed columns die. The repack after it
+    writes layer 2's inputs as codes for 256 values; for 257 it falls back to fp32 tiles."""
+    n, m = 6000, 2600
+    rng = np.random.default_rng(73)
+    cp0 = np.arange(n + 1, dtype=np.int64)
+    ri0 = np.arange(n, dtype=np.int32)
+    v1 = (1.0 + (np.arange(n) % (nvals - 1)) / 8192.0).astype(np.float32)
+    b1 = np.where(np.arange(n) < n // 2, -0.5, -5.0).astype(np.float32)
+    cp2, ri2, _ = synth.layers_csc(72, 2, 1, n)
+    w2 = rng.uniform(0.0, 0.125, size=ri2.size).astype(np.float32)
+    layers = [(cp0, ri0, np.ones(n, np.float32), np.zeros(n, np.float32)), (cp0, ri0, v1, b1),
+              (cp2[0], ri2, w2, np.full(n, -0.2, np.float32))]
+    y0 = (rng.random((m, n)) < 0.5).astype(np.float32)
+    dying = rng.random(m) < 0.15
+    y0[dying, : n // 2] = 0.0
+    log(f"repack dictionary capacity: {nvals} values")
+    gpu, o, cats = run_both(n, layers, y0)
+    names = [sdnn_kind(k) for k in gpu.net.layer_info()[0]]
+    counts = gpu.net.live_counts()
+    log(f"kernels {names}, live counts {counts.tolist()}")
+    assert counts[1] == m and 2048 <= counts[2] <= 0.9 * m
+    assert names == ["k_pack_bits+k_layer_bits(codes)", "k_layer_gfm_u8",
+                     "k_layer_gfm_u8" if nvals <= 256 else "k_layer_gfm"]
+    assert_parity(gpu, o, cats)
+
+
 @pytest.mark.parametrize("equal_values", [False, True])
 @pytest.mark.parametrize("nl", [2, 5])
 def test_structured_code_layer_columns(nl, equal_values):
