@@ -418,6 +418,8 @@ def main() -> int:
         "live_edges_per_s": live_edges / t_step,
         "categories": int(cats.size),
         "live_counts_head": [int(c) for c in counts[:8]],
+        # kernel family of each of the first 8 layers of the last run (sdnn_layer_info)
+        "layer_kernels_head": [sdnn.KERNEL_KINDS.get(int(k), str(int(k))) for k in net.layer_info()[0][:8]],
     }
     print(json.dumps(out))
     return 0
