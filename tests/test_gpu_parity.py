@@ -502,7 +502,7 @@ def test_structured_lds_columns(case):
     assert_parity(gpu, o, cats)
 
 
-@pytest.mark.parametrize("n,ell", [(40000, False), (40000, True), (6000, False)])
+@pytest.mark.parametrize("n,ell", [(40000, False), (40001, True), (6000, False)])
 def test_two_byte_codes(n, ell):
     """Layer inputs of 257 to 4096 distinct values are gathered as two-byte codes where the fp32
     tiles are larger than an XCD's L2 (40,000 neurons: 5 MB; at 6000 the same layers gather fp32).
@@ -514,7 +514,7 @@ def test_two_byte_codes(n, ell):
     weights, multiples of 1/2048 on inputs of 32, give a few hundred values again, so layer 4
     gathers two-byte codes after the one-byte success re-enabled them; layer 5 reads fp32 (one
     value per column, n in all). With ell, layers 1 and 4 have columns of up to 40 sources (the ELL
-    form of the kernels)."""
+    form of the kernels), on a width that is not a multiple of 32."""
     m = 2600
     rng = np.random.default_rng(57 + ell + n)
 
