@@ -508,7 +508,8 @@ def test_two_byte_codes(n, ell):
     tiles are larger than an XCD's L2 (40,000 neurons: 5 MB; at 6000 the same layers gather fp32).
     Weights that are multiples of 1/64 on binary inputs give layer 0 a few hundred output values:
     its one-byte codes overflow (it writes fp32), and the rows with two nonzero inputs (15%) die, so
-    the repack after it encodes layer 1's inputs: one-byte codes overflow, two-byte ones hold.
+    layer 1's inputs come through the repack: its one-byte codes overflow, and the two-byte encoding
+    of the repacked tiles holds.
     Layer 1's random weights give millions of values: both encodings of layer 2's inputs overflow
     (fp32 gather). Layer 2 saturates every entry (one value: one-byte codes for layer 3); layer 3's
     weights, multiples of 1/2048 on inputs of 32, give a few hundred values again, so layer 4
